@@ -1,0 +1,740 @@
+/*
+ * tangram_oracle.c -- plain, slow, single-threaded CPU oracle for the
+ * model-slice / GPU-island plan search of Tangram (arXiv 2606.16907).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this file's library.  It shares no code,
+ * header, table or constant generator with the HIP library; the two are
+ * written separately from the same definitions.
+ *
+ * What it computes (every quantity is a plain definition written out):
+ *   1. the candidate space: every contiguous layer range [i, j) ("model slice",
+ *      Sec. 4.2) times every island (Sec. 4.1) times every intra-island config
+ *      (tp, dp, ep, zero stage, micro-batch) -- the model-slice/island pairs
+ *      that Sec. 5.1 enumerates and hands to a homogeneous parallelizer;
+ *   2. per candidate an analytic step-time cost and the deepest 1F1B pipeline
+ *      position it fits at (Sec. 5.2: memory depends on the stage's position,
+ *      a plan is reused "until it is no longer feasible");
+ *   3. pruning (Sec. 5.1 infeasibility pruning, the incompatibility pruning of
+ *      the contributions and of the Fig. 12 ablation, and dominance): the
+ *      surviving set;
+ *   4. pipeline composition (Sec. 5.2, steps (1)-(3) of the composition
+ *      algorithm): lowest bottleneck first, then lowest fill at that bottleneck,
+ *      islands used at most once and possibly eliminated.
+ * The paper delegates the cost model to the parallelizer's profile() and
+ * parallelize() (Tab. 2); the analytic model below is this project's stated
+ * reading of it.  Floating point is IEEE binary64, each operation rounded once
+ * in the parenthesised order written here; build with -ffp-contract=off.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define TGO_OK 0
+#define TGO_EINVAL (-1)
+#define TGO_ENOMEM (-2)
+#define TGO_ECAPACITY (-4)
+#define TGO_ENOPLAN (-5)
+
+#define NF 7 /* per-layer fields */
+enum { F_FLOPS = 0, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A, F_OUTACT };
+
+typedef struct {
+    int32_t island, first_layer, end_layer, tp, dp, ep, zero, mb, depth, pad;
+    int64_t pair_index;
+    double cost, mem_bytes, link_out;
+} tgo_stage;
+
+typedef struct {
+    int32_t status, b, m, S;
+    double P, F, T;
+    tgo_stage stage[255];
+} tgo_plan;
+
+typedef struct {
+    int k, tp, dp, ep, z, mb;
+    int64_t b;
+} ocfg;
+
+typedef struct {
+    int L, K;
+    int64_t *layer[NF]; /* [f][L] */
+    int32_t *n_gpus;
+    double *peak, *hbm, *intra, *inter; /* inter: K*K row-major */
+    int64_t B;
+    int n_experts;
+    int ntp, tp[8], nep, ep[8], nmb, mb[8], nz, zs[4];
+    double eta, mem_frac;
+    /* derived */
+    int64_t NS, ncfg, N;
+    int64_t *cfg_off; /* K+1 */
+    ocfg *cfg;        /* ncfg */
+    int64_t *slice_sum; /* NS x 6: flops, dparam, eparam, act, tpcomm, a2a */
+    int nb;
+    int64_t *bvals; /* distinct compatible b, ascending */
+} oprob;
+
+/* ------------------------------------------------------------------------ */
+/* slices: s enumerates 0 <= i < j <= L lexicographically (i, then j)       */
+/* ------------------------------------------------------------------------ */
+static int64_t slice_index(int L, int i, int j) {
+    /* number of slices with first layer < i, plus the offset of j */
+    int64_t before = 0;
+    for (int a = 0; a < i; a++) before += (int64_t)(L - a);
+    return before + (int64_t)(j - i - 1);
+}
+
+static void slice_ij(int L, int64_t s, int *pi, int *pj) {
+    int i = 0;
+    while (s >= (int64_t)(L - i)) { s -= (int64_t)(L - i); i++; }
+    *pi = i;
+    *pj = i + 1 + (int)s;
+}
+
+/* ------------------------------------------------------------------------ */
+/* configs of one island: lexicographic (tp, dp, ep, z, mb)                  */
+/* ------------------------------------------------------------------------ */
+static int ep_admissible(const oprob *p, int ep, int dp) {
+    if (dp % ep != 0) return 0;
+    if (p->n_experts == 0) return ep == 1;
+    return p->n_experts % ep == 0;
+}
+
+static int64_t island_configs(const oprob *p, int k, ocfg *out) {
+    int64_t c = 0;
+    int n = p->n_gpus[k];
+    for (int a = 0; a < p->ntp; a++) {
+        int tp = p->tp[a];
+        if (tp > n) continue;
+        for (int dp = 1; dp <= n / tp; dp++)
+            for (int e = 0; e < p->nep; e++) {
+                if (!ep_admissible(p, p->ep[e], dp)) continue;
+                for (int zi = 0; zi < p->nz; zi++)
+                    for (int mi = 0; mi < p->nmb; mi++) {
+                        if (out) {
+                            ocfg *q = &out[c];
+                            q->k = k; q->tp = tp; q->dp = dp; q->ep = p->ep[e];
+                            q->z = p->zs[zi]; q->mb = p->mb[mi];
+                            q->b = (int64_t)dp * (int64_t)p->mb[mi];
+                        }
+                        c++;
+                    }
+            }
+    }
+    return c;
+}
+
+static int strictly_ascending_pos(const int32_t *v, int n) {
+    if (n < 1 || n > 8) return 0;
+    for (int a = 0; a < n; a++) {
+        if (v[a] < 1) return 0;
+        if (a > 0 && v[a] <= v[a - 1]) return 0;
+    }
+    return 1;
+}
+
+static int cmp_i64(const void *a, const void *b) {
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    return (x > y) - (x < y);
+}
+
+void tgo_destroy(void *h) {
+    oprob *p = (oprob *)h;
+    if (!p) return;
+    for (int f = 0; f < NF; f++) free(p->layer[f]);
+    free(p->n_gpus); free(p->peak); free(p->hbm); free(p->intra); free(p->inter);
+    free(p->cfg_off); free(p->cfg); free(p->slice_sum); free(p->bvals);
+    free(p);
+}
+
+/* layers: NF*L int64, field-major (all fwd_flops, then dense_params, ...). */
+int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double *peak,
+               const double *hbm, const double *intra, int K, const double *inter,
+               int64_t global_batch, int n_experts, const int32_t *tp, int ntp,
+               const int32_t *ep, int nep, const int32_t *mb, int nmb, uint32_t zero_mask,
+               double eta, double mem_frac, void **out) {
+    *out = NULL;
+    if (L < 1 || L > 512 || K < 1 || K > 255) return TGO_EINVAL;
+    if (global_batch < 1 || n_experts < 0) return TGO_EINVAL;
+    if (!strictly_ascending_pos(tp, ntp) || !strictly_ascending_pos(ep, nep) ||
+        !strictly_ascending_pos(mb, nmb))
+        return TGO_EINVAL;
+    if (zero_mask == 0 || (zero_mask & ~0xFu)) return TGO_EINVAL;
+    if (!(eta > 0.0) || !isfinite(eta) || !(mem_frac > 0.0) || !isfinite(mem_frac))
+        return TGO_EINVAL;
+    for (int k = 0; k < K; k++) {
+        if (n_gpus[k] < 1 || n_gpus[k] > 65536) return TGO_EINVAL;
+        if (!(peak[k] > 0.0) || !isfinite(peak[k])) return TGO_EINVAL;
+        if (!(hbm[k] > 0.0) || !isfinite(hbm[k])) return TGO_EINVAL;
+        if (!(intra[k] > 0.0) || !isfinite(intra[k])) return TGO_EINVAL;
+    }
+    for (int a = 0; a < K * K; a++)
+        if (!(inter[a] >= 0.0)) return TGO_EINVAL; /* rejects NaN and negatives; +inf allowed */
+    /* every layer value >= 0 and every whole-model sum < 2^62 */
+    for (int f = 0; f < NF; f++) {
+        int64_t acc = 0;
+        for (int l = 0; l < L; l++) {
+            int64_t v = layers[(int64_t)f * L + l];
+            if (v < 0 || v >= ((int64_t)1 << 62) - acc) return TGO_EINVAL;
+            acc += v;
+        }
+    }
+
+    oprob *p = (oprob *)calloc(1, sizeof(oprob));
+    if (!p) return TGO_ENOMEM;
+    p->L = L; p->K = K;
+    for (int f = 0; f < NF; f++) {
+        p->layer[f] = (int64_t *)malloc(sizeof(int64_t) * L);
+        memcpy(p->layer[f], layers + (int64_t)f * L, sizeof(int64_t) * L);
+    }
+    p->n_gpus = (int32_t *)malloc(sizeof(int32_t) * K);
+    p->peak = (double *)malloc(sizeof(double) * K);
+    p->hbm = (double *)malloc(sizeof(double) * K);
+    p->intra = (double *)malloc(sizeof(double) * K);
+    p->inter = (double *)malloc(sizeof(double) * K * K);
+    memcpy(p->n_gpus, n_gpus, sizeof(int32_t) * K);
+    memcpy(p->peak, peak, sizeof(double) * K);
+    memcpy(p->hbm, hbm, sizeof(double) * K);
+    memcpy(p->intra, intra, sizeof(double) * K);
+    memcpy(p->inter, inter, sizeof(double) * K * K);
+    p->B = global_batch;
+    p->n_experts = n_experts;
+    p->ntp = ntp; memcpy(p->tp, tp, sizeof(int32_t) * ntp);
+    p->nep = nep; memcpy(p->ep, ep, sizeof(int32_t) * nep);
+    p->nmb = nmb; memcpy(p->mb, mb, sizeof(int32_t) * nmb);
+    p->nz = 0;
+    for (int z = 0; z < 4; z++)
+        if (zero_mask & (1u << z)) p->zs[p->nz++] = z;
+    p->eta = eta;
+    p->mem_frac = mem_frac;
+
+    p->NS = (int64_t)L * (L + 1) / 2;
+    p->cfg_off = (int64_t *)malloc(sizeof(int64_t) * (K + 1));
+    p->cfg_off[0] = 0;
+    for (int k = 0; k < K; k++) p->cfg_off[k + 1] = p->cfg_off[k] + island_configs(p, k, NULL);
+    p->ncfg = p->cfg_off[K];
+    p->N = p->ncfg * p->NS;
+    p->cfg = (ocfg *)malloc(sizeof(ocfg) * (p->ncfg > 0 ? p->ncfg : 1));
+    for (int k = 0; k < K; k++) island_configs(p, k, p->cfg + p->cfg_off[k]);
+
+    /* Slice sums by running accumulation over the layers of [i, j) (the
+       "concatenate" of Tab. 2 for integer per-layer quantities). */
+    p->slice_sum = (int64_t *)malloc(sizeof(int64_t) * 6 * p->NS);
+    const int fmap[6] = {F_FLOPS, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A};
+    int64_t s = 0;
+    for (int i = 0; i < L; i++) {
+        int64_t acc[6] = {0, 0, 0, 0, 0, 0};
+        for (int j = i + 1; j <= L; j++, s++)
+            for (int q = 0; q < 6; q++) {
+                acc[q] += p->layer[fmap[q]][j - 1];
+                p->slice_sum[s * 6 + q] = acc[q];
+            }
+    }
+
+    /* distinct compatible micro-batch sizes b = dp * mb with B mod b == 0 */
+    p->bvals = (int64_t *)malloc(sizeof(int64_t) * (p->ncfg > 0 ? p->ncfg : 1));
+    int64_t nb = 0;
+    for (int64_t g = 0; g < p->ncfg; g++) {
+        int64_t b = p->cfg[g].b;
+        if (p->B % b != 0) continue;
+        int seen = 0;
+        for (int64_t a = 0; a < nb; a++) if (p->bvals[a] == b) { seen = 1; break; }
+        if (!seen) p->bvals[nb++] = b;
+    }
+    qsort(p->bvals, (size_t)nb, sizeof(int64_t), cmp_i64);
+    p->nb = (int)nb;
+    *out = p;
+    return TGO_OK;
+}
+
+int tgo_counts(void *h, int64_t *out) {
+    oprob *p = (oprob *)h;
+    out[0] = p->NS; out[1] = p->ncfg; out[2] = p->N; out[3] = p->nb;
+    return TGO_OK;
+}
+
+int tgo_bvalues(void *h, int64_t *out) {
+    oprob *p = (oprob *)h;
+    for (int a = 0; a < p->nb; a++) out[a] = p->bvals[a];
+    return p->nb;
+}
+
+/* idx = (cfg_off[k] + c) * NS + s  ->  (i, j, k, tp, dp, ep, z, mb) */
+int tgo_decode(void *h, int64_t idx, int32_t *out) {
+    oprob *p = (oprob *)h;
+    if (idx < 0 || idx >= p->N) return TGO_EINVAL;
+    int64_t g = idx / p->NS, s = idx % p->NS;
+    int i, j;
+    slice_ij(p->L, s, &i, &j);
+    const ocfg *c = &p->cfg[g];
+    out[0] = i; out[1] = j; out[2] = c->k; out[3] = c->tp; out[4] = c->dp;
+    out[5] = c->ep; out[6] = c->z; out[7] = c->mb;
+    return TGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* cost model (stated reading of profile()/parallelize(), Tab. 2)            */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    double alpha, beta, gamma, delta_d, delta_e, mu_d, mu_e, rho, H, m_real;
+} ocoef;
+
+/* ring collectives over D GPUs move (D-1)/D of the data per phase */
+static double ring_r(int64_t D) { return (double)(D - 1) / (double)D; }
+
+/* bf16 bytes per parameter moved once per micro-batch for data-parallel sync */
+static double zero_per_mb(int z, int64_t D) {
+    if (z <= 1) return 0.0;            /* grads all-reduced once per iteration */
+    if (z == 2) return 2.0 * ring_r(D); /* reduce-scatter of grads every micro-batch */
+    return 6.0 * ring_r(D);             /* ZeRO-3: all-gather fwd + all-gather bwd + RS */
+}
+
+/* bf16 bytes per parameter moved once per iteration */
+static double zero_per_iter(int z, int64_t D) {
+    if (z <= 1) return 4.0 * ring_r(D); /* all-reduce (or RS + AG) of grads */
+    if (z == 2) return 2.0 * ring_r(D); /* all-gather of updated params */
+    return 0.0;
+}
+
+/* model-state bytes per parameter: bf16 param + bf16 grad + fp32 master/m/v */
+static double state_bytes(int z, int64_t D) {
+    if (z == 0) return 16.0;
+    if (z == 1) return 4.0 + 12.0 / (double)D;
+    if (z == 2) return 2.0 + 14.0 / (double)D;
+    return 16.0 / (double)D;
+}
+
+static void config_coef(const oprob *p, const ocfg *c, ocoef *o) {
+    double Fk = p->peak[c->k], Wk = p->intra[c->k], Mk = p->hbm[c->k];
+    int64_t Dd = c->dp, De = c->dp / c->ep;
+    double qd = (double)c->tp, qe = (double)((int64_t)c->tp * c->ep);
+    o->m_real = (double)p->B / (double)c->b;
+    /* forward + backward = 3x forward FLOPs, split over tp GPUs */
+    o->alpha = (3.0 * (double)c->mb) / (((double)c->tp * Fk) * p->eta);
+    /* two passes of ring all-reduce-equivalent TP collectives, 2(t-1)/t each */
+    o->beta = c->tp > 1 ? ((4.0 * (double)c->mb) * (double)(c->tp - 1)) / ((double)c->tp * Wk) : 0.0;
+    /* all-to-all forward and backward, (e-1)/e leaves the GPU, tokens split by tp */
+    o->gamma = c->ep > 1
+                   ? ((2.0 * (double)c->mb) * (double)(c->ep - 1)) / (((double)c->ep * (double)c->tp) * Wk)
+                   : 0.0;
+    o->delta_d = ((zero_per_mb(c->z, Dd) / qd) / Wk) + (((zero_per_iter(c->z, Dd) / qd) / Wk) / o->m_real);
+    o->delta_e = ((zero_per_mb(c->z, De) / qe) / Wk) + (((zero_per_iter(c->z, De) / qe) / Wk) / o->m_real);
+    o->mu_d = state_bytes(c->z, Dd) / qd;
+    o->mu_e = state_bytes(c->z, De) / qe;
+    o->rho = (double)c->mb / (double)c->tp;
+    o->H = Mk * p->mem_frac;
+}
+
+/* 1F1B: a stage with d stages at or after it holds min(d, m) micro-batches of
+   stashed activations (Sec. 5.2: memory depends on the pipeline position). */
+static int fits(double state, double A1, double H, double m_real, int d) {
+    double inflight = (double)d < m_real ? (double)d : m_real;
+    return (state + (inflight * A1)) <= H;
+}
+
+static void score_candidate(const oprob *p, const ocoef *o, const int64_t *sum, double *cost,
+                            int *dmax, double *state_out, double *A1_out) {
+    double Fl = (double)sum[0], Pd = (double)sum[1], Pe = (double)sum[2];
+    double Act = (double)sum[3], Tb = (double)sum[4], Ab = (double)sum[5];
+    double c = o->alpha * Fl;
+    c = c + (o->beta * Tb);
+    c = c + (o->gamma * Ab);
+    c = c + (o->delta_d * Pd);
+    c = c + (o->delta_e * Pe);
+    double state = (o->mu_d * Pd) + (o->mu_e * Pe);
+    double A1 = o->rho * Act;
+    /* d_max = largest d in 1..K that fits, 0 if none.  fits() is monotone in d
+       (min(d, m) and each rounded operation are non-decreasing), so a binary
+       search over d finds exactly the largest fitting depth. */
+    int lo = 0, hi = p->K; /* invariant: fits(lo) or lo == 0; !fits(hi+1) */
+    while (lo < hi) {
+        int mid = lo + (hi - lo + 1) / 2;
+        if (fits(state, A1, o->H, o->m_real, mid)) lo = mid; else hi = mid - 1;
+    }
+    *cost = c;
+    *dmax = lo;
+    if (state_out) *state_out = state;
+    if (A1_out) *A1_out = A1;
+}
+
+int tgo_coef(void *h, int64_t g, double *out /* 10 */) {
+    oprob *p = (oprob *)h;
+    if (g < 0 || g >= p->ncfg) return TGO_EINVAL;
+    ocoef o;
+    config_coef(p, &p->cfg[g], &o);
+    out[0] = o.alpha; out[1] = o.beta; out[2] = o.gamma; out[3] = o.delta_d; out[4] = o.delta_e;
+    out[5] = o.mu_d; out[6] = o.mu_e; out[7] = o.rho; out[8] = o.H; out[9] = o.m_real;
+    return TGO_OK;
+}
+
+int tgo_score(void *h, int64_t first, int64_t count, double *cost, uint8_t *dmax) {
+    oprob *p = (oprob *)h;
+    if (first < 0 || count < 0 || first > p->N || count > p->N - first) return TGO_EINVAL;
+    int64_t prev_g = -1;
+    ocoef o;
+    for (int64_t t = 0; t < count; t++) {
+        int64_t idx = first + t, g = idx / p->NS, s = idx % p->NS;
+        if (g != prev_g) { config_coef(p, &p->cfg[g], &o); prev_g = g; }
+        int dm;
+        score_candidate(p, &o, &p->slice_sum[s * 6], &cost[t], &dm, NULL, NULL);
+        dmax[t] = (uint8_t)dm;
+    }
+    return TGO_OK;
+}
+
+/* score an arbitrary list of candidate indices */
+int tgo_score_list(void *h, const int64_t *idx, int64_t n, double *cost, uint8_t *dmax) {
+    oprob *p = (oprob *)h;
+    for (int64_t t = 0; t < n; t++) {
+        if (idx[t] < 0 || idx[t] >= p->N) return TGO_EINVAL;
+        int64_t g = idx[t] / p->NS, s = idx[t] % p->NS;
+        ocoef o;
+        config_coef(p, &p->cfg[g], &o);
+        int dm;
+        score_candidate(p, &o, &p->slice_sum[s * 6], &cost[t], &dm, NULL, NULL);
+        dmax[t] = (uint8_t)dm;
+    }
+    return TGO_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* pruning: the surviving set                                                */
+/* ------------------------------------------------------------------------ */
+/* A group is (slice, island, b).  Preference key (cost, -d_max, idx) ascending.
+   rep(G, d) = min-key member with d_max >= d; the surviving set is the union of
+   rep(G, d) over d = 1..K.  Equivalently p survives iff p is compatible,
+   d_max_p >= 1 and no member q has key_q < key_p with d_max_q >= d_max_p, i.e.
+   d_max_p exceeds the largest d_max among all members preceding p in key
+   order.  Sorting by key and sweeping a running maximum evaluates exactly that. */
+typedef struct {
+    double cost;
+    int dmax;
+    int64_t idx;
+} omember;
+
+static int cmp_key(const void *a, const void *b) {
+    const omember *x = (const omember *)a, *y = (const omember *)b;
+    if (x->cost < y->cost) return -1;
+    if (x->cost > y->cost) return 1;
+    if (x->dmax > y->dmax) return -1;
+    if (x->dmax < y->dmax) return 1;
+    return (x->idx > y->idx) - (x->idx < y->idx);
+}
+
+typedef struct {
+    int64_t *v;
+    int64_t n, cap;
+} ivec;
+
+static int ivec_push(ivec *a, int64_t x) {
+    if (a->n == a->cap) {
+        int64_t nc = a->cap ? a->cap * 2 : 1024;
+        int64_t *nv = (int64_t *)realloc(a->v, sizeof(int64_t) * nc);
+        if (!nv) return TGO_ENOMEM;
+        a->v = nv; a->cap = nc;
+    }
+    a->v[a->n++] = x;
+    return TGO_OK;
+}
+
+int tgo_prune(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
+    oprob *p = (oprob *)h;
+    ivec surv = {0, 0, 0};
+    int64_t maxc = 0;
+    for (int k = 0; k < p->K; k++)
+        if (p->cfg_off[k + 1] - p->cfg_off[k] > maxc) maxc = p->cfg_off[k + 1] - p->cfg_off[k];
+    omember *mem = (omember *)malloc(sizeof(omember) * (maxc > 0 ? maxc : 1));
+    ocoef *coef = (ocoef *)malloc(sizeof(ocoef) * (maxc > 0 ? maxc : 1));
+    int64_t *members = (int64_t *)malloc(sizeof(int64_t) * (maxc > 0 ? maxc : 1));
+    for (int k = 0; k < p->K; k++) {
+        int64_t c0 = p->cfg_off[k], nc = p->cfg_off[k + 1] - c0;
+        for (int64_t c = 0; c < nc; c++) config_coef(p, &p->cfg[c0 + c], &coef[c]);
+        for (int bi = 0; bi < p->nb; bi++) {
+            int64_t b = p->bvals[bi];
+            /* the group's members: configs of island k with this b */
+            int64_t nm = 0;
+            for (int64_t c = 0; c < nc; c++)
+                if (p->cfg[c0 + c].b == b) members[nm++] = c;
+            if (nm == 0) continue;
+            for (int64_t s = 0; s < p->NS; s++) {
+                int64_t n = 0;
+                for (int64_t a = 0; a < nm; a++) {
+                    int64_t c = members[a];
+                    omember *m = &mem[n++];
+                    score_candidate(p, &coef[c], &p->slice_sum[s * 6], &m->cost, &m->dmax, NULL, NULL);
+                    m->idx = (c0 + c) * p->NS + s;
+                }
+                qsort(mem, (size_t)n, sizeof(omember), cmp_key);
+                int run = 0;
+                for (int64_t a = 0; a < n; a++)
+                    if (mem[a].dmax > run) {
+                        if (ivec_push(&surv, mem[a].idx) != TGO_OK) {
+                            free(mem); free(coef); free(members); free(surv.v);
+                            return TGO_ENOMEM;
+                        }
+                        run = mem[a].dmax;
+                    }
+            }
+        }
+    }
+    free(mem);
+    free(coef);
+    free(members);
+    qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64);
+    *n_out = surv.n;
+    int rc = TGO_OK;
+    if (surv.n > cap) rc = TGO_ECAPACITY;
+    else if (out) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
+    free(surv.v);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* composition (Sec. 5.2)                                                    */
+/* ------------------------------------------------------------------------ */
+/* An entry is one usable candidate of the list handed to composition. */
+typedef struct {
+    int64_t gkey; /* (b_index * NS + s) * K + position of the island */
+    double cost;
+    int dmax;
+    int64_t idx;
+} oentry;
+
+static int cmp_entry(const void *a, const void *b) {
+    const oentry *x = (const oentry *)a, *y = (const oentry *)b;
+    if (x->gkey != y->gkey) return (x->gkey > y->gkey) - (x->gkey < y->gkey);
+    if (x->cost < y->cost) return -1;
+    if (x->cost > y->cost) return 1;
+    if (x->dmax > y->dmax) return -1;
+    if (x->dmax < y->dmax) return 1;
+    return (x->idx > y->idx) - (x->idx < y->idx);
+}
+
+static double maxd(double a, double b) { return a > b ? a : b; }
+
+/* Activation transfer across boundary j (after layer j-1) from island ka to
+   island kb: forward activations and backward gradients of one micro-batch of
+   b samples, over the inter-island link (Sec. 5.2: PP only moves stage
+   inputs and outputs).  No link (bandwidth 0) is unusable. */
+static double transfer(const oprob *p, int64_t b, int j, int ka, int kb) {
+    double E = p->inter[(int64_t)ka * p->K + kb];
+    if (E == 0.0) return INFINITY;
+    return ((2.0 * (double)b) * (double)p->layer[F_OUTACT][j - 1]) / E;
+}
+
+int tgo_compose(void *h, const int64_t *cands, int64_t n, const int32_t *order, tgo_plan *plan,
+                double *per_b /* nb x 3: P*, F*, T; may be NULL */) {
+    oprob *p = (oprob *)h;
+    const int L = p->L, K = p->K;
+    const int64_t NS = p->NS;
+    memset(plan, 0, sizeof(tgo_plan));
+    plan->status = TGO_ENOPLAN;
+    plan->T = INFINITY; plan->P = INFINITY; plan->F = INFINITY;
+
+    int *pos = (int *)malloc(sizeof(int) * K);
+    for (int k = 0; k < K; k++) pos[k] = -1;
+    for (int o = 0; o < K; o++) {
+        if (order[o] < 0 || order[o] >= K || pos[order[o]] != -1) { free(pos); return TGO_EINVAL; }
+        pos[order[o]] = o;
+    }
+    /* entries: compatible candidates with d_max >= 1, strictly ascending idx */
+    oentry *ent = (oentry *)malloc(sizeof(oentry) * (n > 0 ? n : 1));
+    int64_t ne = 0;
+    for (int64_t t = 0; t < n; t++) {
+        int64_t idx = cands[t];
+        if (idx < 0 || idx >= p->N || (t > 0 && idx <= cands[t - 1])) {
+            free(pos); free(ent); return TGO_EINVAL;
+        }
+        int64_t g = idx / NS, s = idx % NS;
+        const ocfg *c = &p->cfg[g];
+        if (p->B % c->b != 0) { free(pos); free(ent); return TGO_EINVAL; }
+        int bi = 0;
+        while (p->bvals[bi] != c->b) bi++;
+        ocoef o;
+        config_coef(p, c, &o);
+        oentry *e = &ent[ne];
+        score_candidate(p, &o, &p->slice_sum[s * 6], &e->cost, &e->dmax, NULL, NULL);
+        if (e->dmax < 1) continue;
+        e->gkey = ((int64_t)bi * NS + s) * K + pos[c->k];
+        e->idx = idx;
+        ne++;
+    }
+    qsort(ent, (size_t)ne, sizeof(oentry), cmp_entry);
+
+    const int D = K < L ? K : L; /* a pipeline has at most min(K, L) stages */
+    const int64_t cell = (int64_t)(L + 1) * K;
+    double *V = (double *)malloc(sizeof(double) * (D + 1) * cell);
+    double *Wt = (double *)malloc(sizeof(double) * (D + 1) * cell);
+    double *Td = (double *)malloc(sizeof(double) * (D + 1) * NS * K); /* Td[d][s][o] */
+    double *X = (double *)malloc(sizeof(double) * (L + 1) * K * K);   /* X[j][o][o'] */
+    int64_t *gstart = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    int64_t *gend = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    if (!V || !Wt || !Td || !X || !gstart || !gend) {
+        free(pos); free(ent); free(V); free(Wt); free(Td); free(X); free(gstart); free(gend);
+        return TGO_ENOMEM;
+    }
+#define AT(A, d, i, o) A[((int64_t)(d) * (L + 1) + (i)) * K + (o)]
+#define TD(d, s, o) Td[((int64_t)(d) * NS + (s)) * K + (o)]
+#define XA(j, o, o2) X[((int64_t)(j) * K + (o)) * K + (o2)]
+
+    double bestT = INFINITY;
+    int best_bi = -1, best_o = -1, best_S = -1;
+    double bestP = INFINITY, bestF = INFINITY;
+    int64_t e0 = 0;
+    for (int bi = 0; bi < p->nb; bi++) {
+        int64_t b = p->bvals[bi];
+        int64_t m = p->B / b;
+        if (per_b) { per_b[bi * 3] = INFINITY; per_b[bi * 3 + 1] = INFINITY; per_b[bi * 3 + 2] = INFINITY; }
+        /* group ranges of this b */
+        for (int64_t a = 0; a < NS * K; a++) { gstart[a] = 0; gend[a] = 0; }
+        int64_t e1 = e0;
+        while (e1 < ne && ent[e1].gkey / (NS * K) == bi) e1++;
+        for (int64_t a = e0; a < e1; a++) {
+            int64_t gk = ent[a].gkey % (NS * K);
+            if (gend[gk] == 0) gstart[gk] = a;
+            gend[gk] = a + 1;
+        }
+        /* stage table: Td(d, s, o) = least cost of the group's entries that fit
+           at depth d; entries are key-sorted, so the first fitting one. */
+        for (int d = 1; d <= D; d++)
+            for (int64_t s = 0; s < NS; s++)
+                for (int o = 0; o < K; o++) {
+                    double v = INFINITY;
+                    int64_t gk = s * K + o;
+                    for (int64_t a = gstart[gk]; a < gend[gk]; a++)
+                        if (ent[a].dmax >= d) { v = ent[a].cost; break; }
+                    TD(d, s, o) = v;
+                }
+        for (int j = 1; j < L; j++)
+            for (int o = 0; o < K; o++)
+                for (int o2 = 0; o2 < K; o2++)
+                    XA(j, o, o2) = transfer(p, b, j, order[o], order[o2]);
+
+        /* Phase 1, steps (1)-(2): least achievable bottleneck.
+           V(d,i,o): best bottleneck covering layers [i, L) with d stages, the
+           first on island position o and the rest on later positions.
+           W(d,j,o): best continuation after a stage on position o ends at j. */
+        for (int d = 1; d <= D; d++) {
+            for (int i = 0; i < L; i++)
+                for (int o = 0; o < K; o++) {
+                    double v = INFINITY;
+                    if (d == 1) v = TD(1, slice_index(L, i, L), o);
+                    else
+                        for (int j = i + 1; j <= L - d + 1; j++) {
+                            double c = maxd(TD(d, slice_index(L, i, j), o), AT(Wt, d - 1, j, o));
+                            if (c < v) v = c;
+                        }
+                    AT(V, d, i, o) = v;
+                }
+            for (int j = 1; j < L; j++)
+                for (int o = 0; o < K; o++) {
+                    double w = INFINITY;
+                    for (int o2 = o + 1; o2 < K; o2++) {
+                        double c = maxd(XA(j, o, o2), AT(V, d, j, o2));
+                        if (c < w) w = c;
+                    }
+                    AT(Wt, d, j, o) = w;
+                }
+        }
+        double Pst = INFINITY;
+        for (int d = 1; d <= D; d++)
+            for (int o = 0; o < K; o++)
+                if (AT(V, d, 0, o) < Pst) Pst = AT(V, d, 0, o);
+        if (!(Pst < INFINITY)) { e0 = e1; continue; }
+
+        /* Phase 2, step (3): least fill among plans whose every stage and link
+           stays within the bottleneck P*.  Fill = f1 + (x1 + (f2 + ... + fS)),
+           a right fold; F and G reuse the V and W arrays. */
+        for (int d = 1; d <= D; d++) {
+            for (int i = 0; i < L; i++)
+                for (int o = 0; o < K; o++) {
+                    double v = INFINITY;
+                    if (d == 1) {
+                        double t = TD(1, slice_index(L, i, L), o);
+                        if (t <= Pst) v = t;
+                    } else
+                        for (int j = i + 1; j <= L - d + 1; j++) {
+                            double t = TD(d, slice_index(L, i, j), o);
+                            if (!(t <= Pst)) continue;
+                            double c = t + AT(Wt, d - 1, j, o);
+                            if (c < v) v = c;
+                        }
+                    AT(V, d, i, o) = v;
+                }
+            for (int j = 1; j < L; j++)
+                for (int o = 0; o < K; o++) {
+                    double w = INFINITY;
+                    for (int o2 = o + 1; o2 < K; o2++) {
+                        double x = XA(j, o, o2);
+                        if (!(x <= Pst)) continue;
+                        double c = x + AT(V, d, j, o2);
+                        if (c < w) w = c;
+                    }
+                    AT(Wt, d, j, o) = w;
+                }
+        }
+        /* root: least fill, ties to the earliest island position, then fewer stages */
+        double Fst = INFINITY;
+        int ro = -1, rS = -1;
+        for (int o = 0; o < K; o++)
+            for (int d = 1; d <= D; d++)
+                if (AT(V, d, 0, o) < Fst) { Fst = AT(V, d, 0, o); ro = o; rS = d; }
+        if (ro < 0) { e0 = e1; continue; }
+        double Tb = ((double)(m - 1) * Pst) + Fst;
+        if (per_b) { per_b[bi * 3] = Pst; per_b[bi * 3 + 1] = Fst; per_b[bi * 3 + 2] = Tb; }
+        if (Tb < bestT) {
+            /* backtrack now, while this b's tables are live */
+            bestT = Tb; best_bi = bi; best_o = ro; best_S = rS; bestP = Pst; bestF = Fst;
+            plan->status = TGO_OK;
+            plan->b = (int32_t)b; plan->m = (int32_t)m; plan->S = rS;
+            plan->P = Pst; plan->F = Fst; plan->T = Tb;
+            int i = 0, o = ro;
+            for (int t = 0; t < rS; t++) {
+                int d = rS - t, j, o_next = -1;
+                if (d == 1) j = L;
+                else {
+                    /* smallest j attaining F(d, i, o) */
+                    for (j = i + 1; j <= L - d + 1; j++) {
+                        double tt = TD(d, slice_index(L, i, j), o);
+                        if (tt <= Pst && tt + AT(Wt, d - 1, j, o) == AT(V, d, i, o)) break;
+                    }
+                    /* smallest later position attaining G(d-1, j, o) */
+                    for (o_next = o + 1; o_next < K; o_next++) {
+                        double x = XA(j, o, o_next);
+                        if (x <= Pst && x + AT(V, d - 1, j, o_next) == AT(Wt, d - 1, j, o)) break;
+                    }
+                }
+                tgo_stage *st = &plan->stage[t];
+                int64_t s = slice_index(L, i, j);
+                int64_t gk = s * K + o;
+                int64_t rep = -1;
+                for (int64_t a = gstart[gk]; a < gend[gk]; a++)
+                    if (ent[a].dmax >= d) { rep = a; break; }
+                const oentry *e = &ent[rep];
+                int64_t g = e->idx / NS;
+                const ocfg *c = &p->cfg[g];
+                ocoef co;
+                config_coef(p, c, &co);
+                double cost, state, A1;
+                int dm;
+                score_candidate(p, &co, &p->slice_sum[s * 6], &cost, &dm, &state, &A1);
+                double inflight = (double)d < co.m_real ? (double)d : co.m_real;
+                st->island = order[o]; st->first_layer = i; st->end_layer = j;
+                st->tp = c->tp; st->dp = c->dp; st->ep = c->ep; st->zero = c->z; st->mb = c->mb;
+                st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
+                st->mem_bytes = state + (inflight * A1);
+                st->link_out = d > 1 ? XA(j, o, o_next) : 0.0;
+                i = j;
+                o = o_next;
+            }
+        }
+        e0 = e1;
+    }
+    (void)best_bi; (void)best_o; (void)best_S; (void)bestP; (void)bestF;
+#undef AT
+#undef TD
+#undef XA
+    free(pos); free(ent); free(V); free(Wt); free(Td); free(X); free(gstart); free(gend);
+    return plan->status;
+}
