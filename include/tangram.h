@@ -1,0 +1,234 @@
+/*
+ * tangram.h -- C ABI of the MI355X (gfx950) plan-search library.
+ *
+ * The library computes the search at the core of Tangram's heterogeneous
+ * planner (arXiv 2606.16907): every model slice (a contiguous layer range,
+ * Sec. 4.2) is paired with every GPU island (Sec. 4.1) and every intra-island
+ * parallel configuration; each pair gets an analytic step-time cost and the
+ * deepest 1F1B pipeline position it fits at (Sec. 5.2); incompatible,
+ * infeasible and dominated pairs are pruned (Sec. 5.1); the survivors are
+ * composed into a work-balanced pipeline across islands, lowest bottleneck
+ * first, then lowest fill (Sec. 5.2, composition steps (1)-(3)).
+ *
+ * Conventions shared by every entry point:
+ *   - Units: FLOPs, parameters and bytes are per sample (one sequence), for
+ *     the forward pass of one layer; FLOP/s, bytes and bytes/s are per GPU.
+ *   - Device buffers ("d_" prefix) are allocated and owned by the caller and
+ *     must live on the device that was current at tg_problem_create; host
+ *     pointers are plain host memory.  The library allocates device memory
+ *     only inside tg_problem_create (small input tables) and frees it in
+ *     tg_problem_destroy.
+ *   - `stream` is a hipStream_t (NULL: the default stream).  Calls are
+ *     asynchronous on it except where a host result is returned; those calls
+ *     synchronise the stream once.
+ *   - Errors are returned as tg_status; no call throws.  tg_last_error()
+ *     returns a message for the calling thread's most recent failure.
+ *   - Results are a pure function of the inputs, independent of launch
+ *     configuration and repeatable bit for bit.
+ *   - Floating point is IEEE binary64 with one rounding per operation in a
+ *     fixed order; no operation is fused or reassociated.
+ */
+#ifndef TANGRAM_H
+#define TANGRAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *tg_stream; /* a hipStream_t */
+
+typedef enum {
+    TG_OK = 0,
+    TG_EINVAL = -1,    /* invalid argument or input table */
+    TG_ENOMEM = -2,    /* device allocation failed, or workspace too small */
+    TG_EDEVICE = -3,   /* a HIP runtime call or kernel launch failed */
+    TG_ECAPACITY = -4, /* output buffer too small; the required count is returned */
+    TG_ENOPLAN = -5    /* no pipeline fits the cluster */
+} tg_status;
+
+/* One model atom (a layer), Sec. 4.2 / Tab. 2 slice_model().  All values are
+   integers >= 0 and every whole-model sum must stay below 2^62. */
+typedef struct {
+    int64_t fwd_flops;       /* forward FLOPs per sample */
+    int64_t dense_params;    /* parameters replicated across expert-parallel ranks */
+    int64_t expert_params;   /* expert parameters, sharded by expert parallelism */
+    int64_t act_stash_bytes; /* activation bytes kept per sample for the backward pass */
+    int64_t tp_comm_bytes;   /* bytes per sample in the layer's tensor-parallel collectives, one pass */
+    int64_t a2a_bytes;       /* bytes per sample moved by the layer's all-to-alls, one pass */
+    int64_t out_act_bytes;   /* bytes per sample of the layer's output activation */
+} tg_layer;
+
+/* One GPU island (Sec. 4.1): nodes of identical GPUs.  n_gpus in [1, 65536];
+   the three rates are finite and > 0. */
+typedef struct {
+    int32_t n_gpus;
+    int32_t reserved; /* must be 0 */
+    double peak_flops; /* FLOP/s per GPU */
+    double hbm_bytes;  /* memory per GPU */
+    double intra_bw;   /* bytes/s per GPU for intra-island collectives */
+} tg_island;
+
+/* The intra-island configuration space.  Each set holds 1..8 strictly
+   ascending entries >= 1.  zero_mask: bit z set admits ZeRO stage z (0..3);
+   it must be non-zero.  n_experts = 0 describes a dense model (then only
+   ep = 1 is admitted); otherwise ep must divide n_experts.  eta scales peak
+   FLOP/s (efficiency), mem_frac scales usable memory; both finite and > 0. */
+typedef struct {
+    int64_t global_batch; /* samples per iteration, >= 1 */
+    int32_t n_experts;
+    int32_t n_tp;
+    int32_t tp[8];
+    int32_t n_ep;
+    int32_t ep[8];
+    int32_t n_mb;
+    int32_t mb[8];
+    uint32_t zero_mask;
+    int32_t reserved; /* must be 0 */
+    double eta;
+    double mem_frac;
+} tg_space;
+
+/* A decoded candidate: layers [i, j) on island `island` with the given
+   degrees, ZeRO stage and micro-batch size (samples per DP rank). */
+typedef struct {
+    int32_t i, j, island, tp, dp, ep, zero, mb;
+} tg_pair;
+
+/* One pipeline stage of a plan; stage 0 is the pipeline front. */
+typedef struct {
+    int32_t island, first_layer, end_layer, tp, dp, ep, zero, mb;
+    int32_t depth; /* stages from this one to the pipeline end, inclusive */
+    int32_t reserved;
+    int64_t pair_index; /* candidate index of the chosen pair */
+    double cost;        /* seconds per micro-batch (step-time cost of the pair) */
+    double mem_bytes;   /* per-GPU memory at this depth */
+    double link_out;    /* seconds per micro-batch on the link to the next stage (0 for the last) */
+} tg_stage;
+
+/* A composed plan.  b = samples per pipeline micro-batch (dp * mb, the same
+   for every stage), m = global_batch / b micro-batches, S stages,
+   P = bottleneck, F = pipeline fill, T = (m - 1) * P + F. */
+typedef struct {
+    int32_t b, m, S, reserved;
+    double P, F, T;
+    tg_stage stage[255];
+} tg_plan;
+
+/* Problem sizes after create. */
+typedef struct {
+    int32_t L, K;
+    int32_t n_b;        /* distinct compatible b values (B mod b == 0) */
+    int32_t dense;      /* 1 when no layer has expert parameters or all-to-all bytes */
+    int64_t NS;         /* slices = L (L + 1) / 2 */
+    int64_t n_configs;  /* intra-island configs summed over islands */
+    int64_t N;          /* candidates = NS * n_configs */
+    int64_t n_compatible_configs;
+} tg_info;
+
+typedef struct tg_problem tg_problem;
+
+/*
+ * Validates and copies one planning instance to the current device.
+ *   layers[L], L in [1, 512]; islands[K], K in [1, 255];
+ *   inter_bw: K*K row-major bytes/s from island a to island b (>= 0 or +inf;
+ *             0 means no link; the diagonal is ignored);
+ *   space: the configuration space.
+ * Candidate order (the linear index used by every other call):
+ *   idx = (cfg_off[k] + c) * NS + s, where s enumerates slices 0 <= i < j <= L
+ *   lexicographically (i, then j), c enumerates island k's configs
+ *   lexicographically over (tp, dp, ep, zero, mb) with tp in space.tp,
+ *   tp <= n_gpus, dp in 1..floor(n_gpus / tp), ep admitted and dividing dp,
+ *   zero in zero_mask, mb in space.mb; cfg_off is the running count over
+ *   islands in input order.
+ * Returns TG_EINVAL on any invalid value, TG_ENOMEM / TG_EDEVICE on device
+ * failures; *out is NULL on failure.
+ */
+tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
+                            const double *inter_bw, const tg_space *space, tg_problem **out);
+void tg_problem_destroy(tg_problem *p);
+tg_status tg_problem_info(const tg_problem *p, tg_info *out);
+/* Writes the n_b distinct compatible micro-batch sizes, ascending, into out
+   (capacity entries).  Returns TG_ECAPACITY if capacity < n_b. */
+tg_status tg_problem_bvalues(const tg_problem *p, int64_t *out, int32_t capacity);
+
+/*
+ * Enumeration of the model-slice/island/config candidates (Sec. 5.1):
+ * *n_candidates = N.  When d_out is not NULL, decodes candidates
+ * [first, first + count) into d_out[0 .. count) on the device.
+ * TG_EINVAL if the range leaves [0, N).
+ */
+tg_status tg_enumerate_pairs(const tg_problem *p, int64_t *n_candidates, int64_t first, int64_t count,
+                             tg_pair *d_out, tg_stream stream);
+
+/*
+ * Scoring (the per-pair profile()/parallelize() query of Tab. 2, made
+ * analytic): for every candidate in [first, first + count) writes
+ *   d_cost[idx - first]: seconds per micro-batch, including data-parallel
+ *                        synchronisation amortised over the iteration;
+ *   d_dmax[idx - first]: the largest pipeline depth d in 1..K at which the
+ *                        pair fits in memory when min(d, m) micro-batches of
+ *                        activations are in flight (1F1B, Sec. 5.2), or 0.
+ * With b = dp*mb, m = B/b, r(D) = (D-1)/D, De = dp/ep, W the island's intra
+ * bandwidth, F its peak, and slice sums Fl, Tb, Ab, Pd, Pe, Act of the
+ * tg_layer fields over [i, j):
+ *   cost  = alpha*Fl + beta*Tb + gamma*Ab + dd*Pd + de*Pe   (summed left to right)
+ *   alpha = 3 mb / (tp F eta)                    forward + backward compute
+ *   beta  = 4 mb (tp-1) / (tp W)                 TP collectives, 2 passes x 2r
+ *   gamma = 2 mb (ep-1) / (ep tp W)              all-to-all, 2 passes
+ *   dd/de = (zm/q)/W + ((zi/q)/W)/m with q = tp (dense) or tp*ep (expert),
+ *           D = dp (dense) or De (expert), and per-parameter bf16 traffic
+ *           zm = {0, 0, 2r, 6r} per micro-batch, zi = {4r, 4r, 2r, 0} per
+ *           iteration for ZeRO stage 0..3
+ *   state = (w(dp)/tp)*Pd + (w(De)/(tp ep))*Pe, w(D) = {16, 4+12/D, 2+14/D, 16/D}
+ *   fits(d) <=> state + min(d, m) * (mb/tp) * Act <= hbm * mem_frac
+ * Asynchronous.  TG_EINVAL if the range leaves [0, N).
+ */
+tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, double *d_cost,
+                         uint8_t *d_dmax, tg_stream stream);
+
+/*
+ * Pruning (Sec. 5.1 infeasibility and incompatibility pruning, plus
+ * dominance): from the full score arrays (d_cost, d_dmax over all N
+ * candidates) writes the ascending list of survivors to d_survivors.  A
+ * candidate survives iff its micro-batch b divides the global batch, its
+ * d_max >= 1, and it has the least key (cost, -d_max, idx) among the members
+ * of its group (same slice, island and b) whose d_max reaches its own d_max.
+ * *n_survivors (host) receives the count; if it exceeds `capacity`, nothing
+ * past capacity is written and TG_ECAPACITY is returned.  d_ws: caller
+ * workspace of at least tg_prune_workspace_bytes(p) bytes (TG_ENOMEM if
+ * smaller).  Synchronises the stream once to read the count.
+ */
+size_t tg_prune_workspace_bytes(const tg_problem *p);
+tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                   int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream);
+
+/*
+ * Composition (Sec. 5.2): builds the pipeline from the candidates listed in
+ * d_survivors (strictly ascending indices of compatible candidates; entries
+ * with d_max 0 are ignored; any other list is TG_EINVAL), scored by d_cost /
+ * d_dmax over all N.  island_order (host, a permutation of 0..K-1) fixes the
+ * order in which islands may appear from pipeline front to back; islands may
+ * be skipped.  For each b the plan minimises the bottleneck P = max of stage
+ * costs and link times, then the fill F = f1 + (x1 + (f2 + ... + fS)) among
+ * plans with that bottleneck; across b it minimises T = (m - 1) P + F, ties
+ * to the smaller b.  Ties inside a b go to the earliest first island, then
+ * fewer stages, then the earliest cut, then the earliest next island.
+ * Writes *out; TG_ENOPLAN (out->S = 0, out->T = +inf) if nothing fits.
+ * d_ws: at least tg_compose_workspace_bytes(p, n_survivors) bytes.
+ * Synchronises the stream once.
+ */
+size_t tg_compose_workspace_bytes(const tg_problem *p, int64_t n_survivors);
+tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                              const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                              tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char *tg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TANGRAM_H */

@@ -1,0 +1,423 @@
+// api.hip -- the C ABI declared in include/tangram.h: validation, the
+// problem's device tables, and the entry points that launch the kernels.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "tg_device.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tg_status fail(tg_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+tg_status hip_fail(hipError_t e, const char *what) {
+    return fail(e == hipErrorOutOfMemory ? TG_ENOMEM : TG_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool ascending_set(const int32_t *v, int32_t n) {
+    if (n < 1 || n > 8) return false;
+    for (int a = 0; a < n; ++a) {
+        if (v[a] < 1) return false;
+        if (a > 0 && v[a] <= v[a - 1]) return false;
+    }
+    return true;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+struct tg_problem {
+    int device;
+    tg::DevProblem P;
+    void *dev_block;
+    std::vector<int64_t> bvals;
+    int64_t n_compat_cfg;
+};
+
+extern "C" {
+
+const char *tg_last_error(void) { return g_err; }
+
+tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
+                            const double *inter_bw, const tg_space *space, tg_problem **out) {
+    g_err[0] = 0;
+    if (!out) return fail(TG_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!layers || !islands || !inter_bw || !space) return fail(TG_EINVAL, "NULL input table");
+    if (L < 1 || L > 512) return fail(TG_EINVAL, "L=%d outside [1, 512]", L);
+    if (K < 1 || K > 255) return fail(TG_EINVAL, "K=%d outside [1, 255]", K);
+    const tg_space &sp = *space;
+    if (sp.global_batch < 1) return fail(TG_EINVAL, "global_batch < 1");
+    if (sp.n_experts < 0) return fail(TG_EINVAL, "n_experts < 0");
+    if (sp.reserved != 0) return fail(TG_EINVAL, "space reserved field not 0");
+    if (!ascending_set(sp.tp, sp.n_tp)) return fail(TG_EINVAL, "tp set invalid");
+    if (!ascending_set(sp.ep, sp.n_ep)) return fail(TG_EINVAL, "ep set invalid");
+    if (!ascending_set(sp.mb, sp.n_mb)) return fail(TG_EINVAL, "mb set invalid");
+    if (sp.zero_mask == 0 || (sp.zero_mask & ~0xFu)) return fail(TG_EINVAL, "zero_mask invalid");
+    if (!(sp.eta > 0.0) || !std::isfinite(sp.eta)) return fail(TG_EINVAL, "eta invalid");
+    if (!(sp.mem_frac > 0.0) || !std::isfinite(sp.mem_frac)) return fail(TG_EINVAL, "mem_frac invalid");
+    for (int k = 0; k < K; ++k) {
+        const tg_island &is = islands[k];
+        if (is.n_gpus < 1 || is.n_gpus > 65536) return fail(TG_EINVAL, "island %d: n_gpus", k);
+        if (is.reserved != 0) return fail(TG_EINVAL, "island %d: reserved field not 0", k);
+        if (!(is.peak_flops > 0.0) || !std::isfinite(is.peak_flops)) return fail(TG_EINVAL, "island %d: peak", k);
+        if (!(is.hbm_bytes > 0.0) || !std::isfinite(is.hbm_bytes)) return fail(TG_EINVAL, "island %d: hbm", k);
+        if (!(is.intra_bw > 0.0) || !std::isfinite(is.intra_bw)) return fail(TG_EINVAL, "island %d: intra", k);
+    }
+    for (int a = 0; a < K * K; ++a)
+        if (!(inter_bw[a] >= 0.0)) return fail(TG_EINVAL, "inter_bw[%d] negative or NaN", a);
+
+    // prefix sums of the six summed layer fields; every whole-model sum < 2^62
+    const int64_t Lp = L + 1;
+    std::vector<int64_t> pre(6 * Lp, 0), outact(L);
+    const int64_t lim = (int64_t)1 << 62;
+    for (int l = 0; l < L; ++l) {
+        const tg_layer &y = layers[l];
+        const int64_t f[6] = {y.fwd_flops, y.dense_params, y.expert_params, y.act_stash_bytes, y.tp_comm_bytes,
+                              y.a2a_bytes};
+        for (int q = 0; q < 6; ++q) {
+            if (f[q] < 0 || f[q] >= lim - pre[q * Lp + l]) return fail(TG_EINVAL, "layer %d field %d", l, q);
+            pre[q * Lp + l + 1] = pre[q * Lp + l] + f[q];
+        }
+        if (y.out_act_bytes < 0) return fail(TG_EINVAL, "layer %d out_act_bytes", l);
+        outact[l] = y.out_act_bytes;
+    }
+    int64_t oa_sum = 0;
+    for (int l = 0; l < L; ++l) {
+        if (outact[l] >= lim - oa_sum) return fail(TG_EINVAL, "out_act_bytes sum too large");
+        oa_sum += outact[l];
+    }
+    const int dense = (pre[2 * Lp + L] == 0 && pre[5 * Lp + L] == 0) ? 1 : 0;
+
+    // the config list of every island: lexicographic (tp, dp, ep, z, mb)
+    std::vector<tg::Coef> cfg;
+    std::vector<int> zs;
+    for (int z = 0; z < 4; ++z)
+        if (sp.zero_mask & (1u << z)) zs.push_back(z);
+    for (int k = 0; k < K; ++k) {
+        const int n = islands[k].n_gpus;
+        for (int a = 0; a < sp.n_tp; ++a) {
+            const int tp = sp.tp[a];
+            if (tp > n) continue;
+            for (int dp = 1; dp <= n / tp; ++dp)
+                for (int e = 0; e < sp.n_ep; ++e) {
+                    const int ep = sp.ep[e];
+                    if (dp % ep) continue;
+                    if (sp.n_experts == 0 ? ep != 1 : (sp.n_experts % ep) != 0) continue;
+                    for (int z : zs)
+                        for (int mi = 0; mi < sp.n_mb; ++mi) {
+                            tg::Coef c;
+                            std::memset(&c, 0, sizeof(c));
+                            c.k = k;
+                            c.tp = tp;
+                            c.dp = dp;
+                            c.ep = ep;
+                            c.z = z;
+                            c.mb = sp.mb[mi];
+                            cfg.push_back(c);
+                        }
+                }
+        }
+    }
+    const int64_t ncfg = (int64_t)cfg.size();
+    const int64_t NS = (int64_t)L * (L + 1) / 2;
+    if (ncfg > ((int64_t)1 << 31) - 1 || NS * ncfg >= ((int64_t)1 << 62))
+        return fail(TG_EINVAL, "candidate space too large");
+
+    // compatible b values, bitmap rows, (island, b) groups
+    std::vector<int64_t> bv;
+    for (auto &c : cfg) {
+        const int64_t b = (int64_t)c.dp * c.mb;
+        if (sp.global_batch % b == 0) bv.push_back(b);
+    }
+    std::sort(bv.begin(), bv.end());
+    bv.erase(std::unique(bv.begin(), bv.end()), bv.end());
+    const int nb = (int)bv.size();
+    std::vector<int32_t> row_cfg;
+    for (int64_t g = 0; g < ncfg; ++g) {
+        const int64_t b = (int64_t)cfg[g].dp * cfg[g].mb;
+        auto it = std::lower_bound(bv.begin(), bv.end(), b);
+        if (it != bv.end() && *it == b) {
+            cfg[g].b_idx = (int32_t)(it - bv.begin());
+            cfg[g].row = (int32_t)row_cfg.size();
+            row_cfg.push_back((int32_t)g);
+        } else {
+            cfg[g].b_idx = -1;
+            cfg[g].row = -1;
+        }
+    }
+    std::vector<int32_t> kb_off(1, 0), kb_members, kb_island, kb_bidx;
+    int max_members = 0;
+    {
+        int64_t c0 = 0;
+        for (int k = 0; k < K; ++k) {
+            int64_t c1 = c0;
+            while (c1 < ncfg && cfg[c1].k == k) ++c1;
+            for (int bi = 0; bi < nb; ++bi) {
+                int cnt = 0;
+                for (int64_t g = c0; g < c1; ++g)
+                    if (cfg[g].b_idx == bi) {
+                        kb_members.push_back((int32_t)g);
+                        ++cnt;
+                    }
+                if (cnt) {
+                    kb_off.push_back((int32_t)kb_members.size());
+                    kb_island.push_back(k);
+                    kb_bidx.push_back(bi);
+                    max_members = std::max(max_members, cnt);
+                }
+            }
+            c0 = c1;
+        }
+    }
+    std::vector<uint32_t> sij(NS);
+    {
+        int64_t s = 0;
+        for (int i = 0; i < L; ++i)
+            for (int j = i + 1; j <= L; ++j) sij[s++] = (uint32_t)i | ((uint32_t)j << 16);
+    }
+
+    // one device block for all tables
+    struct Part {
+        const void *src;
+        size_t bytes;
+        size_t off;
+    };
+    std::vector<double> peak(K), hbm(K), intra(K);
+    for (int k = 0; k < K; ++k) {
+        peak[k] = islands[k].peak_flops;
+        hbm[k] = islands[k].hbm_bytes;
+        intra[k] = islands[k].intra_bw;
+    }
+    Part parts[] = {
+        {pre.data(), pre.size() * 8, 0},
+        {outact.data(), outact.size() * 8, 0},
+        {inter_bw, (size_t)K * K * 8, 0},
+        {sij.data(), sij.size() * 4, 0},
+        {cfg.data(), cfg.size() * sizeof(tg::Coef), 0},
+        {bv.data(), bv.size() * 8, 0},
+        {kb_off.data(), kb_off.size() * 4, 0},
+        {kb_members.data(), kb_members.size() * 4, 0},
+        {kb_island.data(), kb_island.size() * 4, 0},
+        {kb_bidx.data(), kb_bidx.size() * 4, 0},
+        {row_cfg.data(), row_cfg.size() * 4, 0},
+        {peak.data(), (size_t)K * 8, 0},
+        {hbm.data(), (size_t)K * 8, 0},
+        {intra.data(), (size_t)K * 8, 0},
+    };
+    size_t total = 0;
+    for (auto &p : parts) {
+        p.off = total;
+        total += align256(p.bytes > 0 ? p.bytes : 1);
+    }
+    tg_problem *pr = new (std::nothrow) tg_problem();
+    if (!pr) return fail(TG_ENOMEM, "host allocation");
+    hipError_t e = hipGetDevice(&pr->device);
+    if (e != hipSuccess) {
+        delete pr;
+        return hip_fail(e, "hipGetDevice");
+    }
+    e = hipMalloc(&pr->dev_block, total);
+    if (e != hipSuccess) {
+        delete pr;
+        return hip_fail(e, "hipMalloc");
+    }
+    char *base = (char *)pr->dev_block;
+    for (auto &p : parts) {
+        if (p.bytes == 0) continue;
+        e = hipMemcpy(base + p.off, p.src, p.bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(pr->dev_block);
+            delete pr;
+            return hip_fail(e, "hipMemcpy");
+        }
+    }
+    tg::DevProblem &P = pr->P;
+    P.L = L;
+    P.K = K;
+    P.nb = nb;
+    P.dense = dense;
+    P.NS = NS;
+    P.ncfg = ncfg;
+    P.N = NS * ncfg;
+    P.B = sp.global_batch;
+    P.n_kb = (int32_t)kb_island.size();
+    P.max_members = max_members;
+    P.n_rows = (int32_t)row_cfg.size();
+    P.words = (int32_t)((NS + 63) / 64);
+    P.pre = (const int64_t *)(base + parts[0].off);
+    P.outact = (const int64_t *)(base + parts[1].off);
+    P.E = (const double *)(base + parts[2].off);
+    P.sij = (const uint32_t *)(base + parts[3].off);
+    P.coef = (const tg::Coef *)(base + parts[4].off);
+    P.bvals = (const int64_t *)(base + parts[5].off);
+    P.kb_off = (const int32_t *)(base + parts[6].off);
+    P.kb_members = (const int32_t *)(base + parts[7].off);
+    P.kb_island = (const int32_t *)(base + parts[8].off);
+    P.kb_bidx = (const int32_t *)(base + parts[9].off);
+    P.row_cfg = (const int32_t *)(base + parts[10].off);
+    P.peak = (const double *)(base + parts[11].off);
+    P.hbm = (const double *)(base + parts[12].off);
+    P.intra = (const double *)(base + parts[13].off);
+    P.eta = sp.eta;
+    P.mem_frac = sp.mem_frac;
+    pr->bvals = bv;
+    pr->n_compat_cfg = (int64_t)row_cfg.size();
+    // the per-config coefficients are computed on the device
+    e = tg::launch_coef(P, (tg::Coef *)(base + parts[4].off), nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        (void)hipFree(pr->dev_block);
+        delete pr;
+        return hip_fail(e, "coefficient kernel");
+    }
+    *out = pr;
+    return TG_OK;
+}
+
+void tg_problem_destroy(tg_problem *p) {
+    if (!p) return;
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(p->device);
+    (void)hipFree(p->dev_block);
+    (void)hipSetDevice(cur);
+    delete p;
+}
+
+tg_status tg_problem_info(const tg_problem *p, tg_info *out) {
+    if (!p || !out) return fail(TG_EINVAL, "NULL argument");
+    out->L = p->P.L;
+    out->K = p->P.K;
+    out->n_b = p->P.nb;
+    out->dense = p->P.dense;
+    out->NS = p->P.NS;
+    out->n_configs = p->P.ncfg;
+    out->N = p->P.N;
+    out->n_compatible_configs = p->n_compat_cfg;
+    return TG_OK;
+}
+
+tg_status tg_problem_bvalues(const tg_problem *p, int64_t *out, int32_t capacity) {
+    if (!p) return fail(TG_EINVAL, "NULL problem");
+    if (capacity < p->P.nb) return fail(TG_ECAPACITY, "capacity %d < n_b %d", capacity, p->P.nb);
+    for (int a = 0; a < p->P.nb; ++a) out[a] = p->bvals[a];
+    return TG_OK;
+}
+
+tg_status tg_enumerate_pairs(const tg_problem *p, int64_t *n_candidates, int64_t first, int64_t count,
+                             tg_pair *d_out, tg_stream stream) {
+    if (!p) return fail(TG_EINVAL, "NULL problem");
+    if (n_candidates) *n_candidates = p->P.N;
+    if (!d_out) return TG_OK;
+    if (first < 0 || count < 0 || first > p->P.N || count > p->P.N - first)
+        return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
+                    (long long)p->P.N);
+    hipError_t e = tg::launch_enumerate(p->P, first, count, d_out, (hipStream_t)stream);
+    return e == hipSuccess ? TG_OK : hip_fail(e, "enumerate kernel");
+}
+
+tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, double *d_cost, uint8_t *d_dmax,
+                         tg_stream stream) {
+    if (!p) return fail(TG_EINVAL, "NULL problem");
+    if (first < 0 || count < 0 || first > p->P.N || count > p->P.N - first)
+        return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
+                    (long long)p->P.N);
+    if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
+    hipError_t e = tg::launch_score(p->P, first, count, d_cost, d_dmax, (hipStream_t)stream);
+    return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
+}
+
+size_t tg_prune_workspace_bytes(const tg_problem *p) { return p ? tg::prune_ws_bytes(p->P) : 0; }
+
+tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                   int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    if (!p || !n_survivors) return fail(TG_EINVAL, "NULL argument");
+    if (!d_cost || !d_dmax) return fail(TG_EINVAL, "NULL score arrays");
+    if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
+    if (!d_ws || ws_bytes < tg::prune_ws_bytes(p->P))
+        return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
+    int64_t *d_total = nullptr;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
+    if (e != hipSuccess) return hip_fail(e, "prune kernels");
+    int64_t total = 0;
+    e = hipMemcpyAsync(&total, d_total, sizeof(total), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "prune count");
+    *n_survivors = total;
+    if (total > capacity)
+        return fail(TG_ECAPACITY, "%lld survivors exceed capacity %lld", (long long)total, (long long)capacity);
+    return TG_OK;
+}
+
+size_t tg_compose_workspace_bytes(const tg_problem *p, int64_t n_survivors) {
+    if (!p || n_survivors < 0) return 0;
+    return tg::compose_ws_bytes(p->P, n_survivors);
+}
+
+tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                              const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                              tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    if (!p || !out || !island_order) return fail(TG_EINVAL, "NULL argument");
+    std::memset(out, 0, sizeof(*out));
+    out->P = out->F = out->T = HUGE_VAL;
+    const int K = p->P.K;
+    std::vector<int> seen(K, 0);
+    for (int o = 0; o < K; ++o) {
+        const int k = island_order[o];
+        if (k < 0 || k >= K || seen[k]) return fail(TG_EINVAL, "island_order is not a permutation");
+        seen[k] = 1;
+    }
+    if (n_survivors < 0 || n_survivors > ((int64_t)1 << 30) || (n_survivors > 0 && !d_survivors))
+        return fail(TG_EINVAL, "bad survivor list");
+    if (n_survivors > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL score arrays");
+    if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31))
+        return fail(TG_EINVAL, "stage table too large");
+    const size_t need = tg::compose_ws_bytes(p->P, n_survivors);
+    if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    if (p->P.nb == 0) return fail(TG_ENOPLAN, "no micro-batch size divides the global batch");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipMemcpyAsync((char *)d_ws + tg::compose_order_offset(p->P, n_survivors), island_order,
+                                  sizeof(int32_t) * K, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "order upload");
+    tg::ComposeResult *res_dev = nullptr;
+    e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
+    if (e != hipSuccess) return hip_fail(e, "compose kernels");
+    tg::ComposeResult *res = new (std::nothrow) tg::ComposeResult;
+    if (!res) return fail(TG_ENOMEM, "host allocation");
+    e = hipMemcpyAsync(res, res_dev, sizeof(*res), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        delete res;
+        return hip_fail(e, "compose result");
+    }
+    tg_status st = TG_OK;
+    if (res->err & 3) {
+        st = fail(TG_EINVAL, "candidate list invalid (code %d): not strictly ascending, out of range, or "
+                             "incompatible", res->err);
+    } else if (res->err) {
+        st = fail(TG_EDEVICE, "internal consistency check failed during backtracking (code %d)", res->err);
+    } else if (res->status != TG_OK) {
+        st = fail(TG_ENOPLAN, "no pipeline fits");
+    } else {
+        *out = res->plan;
+    }
+    delete res;
+    return st;
+}
+
+}  // extern "C"

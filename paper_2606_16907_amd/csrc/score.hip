@@ -1,0 +1,195 @@
+// score.hip -- per-config coefficients, candidate scoring and decoding.
+//
+// Scoring is the analytic stand-in for the per-pair parallelizer query of
+// Tab. 2 (profile() + parallelize()): a step-time cost per micro-batch and the
+// deepest 1F1B position the pair fits at (Sec. 5.2).  Candidates are
+// idx = g * NS + s (g: global config, s: slice).  A wave owns 64 consecutive
+// slices and walks a run of GC configs: the slice sums live in VGPRs for the
+// whole run, the config's coefficients arrive through scalar loads, and every
+// config writes one coalesced 512-byte row of costs and 64 bytes of depths.
+#include "tg_device.h"
+
+#pragma clang fp contract(off)
+
+namespace tg {
+
+// ---------------------------------------------------------------------------
+// coefficients of one config (exact operation order of the stated model)
+// ---------------------------------------------------------------------------
+__device__ inline double ring_share(int64_t D) { return (double)(D - 1) / (double)D; }
+
+// bf16 bytes per parameter moved for data-parallel sync, per micro-batch
+__device__ inline double sync_per_microbatch(int z, int64_t D) {
+    if (z <= 1) return 0.0;
+    if (z == 2) return 2.0 * ring_share(D);
+    return 6.0 * ring_share(D);
+}
+
+// bf16 bytes per parameter moved for data-parallel sync, per iteration
+__device__ inline double sync_per_iteration(int z, int64_t D) {
+    if (z <= 1) return 4.0 * ring_share(D);
+    if (z == 2) return 2.0 * ring_share(D);
+    return 0.0;
+}
+
+// model-state bytes per parameter (bf16 weight + bf16 grad + fp32 master, m, v)
+__device__ inline double state_per_param(int z, int64_t D) {
+    if (z == 0) return 16.0;
+    if (z == 1) return 4.0 + 12.0 / (double)D;
+    if (z == 2) return 2.0 + 14.0 / (double)D;
+    return 16.0 / (double)D;
+}
+
+__global__ __launch_bounds__(256) void coef_kernel(DevProblem P, Coef *coef) {
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= P.ncfg) return;
+    Coef c = coef[g];
+    const double F = P.peak[c.k], W = P.intra[c.k], M = P.hbm[c.k];
+    const int64_t b = (int64_t)c.dp * c.mb;
+    const int64_t Dd = c.dp, De = c.dp / c.ep;
+    const double qd = (double)c.tp, qe = (double)((int64_t)c.tp * c.ep);
+    c.m_real = (double)P.B / (double)b;
+    c.alpha = (3.0 * (double)c.mb) / (((double)c.tp * F) * P.eta);
+    c.beta = c.tp > 1 ? ((4.0 * (double)c.mb) * (double)(c.tp - 1)) / ((double)c.tp * W) : 0.0;
+    c.gamma = c.ep > 1 ? ((2.0 * (double)c.mb) * (double)(c.ep - 1)) / (((double)c.ep * (double)c.tp) * W) : 0.0;
+    c.dd = ((sync_per_microbatch(c.z, Dd) / qd) / W) + (((sync_per_iteration(c.z, Dd) / qd) / W) / c.m_real);
+    c.de = ((sync_per_microbatch(c.z, De) / qe) / W) + (((sync_per_iteration(c.z, De) / qe) / W) / c.m_real);
+    c.mud = state_per_param(c.z, Dd) / qd;
+    c.mue = state_per_param(c.z, De) / qe;
+    c.rho = (double)c.mb / (double)c.tp;
+    c.H = M * P.mem_frac;
+    c.inv_rho = (double)c.tp / (double)c.mb;
+    coef[g] = c;
+}
+
+hipError_t launch_coef(const DevProblem &P, Coef *coef, hipStream_t s) {
+    const int64_t blocks = (P.ncfg + 255) / 256;
+    coef_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, coef);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// scoring
+// ---------------------------------------------------------------------------
+constexpr int kScoreWaves = 4;   // waves per block
+constexpr int kScoreConfigs = 32;  // configs per wave tile
+
+// Largest d in 1..K with state + min(d, m) * A1 <= H, or 0.  fits() is
+// monotone in d, so a first guess from (H - state) / A1 corrected by exact
+// predicate evaluations yields exactly the largest fitting depth.
+__device__ inline int max_depth(double state, double A1, double H, double m_real, double guess_scale, int K) {
+    auto fits = [&](int d) -> bool {
+        const double inflight = fmin((double)d, m_real);
+        return state + inflight * A1 <= H;
+    };
+    if (fits(K)) return K;
+    // here fits(K) is false, so the answer is < K and (if >= 1) below m
+    const double q = (H - state) * guess_scale;
+    int d = (q >= 1.0) ? (int)fmin(q, (double)(K - 1)) : 0;
+    while (d > 0 && !fits(d)) --d;
+    while (fits(d + 1)) ++d;
+    return d;
+}
+
+template <bool kDense>
+__global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first, int64_t last, int64_t g_lo,
+                                                    int64_t g_hi, int64_t n_stiles, int64_t n_tiles,
+                                                    double *__restrict__ cost, uint8_t *__restrict__ dmax) {
+    const int64_t tile = (int64_t)blockIdx.x * kScoreWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (tile >= n_tiles) return;
+    const int64_t gt = tile / n_stiles;
+    const int64_t st = tile - gt * n_stiles;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t s = st * kWave + lane;
+    const bool sv = s < P.NS;
+
+    // slice sums: exact int64 prefix differences, then one rounding to binary64
+    double Fl = 0.0, Pd = 0.0, Pe = 0.0, Act = 0.0, Tb = 0.0, Ab = 0.0, inv_act = 0.0;
+    if (sv) {
+        const uint32_t ij = P.sij[s];
+        const int i = (int)(ij & 0xFFFFu), j = (int)(ij >> 16);
+        const int64_t *pre = P.pre;
+        const int64_t Lp = P.L + 1;
+        Fl = (double)(pre[j] - pre[i]);
+        Pd = (double)(pre[Lp + j] - pre[Lp + i]);
+        Act = (double)(pre[3 * Lp + j] - pre[3 * Lp + i]);
+        Tb = (double)(pre[4 * Lp + j] - pre[4 * Lp + i]);
+        if (!kDense) {
+            Pe = (double)(pre[2 * Lp + j] - pre[2 * Lp + i]);
+            Ab = (double)(pre[5 * Lp + j] - pre[5 * Lp + i]);
+        }
+        inv_act = 1.0 / Act;
+    }
+    const int K = P.K;
+    const int64_t NS = P.NS;
+    const int64_t g_beg = g_lo + gt * kScoreConfigs;
+    const int64_t g_end = min(g_beg + kScoreConfigs, g_hi + 1);
+    for (int64_t g = g_beg; g < g_end; ++g) {
+        const Coef &c = P.coef[g];
+        double v = c.alpha * Fl;
+        v = v + c.beta * Tb;
+        if (!kDense) v = v + c.gamma * Ab;
+        v = v + c.dd * Pd;
+        if (!kDense) v = v + c.de * Pe;
+        double state = c.mud * Pd;
+        if (!kDense) state = state + c.mue * Pe;
+        const double A1 = c.rho * Act;
+        const int dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * inv_act, K);
+        const int64_t idx = g * NS + s;
+        if (sv && idx >= first && idx < last) {
+            cost[idx - first] = v;
+            dmax[idx - first] = (uint8_t)dm;
+        }
+    }
+}
+
+hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, double *cost, uint8_t *dmax,
+                        hipStream_t s) {
+    if (count <= 0) return hipSuccess;
+    const int64_t last = first + count;
+    const int64_t g_lo = first / P.NS, g_hi = (last - 1) / P.NS;
+    const int64_t n_gtiles = (g_hi - g_lo + kScoreConfigs) / kScoreConfigs;
+    const int64_t n_stiles = (P.NS + kWave - 1) / kWave;
+    const int64_t n_tiles = n_gtiles * n_stiles;
+    const int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    if (P.dense)
+        score_kernel<true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi, n_stiles,
+                                                                         n_tiles, cost, dmax);
+    else
+        score_kernel<false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi, n_stiles,
+                                                                          n_tiles, cost, dmax);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// decoding
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void enumerate_kernel(DevProblem P, int64_t first, int64_t count, tg_pair *out) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= count) return;
+    const int64_t idx = first + t;
+    const int64_t g = idx / P.NS, s = idx - g * P.NS;
+    const uint32_t ij = P.sij[s];
+    const Coef &c = P.coef[g];
+    tg_pair p;
+    p.i = (int32_t)(ij & 0xFFFFu);
+    p.j = (int32_t)(ij >> 16);
+    p.island = c.k;
+    p.tp = c.tp;
+    p.dp = c.dp;
+    p.ep = c.ep;
+    p.zero = c.z;
+    p.mb = c.mb;
+    out[t] = p;
+}
+
+hipError_t launch_enumerate(const DevProblem &P, int64_t first, int64_t count, tg_pair *out, hipStream_t s) {
+    if (count <= 0) return hipSuccess;
+    const int64_t blocks = (count + 255) / 256;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    enumerate_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, count, out);
+    return hipGetLastError();
+}
+
+}  // namespace tg

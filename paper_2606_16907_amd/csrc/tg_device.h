@@ -1,0 +1,125 @@
+// tg_device.h -- device-side problem tables and helpers shared by the HIP
+// kernels of the plan-search library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/tangram.h"
+
+#pragma clang fp contract(off)
+
+namespace tg {
+
+constexpr int kWave = 64;
+constexpr double kInf = __builtin_huge_val();
+
+// Per-config coefficients of the step-time and memory model.  One 128-byte
+// row per config so a wave reads its config with two scalar loads.
+struct alignas(128) Coef {
+    double alpha, beta, gamma, dd, de;  // cost = alpha Fl + beta Tb + gamma Ab + dd Pd + de Pe
+    double mud, mue;                    // state = mud Pd + mue Pe
+    double rho;                         // A1 = rho Act (stash of one micro-batch)
+    double H;                           // usable bytes per GPU
+    double m_real;                      // B / b
+    double inv_rho;                     // 1 / rho, only for the d_max first guess
+    int32_t k, tp, dp, ep, z, mb;       // the config tuple
+    int32_t b_idx;                      // index of b in the compatible list, -1 if B mod b != 0
+    int32_t row;                        // bitmap row of a compatible config, -1 otherwise
+};
+static_assert(sizeof(Coef) == 128, "Coef row must be 128 bytes");
+
+// All device tables of one problem.  Passed to kernels by value.
+struct DevProblem {
+    int32_t L, K, nb, dense;
+    int64_t NS, ncfg, N, B;
+    int32_t n_kb;         // (island, b) groups with at least one compatible config
+    int32_t max_members;  // largest group
+    int32_t n_rows;       // compatible configs = bitmap rows
+    int32_t words;        // 64-bit bitmap words per row = ceil(NS / 64)
+    const int64_t *pre;   // [6][L+1] prefix sums: flops, dparam, eparam, act, tpcomm, a2a
+    const int64_t *outact;  // [L]
+    const double *E;        // [K*K] inter-island bytes/s
+    const uint32_t *sij;    // [NS] slice -> i | j << 16
+    const Coef *coef;       // [ncfg]
+    const int64_t *bvals;   // [nb]
+    const int32_t *kb_off;  // [n_kb+1] offsets into kb_members
+    const int32_t *kb_members;  // config ids of each (island, b) group, ascending
+    const int32_t *kb_island;   // [n_kb]
+    const int32_t *kb_bidx;     // [n_kb]
+    const int32_t *row_cfg;     // [n_rows] config id of each bitmap row
+    const double *peak, *hbm, *intra;  // [K] island rates
+    double eta, mem_frac;
+};
+
+// Slice index of [i, j): slices with first layer < i, then the offset of j.
+__host__ __device__ inline int64_t slice_of(int64_t L, int64_t i, int64_t j) {
+    return i * L - (i * (i - 1)) / 2 + (j - i - 1);
+}
+
+__device__ inline int wave_lane() { return threadIdx.x & (kWave - 1); }
+
+// Inclusive prefix sum across a wave.
+template <typename T>
+__device__ inline T wave_incl_scan(T v) {
+    const int lane = wave_lane();
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        T t = __shfl_up(v, off, kWave);
+        if (lane >= off) v += t;
+    }
+    return v;
+}
+
+// Exclusive prefix sum over a block of blockDim.x (multiple of 64) threads.
+// `lds` holds at least blockDim.x / 64 + 1 entries.  Returns the thread's
+// exclusive prefix and writes the block total to *total.
+template <typename T>
+__device__ inline T block_excl_scan(T v, T *lds, T *total) {
+    const int lane = wave_lane(), wave = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    T inc = wave_incl_scan(v);
+    if (lane == kWave - 1) lds[wave] = inc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        T acc = 0;
+        for (int w = 0; w < nw; w++) {
+            T t = lds[w];
+            lds[w] = acc;
+            acc += t;
+        }
+        lds[nw] = acc;
+    }
+    __syncthreads();
+    T out = inc - v + lds[wave];
+    *total = lds[nw];
+    __syncthreads();
+    return out;
+}
+
+}  // namespace tg
+
+// Host-side launchers (defined in the .hip files), all asynchronous on `s`.
+namespace tg {
+hipError_t launch_coef(const DevProblem &P, Coef *coef_inout, hipStream_t s);
+hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, double *cost, uint8_t *dmax,
+                        hipStream_t s);
+hipError_t launch_enumerate(const DevProblem &P, int64_t first, int64_t count, tg_pair *out, hipStream_t s);
+
+size_t prune_ws_bytes(const DevProblem &P);
+hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
+                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
+
+size_t compose_ws_bytes(const DevProblem &P, int64_t n_surv);
+// Runs composition; on return (after the stream is synchronised by the
+// caller) the result block at *result_dev holds the plan and status.
+struct ComposeResult {
+    int32_t err;     // non-zero: the candidate list was invalid
+    int32_t status;  // TG_OK or TG_ENOPLAN
+    int32_t pad[2];
+    tg_plan plan;
+};
+hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
+                          const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
+                          ComposeResult **result_dev);
+size_t compose_order_offset(const DevProblem &P, int64_t n_surv);  // where the order table lives in ws
+}  // namespace tg
