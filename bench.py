@@ -1,0 +1,189 @@
+"""Benchmark of the plan search on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large]
+
+A step is one whole plan search over a resident instance: score every
+model-slice/island/config candidate (tg_score_pairs), prune to the surviving
+set (tg_prune), compose the pipeline (tg_compose_pipeline, plan returned to
+the host).  The instance's tables and the score buffers are on the device
+before the timed region.  Prints one JSON line:
+  value        candidates per second of whole plan search (N * K / elapsed)
+  ms_per_step  end-to-end plan-search milliseconds
+  roofline     the score kernel: algorithmic bytes (8 B cost + 1 B depth per
+               candidate) per launch / its mean HIP-event duration, against
+               the 8 TB/s HBM peak
+  cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
+               workload (the same 128 layers on the first islands only)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+SCORE_BYTES_PER_CANDIDATE = 9  # 8-byte cost + 1-byte depth written; inputs stay in registers/L2
+METRIC = "slice/island pairs scored/sec; end-to-end plan-search seconds (1 GPU)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_large_traffic.json")
+
+WORKLOADS = {
+    "large": "128-layer dense decoder (h 12288, FFN 49152 GeLU, 96 heads, s 8192, global batch "
+             "4096) on 128 islands of 8-64 GPUs, 5 GPU types, 3-level fabric 400/100/25 GB/s; "
+             "TP{1,2,4,8} x DP 1..n/tp x ZeRO 0-3 x MB{1,2,4,8}",
+    "dense70b": "80-layer dense (h 8192, FFN 28672 SwiGLU, GQA 64/8, s 8192, global batch 1024) "
+                "on 16 islands of 8-64 GPUs",
+    "moe": "48-layer MoE (h 6144, 64 experts top-2, expert FFN 4096, s 4096, global batch 2048) "
+           "on 32 islands of 8-32 GPUs, EP{1,2,4,8,16}",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-islands", type=int, default=24,
+                    help="islands of the CPU-baseline sample (first islands of the workload)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
+    ap.add_argument("--score-only", type=int, default=0,
+                    help="after the timed steps, launch the score kernel this many more times "
+                         "(for profiler counter runs)")
+    return ap.parse_args()
+
+
+def cpu_baseline(inst, n_islands):
+    """The oracle, as it stands, on the workload restricted to its first
+    n_islands islands: score every candidate, prune, compose."""
+    from oracle.oracle import Oracle
+    sub = dict(inst)
+    keep = list(range(n_islands))
+    sub["islands"] = {f: [v[k] for k in keep] for f, v in inst["islands"].items()}
+    sub["inter_bw"] = [[inst["inter_bw"][a][b] for b in keep] for a in keep]
+    sub["island_order"] = [k for k in inst["island_order"] if k < n_islands]
+    o = Oracle(sub)
+    t0 = time.perf_counter()
+    cost, dmax = o.score()
+    t1 = time.perf_counter()
+    surv = o.prune()
+    t2 = time.perf_counter()
+    st, plan, _ = o.compose(surv)
+    t3 = time.perf_counter()
+    del cost, dmax
+    el = t3 - t0
+    return {"value": o.N / el, "unit": "pairs/s", "cores": 1, "kind": "oracle",
+            "sample": f"same 128-layer workload on its first {n_islands} of 128 islands "
+                      f"(N={o.N} candidates): score all, prune, compose; single thread",
+            "seconds": round(el, 3), "score_s": round(t1 - t0, 3), "prune_s": round(t2 - t1, 3),
+            "compose_s": round(t3 - t2, 3), "candidates": o.N, "plan_status": st}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the plan search is a "
+              f"single-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_16907_amd import tangram as T
+    from workloads import load_instance
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    inst = load_instance(args.workload)
+    t_create = time.perf_counter()
+    p = T.Problem(inst)
+    torch.cuda.synchronize()
+    t_create = time.perf_counter() - t_create
+    N = p.N
+    cost = torch.empty(N, dtype=torch.float64, device="cuda")
+    dmax = torch.empty(N, dtype=torch.uint8, device="cuda")
+    pws = p.prune_workspace()
+
+    # size the survivor buffer and composition workspace once (untimed)
+    p.tg_score_pairs(0, N, cost, dmax)
+    surv0 = p.tg_prune(cost, dmax, workspace=pws)
+    n_surv = int(surv0.numel())
+    surv_buf = torch.empty(max(n_surv, 1), dtype=torch.int64, device="cuda")
+    cws = p.compose_workspace(n_surv)
+    del surv0
+
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record(stream)
+        p.tg_score_pairs(0, N, cost, dmax)
+        if e:
+            e[1].record(stream)
+        s = p.tg_prune(cost, dmax, survivors=surv_buf, workspace=pws)
+        if e:
+            e[2].record(stream)
+        st, plan = p.tg_compose_pipeline(s, cost, dmax, workspace=cws)
+        if e:
+            e[3].record(stream)
+        return st, plan, s
+
+    for _ in range(args.warmup):
+        st, plan, s = step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        st, plan, s = step(ev[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    score_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
+    prune_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
+    compose_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.steps)]
+    for _ in range(args.score_only):
+        p.tg_score_pairs(0, N, cost, dmax)
+    torch.cuda.synchronize()
+
+    mean = lambda xs: sum(xs) / len(xs)
+    score_s = mean(score_ms) / 1e3
+    achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            tr = json.load(fh)
+        if tr.get("workload") == args.workload and tr.get("N") == N:
+            traffic = tr.get("bytes_per_launch")
+    out = {
+        "metric": METRIC,
+        "value": N * args.steps / elapsed,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}",
+                   "candidates": N, "survivors": int(s.numel()), "islands": p.K, "layers": p.L,
+                   "plan": {"status": st, "b": plan["b"], "stages": plan["S"], "T": plan["T"]}},
+        "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "breakdown_ms": {"score": mean(score_ms), "prune": mean(prune_ms),
+                         "compose": mean(compose_ms), "create": t_create * 1e3},
+        "score_kernel_pairs_per_s": N / score_s,
+        "end_to_end_s": elapsed / args.steps,
+    }
+    if not args.no_cpu:
+        cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -207,9 +207,11 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
 
 /*
  * Composition (Sec. 5.2): builds the pipeline from the candidates listed in
- * d_survivors (strictly ascending indices of compatible candidates; entries
- * with d_max 0 are ignored; any other list is TG_EINVAL), scored by d_cost /
- * d_dmax over all N.  island_order (host, a permutation of 0..K-1) fixes the
+ * d_survivors, scored by d_cost / d_dmax over all N.  The list holds strictly
+ * ascending indices of compatible candidates (anything else is TG_EINVAL;
+ * entries with d_max 0 are ignored) and must contain the whole surviving set:
+ * tg_prune's output, or any superset of it drawn from the compatible
+ * candidates, which composes to the same plan.  island_order (host, a permutation of 0..K-1) fixes the
  * order in which islands may appear from pipeline front to back; islands may
  * be skipped.  For each b the plan minimises the bottleneck P = max of stage
  * costs and link times, then the fill F = f1 + (x1 + (f2 + ... + fS)) among

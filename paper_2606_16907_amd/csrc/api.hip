@@ -183,6 +183,15 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
             c0 = c1;
         }
     }
+    // distinct inter-island bandwidths (link times need one division per value)
+    std::vector<double> ev(inter_bw, inter_bw + (size_t)K * K);
+    std::sort(ev.begin(), ev.end());
+    ev.erase(std::unique(ev.begin(), ev.end()), ev.end());
+    std::vector<uint16_t> eidx((size_t)K * K, 0);
+    const bool e_table = ev.size() <= (size_t)tg::kMaxDistinctE;
+    if (e_table)
+        for (int a = 0; a < K * K; ++a)
+            eidx[a] = (uint16_t)(std::lower_bound(ev.begin(), ev.end(), inter_bw[a]) - ev.begin());
     std::vector<uint32_t> sij(NS);
     {
         int64_t s = 0;
@@ -217,6 +226,8 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         {peak.data(), (size_t)K * 8, 0},
         {hbm.data(), (size_t)K * 8, 0},
         {intra.data(), (size_t)K * 8, 0},
+        {ev.data(), ev.size() * 8, 0},
+        {eidx.data(), eidx.size() * 2, 0},
     };
     size_t total = 0;
     for (auto &p : parts) {
@@ -274,6 +285,9 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.intra = (const double *)(base + parts[13].off);
     P.eta = sp.eta;
     P.mem_frac = sp.mem_frac;
+    P.n_ev = e_table ? (int32_t)ev.size() : 0;
+    P.Ev = (const double *)(base + parts[14].off);
+    P.Eidx = (const uint16_t *)(base + parts[15].off);
     pr->bvals = bv;
     pr->n_compat_cfg = (int64_t)row_cfg.size();
     // the per-config coefficients are computed on the device

@@ -18,6 +18,14 @@
 // group's least fitting candidate changes; those changes are precomputed as
 // events bucketed by (level, b, first layer i) and applied by the block that
 // reads them, so the table is never rebuilt.
+//
+// T_d(i, j, o) never decreases as j grows (a longer slice costs at least as
+// much under every config and fits in memory under fewer), so a row's scan
+// over j stops at the first T not below the running best: no later j can
+// improve it.  This holds whenever the candidate list contains the surviving
+// set, since then T_d equals the least cost over all group members.
+#include <algorithm>
+
 #include "tg_device.h"
 
 #pragma clang fp contract(off)
@@ -58,7 +66,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_i32(const int32_t *a
     if (threadIdx.x == 0) tile_sum[blockIdx.x] = total;
 }
 
-__global__ __launch_bounds__(1024) void scan_tiles_i64(int64_t *a, int64_t n, int64_t *total) {
+__global__ __launch_bounds__(1024) void scan_tiles_i64(int64_t *a, int64_t n) {
     __shared__ int64_t lds[1024 / kWave + 1];
     int64_t carry = 0;
     for (int64_t base = 0; base < n; base += blockDim.x) {
@@ -69,7 +77,6 @@ __global__ __launch_bounds__(1024) void scan_tiles_i64(int64_t *a, int64_t n, in
         if (i < n) a[i] = carry + ex;
         carry += sum;
     }
-    if (threadIdx.x == 0 && total) *total = carry;
 }
 
 __global__ __launch_bounds__(kScanThreads) void scan_apply_i32(int32_t *a, int64_t n, const int64_t *tile_off) {
@@ -89,37 +96,43 @@ __global__ __launch_bounds__(kScanThreads) void scan_apply_i32(int32_t *a, int64
     }
 }
 
-// In-place exclusive scan of an int32 array; tmp holds >= tiles + 1 int64.
+// In-place exclusive scan of an int32 array; tmp holds >= tiles int64.
 static void scan_i32(int32_t *a, int64_t n, int64_t *tmp, hipStream_t s) {
     if (n <= 0) return;
     const int64_t tiles = (n + kScanTile - 1) / kScanTile;
     scan_reduce_i32<<<dim3((unsigned)tiles), dim3(kScanThreads), 0, s>>>(a, n, tmp);
-    scan_tiles_i64<<<dim3(1), dim3(1024), 0, s>>>(tmp, tiles, nullptr);
+    scan_tiles_i64<<<dim3(1), dim3(1024), 0, s>>>(tmp, tiles);
     scan_apply_i32<<<dim3((unsigned)tiles), dim3(kScanThreads), 0, s>>>(a, n, tmp);
 }
 
 // ---------------------------------------------------------------------------
-// grouping: candidate list -> per-group entry lists -> per-level events
+// workspace
 // ---------------------------------------------------------------------------
 struct Ws {
-    int32_t *pos;     // [K] island -> position
-    double *EoT;      // [K*K] EoT[o2*K + o] = E[order[o]][order[o2]]
-    int32_t *gcnt;    // [n_groups] counts -> offsets -> ends
-    int32_t *entries; // [n_surv] survivor positions grouped
-    int32_t *bcnt;    // [n_buckets] event counts -> offsets -> ends
-    int32_t *ev_cell; // [2 n_surv]
-    double *ev_val;   // [2 n_surv]
-    double *T;        // [n_groups] current stage table, layout [b][s][o]
-    double *Wb[2];    // [nb][L+1][K] continuation rows, double-buffered by level
-    uint16_t *argF;   // [D][nb][L][K]
-    uint8_t *argG;    // [D][nb][L+1][K]
-    double *Pst;      // [nb]
-    double *rootF;    // [nb]
-    int32_t *root_o;  // [nb]
-    int32_t *root_d;  // [nb]
-    int64_t *tmp;     // scan tiles
     ComposeResult *res;
-    int32_t *order;   // [K] copy of the caller's order
+    int32_t *order;    // [K] copy of the caller's order
+    int32_t *pos;      // [K] island -> position
+    double *EoT;       // [K*K] EoT[o2*K + o] = E[order[o]][order[o2]]
+    uint8_t *EiT;      // [K(K-1)/2] index of E[order[o]][order[o2]] (o < o2) in the distinct list
+    int32_t *rec_g;    // [n] group of list entry r, -1 if unused
+    double *rec_c;     // [n] its cost
+    uint8_t *rec_d;    // [n] its d_max
+    int32_t *gcnt;     // [n_groups] counts -> offsets -> ends
+    double *ent_c;     // [n] grouped entries: cost
+    uint8_t *ent_d;    // [n] d_max
+    int64_t *ent_i;    // [n] candidate index
+    int32_t *bcnt;     // [n_buckets + 1] event counts -> bucket starts (last = total)
+    int32_t *ev_cell;  // [2n]
+    double *ev_val;    // [2n]
+    double *T;         // [n_groups] current stage table, layout [b][s][o]
+    double *Wb[2];     // [nb][L+1][K] continuation rows, double-buffered by level
+    uint16_t *argF;    // [D][nb][L][K]
+    uint8_t *argG;     // [D][nb][L+1][K]
+    double *Pst;       // [nb]
+    double *rootF;     // [nb]
+    int32_t *root_o;   // [nb]
+    int32_t *root_d;   // [nb]
+    int64_t *tmp;      // scan tiles
     size_t bytes;
 };
 
@@ -127,7 +140,7 @@ static int64_t n_groups(const DevProblem &P) { return (int64_t)P.nb * P.NS * P.K
 static int levels(const DevProblem &P) { return P.K < P.L ? P.K : P.L; }
 static int64_t n_buckets(const DevProblem &P) { return (int64_t)levels(P) * P.nb * P.L; }
 
-static Ws carve(const DevProblem &P, int64_t n_surv, void *base) {
+static Ws carve(const DevProblem &P, int64_t n, void *base) {
     Ws w{};
     char *p = (char *)base;
     size_t off = 0;
@@ -139,15 +152,22 @@ static Ws carve(const DevProblem &P, int64_t n_surv, void *base) {
     const int64_t G = n_groups(P), D = levels(P), nbk = n_buckets(P);
     const int64_t rows = (int64_t)P.nb * (P.L + 1) * P.K;
     const int64_t tiles = (std::max(G, nbk) + kScanTile - 1) / kScanTile + 1;
+    const int64_t K2 = (int64_t)P.K * P.K;
     w.res = (ComposeResult *)take(sizeof(ComposeResult));
     w.order = (int32_t *)take(sizeof(int32_t) * P.K);
     w.pos = (int32_t *)take(sizeof(int32_t) * P.K);
-    w.EoT = (double *)take(sizeof(double) * P.K * P.K);
+    w.EoT = (double *)take(sizeof(double) * K2);
+    w.EiT = (uint8_t *)take((size_t)K2 / 2 + 4);
+    w.rec_g = (int32_t *)take(sizeof(int32_t) * n);
+    w.rec_c = (double *)take(sizeof(double) * n);
+    w.rec_d = (uint8_t *)take(n);
     w.gcnt = (int32_t *)take(sizeof(int32_t) * G);
-    w.entries = (int32_t *)take(sizeof(int32_t) * n_surv);
-    w.bcnt = (int32_t *)take(sizeof(int32_t) * nbk);
-    w.ev_cell = (int32_t *)take(sizeof(int32_t) * 2 * n_surv);
-    w.ev_val = (double *)take(sizeof(double) * 2 * n_surv);
+    w.ent_c = (double *)take(sizeof(double) * n);
+    w.ent_d = (uint8_t *)take(n);
+    w.ent_i = (int64_t *)take(sizeof(int64_t) * n);
+    w.bcnt = (int32_t *)take(sizeof(int32_t) * (nbk + 1));
+    w.ev_cell = (int32_t *)take(sizeof(int32_t) * 2 * n);
+    w.ev_val = (double *)take(sizeof(double) * 2 * n);
     w.T = (double *)take(sizeof(double) * G);
     w.Wb[0] = (double *)take(sizeof(double) * rows);
     w.Wb[1] = (double *)take(sizeof(double) * rows);
@@ -164,16 +184,23 @@ static Ws carve(const DevProblem &P, int64_t n_surv, void *base) {
 
 size_t compose_ws_bytes(const DevProblem &P, int64_t n_surv) { return carve(P, n_surv, nullptr).bytes; }
 size_t compose_order_offset(const DevProblem &P, int64_t n_surv) {
+    (void)P;
     (void)n_surv;
     return align256(sizeof(ComposeResult));
 }
 
-__global__ void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, double *EoT, ComposeResult *res) {
+// Index of the pair of positions (o, o2), o < o2, in a packed triangle.
+__host__ __device__ inline int tri(int o, int o2) { return o2 * (o2 - 1) / 2 + o; }
+
+__global__ void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, double *EoT, uint8_t *EiT,
+                            ComposeResult *res) {
     const int K = P.K;
     for (int t = threadIdx.x; t < K; t += blockDim.x) pos[order[t]] = t;
     for (int t = threadIdx.x; t < K * K; t += blockDim.x) {
         const int o2 = t / K, o = t - o2 * K;
-        EoT[t] = P.E[(int64_t)order[o] * K + order[o2]];
+        const int64_t e = (int64_t)order[o] * K + order[o2];
+        EoT[t] = P.E[e];
+        if (o < o2) EiT[tri(o, o2)] = P.n_ev ? (uint8_t)P.Eidx[e] : 0;
     }
     if (threadIdx.x == 0) {
         res->err = 0;
@@ -181,119 +208,219 @@ __global__ void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, do
     }
 }
 
-// Validates entry r and returns its group (or -1 when it has d_max 0).
-__device__ inline int64_t group_of(const DevProblem &P, const int64_t *surv, int64_t r, const uint8_t *dmax,
-                                   const int32_t *pos, ComposeResult *res) {
-    const int64_t idx = surv[r];
-    if (idx < 0 || idx >= P.N || (r > 0 && surv[r - 1] >= idx)) {
-        atomicOr(&res->err, 1);
-        return -1;
+// ---------------------------------------------------------------------------
+// grouping: candidate list -> per-group entry records -> per-level events
+// ---------------------------------------------------------------------------
+// Reads each listed candidate's score once (the list is ascending, so the
+// reads walk the score arrays forward) and counts the group sizes.
+__global__ __launch_bounds__(256) void gather_kernel(DevProblem P, const int64_t *surv, int64_t n,
+                                                     const double *cost, const uint8_t *dmax, const int32_t *pos,
+                                                     int32_t *rec_g, double *rec_c, uint8_t *rec_d, int32_t *gcnt,
+                                                     ComposeResult *res) {
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+        int32_t G = -1;
+        const int64_t idx = surv[r];
+        if (idx < 0 || idx >= P.N || (r > 0 && surv[r - 1] >= idx)) {
+            atomicOr(&res->err, 1);
+        } else {
+            const int64_t g = idx / P.NS, s = idx - g * P.NS;
+            const Coef &c = P.coef[g];
+            if (c.b_idx < 0) {
+                atomicOr(&res->err, 2);
+            } else {
+                const uint8_t d = dmax[idx];
+                if (d > 0) {
+                    G = (int32_t)(((int64_t)c.b_idx * P.NS + s) * P.K + pos[c.k]);
+                    rec_c[r] = cost[idx];
+                    rec_d[r] = d;
+                    atomicAdd(&gcnt[G], 1);
+                }
+            }
+        }
+        rec_g[r] = G;
     }
-    const int64_t g = idx / P.NS, s = idx - g * P.NS;
-    const Coef &c = P.coef[g];
-    if (c.b_idx < 0) {
-        atomicOr(&res->err, 2);
-        return -1;
-    }
-    if (dmax[idx] == 0) return -1;
-    return ((int64_t)c.b_idx * P.NS + s) * P.K + pos[c.k];
 }
 
-__global__ __launch_bounds__(256) void count_groups(DevProblem P, const int64_t *surv, int64_t n, const uint8_t *dmax,
-                                                    const int32_t *pos, int32_t *gcnt, ComposeResult *res) {
+__global__ __launch_bounds__(256) void scatter_kernel(const int64_t *surv, int64_t n, const int32_t *rec_g,
+                                                      const double *rec_c, const uint8_t *rec_d, int32_t *gcnt,
+                                                      double *ent_c, uint8_t *ent_d, int64_t *ent_i) {
     for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t G = group_of(P, surv, r, dmax, pos, res);
-        if (G >= 0) atomicAdd(&gcnt[G], 1);
+        const int32_t G = rec_g[r];
+        if (G < 0) continue;
+        const int32_t slot = atomicAdd(&gcnt[G], 1);
+        ent_c[slot] = rec_c[r];
+        ent_d[slot] = rec_d[r];
+        ent_i[slot] = surv[r];
     }
 }
 
-__global__ __launch_bounds__(256) void scatter_groups(DevProblem P, const int64_t *surv, int64_t n,
-                                                      const uint8_t *dmax, const int32_t *pos, int32_t *gcnt,
-                                                      int32_t *entries, ComposeResult *res) {
-    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t G = group_of(P, surv, r, dmax, pos, res);
-        if (G >= 0) entries[atomicAdd(&gcnt[G], 1)] = (int32_t)r;
+// Stage table at depth 1: the least cost of each group.
+__global__ __launch_bounds__(256) void table_init(int64_t n_groups, const int32_t *__restrict__ gcnt,
+                                                  const double *__restrict__ ent_c, double *__restrict__ T) {
+    for (int64_t G = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; G < n_groups;
+         G += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+        double v = kInf;
+        for (int32_t e = st; e < en; ++e) v = fmin(v, ent_c[e]);
+        T[G] = v;
     }
 }
 
 // Per group: entry e is the least fitting candidate at depths (D_e, d_e],
 // D_e = the largest d_max among entries with a smaller key; it sets T at
-// level D_e + 1.  After the group's largest d_max M nothing fits: T = +inf
-// from level M + 1.  At most one event per (group, level).
+// level D_e + 1 (level 1 is written by table_init).  After the group's
+// largest d_max M nothing fits: T = +inf from level M + 1.  At most one event
+// per (group, level).  Block (i, b) owns the groups of the slices starting at
+// layer i, and with them every bucket (level, b, i): counts and slots come
+// from LDS, with no global atomics.
 template <bool kEmit>
-__global__ __launch_bounds__(256) void group_events(DevProblem P, const int64_t *surv, const double *cost,
-                                                    const uint8_t *dmax, const int32_t *gcnt,
-                                                    const int32_t *entries, int32_t *bcnt, int32_t *ev_cell,
-                                                    double *ev_val) {
-    const int64_t NG = (int64_t)P.nb * P.NS * P.K;
-    const int D = P.K < P.L ? P.K : P.L;
-    for (int64_t G = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; G < NG; G += (int64_t)gridDim.x * blockDim.x) {
+__global__ __launch_bounds__(256) void group_events(DevProblem P, const int32_t *__restrict__ gcnt,
+                                                    const double *__restrict__ ent_c,
+                                                    const uint8_t *__restrict__ ent_d,
+                                                    const int64_t *__restrict__ ent_i, int32_t *bcnt,
+                                                    int32_t *__restrict__ ev_cell, double *__restrict__ ev_val) {
+    __shared__ int32_t hist[256];
+    const int i = blockIdx.x, bi = blockIdx.y;
+    const int L = P.L, K = P.K;
+    const int D = K < L ? K : L;
+    for (int lev = threadIdx.x; lev < D; lev += blockDim.x)
+        hist[lev] = kEmit ? bcnt[((int64_t)lev * P.nb + bi) * L + i] : 0;
+    __syncthreads();
+    const int64_t G0 = ((int64_t)bi * P.NS + slice_of(L, i, i + 1)) * K;
+    const int64_t ncell = (int64_t)(L - i) * K;
+    for (int64_t t = threadIdx.x; t < ncell; t += blockDim.x) {
+        const int64_t G = G0 + t;
         const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
         if (st == en) continue;
-        const int64_t bs = G / P.K;
-        const int64_t bi = bs / P.NS, s = bs - bi * P.NS;
-        const int i = (int)(P.sij[s] & 0xFFFFu);
         auto emit = [&](int level, double v) {
-            const int64_t bucket = ((int64_t)(level - 1) * P.nb + bi) * P.L + i;
             if (kEmit) {
-                const int32_t slot = atomicAdd(&bcnt[bucket], 1);
+                const int32_t slot = atomicAdd(&hist[level - 1], 1);
                 ev_cell[slot] = (int32_t)G;
                 ev_val[slot] = v;
             } else {
-                atomicAdd(&bcnt[bucket], 1);
+                atomicAdd(&hist[level - 1], 1);
             }
         };
         int M = 0;
         for (int32_t e = st; e < en; ++e) {
-            const int64_t ie = surv[entries[e]];
-            const double ce = cost[ie];
-            const int de = dmax[ie];
+            const double ce = ent_c[e];
+            const int de = ent_d[e];
+            const int64_t ie = ent_i[e];
             M = max(M, de);
             int De = 0;
             for (int32_t q = st; q < en; ++q) {
-                const int64_t iq = surv[entries[q]];
-                const double cq = cost[iq];
-                const int dq = dmax[iq];
-                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && iq < ie)));
+                const double cq = ent_c[q];
+                const int dq = ent_d[q];
+                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
                 if (less) De = max(De, dq);
             }
-            if (De < de && De + 1 <= D) emit(De + 1, ce);
+            if (De >= 1 && De < de && De + 1 <= D) emit(De + 1, ce);
         }
         if (M + 1 <= D) emit(M + 1, kInf);
+    }
+    if (!kEmit) {
+        __syncthreads();
+        for (int lev = threadIdx.x; lev < D; lev += blockDim.x) bcnt[((int64_t)lev * P.nb + bi) * L + i] = hist[lev];
     }
 }
 
 // ---------------------------------------------------------------------------
 // dynamic program, one launch per level
 // ---------------------------------------------------------------------------
-__device__ inline void apply_events(const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
-                                    int64_t bucket) {
-    const int32_t st = bucket ? bcnt[bucket - 1] : 0, en = bcnt[bucket];
-    for (int32_t e = st + threadIdx.x; e < en; e += blockDim.x) T[ev_cell[e]] = ev_val[e];
+__device__ inline void apply_events(const int32_t *__restrict__ bcnt, const int32_t *__restrict__ ev_cell,
+                                    const double *__restrict__ ev_val, double *__restrict__ T, int64_t bucket) {
+    const int32_t st = bcnt[bucket], en = bcnt[bucket + 1];
+    const int step = blockDim.x;
+    for (int32_t base = st + threadIdx.x; base < en; base += 4 * step) {
+        int32_t c[4];
+        double v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int32_t e = base + k * step;
+            c[k] = e < en ? ev_cell[e] : -1;
+            v[k] = e < en ? ev_val[e] : 0.0;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (c[k] >= 0) T[c[k]] = v[k];
+    }
 }
 
-// Phase 1: bottleneck values.
+// Link times of the boundary after layer i-1 for this block's b.  With few
+// distinct bandwidths (the usual case) the block divides once per distinct
+// value and keeps the per-pair index triangle in LDS; otherwise it divides
+// per pair.
+struct Links {
+    const double *xs;      // LDS [n_ev]
+    const uint8_t *tri_s;  // LDS triangle of indices
+    const double *EoT;     // global, used without a table
+    double num;
+    bool table;
+    __device__ inline double operator()(int o, int o2, int K) const {
+        if (table) return xs[tri_s[tri(o, o2)]];
+        const double E = EoT[(int64_t)o2 * K + o];
+        return E == 0.0 ? kInf : num / E;
+    }
+};
+
+// Fills the block's LDS link tables for positions o < o2 <= top.
+__device__ inline Links stage_links(const DevProblem &P, int i, int bi, int top, const uint8_t *EiT,
+                                    const double *EoT, double *xs, uint8_t *tri_s) {
+    Links X{xs, tri_s, EoT, 0.0, P.n_ev > 0};
+    if (i == 0) return X;
+    X.num = (2.0 * (double)P.bvals[bi]) * (double)P.outact[i - 1];
+    if (X.table) {
+        for (int u = threadIdx.x; u < P.n_ev; u += blockDim.x) {
+            const double E = P.Ev[u];
+            xs[u] = E == 0.0 ? kInf : X.num / E;
+        }
+        const int nbytes = top * (top + 1) / 2;  // rows o2 <= top
+        const int nwords = (nbytes + 3) / 4;
+        const uint32_t *src = (const uint32_t *)EiT;
+        uint32_t *dst = (uint32_t *)tri_s;
+        for (int t = threadIdx.x; t < nwords; t += blockDim.x) dst[t] = src[t];
+    }
+    return X;
+}
+
+// Phase 1: bottleneck values.  Block (i, b), thread o.
 __global__ __launch_bounds__(256) void level_bottleneck(DevProblem P, int d, const int32_t *bcnt,
                                                         const int32_t *ev_cell, const double *ev_val, double *T,
                                                         const double *Wprev, double *Wnext, const double *EoT,
-                                                        double *Pst) {
+                                                        const uint8_t *EiT, double *Pst) {
+    extern __shared__ uint32_t tri_w[];
+    uint8_t *tri_s = (uint8_t *)tri_w;
     __shared__ double Vs[256];
+    __shared__ double xs[kMaxDistinctE];
     const int i = blockIdx.x, bi = blockIdx.y, o = threadIdx.x;
     const int L = P.L, K = P.K;
-    if (i > L - d) return;
     apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
+    const Links X = stage_links(P, i, bi, K - d, EiT, EoT, xs, tri_s);
     __syncthreads();
-    const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);  // slice (i, i+1); (i, j) is + j-i-1
+    const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);  // slice (i, j) is srow + j-i-1
     double v = kInf;
     if (o < K && o <= K - d) {
         if (d == 1) {
             v = T[(srow + (L - i - 1)) * K + o];
         } else {
             const double *Wp = Wprev + (int64_t)bi * (L + 1) * K + o;
-            for (int j = i + 1; j <= L - d + 1; ++j) {
-                const double t = T[(srow + (j - i - 1)) * K + o];
-                const double w = Wp[(int64_t)j * K];
-                v = fmin(v, fmax(t, w));
+            const double *Tp = T + srow * K + o;
+            const int jmax = L - d + 1;
+            for (int j0 = i + 1; j0 <= jmax; j0 += 4) {
+                double t[4], w[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int j = j0 + k;
+                    t[k] = j <= jmax ? Tp[(int64_t)(j - i - 1) * K] : kInf;
+                    w[k] = j <= jmax ? Wp[(int64_t)j * K] : kInf;
+                }
+                bool stop = false;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if (!stop && !(t[k] < v)) stop = true;  // T never decreases in j
+                    if (!stop) v = fmin(v, fmax(t[k], w[k]));
+                }
+                if (stop) break;
             }
         }
     }
@@ -309,12 +436,7 @@ __global__ __launch_bounds__(256) void level_bottleneck(DevProblem P, int d, con
     }
     if (o < K) {
         double w = kInf;
-        const double num = (2.0 * (double)P.bvals[bi]) * (double)P.outact[i - 1];
-        for (int o2 = o + 1; o2 <= K - d; ++o2) {
-            const double E = EoT[(int64_t)o2 * K + o];
-            const double x = E == 0.0 ? kInf : num / E;
-            w = fmin(w, fmax(x, Vs[o2]));
-        }
+        for (int o2 = o + 1; o2 <= K - d; ++o2) w = fmin(w, fmax(X(o, o2, K), Vs[o2]));
         Wnext[((int64_t)bi * (L + 1) + i) * K + o] = w;
     }
 }
@@ -322,15 +444,19 @@ __global__ __launch_bounds__(256) void level_bottleneck(DevProblem P, int d, con
 // Phase 2: fill values and argmins at the bottleneck P*.
 __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell,
                                                   const double *ev_val, double *T, const double *Gprev,
-                                                  double *Gnext, const double *EoT, const double *Pst,
-                                                  uint16_t *argF, uint8_t *argG, double *rootF, int32_t *root_o,
-                                                  int32_t *root_d) {
+                                                  double *Gnext, const double *EoT, const uint8_t *EiT,
+                                                  const double *Pst, uint16_t *argF, uint8_t *argG, double *rootF,
+                                                  int32_t *root_o, int32_t *root_d) {
+    extern __shared__ uint32_t tri_w[];
+    uint8_t *tri_s = (uint8_t *)tri_w;
     __shared__ double Fs[256];
+    __shared__ double xs[kMaxDistinctE];
     const int i = blockIdx.x, bi = blockIdx.y, o = threadIdx.x;
     const int L = P.L, K = P.K;
     const double Ps = Pst[bi];
-    if (!(Ps < kInf) || i > L - d) return;
+    if (!(Ps < kInf)) return;
     apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
+    const Links X = stage_links(P, i, bi, K - d, EiT, EoT, xs, tri_s);
     __syncthreads();
     const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);
     double v = kInf;
@@ -344,14 +470,29 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
             }
         } else {
             const double *Gp = Gprev + (int64_t)bi * (L + 1) * K + o;
-            for (int j = i + 1; j <= L - d + 1; ++j) {
-                const double t = T[(srow + (j - i - 1)) * K + o];
-                if (!(t <= Ps)) continue;
-                const double c = t + Gp[(int64_t)j * K];
-                if (c < v) {
-                    v = c;
-                    arg = j;
+            const double *Tp = T + srow * K + o;
+            const int jmax = L - d + 1;
+            for (int j0 = i + 1; j0 <= jmax; j0 += 4) {
+                double t[4], g[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int j = j0 + k;
+                    t[k] = j <= jmax ? Tp[(int64_t)(j - i - 1) * K] : kInf;
+                    g[k] = j <= jmax ? Gp[(int64_t)j * K] : kInf;
                 }
+                bool stop = false;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if (!stop && (!(t[k] <= Ps) || !(t[k] < v))) stop = true;  // T never decreases in j
+                    if (!stop) {
+                        const double c = t[k] + g[k];
+                        if (c < v) {
+                            v = c;
+                            arg = j0 + k;
+                        }
+                    }
+                }
+                if (stop) break;
             }
         }
     }
@@ -379,10 +520,8 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
     if (o < K) {
         double w = kInf;
         int a = 0xFF;
-        const double num = (2.0 * (double)P.bvals[bi]) * (double)P.outact[i - 1];
         for (int o2 = o + 1; o2 <= K - d; ++o2) {
-            const double E = EoT[(int64_t)o2 * K + o];
-            const double x = E == 0.0 ? kInf : num / E;
+            const double x = X(o, o2, K);
             if (!(x <= Ps)) continue;
             const double c = x + Fs[o2];
             if (c < w) {
@@ -398,11 +537,10 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
 // ---------------------------------------------------------------------------
 // choose b, walk the argmins, resolve each stage's candidate
 // ---------------------------------------------------------------------------
-__global__ void finish_kernel(DevProblem P, const int64_t *surv, const double *cost, const uint8_t *dmax,
-                              const int32_t *gcnt, const int32_t *entries, const int32_t *order,
-                              const double *EoT, const double *Pst, const double *rootF, const int32_t *root_o,
-                              const int32_t *root_d, const uint16_t *argF, const uint8_t *argG,
-                              ComposeResult *res) {
+__global__ void finish_kernel(DevProblem P, const int32_t *gcnt, const double *ent_c, const uint8_t *ent_d,
+                              const int64_t *ent_i, const int32_t *order, const double *EoT, const double *Pst,
+                              const double *rootF, const int32_t *root_o, const int32_t *root_d,
+                              const uint16_t *argF, const uint8_t *argG, ComposeResult *res) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     const int L = P.L, K = P.K;
     tg_plan &plan = res->plan;
@@ -460,9 +598,9 @@ __global__ void finish_kernel(DevProblem P, const int64_t *surv, const double *c
         double bc = kInf;
         int bd = 0;
         for (int32_t e = st; e < en; ++e) {
-            const int64_t ie = surv[entries[e]];
-            const double c = cost[ie];
-            const int dd = dmax[ie];
+            const int64_t ie = ent_i[e];
+            const double c = ent_c[e];
+            const int dd = ent_d[e];
             if (dd < d) continue;
             if (best < 0 || c < bc || (c == bc && (dd > bd || (dd == bd && ie < best)))) {
                 best = ie;
@@ -511,58 +649,59 @@ __global__ void finish_kernel(DevProblem P, const int64_t *surv, const double *c
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
                           ComposeResult **result_dev) {
+    (void)order_dev;
     Ws w = carve(P, n_surv, ws);
     *result_dev = w.res;
     const int64_t G = n_groups(P), nbk = n_buckets(P);
     const int D = levels(P);
     const int64_t rows = (int64_t)P.nb * (P.L + 1) * P.K;
-    (void)order_dev;
-    prep_kernel<<<dim3(1), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT, w.res);
+    prep_kernel<<<dim3(1), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT, w.EiT, w.res);
     fill<int32_t>(w.gcnt, G, 0, s);
-    fill<int32_t>(w.bcnt, nbk, 0, s);
+    fill<int32_t>(w.bcnt, nbk + 1, 0, s);
     fill<double>(w.Pst, P.nb, kInf, s);
     fill<double>(w.rootF, P.nb, kInf, s);
     fill<int32_t>(w.root_o, P.nb, -1, s);
     fill<int32_t>(w.root_d, P.nb, -1, s);
-    fill<double>(w.Wb[0], rows, kInf, s);
-    fill<double>(w.Wb[1], rows, kInf, s);
     if (n_surv > 0) {
         int64_t blocks = (n_surv + 255) / 256;
         if (blocks > 65536) blocks = 65536;
-        count_groups<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, dmax, w.pos, w.gcnt, w.res);
+        gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, cost, dmax, w.pos, w.rec_g,
+                                                                    w.rec_c, w.rec_d, w.gcnt, w.res);
         scan_i32(w.gcnt, G, w.tmp, s);
-        scatter_groups<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, dmax, w.pos, w.gcnt,
-                                                                     w.entries, w.res);
-        int64_t gblocks = (G + 255) / 256;
-        if (gblocks > 65536) gblocks = 65536;
-        group_events<false><<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(P, surv, cost, dmax, w.gcnt, w.entries,
-                                                                          w.bcnt, w.ev_cell, w.ev_val);
-        scan_i32(w.bcnt, nbk, w.tmp, s);
-        group_events<true><<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(P, surv, cost, dmax, w.gcnt, w.entries,
-                                                                         w.bcnt, w.ev_cell, w.ev_val);
+        scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n_surv, w.rec_g, w.rec_c, w.rec_d,
+                                                                     w.gcnt, w.ent_c, w.ent_d, w.ent_i);
+        const dim3 egrid((unsigned)P.L, (unsigned)P.nb);
+        group_events<false><<<egrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt, w.ev_cell,
+                                                       w.ev_val);
+        scan_i32(w.bcnt, nbk + 1, w.tmp, s);
+        group_events<true><<<egrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt, w.ev_cell,
+                                                      w.ev_val);
     } else {
         scan_i32(w.gcnt, G, w.tmp, s);  // all zeros: offsets stay zero
-        scan_i32(w.bcnt, nbk, w.tmp, s);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int threads = P.K <= 64 ? 64 : (P.K <= 128 ? 128 : (P.K <= 192 ? 192 : 256));
-    const dim3 grid((unsigned)P.L, (unsigned)P.nb);
+    const size_t tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
+    int64_t gblocks = (G + 255) / 256;
+    if (gblocks > 65536) gblocks = 65536;
     // phase 1: least bottleneck per b
-    fill<double>(w.T, G, kInf, s);
-    for (int d = 1; d <= D; ++d)
-        level_bottleneck<<<grid, dim3(threads), 0, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1],
-                                                        w.Wb[d & 1], w.EoT, w.Pst);
-    // phase 2: least fill at that bottleneck
-    fill<double>(w.T, G, kInf, s);
+    table_init<<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(G, w.gcnt, w.ent_c, w.T);
     fill<double>(w.Wb[0], rows, kInf, s);
     fill<double>(w.Wb[1], rows, kInf, s);
     for (int d = 1; d <= D; ++d)
-        level_fill<<<grid, dim3(threads), 0, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1],
-                                                  w.Wb[d & 1], w.EoT, w.Pst, w.argF, w.argG, w.rootF, w.root_o,
-                                                  w.root_d);
-    finish_kernel<<<dim3(1), dim3(64), 0, s>>>(P, surv, cost, dmax, w.gcnt, w.entries, w.order, w.EoT, w.Pst,
-                                                w.rootF, w.root_o, w.root_d, w.argF, w.argG, w.res);
+        level_bottleneck<<<dim3((unsigned)(P.L - d + 1), (unsigned)P.nb), dim3(threads), tri_lds, s>>>(
+            P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1], w.Wb[d & 1], w.EoT, w.EiT, w.Pst);
+    // phase 2: least fill at that bottleneck
+    table_init<<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(G, w.gcnt, w.ent_c, w.T);
+    fill<double>(w.Wb[0], rows, kInf, s);
+    fill<double>(w.Wb[1], rows, kInf, s);
+    for (int d = 1; d <= D; ++d)
+        level_fill<<<dim3((unsigned)(P.L - d + 1), (unsigned)P.nb), dim3(threads), tri_lds, s>>>(
+            P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1], w.Wb[d & 1], w.EoT, w.EiT, w.Pst, w.argF,
+            w.argG, w.rootF, w.root_o, w.root_d);
+    finish_kernel<<<dim3(1), dim3(64), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT, w.Pst, w.rootF,
+                                                w.root_o, w.root_d, w.argF, w.argG, w.res);
     return hipGetLastError();
 }
 

@@ -50,7 +50,14 @@ struct DevProblem {
     const int32_t *row_cfg;     // [n_rows] config id of each bitmap row
     const double *peak, *hbm, *intra;  // [K] island rates
     double eta, mem_frac;
+    int32_t n_ev;            // distinct inter-island bandwidth values (<= kMaxDistinctE), else 0
+    int32_t pad_;
+    const double *Ev;        // [n_ev] the distinct values, ascending
+    const uint16_t *Eidx;    // [K*K] index of E[a][b] in Ev
 };
+
+// Link times use one division per distinct bandwidth when there are few.
+constexpr int kMaxDistinctE = 256;
 
 // Slice index of [i, j): slices with first layer < i, then the offset of j.
 __host__ __device__ inline int64_t slice_of(int64_t L, int64_t i, int64_t j) {
