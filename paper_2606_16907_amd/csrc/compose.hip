@@ -383,17 +383,29 @@ __device__ inline Links stage_links(const DevProblem &P, int i, int bi, int top,
     return X;
 }
 
-// Phase 1: bottleneck values.  Block (i, b), thread o.
-__global__ __launch_bounds__(256) void level_bottleneck(DevProblem P, int d, const int32_t *bcnt,
-                                                        const int32_t *ev_cell, const double *ev_val, double *T,
-                                                        const double *Wprev, double *Wnext, const double *EoT,
-                                                        const uint8_t *EiT, double *Pst) {
+// Each cell (i, o) is served by kSplit threads: sub-thread k scans
+// j = i+1+k, i+1+k+kSplit, ... and o2 = o+1+k, o+1+k+kSplit, ..., and LDS
+// combines them.  A sub-thread may stop at its own first T not below its own
+// running best: everything it skips is no smaller than that best, which it
+// reached at a smaller j, so neither the minimum nor the least j attaining it
+// can be among the skipped ones.
+constexpr int kSplit = 4;
+
+__device__ inline int cell_pad(int K) { return K <= 64 ? 64 : (K <= 128 ? 128 : (K <= 192 ? 192 : 256)); }
+
+// Phase 1: bottleneck values.  Block (i, b), thread (sub, o).
+__global__ __launch_bounds__(1024) void level_bottleneck(DevProblem P, int d, const int32_t *bcnt,
+                                                         const int32_t *ev_cell, const double *ev_val, double *T,
+                                                         const double *Wprev, double *Wnext, const double *EoT,
+                                                         const uint8_t *EiT, double *Pst) {
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
+    __shared__ double part[kSplit][256];
     __shared__ double Vs[256];
     __shared__ double xs[kMaxDistinctE];
-    const int i = blockIdx.x, bi = blockIdx.y, o = threadIdx.x;
-    const int L = P.L, K = P.K;
+    const int i = blockIdx.x, bi = blockIdx.y;
+    const int L = P.L, K = P.K, KP = cell_pad(K);
+    const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
     const Links X = stage_links(P, i, bi, K - d, EiT, EoT, xs, tri_s);
     __syncthreads();
@@ -401,58 +413,73 @@ __global__ __launch_bounds__(256) void level_bottleneck(DevProblem P, int d, con
     double v = kInf;
     if (o < K && o <= K - d) {
         if (d == 1) {
-            v = T[(srow + (L - i - 1)) * K + o];
+            if (sub == 0) v = T[(srow + (L - i - 1)) * K + o];
         } else {
             const double *Wp = Wprev + (int64_t)bi * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
-            for (int j0 = i + 1; j0 <= jmax; j0 += 4) {
-                double t[4], w[4];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int j = j0 + k;
-                    t[k] = j <= jmax ? Tp[(int64_t)(j - i - 1) * K] : kInf;
-                    w[k] = j <= jmax ? Wp[(int64_t)j * K] : kInf;
-                }
-                bool stop = false;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    if (!stop && !(t[k] < v)) stop = true;  // T never decreases in j
-                    if (!stop) v = fmin(v, fmax(t[k], w[k]));
-                }
-                if (stop) break;
+            for (int j0 = i + 1 + sub; j0 <= jmax; j0 += 2 * kSplit) {
+                const int j1 = j0 + kSplit;
+                const double t0 = Tp[(int64_t)(j0 - i - 1) * K], w0 = Wp[(int64_t)j0 * K];
+                const double t1 = j1 <= jmax ? Tp[(int64_t)(j1 - i - 1) * K] : kInf;
+                const double w1 = j1 <= jmax ? Wp[(int64_t)j1 * K] : kInf;
+                if (!(t0 < v)) break;  // T never decreases in j
+                v = fmin(v, fmax(t0, w0));
+                if (!(t1 < v)) break;
+                v = fmin(v, fmax(t1, w1));
             }
         }
     }
-    Vs[o] = v;
+    part[sub][o] = v;
+    __syncthreads();
+    if (sub == 0) {
+        double m = part[0][o];
+#pragma unroll
+        for (int k = 1; k < kSplit; ++k) m = fmin(m, part[k][o]);
+        Vs[o] = m;
+    }
     __syncthreads();
     if (i == 0) {
-        if (o == 0) {
+        if (threadIdx.x == 0) {
             double m = kInf;
             for (int t = 0; t < K; ++t) m = fmin(m, Vs[t]);
             Pst[bi] = fmin(Pst[bi], m);
         }
         return;
     }
-    if (o < K) {
-        double w = kInf;
-        for (int o2 = o + 1; o2 <= K - d; ++o2) w = fmin(w, fmax(X(o, o2, K), Vs[o2]));
-        Wnext[((int64_t)bi * (L + 1) + i) * K + o] = w;
+    double w = kInf;
+    if (o < K)
+        for (int o2 = o + 1 + sub; o2 <= K - d; o2 += kSplit) w = fmin(w, fmax(X(o, o2, K), Vs[o2]));
+    part[sub][o] = w;
+    __syncthreads();
+    if (sub == 0 && o < K) {
+        double m = part[0][o];
+#pragma unroll
+        for (int k = 1; k < kSplit; ++k) m = fmin(m, part[k][o]);
+        Wnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
     }
 }
 
+// (value, index) pairs: the smaller value, ties to the smaller index.
+__device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
+    return v1 < v2 || (v1 == v2 && a1 < a2);
+}
+
 // Phase 2: fill values and argmins at the bottleneck P*.
-__global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell,
-                                                  const double *ev_val, double *T, const double *Gprev,
-                                                  double *Gnext, const double *EoT, const uint8_t *EiT,
-                                                  const double *Pst, uint16_t *argF, uint8_t *argG, double *rootF,
-                                                  int32_t *root_o, int32_t *root_d) {
+__global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell,
+                                                   const double *ev_val, double *T, const double *Gprev,
+                                                   double *Gnext, const double *EoT, const uint8_t *EiT,
+                                                   const double *Pst, uint16_t *argF, uint8_t *argG,
+                                                   double *rootF, int32_t *root_o, int32_t *root_d) {
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
+    __shared__ double part[kSplit][256];
+    __shared__ int32_t parg[kSplit][256];
     __shared__ double Fs[256];
     __shared__ double xs[kMaxDistinctE];
-    const int i = blockIdx.x, bi = blockIdx.y, o = threadIdx.x;
-    const int L = P.L, K = P.K;
+    const int i = blockIdx.x, bi = blockIdx.y;
+    const int L = P.L, K = P.K, KP = cell_pad(K);
+    const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     const double Ps = Pst[bi];
     if (!(Ps < kInf)) return;
     apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
@@ -463,44 +490,55 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
     int arg = 0xFFFF;
     if (o < K && o <= K - d) {
         if (d == 1) {
-            const double t = T[(srow + (L - i - 1)) * K + o];
-            if (t <= Ps) {
-                v = t;
-                arg = L;
+            if (sub == 0) {
+                const double t = T[(srow + (L - i - 1)) * K + o];
+                if (t <= Ps) {
+                    v = t;
+                    arg = L;
+                }
             }
         } else {
             const double *Gp = Gprev + (int64_t)bi * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
-            for (int j0 = i + 1; j0 <= jmax; j0 += 4) {
-                double t[4], g[4];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int j = j0 + k;
-                    t[k] = j <= jmax ? Tp[(int64_t)(j - i - 1) * K] : kInf;
-                    g[k] = j <= jmax ? Gp[(int64_t)j * K] : kInf;
+            for (int j0 = i + 1 + sub; j0 <= jmax; j0 += 2 * kSplit) {
+                const int j1 = j0 + kSplit;
+                const double t0 = Tp[(int64_t)(j0 - i - 1) * K], g0 = Gp[(int64_t)j0 * K];
+                const double t1 = j1 <= jmax ? Tp[(int64_t)(j1 - i - 1) * K] : kInf;
+                const double g1 = j1 <= jmax ? Gp[(int64_t)j1 * K] : kInf;
+                if (!(t0 <= Ps) || !(t0 < v)) break;  // T never decreases in j
+                const double c0 = t0 + g0;
+                if (c0 < v) {
+                    v = c0;
+                    arg = j0;
                 }
-                bool stop = false;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    if (!stop && (!(t[k] <= Ps) || !(t[k] < v))) stop = true;  // T never decreases in j
-                    if (!stop) {
-                        const double c = t[k] + g[k];
-                        if (c < v) {
-                            v = c;
-                            arg = j0 + k;
-                        }
-                    }
+                if (!(t1 <= Ps) || !(t1 < v)) break;
+                const double c1 = t1 + g1;
+                if (c1 < v) {
+                    v = c1;
+                    arg = j1;
                 }
-                if (stop) break;
             }
         }
     }
-    if (o < K) argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)arg;
-    Fs[o] = v;
+    part[sub][o] = v;
+    parg[sub][o] = arg;
+    __syncthreads();
+    if (sub == 0) {
+        double m = part[0][o];
+        int a = parg[0][o];
+#pragma unroll
+        for (int k = 1; k < kSplit; ++k)
+            if (lex_less(part[k][o], parg[k][o], m, a)) {
+                m = part[k][o];
+                a = parg[k][o];
+            }
+        Fs[o] = m;
+        if (o < K) argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)(m < kInf ? a : 0xFFFF);
+    }
     __syncthreads();
     if (i == 0) {
-        if (o == 0) {
+        if (threadIdx.x == 0) {
             double m = kInf;
             int mo = -1;
             for (int t = 0; t < K; ++t)
@@ -517,10 +555,10 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
         }
         return;
     }
-    if (o < K) {
-        double w = kInf;
-        int a = 0xFF;
-        for (int o2 = o + 1; o2 <= K - d; ++o2) {
+    double w = kInf;
+    int a = 0xFF;
+    if (o < K)
+        for (int o2 = o + 1 + sub; o2 <= K - d; o2 += kSplit) {
             const double x = X(o, o2, K);
             if (!(x <= Ps)) continue;
             const double c = x + Fs[o2];
@@ -529,8 +567,20 @@ __global__ __launch_bounds__(256) void level_fill(DevProblem P, int d, const int
                 a = o2;
             }
         }
-        Gnext[((int64_t)bi * (L + 1) + i) * K + o] = w;
-        argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)a;
+    part[sub][o] = w;
+    parg[sub][o] = a;
+    __syncthreads();
+    if (sub == 0 && o < K) {
+        double m = part[0][o];
+        int aa = parg[0][o];
+#pragma unroll
+        for (int k = 1; k < kSplit; ++k)
+            if (lex_less(part[k][o], parg[k][o], m, aa)) {
+                m = part[k][o];
+                aa = parg[k][o];
+            }
+        Gnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
+        argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)(m < kInf ? aa : 0xFF);
     }
 }
 
@@ -681,7 +731,7 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int threads = P.K <= 64 ? 64 : (P.K <= 128 ? 128 : (P.K <= 192 ? 192 : 256));
+    const int threads = kSplit * (P.K <= 64 ? 64 : (P.K <= 128 ? 128 : (P.K <= 192 ? 192 : 256)));
     const size_t tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
     int64_t gblocks = (G + 255) / 256;
     if (gblocks > 65536) gblocks = 65536;
