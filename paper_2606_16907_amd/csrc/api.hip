@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "tg_device.h"
+#include "tg_problem.h"
 
 namespace {
 
@@ -39,13 +40,6 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-struct tg_problem {
-    int device;
-    tg::DevProblem P;
-    void *dev_block;
-    std::vector<int64_t> bvals;
-    int64_t n_compat_cfg;
-};
 
 extern "C" {
 

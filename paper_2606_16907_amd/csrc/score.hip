@@ -4,9 +4,11 @@
 // Tab. 2 (profile() + parallelize()): a step-time cost per micro-batch and the
 // deepest 1F1B position the pair fits at (Sec. 5.2).  Candidates are
 // idx = g * NS + s (g: global config, s: slice).  A wave owns 64 consecutive
-// slices and walks a run of GC configs: the slice sums live in VGPRs for the
-// whole run, the config's coefficients arrive through scalar loads, and every
-// config writes one coalesced 512-byte row of costs and 64 bytes of depths.
+// slices and walks a run of 16 configs: the slice sums live in VGPRs for the
+// whole run, the run's coefficients are staged once in LDS, and every
+// config writes one coalesced 512-byte row of costs and 64 bytes of depths
+// with streaming (nontemporal) stores.  The kernel is bound by HBM writes
+// (9 bytes per candidate).
 #include "tg_device.h"
 
 #pragma clang fp contract(off)
@@ -71,37 +73,70 @@ hipError_t launch_coef(const DevProblem &P, Coef *coef, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // scoring
 // ---------------------------------------------------------------------------
-constexpr int kScoreWaves = 4;   // waves per block
-constexpr int kScoreConfigs = 32;  // configs per wave tile
+constexpr int kScoreWaves = 4;     // waves per block
+constexpr int kScoreConfigs = 16;  // configs per wave tile
 
 // Largest d in 1..K with state + min(d, m) * A1 <= H, or 0.  fits() is
-// monotone in d, so a first guess from (H - state) / A1 corrected by exact
-// predicate evaluations yields exactly the largest fitting depth.
+// monotone in d, so a first guess d0 from (H - state) / A1 (K once the
+// stash saturates at m micro-batches) is the answer exactly when d0 fits and
+// d0 + 1 does not; otherwise a short walk from d0 finds it.  Every decision
+// is an exact evaluation of fits(); the guess only picks where to look.
 __device__ inline int max_depth(double state, double A1, double H, double m_real, double guess_scale, int K) {
     auto fits = [&](int d) -> bool {
         const double inflight = fmin((double)d, m_real);
         return state + inflight * A1 <= H;
     };
-    if (fits(K)) return K;
-    // here fits(K) is false, so the answer is < K and (if >= 1) below m
     const double q = (H - state) * guess_scale;
-    int d = (q >= 1.0) ? (int)fmin(q, (double)(K - 1)) : 0;
+    const int d0 = (q >= m_real) ? K : (q >= 1.0 ? (int)fmin(q, (double)K) : 0);
+    const bool lo_ok = d0 == 0 || fits(d0);
+    const bool hi_ok = d0 == K || !fits(d0 + 1);
+    if (lo_ok && hi_ok) return d0;
+    int d = d0 > K - 1 ? K - 1 : d0;
+#pragma nounroll
     while (d > 0 && !fits(d)) --d;
-    while (fits(d + 1)) ++d;
+#pragma nounroll
+    while (d < K && fits(d + 1)) ++d;
     return d;
 }
+
+// Blocks are dispatched round-robin over the 8 XCDs.  Renumbering them so
+// that consecutive tiles run on the same XCD keeps every cache line of the
+// output (depth rows are not line-aligned) inside one L2, which merges the
+// partial lines before they reach HBM.
+constexpr int kXcds = 8;
+
+// The coefficients a wave needs for its run of configs, staged in LDS: one
+// coalesced load per lane at the start of the tile instead of scalar loads in
+// every iteration (the coefficient table falls out of L2 under the streaming
+// writes, and scalar misses would stall each iteration).
+struct StagedCoef {
+    double alpha, beta, gamma, dd, de, mud, mue, rho, H, m_real, inv_rho;
+};
 
 template <bool kDense>
 __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first, int64_t last, int64_t g_lo,
                                                     int64_t g_hi, int64_t n_stiles, int64_t n_tiles,
                                                     double *__restrict__ cost, uint8_t *__restrict__ dmax) {
-    const int64_t tile = (int64_t)blockIdx.x * kScoreWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    __shared__ StagedCoef cs[kScoreWaves][kScoreConfigs];
+    const int64_t per_xcd = gridDim.x / kXcds;
+    const int64_t blk = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t tile = blk * kScoreWaves + wv;
     if (tile >= n_tiles) return;
     const int64_t gt = tile / n_stiles;
     const int64_t st = tile - gt * n_stiles;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t s = st * kWave + lane;
     const bool sv = s < P.NS;
+    const int64_t g_beg = g_lo + gt * kScoreConfigs;
+    const int ng = (int)(min(g_beg + kScoreConfigs, g_hi + 1) - g_beg);
+    if (lane < ng) {
+        const Coef &c = P.coef[g_beg + lane];
+        cs[wv][lane] = StagedCoef{c.alpha, c.beta, c.gamma, c.dd, c.de, c.mud, c.mue, c.rho, c.H, c.m_real, c.inv_rho};
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
     // slice sums: exact int64 prefix differences, then one rounding to binary64
     double Fl = 0.0, Pd = 0.0, Pe = 0.0, Act = 0.0, Tb = 0.0, Ab = 0.0, inv_act = 0.0;
@@ -122,10 +157,8 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
     }
     const int K = P.K;
     const int64_t NS = P.NS;
-    const int64_t g_beg = g_lo + gt * kScoreConfigs;
-    const int64_t g_end = min(g_beg + kScoreConfigs, g_hi + 1);
-    for (int64_t g = g_beg; g < g_end; ++g) {
-        const Coef &c = P.coef[g];
+    for (int t = 0; t < ng; ++t) {
+        const StagedCoef &c = cs[wv][t];
         double v = c.alpha * Fl;
         v = v + c.beta * Tb;
         if (!kDense) v = v + c.gamma * Ab;
@@ -135,10 +168,11 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
         if (!kDense) state = state + c.mue * Pe;
         const double A1 = c.rho * Act;
         const int dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * inv_act, K);
-        const int64_t idx = g * NS + s;
+        const int64_t idx = (g_beg + t) * NS + s;
         if (sv && idx >= first && idx < last) {
-            cost[idx - first] = v;
-            dmax[idx - first] = (uint8_t)dm;
+            // streaming stores: the arrays are far larger than the caches
+            __builtin_nontemporal_store(v, cost + (idx - first));
+            __builtin_nontemporal_store((uint8_t)dm, dmax + (idx - first));
         }
     }
 }
@@ -151,7 +185,8 @@ hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, doubl
     const int64_t n_gtiles = (g_hi - g_lo + kScoreConfigs) / kScoreConfigs;
     const int64_t n_stiles = (P.NS + kWave - 1) / kWave;
     const int64_t n_tiles = n_gtiles * n_stiles;
-    const int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
+    int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
+    blocks = (blocks + kXcds - 1) / kXcds * kXcds;  // whole rounds over the XCDs
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     if (P.dense)
         score_kernel<true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi, n_stiles,

@@ -1,0 +1,14 @@
+// tg_problem.h -- host-side definition of the opaque tg_problem handle.
+#pragma once
+
+#include <vector>
+
+#include "tg_device.h"
+
+struct tg_problem {
+    int device;                  // device that was current at create
+    tg::DevProblem P;            // device tables (one allocation, dev_block)
+    void *dev_block;
+    std::vector<int64_t> bvals;  // compatible micro-batch sizes, ascending
+    int64_t n_compat_cfg;
+};
