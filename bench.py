@@ -30,7 +30,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 SCORE_BYTES_PER_CANDIDATE = 9  # 8-byte cost + 1-byte depth written; inputs stay in registers/L2
 METRIC = "slice/island pairs scored/sec; end-to-end plan-search seconds (1 GPU)"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_large_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_large_traffic.txt")
+SCORE_SOURCES = [os.path.join(ROOT, "paper_2606_16907_amd", "csrc", f) for f in ("score.hip", "tg_device.h")]
 
 WORKLOADS = {
     "large": "128-layer dense decoder (h 12288, FFN 49152 GeLU, 96 heads, s 8192, global batch "
@@ -52,9 +53,9 @@ def parse():
     ap.add_argument("--cpu-islands", type=int, default=24,
                     help="islands of the CPU-baseline sample (first islands of the workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
-    ap.add_argument("--score-only", type=int, default=0,
-                    help="after the timed steps, launch the score kernel this many more times "
-                         "(for profiler counter runs)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="before the steps, copy BYTES between two device buffers (a plain copy of "
+                         "known size that scales profiler byte counters)")
     return ap.parse_args()
 
 
@@ -84,6 +85,34 @@ def cpu_baseline(inst, n_islands):
             "compose_s": round(t3 - t2, 3), "candidates": o.N, "plan_status": st}
 
 
+def score_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in SCORE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, N):
+    """HBM bytes per score-kernel launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None
+    when it was taken on another workload or the kernel source has changed."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("workload") != workload or kv.get("candidates") != str(N):
+        return None
+    if kv.get("score_source_sha256") != score_source_digest():
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -97,6 +126,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     inst = load_instance(args.workload)
+    if args.copy_calibration > 0:
+        a = torch.ones(args.copy_calibration // 8, dtype=torch.float64, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     t_create = time.perf_counter()
     p = T.Problem(inst)
     torch.cuda.synchronize()
@@ -142,19 +177,11 @@ def main():
     score_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
     prune_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
     compose_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.steps)]
-    for _ in range(args.score_only):
-        p.tg_score_pairs(0, N, cost, dmax)
-    torch.cuda.synchronize()
 
     mean = lambda xs: sum(xs) / len(xs)
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as fh:
-            tr = json.load(fh)
-        if tr.get("workload") == args.workload and tr.get("N") == N:
-            traffic = tr.get("bytes_per_launch")
+    traffic = measured_traffic(args.workload, N)
     out = {
         "metric": METRIC,
         "value": N * args.steps / elapsed,
