@@ -10,7 +10,10 @@
 //
 // Frontier: a wave owns 64 consecutive slices of one (island, b) group list;
 // every lane walks the same members (a scalar loop), reading one coalesced
-// 512-byte row of costs and 64 bytes of depths per member.  Survivors are
+// 512-byte row of costs and 64 bytes of depths per member, eight members in
+// flight.  The first pass also finds the group's largest d_max, so a lane
+// stops as soon as its rep reaches it instead of spending a pass to find
+// nothing deeper.  Survivors are
 // recorded in an LDS bit mask per member (lane bit = slice) and written as
 // whole 64-bit words of a bitmap with one row per compatible config.
 // Compaction: popcount per tile, scan of tile counts, then each thread writes
@@ -48,29 +51,43 @@ __global__ __launch_bounds__(256) void frontier_kernel(DevProblem P, const doubl
         const int64_t NS = P.NS;
         const int K = P.K;
         bool live = s < NS;
-        int prev = 0;  // d_max of the previous rep of this lane's group
+        int prev = 0;   // d_max of the previous rep of this lane's group
+        int top = -1;   // the group's largest d_max, known after the first pass
         while (__ballot(live) != 0) {
             double bc = kInf;
-            int bd = 0, bm = -1;
-            for (int m = 0; m < nm; ++m) {
-                const int64_t g = P.kb_members[m0 + m];
-                if (live) {
-                    const int64_t idx = g * NS + s;
-                    const double c = cost[idx];
-                    const int d = dmax[idx];
-                    // members come in ascending idx, so equal (cost, d_max) keeps the earlier one
-                    if (d > prev && (c < bc || (c == bc && d > bd))) {
-                        bc = c;
-                        bd = d;
-                        bm = m;
+            int bd = 0, bm = -1, mx = 0;
+            // members in batches of eight loads in flight; they come in ascending
+            // idx, so equal (cost, d_max) keeps the earlier one
+            for (int mb = 0; mb < nm; mb += 8) {
+                double c[8];
+                int d[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    c[u] = kInf;
+                    d[u] = 0;
+                    if (mb + u < nm && live) {
+                        const int64_t idx = (int64_t)P.kb_members[m0 + mb + u] * NS + s;
+                        c[u] = cost[idx];
+                        d[u] = dmax[idx];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    mx = max(mx, d[u]);
+                    if (d[u] > prev && (c[u] < bc || (c[u] == bc && d[u] > bd))) {
+                        bc = c[u];
+                        bd = d[u];
+                        bm = mb + u;
                     }
                 }
             }
+            if (top < 0) top = mx;
             if (live) {
                 if (bm >= 0) {
                     atomicOr((unsigned long long *)&mask[bm], 1ull << lane);
                     prev = bd;
-                    if (prev >= K) live = false;
+                    // nothing reaches deeper than the group's largest d_max
+                    if (prev >= K || prev >= top) live = false;
                 } else {
                     live = false;
                 }
