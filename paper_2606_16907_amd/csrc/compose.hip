@@ -273,6 +273,8 @@ __global__ __launch_bounds__(256) void table_init(int64_t n_groups, const int32_
 // per (group, level).  Block (i, b) owns the groups of the slices starting at
 // layer i, and with them every bucket (level, b, i): counts and slots come
 // from LDS, with no global atomics.
+constexpr int kGroupRegs = 8;
+
 template <bool kEmit>
 __global__ __launch_bounds__(256) void group_events(DevProblem P, const int32_t *__restrict__ gcnt,
                                                     const double *__restrict__ ent_c,
@@ -302,19 +304,45 @@ __global__ __launch_bounds__(256) void group_events(DevProblem P, const int32_t 
             }
         };
         int M = 0;
-        for (int32_t e = st; e < en; ++e) {
-            const double ce = ent_c[e];
-            const int de = ent_d[e];
-            const int64_t ie = ent_i[e];
-            M = max(M, de);
-            int De = 0;
-            for (int32_t q = st; q < en; ++q) {
-                const double cq = ent_c[q];
-                const int dq = ent_d[q];
-                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
-                if (less) De = max(De, dq);
+        if (en - st <= kGroupRegs) {
+            // small group (the usual staircase): entries in registers, compared there
+            double c[kGroupRegs];
+            int d[kGroupRegs];
+            int64_t id[kGroupRegs];
+            const int n = en - st;
+#pragma unroll
+            for (int e = 0; e < kGroupRegs; ++e) {
+                c[e] = e < n ? ent_c[st + e] : kInf;
+                d[e] = e < n ? (int)ent_d[st + e] : 0;
+                id[e] = e < n ? ent_i[st + e] : 0;
             }
-            if (De >= 1 && De < de && De + 1 <= D) emit(De + 1, ce);
+#pragma unroll
+            for (int e = 0; e < kGroupRegs; ++e) {
+                if (e >= n) break;
+                M = max(M, d[e]);
+                int De = 0;
+#pragma unroll
+                for (int q = 0; q < kGroupRegs; ++q) {
+                    const bool less = q < n && (c[q] < c[e] || (c[q] == c[e] && (d[q] > d[e] || (d[q] == d[e] && id[q] < id[e]))));
+                    if (less) De = max(De, d[q]);
+                }
+                if (De >= 1 && De < d[e] && De + 1 <= D) emit(De + 1, c[e]);
+            }
+        } else {
+            for (int32_t e = st; e < en; ++e) {
+                const double ce = ent_c[e];
+                const int de = ent_d[e];
+                const int64_t ie = ent_i[e];
+                M = max(M, de);
+                int De = 0;
+                for (int32_t q = st; q < en; ++q) {
+                    const double cq = ent_c[q];
+                    const int dq = ent_d[q];
+                    const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
+                    if (less) De = max(De, dq);
+                }
+                if (De >= 1 && De < de && De + 1 <= D) emit(De + 1, ce);
+            }
         }
         if (M + 1 <= D) emit(M + 1, kInf);
     }
