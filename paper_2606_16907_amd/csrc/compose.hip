@@ -189,6 +189,17 @@ size_t compose_order_offset(const DevProblem &P, int64_t n_surv) {
     return align256(sizeof(ComposeResult));
 }
 
+// Groups (slice, island position, b) are numbered position-major, then b,
+// then slice: the candidate list runs through each config's slices in
+// ascending order, so building the groups touches consecutive counters.  The
+// stage table keeps the DP's layout [b][slice][position].
+__host__ __device__ inline int64_t group_id(const DevProblem &P, int64_t o, int64_t bi, int64_t s) {
+    return (o * P.nb + bi) * P.NS + s;
+}
+__host__ __device__ inline int64_t cell_id(const DevProblem &P, int64_t bi, int64_t s, int64_t o) {
+    return (bi * P.NS + s) * P.K + o;
+}
+
 // Index of the pair of positions (o, o2), o < o2, in a packed triangle.
 __host__ __device__ inline int tri(int o, int o2) { return o2 * (o2 - 1) / 2 + o; }
 
@@ -230,7 +241,7 @@ __global__ __launch_bounds__(256) void gather_kernel(DevProblem P, const int64_t
             } else {
                 const uint8_t d = dmax[idx];
                 if (d > 0) {
-                    G = (int32_t)(((int64_t)c.b_idx * P.NS + s) * P.K + pos[c.k]);
+                    G = (int32_t)group_id(P, pos[c.k], c.b_idx, s);
                     rec_c[r] = cost[idx];
                     rec_d[r] = d;
                     atomicAdd(&gcnt[G], 1);
@@ -254,15 +265,34 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int64_t *surv, int64
     }
 }
 
-// Stage table at depth 1: the least cost of each group.
-__global__ __launch_bounds__(256) void table_init(int64_t n_groups, const int32_t *__restrict__ gcnt,
+// Stage table at depth 1: the least cost of each group.  A block transposes a
+// tile of 64 slices x 32 positions of one b through LDS, so it reads the group
+// offsets along slices and writes the table along positions.
+constexpr int kTileS = 64, kTileO = 32;
+
+__global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *__restrict__ gcnt,
                                                   const double *__restrict__ ent_c, double *__restrict__ T) {
-    for (int64_t G = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; G < n_groups;
-         G += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+    __shared__ double tile[kTileO][kTileS + 1];
+    const int64_t s0 = (int64_t)blockIdx.x * kTileS;
+    const int o0 = blockIdx.y * kTileO, bi = blockIdx.z;
+    for (int t = threadIdx.x; t < kTileS * kTileO; t += blockDim.x) {
+        const int sl = t % kTileS, ol = t / kTileS;
+        const int64_t s = s0 + sl;
+        const int o = o0 + ol;
         double v = kInf;
-        for (int32_t e = st; e < en; ++e) v = fmin(v, ent_c[e]);
-        T[G] = v;
+        if (s < P.NS && o < P.K) {
+            const int64_t G = group_id(P, o, bi, s);
+            const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+            for (int32_t e = st; e < en; ++e) v = fmin(v, ent_c[e]);
+        }
+        tile[ol][sl] = v;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTileS * kTileO; t += blockDim.x) {
+        const int ol = t % kTileO, sl = t / kTileO;
+        const int64_t s = s0 + sl;
+        const int o = o0 + ol;
+        if (s < P.NS && o < P.K) T[cell_id(P, bi, s, o)] = tile[ol][sl];
     }
 }
 
@@ -288,16 +318,19 @@ __global__ __launch_bounds__(256) void group_events(DevProblem P, const int32_t 
     for (int lev = threadIdx.x; lev < D; lev += blockDim.x)
         hist[lev] = kEmit ? bcnt[((int64_t)lev * P.nb + bi) * L + i] : 0;
     __syncthreads();
-    const int64_t G0 = ((int64_t)bi * P.NS + slice_of(L, i, i + 1)) * K;
-    const int64_t ncell = (int64_t)(L - i) * K;
+    const int64_t s0 = slice_of(L, i, i + 1);
+    const int64_t n_sl = L - i;
+    const int64_t ncell = n_sl * K;
     for (int64_t t = threadIdx.x; t < ncell; t += blockDim.x) {
-        const int64_t G = G0 + t;
+        const int64_t o = t / n_sl, s = s0 + (t - o * n_sl);
+        const int64_t G = group_id(P, o, bi, s);
         const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
         if (st == en) continue;
+        const int64_t cell = cell_id(P, bi, s, o);
         auto emit = [&](int level, double v) {
             if (kEmit) {
                 const int32_t slot = atomicAdd(&hist[level - 1], 1);
-                ev_cell[slot] = (int32_t)G;
+                ev_cell[slot] = (int32_t)cell;
                 ev_val[slot] = v;
             } else {
                 atomicAdd(&hist[level - 1], 1);
@@ -670,7 +703,7 @@ __global__ void finish_kernel(DevProblem P, const int32_t *gcnt, const double *e
             }
         }
         const int64_t s = slice_of(L, i, j);
-        const int64_t G = ((int64_t)bb * P.NS + s) * K + o;
+        const int64_t G = group_id(P, o, bb, s);
         const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
         int64_t best = -1;
         double bc = kInf;
@@ -761,17 +794,17 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     if (e != hipSuccess) return e;
     const int threads = kSplit * (P.K <= 64 ? 64 : (P.K <= 128 ? 128 : (P.K <= 192 ? 192 : 256)));
     const size_t tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
-    int64_t gblocks = (G + 255) / 256;
-    if (gblocks > 65536) gblocks = 65536;
+    const dim3 tgrid((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
+                     (unsigned)P.nb);
     // phase 1: least bottleneck per b
-    table_init<<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(G, w.gcnt, w.ent_c, w.T);
+    table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.T);
     fill<double>(w.Wb[0], rows, kInf, s);
     fill<double>(w.Wb[1], rows, kInf, s);
     for (int d = 1; d <= D; ++d)
         level_bottleneck<<<dim3((unsigned)(P.L - d + 1), (unsigned)P.nb), dim3(threads), tri_lds, s>>>(
             P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1], w.Wb[d & 1], w.EoT, w.EiT, w.Pst);
     // phase 2: least fill at that bottleneck
-    table_init<<<dim3((unsigned)gblocks), dim3(256), 0, s>>>(G, w.gcnt, w.ent_c, w.T);
+    table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.T);
     fill<double>(w.Wb[0], rows, kInf, s);
     fill<double>(w.Wb[1], rows, kInf, s);
     for (int d = 1; d <= D; ++d)
