@@ -25,6 +25,8 @@
 // improve it.  This holds whenever the candidate list contains the surviving
 // set, since then T_d equals the least cost over all group members.
 #include <algorithm>
+#include <climits>
+#include <type_traits>
 
 #include "tg_device.h"
 
@@ -45,6 +47,12 @@ template <typename T>
 __global__ __launch_bounds__(256) void fill_kernel(T *a, int64_t n, T v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         a[i] = v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void copy_kernel(const T *a, T *b, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) b[i] = a[i];
 }
 
 template <typename T>
@@ -125,6 +133,8 @@ struct Ws {
     int32_t *ev_cell;  // [2n]
     double *ev_val;    // [2n]
     double *T;         // [n_groups] current stage table, layout [b][s][o]
+    double *T1;        // [nb][L][K] depth-1 table of the slices (i, L)
+    int32_t *bcur;     // [n_buckets + 1] per-bucket write cursors
     double *Wb[2];     // [nb][L+1][K] continuation rows, double-buffered by level
     uint16_t *argF;    // [D][nb][L][K]
     uint8_t *argG;     // [D][nb][L+1][K]
@@ -169,6 +179,8 @@ static Ws carve(const DevProblem &P, int64_t n, void *base) {
     w.ev_cell = (int32_t *)take(sizeof(int32_t) * 2 * n);
     w.ev_val = (double *)take(sizeof(double) * 2 * n);
     w.T = (double *)take(sizeof(double) * G);
+    w.T1 = (double *)take(sizeof(double) * P.nb * P.L * P.K);
+    w.bcur = (int32_t *)take(sizeof(int32_t) * (nbk + 1));
     w.Wb[0] = (double *)take(sizeof(double) * rows);
     w.Wb[1] = (double *)take(sizeof(double) * rows);
     w.argF = (uint16_t *)take(sizeof(uint16_t) * D * P.nb * P.L * P.K);
@@ -203,17 +215,18 @@ __host__ __device__ inline int64_t cell_id(const DevProblem &P, int64_t bi, int6
 // Index of the pair of positions (o, o2), o < o2, in a packed triangle.
 __host__ __device__ inline int tri(int o, int o2) { return o2 * (o2 - 1) / 2 + o; }
 
-__global__ void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, double *EoT, uint8_t *EiT,
-                            ComposeResult *res) {
+__global__ __launch_bounds__(256) void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, double *EoT,
+                                                   uint8_t *EiT, ComposeResult *res) {
     const int K = P.K;
-    for (int t = threadIdx.x; t < K; t += blockDim.x) pos[order[t]] = t;
-    for (int t = threadIdx.x; t < K * K; t += blockDim.x) {
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < K) pos[order[t]] = t;
+    if (t < K * K) {
         const int o2 = t / K, o = t - o2 * K;
         const int64_t e = (int64_t)order[o] * K + order[o2];
         EoT[t] = P.E[e];
         if (o < o2) EiT[tri(o, o2)] = P.n_ev ? (uint8_t)P.Eidx[e] : 0;
     }
-    if (threadIdx.x == 0) {
+    if (t == 0) {
         res->err = 0;
         res->status = TG_ENOPLAN;
     }
@@ -265,13 +278,16 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int64_t *surv, int64
     }
 }
 
-// Stage table at depth 1: the least cost of each group.  A block transposes a
-// tile of 64 slices x 32 positions of one b through LDS, so it reads the group
+// Starting tables.  Depth 1 is read only for the slices (i, L) (a single
+// stage covers the rest of the model), so those values go to a small table
+// T1[b][i][o]; the full table starts at depth 2.  A block transposes a tile
+// of 64 slices x 32 positions of one b through LDS, so it reads the group
 // offsets along slices and writes the table along positions.
 constexpr int kTileS = 64, kTileO = 32;
 
 __global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *__restrict__ gcnt,
-                                                  const double *__restrict__ ent_c, double *__restrict__ T) {
+                                                  const double *__restrict__ ent_c, const uint8_t *__restrict__ ent_d,
+                                                  double *__restrict__ T, double *__restrict__ T1) {
     __shared__ double tile[kTileO][kTileS + 1];
     const int64_t s0 = (int64_t)blockIdx.x * kTileS;
     const int o0 = blockIdx.y * kTileO, bi = blockIdx.z;
@@ -279,13 +295,20 @@ __global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *_
         const int sl = t % kTileS, ol = t / kTileS;
         const int64_t s = s0 + sl;
         const int o = o0 + ol;
-        double v = kInf;
+        double v2 = kInf;
         if (s < P.NS && o < P.K) {
             const int64_t G = group_id(P, o, bi, s);
             const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
-            for (int32_t e = st; e < en; ++e) v = fmin(v, ent_c[e]);
+            double v1 = kInf;
+            for (int32_t e = st; e < en; ++e) {
+                const double c = ent_c[e];
+                v1 = fmin(v1, c);
+                if (ent_d[e] >= 2) v2 = fmin(v2, c);
+            }
+            const uint32_t ij = P.sij[s];
+            if ((int)(ij >> 16) == P.L) T1[((int64_t)bi * P.L + (ij & 0xFFFFu)) * P.K + o] = v1;
         }
-        tile[ol][sl] = v;
+        tile[ol][sl] = v2;
     }
     __syncthreads();
     for (int t = threadIdx.x; t < kTileS * kTileO; t += blockDim.x) {
@@ -298,111 +321,183 @@ __global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *_
 
 // Per group: entry e is the least fitting candidate at depths (D_e, d_e],
 // D_e = the largest d_max among entries with a smaller key; it sets T at
-// level D_e + 1 (level 1 is written by table_init).  After the group's
-// largest d_max M nothing fits: T = +inf from level M + 1.  At most one event
-// per (group, level).  Block (i, b) owns the groups of the slices starting at
-// layer i, and with them every bucket (level, b, i): counts and slots come
-// from LDS, with no global atomics.
+// level D_e + 1.  After the group's largest d_max M nothing fits: T = +inf
+// from level M + 1.  At most one change per (group, level).  Levels 1 and 2
+// come from table_init, so only changes at levels >= 3 become events.
 constexpr int kGroupRegs = 8;
 
+template <typename Emit>
+__device__ inline void cell_events(const int32_t *__restrict__ gcnt, const double *__restrict__ ent_c,
+                                   const uint8_t *__restrict__ ent_d, const int64_t *__restrict__ ent_i, int64_t G,
+                                   int D, Emit emit) {
+    const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+    if (st == en) return;
+    int M = 0;
+    if (en - st <= kGroupRegs) {
+        // small group (the usual staircase): entries in registers, compared there
+        double c[kGroupRegs];
+        int d[kGroupRegs];
+        int64_t id[kGroupRegs];
+        const int n = en - st;
+#pragma unroll
+        for (int e = 0; e < kGroupRegs; ++e) {
+            c[e] = e < n ? ent_c[st + e] : kInf;
+            d[e] = e < n ? (int)ent_d[st + e] : 0;
+            id[e] = e < n ? ent_i[st + e] : 0;
+        }
+#pragma unroll
+        for (int e = 0; e < kGroupRegs; ++e) {
+            if (e >= n) break;
+            M = max(M, d[e]);
+            int De = 0;
+#pragma unroll
+            for (int q = 0; q < kGroupRegs; ++q) {
+                const bool less =
+                    q < n && (c[q] < c[e] || (c[q] == c[e] && (d[q] > d[e] || (d[q] == d[e] && id[q] < id[e]))));
+                if (less) De = max(De, d[q]);
+            }
+            if (De >= 2 && De < d[e] && De + 1 <= D) emit(De + 1, c[e]);
+        }
+    } else {
+        for (int32_t e = st; e < en; ++e) {
+            const double ce = ent_c[e];
+            const int de = ent_d[e];
+            const int64_t ie = ent_i[e];
+            M = max(M, de);
+            int De = 0;
+            for (int32_t q = st; q < en; ++q) {
+                const double cq = ent_c[q];
+                const int dq = ent_d[q];
+                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
+                if (less) De = max(De, dq);
+            }
+            if (De >= 2 && De < de && De + 1 <= D) emit(De + 1, ce);
+        }
+    }
+    if (M >= 2 && M + 1 <= D) emit(M + 1, kInf);
+}
+
+// Events are bucketed by (level, b, first layer i).  A row's cells (slices
+// starting at i, times positions) are split over `nch` blocks of at most
+// kEventCells cells; a block counts its events per level in LDS.  The count
+// pass adds the block's counts to the buckets; the emit pass recounts,
+// reserves its ranges from per-bucket cursors and writes.  The order of
+// events inside a bucket does not matter: they touch distinct cells.
+constexpr int kEventCells = 1024;
+
 template <bool kEmit>
-__global__ __launch_bounds__(256) void group_events(DevProblem P, const int32_t *__restrict__ gcnt,
+__global__ __launch_bounds__(256) void group_events(DevProblem P, int nch, const int32_t *__restrict__ gcnt,
                                                     const double *__restrict__ ent_c,
                                                     const uint8_t *__restrict__ ent_d,
                                                     const int64_t *__restrict__ ent_i, int32_t *bcnt,
                                                     int32_t *__restrict__ ev_cell, double *__restrict__ ev_val) {
     __shared__ int32_t hist[256];
-    const int i = blockIdx.x, bi = blockIdx.y;
+    __shared__ int32_t base[256];
+    const int i = blockIdx.x / nch, ch = blockIdx.x % nch, bi = blockIdx.y;
     const int L = P.L, K = P.K;
     const int D = K < L ? K : L;
-    for (int lev = threadIdx.x; lev < D; lev += blockDim.x)
-        hist[lev] = kEmit ? bcnt[((int64_t)lev * P.nb + bi) * L + i] : 0;
-    __syncthreads();
     const int64_t s0 = slice_of(L, i, i + 1);
     const int64_t n_sl = L - i;
     const int64_t ncell = n_sl * K;
-    for (int64_t t = threadIdx.x; t < ncell; t += blockDim.x) {
+    const int64_t per = (ncell + nch - 1) / nch;
+    const int64_t c0 = (int64_t)ch * per, c1 = min(ncell, c0 + per);
+    if (c0 >= c1) return;
+    for (int lev = threadIdx.x; lev < D; lev += blockDim.x) hist[lev] = 0;
+    __syncthreads();
+    auto bucket = [&](int lev) { return ((int64_t)lev * P.nb + bi) * L + i; };  // lev = level - 1
+    for (int64_t t = c0 + threadIdx.x; t < c1; t += blockDim.x) {
         const int64_t o = t / n_sl, s = s0 + (t - o * n_sl);
-        const int64_t G = group_id(P, o, bi, s);
-        const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
-        if (st == en) continue;
-        const int64_t cell = cell_id(P, bi, s, o);
-        auto emit = [&](int level, double v) {
-            if (kEmit) {
-                const int32_t slot = atomicAdd(&hist[level - 1], 1);
-                ev_cell[slot] = (int32_t)cell;
-                ev_val[slot] = v;
-            } else {
-                atomicAdd(&hist[level - 1], 1);
-            }
-        };
-        int M = 0;
-        if (en - st <= kGroupRegs) {
-            // small group (the usual staircase): entries in registers, compared there
-            double c[kGroupRegs];
-            int d[kGroupRegs];
-            int64_t id[kGroupRegs];
-            const int n = en - st;
-#pragma unroll
-            for (int e = 0; e < kGroupRegs; ++e) {
-                c[e] = e < n ? ent_c[st + e] : kInf;
-                d[e] = e < n ? (int)ent_d[st + e] : 0;
-                id[e] = e < n ? ent_i[st + e] : 0;
-            }
-#pragma unroll
-            for (int e = 0; e < kGroupRegs; ++e) {
-                if (e >= n) break;
-                M = max(M, d[e]);
-                int De = 0;
-#pragma unroll
-                for (int q = 0; q < kGroupRegs; ++q) {
-                    const bool less = q < n && (c[q] < c[e] || (c[q] == c[e] && (d[q] > d[e] || (d[q] == d[e] && id[q] < id[e]))));
-                    if (less) De = max(De, d[q]);
-                }
-                if (De >= 1 && De < d[e] && De + 1 <= D) emit(De + 1, c[e]);
-            }
-        } else {
-            for (int32_t e = st; e < en; ++e) {
-                const double ce = ent_c[e];
-                const int de = ent_d[e];
-                const int64_t ie = ent_i[e];
-                M = max(M, de);
-                int De = 0;
-                for (int32_t q = st; q < en; ++q) {
-                    const double cq = ent_c[q];
-                    const int dq = ent_d[q];
-                    const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
-                    if (less) De = max(De, dq);
-                }
-                if (De >= 1 && De < de && De + 1 <= D) emit(De + 1, ce);
-            }
-        }
-        if (M + 1 <= D) emit(M + 1, kInf);
+        cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s), D,
+                    [&](int level, double) { atomicAdd(&hist[level - 1], 1); });
     }
+    __syncthreads();
     if (!kEmit) {
-        __syncthreads();
-        for (int lev = threadIdx.x; lev < D; lev += blockDim.x) bcnt[((int64_t)lev * P.nb + bi) * L + i] = hist[lev];
+        for (int lev = threadIdx.x; lev < D; lev += blockDim.x)
+            if (hist[lev]) atomicAdd(&bcnt[bucket(lev)], hist[lev]);
+        return;
+    }
+    for (int lev = threadIdx.x; lev < D; lev += blockDim.x) {
+        base[lev] = hist[lev] ? atomicAdd(&bcnt[bucket(lev)], hist[lev]) : 0;
+        hist[lev] = 0;
+    }
+    __syncthreads();
+    for (int64_t t = c0 + threadIdx.x; t < c1; t += blockDim.x) {
+        const int64_t o = t / n_sl, s = s0 + (t - o * n_sl);
+        const int64_t cell = cell_id(P, bi, s, o);
+        cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s), D, [&](int level, double v) {
+            const int32_t slot = base[level - 1] + atomicAdd(&hist[level - 1], 1);
+            ev_cell[slot] = (int32_t)cell;
+            ev_val[slot] = v;
+        });
     }
 }
 
 // ---------------------------------------------------------------------------
 // dynamic program, one launch per level
 // ---------------------------------------------------------------------------
-__device__ inline void apply_events(const int32_t *__restrict__ bcnt, const int32_t *__restrict__ ev_cell,
-                                    const double *__restrict__ ev_val, double *__restrict__ T, int64_t bucket) {
-    const int32_t st = bcnt[bucket], en = bcnt[bucket + 1];
-    const int step = blockDim.x;
-    for (int32_t base = st + threadIdx.x; base < en; base += 4 * step) {
-        int32_t c[4];
-        double v[4];
+// Block (i, b) owns row i of one level for every position o; each cell (i, o)
+// is served by SPLIT threads (sub-threads 0..SPLIT-1), and LDS combines them.
+// The level kernels are latency chains, so each block starts its row's table
+// and continuation reads and its link loads at once.  It also applies the next
+// level's table changes for its row (bucket (d+1, b, i)): they touch only
+// slices starting at layer i, which no other block reads, so they are loaded
+// once the block's own table reads are done and written at its end.
+constexpr int kEvRegs = 2;
+constexpr int kEvBatch = 8;
+constexpr int kAhead = 4;  // scan steps read at a time
+
+// Waves per SIMD the level kernels are compiled for: the most a SIMD holds (8,
+// so at most 64 VGPRs) rounded down to whole blocks.
+constexpr int level_waves(int threads) {
+    const int per_simd = (threads / kWave + 3) / 4;
+    return (8 / per_simd) * per_simd;
+}
+
+struct RowEvents {
+    int32_t st, en;
+    int32_t c[kEvRegs];
+    double v[kEvRegs];
+};
+
+__device__ inline void event_bounds(RowEvents &R, const DevProblem &P, int d, int bi, int i, const int32_t *bcnt) {
+    const int D = P.K < P.L ? P.K : P.L;
+    R.st = 0;
+    R.en = 0;
+    if (d < D) {
+        const int64_t bucket = ((int64_t)d * P.nb + bi) * P.L + i;
+        R.st = bcnt[bucket];
+        R.en = bcnt[bucket + 1];
+    }
+}
+
+__device__ inline void load_events(RowEvents &R, const int32_t *__restrict__ ev_cell,
+                                   const double *__restrict__ ev_val) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < kEvRegs; ++k) {
+        const int32_t e = R.st + (int32_t)threadIdx.x + k * (int32_t)blockDim.x;
+        R.c[k] = e < R.en ? ev_cell[e] : -1;
+        R.v[k] = e < R.en ? ev_val[e] : 0.0;
+    }
+}
+
+__device__ inline void store_events(const RowEvents &R, const int32_t *__restrict__ ev_cell,
+                                    const double *__restrict__ ev_val, double *__restrict__ T) {
+#pragma unroll
+    for (int k = 0; k < kEvRegs; ++k)
+        if (R.c[k] >= 0) T[R.c[k]] = R.v[k];
+    // large buckets (the first levels): the rest in batches of loads in flight
+    const int32_t step = (int32_t)blockDim.x;
+    for (int32_t base = R.st + (int32_t)threadIdx.x + kEvRegs * step; base < R.en; base += kEvBatch * step) {
+        int32_t c[kEvBatch];
+        double v[kEvBatch];
+#pragma unroll
+        for (int k = 0; k < kEvBatch; ++k) {
             const int32_t e = base + k * step;
-            c[k] = e < en ? ev_cell[e] : -1;
-            v[k] = e < en ? ev_val[e] : 0.0;
+            c[k] = e < R.en ? ev_cell[e] : -1;
+            v[k] = e < R.en ? ev_val[e] : 0.0;
         }
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < kEvBatch; ++k)
             if (c[k] >= 0) T[c[k]] = v[k];
     }
 }
@@ -410,94 +505,216 @@ __device__ inline void apply_events(const int32_t *__restrict__ bcnt, const int3
 // Link times of the boundary after layer i-1 for this block's b.  With few
 // distinct bandwidths (the usual case) the block divides once per distinct
 // value and keeps the per-pair index triangle in LDS; otherwise it divides
-// per pair.
+// per pair.  The link data is loaded into registers first and written to LDS
+// after the row scan, so the loads overlap it.
 struct Links {
     const double *xs;      // LDS [n_ev]
     const uint8_t *tri_s;  // LDS triangle of indices
     const double *EoT;     // global, used without a table
     double num;
     bool table;
-    __device__ inline double operator()(int o, int o2, int K) const {
-        if (table) return xs[tri_s[tri(o, o2)]];
+    __device__ inline double tab(int o, int o2) const { return xs[tri_s[tri(o, o2)]]; }
+    __device__ inline double direct(int o, int o2, int K) const {
         const double E = EoT[(int64_t)o2 * K + o];
         return E == 0.0 ? kInf : num / E;
     }
 };
 
-// Fills the block's LDS link tables for positions o < o2 <= top.
-__device__ inline Links stage_links(const DevProblem &P, int i, int bi, int top, const uint8_t *EiT,
-                                    const double *EoT, double *xs, uint8_t *tri_s) {
+template <int THREADS, int KP>
+struct LinkRegs {
+    // triangle words (rows o2 <= KP-1) and distinct bandwidths per thread
+    static constexpr int kWords = (((KP - 1) * KP / 2 + 3) / 4 + THREADS - 1) / THREADS;
+    static constexpr int kE = (kMaxDistinctE + THREADS - 1) / THREADS;
+    double E[kE];
+    uint32_t w[kWords];
+};
+
+template <int THREADS, int KP>
+__device__ inline Links load_links(LinkRegs<THREADS, KP> &R, const DevProblem &P, int i, int bi, int top,
+                                   const uint8_t *EiT, const double *EoT, double *xs, uint8_t *tri_s) {
     Links X{xs, tri_s, EoT, 0.0, P.n_ev > 0};
     if (i == 0) return X;
     X.num = (2.0 * (double)P.bvals[bi]) * (double)P.outact[i - 1];
     if (X.table) {
-        for (int u = threadIdx.x; u < P.n_ev; u += blockDim.x) {
-            const double E = P.Ev[u];
-            xs[u] = E == 0.0 ? kInf : X.num / E;
+#pragma unroll
+        for (int k = 0; k < LinkRegs<THREADS, KP>::kE; ++k) {
+            const int u = (int)threadIdx.x + k * THREADS;
+            R.E[k] = u < P.n_ev ? P.Ev[u] : 0.0;
         }
-        const int nbytes = top * (top + 1) / 2;  // rows o2 <= top
-        const int nwords = (nbytes + 3) / 4;
+        const int nwords = (top * (top + 1) / 2 + 3) / 4;  // rows o2 <= top
         const uint32_t *src = (const uint32_t *)EiT;
-        uint32_t *dst = (uint32_t *)tri_s;
-        for (int t = threadIdx.x; t < nwords; t += blockDim.x) dst[t] = src[t];
+#pragma unroll
+        for (int k = 0; k < LinkRegs<THREADS, KP>::kWords; ++k) {
+            const int t = (int)threadIdx.x + k * THREADS;
+            R.w[k] = t < nwords ? src[t] : 0u;
+        }
     }
     return X;
 }
 
-// Each cell (i, o) is served by kSplit threads: sub-thread k scans
-// j = i+1+k, i+1+k+kSplit, ... and o2 = o+1+k, o+1+k+kSplit, ..., and LDS
-// combines them.  A sub-thread may stop at its own first T not below its own
-// running best: everything it skips is no smaller than that best, which it
-// reached at a smaller j, so neither the minimum nor the least j attaining it
-// can be among the skipped ones.
-constexpr int kSplit = 4;
+template <int THREADS, int KP>
+__device__ inline void store_links(const LinkRegs<THREADS, KP> &R, const Links &X, const DevProblem &P, int i,
+                                   int top, double *xs, uint8_t *tri_s) {
+    if (i == 0 || !X.table) return;
+#pragma unroll
+    for (int k = 0; k < LinkRegs<THREADS, KP>::kE; ++k) {
+        const int u = (int)threadIdx.x + k * THREADS;
+        if (u < P.n_ev) xs[u] = R.E[k] == 0.0 ? kInf : X.num / R.E[k];
+    }
+    const int nwords = (top * (top + 1) / 2 + 3) / 4;
+    uint32_t *dst = (uint32_t *)tri_s;
+#pragma unroll
+    for (int k = 0; k < LinkRegs<THREADS, KP>::kWords; ++k) {
+        const int t = (int)threadIdx.x + k * THREADS;
+        if (t < nwords) dst[t] = R.w[k];
+    }
+}
 
-__device__ inline int cell_pad(int K) { return K <= 64 ? 64 : (K <= 128 ? 128 : (K <= 192 ? 192 : 256)); }
+// Next-position scan.  Only positions with a finite value can give the
+// minimum, so when fewer than half of them are finite the block lists those
+// positions (ascending) and the scan walks the list; otherwise it walks the
+// positions directly.  The threads that combined the values (sub-thread 0,
+// whole waves) publish one ballot mask per wave.
+__device__ inline void publish_live(bool live, uint64_t *lmask) {
+    const uint64_t bal = __ballot(live);
+    if ((threadIdx.x & (kWave - 1)) == 0) lmask[threadIdx.x / kWave] = bal;
+}
 
-// Phase 1: bottleneck values.  Block (i, b), thread (sub, o).
-__global__ __launch_bounds__(1024) void level_bottleneck(DevProblem P, int d, const int32_t *bcnt,
-                                                         const int32_t *ev_cell, const double *ev_val, double *T,
-                                                         const double *Wprev, double *Wnext, const double *EoT,
-                                                         const uint8_t *EiT, double *Pst) {
+struct LiveList {
+    int32_t start;  // finite positions <= o: o's successors start here in the list
+    int32_t total;
+    bool sparse;
+};
+
+// After the barrier that follows publish_live; a sparse list needs one more
+// barrier (taken here, uniformly) before it is read.
+template <int KP>
+__device__ inline LiveList build_live(int o, int sub, int top, const uint64_t *lmask, int32_t *list) {
+    const int w = o / kWave, b = o % kWave;
+    int before = 0, total = 0;
+#pragma unroll
+    for (int u = 0; u < KP / kWave; ++u) {
+        const int c = (int)__popcll(lmask[u]);
+        if (u < w) before += c;
+        total += c;
+    }
+    const uint64_t mw = lmask[w];
+    const uint64_t below = b == 0 ? 0ull : (mw & (~0ull >> (kWave - b)));
+    const int rank = before + (int)__popcll(below);
+    const int self = (int)((mw >> b) & 1ull);
+    const bool sparse = 2 * total <= top + 1;
+    if (sparse) {
+        if (sub == 0 && self) list[rank] = o;
+        __syncthreads();
+    }
+    return LiveList{rank + self, total, sparse};
+}
+
+// Visits this sub-thread's share of the positions after o in ascending order:
+// take(link time, value, position).
+template <int SPLIT, typename Link, typename Take>
+__device__ inline void scan_next(int o, int sub, int top, const LiveList &lv, const int32_t *list,
+                                 const double *vals, Link link, Take take) {
+    if (lv.sparse) {
+        int r = lv.start + sub;
+        for (; r + (kAhead - 1) * SPLIT < lv.total; r += kAhead * SPLIT) {
+            int q[kAhead];
+            double x[kAhead], y[kAhead];
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) q[u] = list[r + u * SPLIT];
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) {
+                x[u] = link(q[u]);
+                y[u] = vals[q[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) take(x[u], y[u], q[u]);
+        }
+        for (; r < lv.total; r += SPLIT) {
+            const int q = list[r];
+            take(link(q), vals[q], q);
+        }
+    } else {
+        int o2 = o + 1 + sub;
+        for (; o2 + (kAhead - 1) * SPLIT <= top; o2 += kAhead * SPLIT) {
+            double x[kAhead], y[kAhead];
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) {
+                x[u] = link(o2 + u * SPLIT);
+                y[u] = vals[o2 + u * SPLIT];
+            }
+#pragma unroll
+            for (int u = 0; u < kAhead; ++u) take(x[u], y[u], o2 + u * SPLIT);
+        }
+        for (; o2 <= top; o2 += SPLIT) take(link(o2), vals[o2], o2);
+    }
+}
+
+// Sub-thread k of a cell scans j = i+1+k, i+1+k+SPLIT, ...  It may stop at
+// its own first T not below its own running best: everything it skips is no
+// smaller than that best, which it reached at a smaller j, so neither the
+// minimum nor the least j attaining it can be among the skipped ones.
+
+// Phase 1: bottleneck values.  KP = K padded to whole waves.
+template <int KP, int SPLIT>
+__global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bottleneck(
+    DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
+    const double *T1, const double *Wprev, double *Wnext, const double *EoT, const uint8_t *EiT, double *Pst) {
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
-    __shared__ double part[kSplit][256];
-    __shared__ double Vs[256];
+    __shared__ double part[SPLIT][KP];
+    __shared__ double Vs[KP];
     __shared__ double xs[kMaxDistinctE];
+    __shared__ uint64_t lmask[KP / kWave];
+    __shared__ int32_t list[KP];
     const int i = blockIdx.x, bi = blockIdx.y;
-    const int L = P.L, K = P.K, KP = cell_pad(K);
+    const int L = P.L, K = P.K;
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
-    apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
-    const Links X = stage_links(P, i, bi, K - d, EiT, EoT, xs, tri_s);
-    __syncthreads();
+    const int top = K - d;
+    RowEvents ev;
+    event_bounds(ev, P, d, bi, i, bcnt);
+    LinkRegs<SPLIT * KP, KP> lr;
+    const Links X = load_links(lr, P, i, bi, top, EiT, EoT, xs, tri_s);
     const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);  // slice (i, j) is srow + j-i-1
     double v = kInf;
-    if (o < K && o <= K - d) {
+    if (o < K && o <= top) {
         if (d == 1) {
-            if (sub == 0) v = T[(srow + (L - i - 1)) * K + o];
+            if (sub == 0) v = T1[((int64_t)bi * L + i) * K + o];  // the slice (i, L)
         } else {
             const double *Wp = Wprev + (int64_t)bi * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
-            for (int j0 = i + 1 + sub; j0 <= jmax; j0 += 2 * kSplit) {
-                const int j1 = j0 + kSplit;
-                const double t0 = Tp[(int64_t)(j0 - i - 1) * K], w0 = Wp[(int64_t)j0 * K];
-                const double t1 = j1 <= jmax ? Tp[(int64_t)(j1 - i - 1) * K] : kInf;
-                const double w1 = j1 <= jmax ? Wp[(int64_t)j1 * K] : kInf;
-                if (!(t0 < v)) break;  // T never decreases in j
-                v = fmin(v, fmax(t0, w0));
-                if (!(t1 < v)) break;
-                v = fmin(v, fmax(t1, w1));
+            bool go = true;
+            for (int j0 = i + 1 + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
+                double t[kAhead], w[kAhead];
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {  // unconditional loads, all in flight at once
+                    const int j = min(j0 + u * SPLIT, jmax);
+                    t[u] = Tp[(int64_t)(j - i - 1) * K];
+                    w[u] = Wp[(int64_t)j * K];
+                }
+#pragma unroll
+                for (int u = 1; u < kAhead; ++u)
+                    if (j0 + u * SPLIT > jmax) t[u] = kInf;
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {
+                    if (go && !(t[u] < v)) go = false;  // T never decreases in j
+                    if (go) v = fmin(v, fmax(t[u], w[u]));
+                }
             }
         }
     }
     part[sub][o] = v;
+    store_links(lr, X, P, i, top, xs, tri_s);
     __syncthreads();
+    // every read of this row's table is done
+    load_events(ev, ev_cell, ev_val);
     if (sub == 0) {
         double m = part[0][o];
 #pragma unroll
-        for (int k = 1; k < kSplit; ++k) m = fmin(m, part[k][o]);
+        for (int k = 1; k < SPLIT; ++k) m = fmin(m, part[k][o]);
         Vs[o] = m;
+        publish_live(o <= top && m < kInf, lmask);
     }
     __syncthreads();
     if (i == 0) {
@@ -506,19 +723,27 @@ __global__ __launch_bounds__(1024) void level_bottleneck(DevProblem P, int d, co
             for (int t = 0; t < K; ++t) m = fmin(m, Vs[t]);
             Pst[bi] = fmin(Pst[bi], m);
         }
+        store_events(ev, ev_cell, ev_val, T);
         return;
     }
+    const LiveList lv = build_live<KP>(o, sub, top, lmask, list);
     double w = kInf;
-    if (o < K)
-        for (int o2 = o + 1 + sub; o2 <= K - d; o2 += kSplit) w = fmin(w, fmax(X(o, o2, K), Vs[o2]));
+    if (o < K) {
+        auto take = [&](double x, double y, int) { w = fmin(w, fmax(x, y)); };
+        if (X.table)
+            scan_next<SPLIT>(o, sub, top, lv, list, Vs, [&](int q) { return X.tab(o, q); }, take);
+        else
+            scan_next<SPLIT>(o, sub, top, lv, list, Vs, [&](int q) { return X.direct(o, q, K); }, take);
+    }
     part[sub][o] = w;
     __syncthreads();
     if (sub == 0 && o < K) {
         double m = part[0][o];
 #pragma unroll
-        for (int k = 1; k < kSplit; ++k) m = fmin(m, part[k][o]);
+        for (int k = 1; k < SPLIT; ++k) m = fmin(m, part[k][o]);
         Wnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
     }
+    store_events(ev, ev_cell, ev_val, T);
 }
 
 // (value, index) pairs: the smaller value, ties to the smaller index.
@@ -527,32 +752,37 @@ __device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
 }
 
 // Phase 2: fill values and argmins at the bottleneck P*.
-__global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell,
-                                                   const double *ev_val, double *T, const double *Gprev,
-                                                   double *Gnext, const double *EoT, const uint8_t *EiT,
-                                                   const double *Pst, uint16_t *argF, uint8_t *argG,
-                                                   double *rootF, int32_t *root_o, int32_t *root_d) {
+template <int KP, int SPLIT>
+__global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fill(
+    DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
+    const double *T1, const double *Gprev, double *Gnext, const double *EoT, const uint8_t *EiT, const double *Pst,
+    uint16_t *argF,
+    uint8_t *argG, double *rootF, int32_t *root_o, int32_t *root_d) {
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
-    __shared__ double part[kSplit][256];
-    __shared__ int32_t parg[kSplit][256];
-    __shared__ double Fs[256];
+    __shared__ double part[SPLIT][KP];
+    __shared__ int32_t parg[SPLIT][KP];
+    __shared__ double Fs[KP];
     __shared__ double xs[kMaxDistinctE];
+    __shared__ uint64_t lmask[KP / kWave];
+    __shared__ int32_t list[KP];
     const int i = blockIdx.x, bi = blockIdx.y;
-    const int L = P.L, K = P.K, KP = cell_pad(K);
+    const int L = P.L, K = P.K;
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
+    const int top = K - d;
     const double Ps = Pst[bi];
     if (!(Ps < kInf)) return;
-    apply_events(bcnt, ev_cell, ev_val, T, ((int64_t)(d - 1) * P.nb + bi) * L + i);
-    const Links X = stage_links(P, i, bi, K - d, EiT, EoT, xs, tri_s);
-    __syncthreads();
+    RowEvents ev;
+    event_bounds(ev, P, d, bi, i, bcnt);
+    LinkRegs<SPLIT * KP, KP> lr;
+    const Links X = load_links(lr, P, i, bi, top, EiT, EoT, xs, tri_s);
     const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);
     double v = kInf;
     int arg = 0xFFFF;
-    if (o < K && o <= K - d) {
+    if (o < K && o <= top) {
         if (d == 1) {
             if (sub == 0) {
-                const double t = T[(srow + (L - i - 1)) * K + o];
+                const double t = T1[((int64_t)bi * L + i) * K + o];  // the slice (i, L)
                 if (t <= Ps) {
                     v = t;
                     arg = L;
@@ -562,40 +792,50 @@ __global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const in
             const double *Gp = Gprev + (int64_t)bi * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
-            for (int j0 = i + 1 + sub; j0 <= jmax; j0 += 2 * kSplit) {
-                const int j1 = j0 + kSplit;
-                const double t0 = Tp[(int64_t)(j0 - i - 1) * K], g0 = Gp[(int64_t)j0 * K];
-                const double t1 = j1 <= jmax ? Tp[(int64_t)(j1 - i - 1) * K] : kInf;
-                const double g1 = j1 <= jmax ? Gp[(int64_t)j1 * K] : kInf;
-                if (!(t0 <= Ps) || !(t0 < v)) break;  // T never decreases in j
-                const double c0 = t0 + g0;
-                if (c0 < v) {
-                    v = c0;
-                    arg = j0;
+            bool go = true;
+            for (int j0 = i + 1 + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
+                double t[kAhead], g[kAhead];
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {  // unconditional loads, all in flight at once
+                    const int j = min(j0 + u * SPLIT, jmax);
+                    t[u] = Tp[(int64_t)(j - i - 1) * K];
+                    g[u] = Gp[(int64_t)j * K];
                 }
-                if (!(t1 <= Ps) || !(t1 < v)) break;
-                const double c1 = t1 + g1;
-                if (c1 < v) {
-                    v = c1;
-                    arg = j1;
+#pragma unroll
+                for (int u = 1; u < kAhead; ++u)
+                    if (j0 + u * SPLIT > jmax) t[u] = kInf;
+#pragma unroll
+                for (int u = 0; u < kAhead; ++u) {
+                    if (go && (!(t[u] <= Ps) || !(t[u] < v))) go = false;  // T never decreases in j
+                    if (go) {
+                        const double c = t[u] + g[u];
+                        if (c < v) {
+                            v = c;
+                            arg = j0 + u * SPLIT;
+                        }
+                    }
                 }
             }
         }
     }
     part[sub][o] = v;
     parg[sub][o] = arg;
+    store_links(lr, X, P, i, top, xs, tri_s);
     __syncthreads();
+    // every read of this row's table is done
+    load_events(ev, ev_cell, ev_val);
     if (sub == 0) {
         double m = part[0][o];
         int a = parg[0][o];
 #pragma unroll
-        for (int k = 1; k < kSplit; ++k)
+        for (int k = 1; k < SPLIT; ++k)
             if (lex_less(part[k][o], parg[k][o], m, a)) {
                 m = part[k][o];
                 a = parg[k][o];
             }
         Fs[o] = m;
         if (o < K) argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)(m < kInf ? a : 0xFFFF);
+        publish_live(o <= top && m < kInf, lmask);
     }
     __syncthreads();
     if (i == 0) {
@@ -614,20 +854,26 @@ __global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const in
                 root_d[bi] = d;
             }
         }
+        store_events(ev, ev_cell, ev_val, T);
         return;
     }
+    const LiveList lv = build_live<KP>(o, sub, top, lmask, list);
     double w = kInf;
     int a = 0xFF;
-    if (o < K)
-        for (int o2 = o + 1 + sub; o2 <= K - d; o2 += kSplit) {
-            const double x = X(o, o2, K);
-            if (!(x <= Ps)) continue;
-            const double c = x + Fs[o2];
+    if (o < K) {
+        auto take = [&](double x, double f, int o2) {
+            if (!(x <= Ps)) return;
+            const double c = x + f;
             if (c < w) {
                 w = c;
                 a = o2;
             }
-        }
+        };
+        if (X.table)
+            scan_next<SPLIT>(o, sub, top, lv, list, Fs, [&](int q) { return X.tab(o, q); }, take);
+        else
+            scan_next<SPLIT>(o, sub, top, lv, list, Fs, [&](int q) { return X.direct(o, q, K); }, take);
+    }
     part[sub][o] = w;
     parg[sub][o] = a;
     __syncthreads();
@@ -635,7 +881,7 @@ __global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const in
         double m = part[0][o];
         int aa = parg[0][o];
 #pragma unroll
-        for (int k = 1; k < kSplit; ++k)
+        for (int k = 1; k < SPLIT; ++k)
             if (lex_less(part[k][o], parg[k][o], m, aa)) {
                 m = part[k][o];
                 aa = parg[k][o];
@@ -643,86 +889,157 @@ __global__ __launch_bounds__(1024) void level_fill(DevProblem P, int d, const in
         Gnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
         argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)(m < kInf ? aa : 0xFF);
     }
+    store_events(ev, ev_cell, ev_val, T);
 }
+
+// Threads per cell for a level of `blocks` blocks: the most (up to 4) whose
+// blocks all fit on the device at once, else 2.  When the device size or the
+// occupancy cannot be queried, four.
+template <int KP>
+struct LevelKernels {
+    template <int SPLIT>
+    static int capacity(int n_cu, size_t lds) {
+        if (n_cu <= 0) return INT_MAX;  // unknown device size: keep four threads per cell
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, level_bottleneck<KP, SPLIT>, SPLIT * KP, lds) !=
+            hipSuccess)
+            return INT_MAX;
+        int per_cu2 = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu2, level_fill<KP, SPLIT>, SPLIT * KP, lds) !=
+            hipSuccess)
+            return INT_MAX;
+        return std::min(per_cu, per_cu2) * n_cu;
+    }
+};
 
 // ---------------------------------------------------------------------------
 // choose b, walk the argmins, resolve each stage's candidate
 // ---------------------------------------------------------------------------
-__global__ void finish_kernel(DevProblem P, const int32_t *gcnt, const double *ent_c, const uint8_t *ent_d,
-                              const int64_t *ent_i, const int32_t *order, const double *EoT, const double *Pst,
-                              const double *rootF, const int32_t *root_o, const int32_t *root_d,
-                              const uint16_t *argF, const uint8_t *argG, ComposeResult *res) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+// The walk is serial (a stage's argmins give the next stage's first layer and
+// position), so one thread follows it and records the stages in LDS; then one
+// wave per stage finds the stage's candidate in its group.
+constexpr int kFinishThreads = 256;
+
+// Candidate order within a group: least cost, then deepest fit, then least
+// index; idx < 0 marks "none".
+__device__ inline bool cand_less(double c1, int d1, int64_t i1, double c2, int d2, int64_t i2) {
+    if (i1 < 0) return false;
+    if (i2 < 0) return true;
+    return c1 < c2 || (c1 == c2 && (d1 > d2 || (d1 == d2 && i1 < i2)));
+}
+
+__global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, const int32_t *gcnt,
+                                                                const double *ent_c, const uint8_t *ent_d,
+                                                                const int64_t *ent_i, const int32_t *order,
+                                                                const double *EoT, const double *Pst,
+                                                                const double *rootF, const int32_t *root_o,
+                                                                const int32_t *root_d, const uint16_t *argF,
+                                                                const uint8_t *argG, ComposeResult *res) {
+    __shared__ int32_t st_i[256], st_j[256], st_o[256], st_on[256];
+    __shared__ int32_t sh_S, sh_bb;
     const int L = P.L, K = P.K;
     tg_plan &plan = res->plan;
-    plan.b = 0;
-    plan.m = 0;
-    plan.S = 0;
-    plan.reserved = 0;
-    plan.P = kInf;
-    plan.F = kInf;
-    plan.T = kInf;
-    if (res->err) return;
-    double bestT = kInf;
-    int bb = -1;
-    for (int bi = 0; bi < P.nb; ++bi) {
-        if (!(Pst[bi] < kInf) || root_o[bi] < 0) continue;
-        const int64_t m = P.B / P.bvals[bi];
-        const double T = ((double)(m - 1) * Pst[bi]) + rootF[bi];
-        if (T < bestT) {
-            bestT = T;
-            bb = bi;
+    if (threadIdx.x == 0) {
+        sh_S = 0;
+        plan.b = 0;
+        plan.m = 0;
+        plan.S = 0;
+        plan.reserved = 0;
+        plan.P = kInf;
+        plan.F = kInf;
+        plan.T = kInf;
+        double bestT = kInf;
+        int bb = -1;
+        if (!res->err)
+            for (int bi = 0; bi < P.nb; ++bi) {
+                if (!(Pst[bi] < kInf) || root_o[bi] < 0) continue;
+                const int64_t m = P.B / P.bvals[bi];
+                const double T = ((double)(m - 1) * Pst[bi]) + rootF[bi];
+                if (T < bestT) {
+                    bestT = T;
+                    bb = bi;
+                }
+            }
+        if (bb >= 0) {
+            const int64_t b = P.bvals[bb];
+            const int S = root_d[bb];
+            plan.b = (int32_t)b;
+            plan.m = (int32_t)(P.B / b);
+            plan.S = S;
+            plan.P = Pst[bb];
+            plan.F = rootF[bb];
+            plan.T = bestT;
+            res->status = TG_OK;
+            int i = 0, o = root_o[bb];
+            bool ok = S >= 1 && S <= 255;
+            for (int t = 0; ok && t < S; ++t) {
+                const int d = S - t;
+                int j = L, o_next = -1;
+                if (d > 1) {
+                    j = argF[(((int64_t)(d - 1) * P.nb + bb) * L + i) * K + o];
+                    // an argmin on the optimal path is always set
+                    ok = j > i && j <= L - d + 1;
+                    if (ok) {
+                        o_next = argG[(((int64_t)(d - 2) * P.nb + bb) * (L + 1) + j) * K + o];
+                        ok = o_next > o && o_next < K;
+                    }
+                }
+                st_i[t] = i;
+                st_j[t] = j;
+                st_o[t] = o;
+                st_on[t] = o_next;
+                i = j;
+                o = o_next;
+            }
+            if (ok) {
+                sh_S = S;
+                sh_bb = bb;
+            } else {
+                res->err = 4;
+                res->status = TG_ENOPLAN;
+            }
         }
     }
-    if (bb < 0) return;
+    __syncthreads();
+    const int S = sh_S;
+    if (S == 0) return;
+    const int bb = sh_bb;
     const int64_t b = P.bvals[bb];
-    plan.b = (int32_t)b;
-    plan.m = (int32_t)(P.B / b);
-    plan.S = root_d[bb];
-    plan.P = Pst[bb];
-    plan.F = rootF[bb];
-    plan.T = bestT;
-    res->status = TG_OK;
-    int i = 0, o = root_o[bb];
-    const int S = root_d[bb];
-    for (int t = 0; t < S; ++t) {
-        const int d = S - t;
-        int j = L, o_next = -1;
-        if (d > 1) {
-            j = argF[(((int64_t)(d - 1) * P.nb + bb) * L + i) * K + o];
-            if (j <= i || j > L - d + 1) {  // an argmin on the optimal path is always set
-                res->err = 4;
-                res->status = TG_ENOPLAN;
-                return;
-            }
-            o_next = argG[(((int64_t)(d - 2) * P.nb + bb) * (L + 1) + j) * K + o];
-            if (o_next <= o || o_next >= K) {
-                res->err = 4;
-                res->status = TG_ENOPLAN;
-                return;
-            }
-        }
+    const int wv = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    for (int t = wv; t < S; t += kFinishThreads / kWave) {
+        const int d = S - t, i = st_i[t], j = st_j[t], o = st_o[t], o_next = st_on[t];
         const int64_t s = slice_of(L, i, j);
         const int64_t G = group_id(P, o, bb, s);
         const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
         int64_t best = -1;
         double bc = kInf;
         int bd = 0;
-        for (int32_t e = st; e < en; ++e) {
-            const int64_t ie = ent_i[e];
-            const double c = ent_c[e];
+        for (int32_t e = st + lane; e < en; e += kWave) {
             const int dd = ent_d[e];
             if (dd < d) continue;
-            if (best < 0 || c < bc || (c == bc && (dd > bd || (dd == bd && ie < best)))) {
+            const double c = ent_c[e];
+            const int64_t ie = ent_i[e];
+            if (cand_less(c, dd, ie, bc, bd, best)) {
                 best = ie;
                 bc = c;
                 bd = dd;
             }
         }
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const double c2 = __shfl_xor(bc, off);
+            const int d2 = __shfl_xor(bd, off);
+            const int64_t i2 = __shfl_xor(best, off);
+            if (cand_less(c2, d2, i2, bc, bd, best)) {
+                best = i2;
+                bc = c2;
+                bd = d2;
+            }
+        }
+        if (lane != 0) continue;
         if (best < 0) {  // the stage table said a candidate fits here
             res->err = 4;
             res->status = TG_ENOPLAN;
-            return;
+            continue;
         }
         const int64_t g = best / P.NS;
         const Coef &c = P.coef[g];
@@ -752,8 +1069,6 @@ __global__ void finish_kernel(DevProblem P, const int32_t *gcnt, const double *e
         } else {
             sg.link_out = 0.0;
         }
-        i = j;
-        o = o_next;
     }
 }
 
@@ -766,7 +1081,7 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     const int64_t G = n_groups(P), nbk = n_buckets(P);
     const int D = levels(P);
     const int64_t rows = (int64_t)P.nb * (P.L + 1) * P.K;
-    prep_kernel<<<dim3(1), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT, w.EiT, w.res);
+    prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT, w.EiT, w.res);
     fill<int32_t>(w.gcnt, G, 0, s);
     fill<int32_t>(w.bcnt, nbk + 1, 0, s);
     fill<double>(w.Pst, P.nb, kInf, s);
@@ -781,37 +1096,84 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
         scan_i32(w.gcnt, G, w.tmp, s);
         scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n_surv, w.rec_g, w.rec_c, w.rec_d,
                                                                      w.gcnt, w.ent_c, w.ent_d, w.ent_i);
-        const dim3 egrid((unsigned)P.L, (unsigned)P.nb);
-        group_events<false><<<egrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt, w.ev_cell,
-                                                       w.ev_val);
+        const int nch = (int)(((int64_t)P.L * P.K + kEventCells - 1) / kEventCells);
+        const dim3 egrid((unsigned)(P.L * nch), (unsigned)P.nb);
+        group_events<false><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt,
+                                                       w.ev_cell, w.ev_val);
         scan_i32(w.bcnt, nbk + 1, w.tmp, s);
-        group_events<true><<<egrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt, w.ev_cell,
-                                                      w.ev_val);
+        copy_kernel<int32_t><<<dim3((unsigned)((nbk + 1 + 255) / 256)), dim3(256), 0, s>>>(w.bcnt, w.bcur, nbk + 1);
+        group_events<true><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcur,
+                                                      w.ev_cell, w.ev_val);
     } else {
         scan_i32(w.gcnt, G, w.tmp, s);  // all zeros: offsets stay zero
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int threads = kSplit * (P.K <= 64 ? 64 : (P.K <= 128 ? 128 : (P.K <= 192 ? 192 : 256)));
     const size_t tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
     const dim3 tgrid((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
                      (unsigned)P.nb);
-    // phase 1: least bottleneck per b
-    table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.T);
-    fill<double>(w.Wb[0], rows, kInf, s);
-    fill<double>(w.Wb[1], rows, kInf, s);
-    for (int d = 1; d <= D; ++d)
-        level_bottleneck<<<dim3((unsigned)(P.L - d + 1), (unsigned)P.nb), dim3(threads), tri_lds, s>>>(
-            P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1], w.Wb[d & 1], w.EoT, w.EiT, w.Pst);
-    // phase 2: least fill at that bottleneck
-    table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.T);
-    fill<double>(w.Wb[0], rows, kInf, s);
-    fill<double>(w.Wb[1], rows, kInf, s);
-    for (int d = 1; d <= D; ++d)
-        level_fill<<<dim3((unsigned)(P.L - d + 1), (unsigned)P.nb), dim3(threads), tri_lds, s>>>(
-            P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.Wb[(d - 1) & 1], w.Wb[d & 1], w.EoT, w.EiT, w.Pst, w.argF,
-            w.argG, w.rootF, w.root_o, w.root_d);
-    finish_kernel<<<dim3(1), dim3(64), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT, w.Pst, w.rootF,
+    int n_cu = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        n_cu = 0;
+    auto levels_run = [&](auto kp) {
+        constexpr int KP = decltype(kp)::value;
+        using LK = LevelKernels<KP>;
+        const int cap4 = LK::template capacity<4>(n_cu, tri_lds);
+        const int cap3 = LK::template capacity<3>(n_cu, tri_lds);
+        auto split_for = [&](int blocks) { return blocks <= cap4 ? 4 : (blocks <= cap3 ? 3 : 2); };
+        auto bottleneck = [&](int d) {
+            const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
+            const int sp = split_for((int)(grid.x * grid.y));
+            const double *Wp = w.Wb[(d - 1) & 1];
+            double *Wn = w.Wb[d & 1];
+            if (sp == 4)
+                level_bottleneck<KP, 4><<<grid, dim3(4 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
+                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
+            else if (sp == 3)
+                level_bottleneck<KP, 3><<<grid, dim3(3 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
+                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
+            else
+                level_bottleneck<KP, 2><<<grid, dim3(2 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
+                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
+        };
+        auto fill_level = [&](int d) {
+            const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
+            const int sp = split_for((int)(grid.x * grid.y));
+            const double *Gp = w.Wb[(d - 1) & 1];
+            double *Gn = w.Wb[d & 1];
+            if (sp == 4)
+                level_fill<KP, 4><<<grid, dim3(4 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
+                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
+                                                                      w.root_o, w.root_d);
+            else if (sp == 3)
+                level_fill<KP, 3><<<grid, dim3(3 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
+                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
+                                                                      w.root_o, w.root_d);
+            else
+                level_fill<KP, 2><<<grid, dim3(2 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
+                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
+                                                                      w.root_o, w.root_d);
+        };
+        // phase 1: least bottleneck per b
+        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
+        fill<double>(w.Wb[0], rows, kInf, s);
+        fill<double>(w.Wb[1], rows, kInf, s);
+        for (int d = 1; d <= D; ++d) bottleneck(d);
+        // phase 2: least fill at that bottleneck
+        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
+        fill<double>(w.Wb[0], rows, kInf, s);
+        fill<double>(w.Wb[1], rows, kInf, s);
+        for (int d = 1; d <= D; ++d) fill_level(d);
+    };
+    if (P.K <= 64)
+        levels_run(std::integral_constant<int, 64>{});
+    else if (P.K <= 128)
+        levels_run(std::integral_constant<int, 128>{});
+    else if (P.K <= 192)
+        levels_run(std::integral_constant<int, 192>{});
+    else
+        levels_run(std::integral_constant<int, 256>{});
+    finish_kernel<<<dim3(1), dim3(kFinishThreads), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT, w.Pst, w.rootF,
                                                 w.root_o, w.root_d, w.argF, w.argG, w.res);
     return hipGetLastError();
 }
