@@ -79,6 +79,7 @@ def lib():
         L.tgo_score_list.argtypes = [vp, i64p, ctypes.c_int64, f64p, u8p]
         L.tgo_prune.argtypes = [vp, i64p, ctypes.c_int64, i64p]
         L.tgo_compose.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
+        L.tgo_compose_relaxed.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
         _lib = L
     return _lib
 
@@ -200,6 +201,20 @@ class Oracle:
         st = lib().tgo_compose(self.h, _ptr(cands, ctypes.c_int64), len(cands),
                                _ptr(order, ctypes.c_int32), ctypes.byref(plan),
                                _ptr(per_b, ctypes.c_double))
+        return st, plan_to_dict(plan), per_b[: self.n_b]
+
+    def compose_relaxed(self, candidates, order=None):
+        """Composition with the relaxation of step (4).  Returns (status, plan
+        dict, per-b array [n_b, 4] of P*, chosen bound, F at it, T)."""
+        if order is None:
+            order = self.inst["island_order"]
+        cands = np.ascontiguousarray(np.asarray(candidates, dtype=np.int64))
+        order = np.ascontiguousarray(np.asarray(order, dtype=np.int32))
+        plan = Plan()
+        per_b = np.full((max(self.n_b, 1), 4), np.inf)
+        st = lib().tgo_compose_relaxed(self.h, _ptr(cands, ctypes.c_int64), len(cands),
+                                       _ptr(order, ctypes.c_int32), ctypes.byref(plan),
+                                       _ptr(per_b, ctypes.c_double))
         return st, plan_to_dict(plan), per_b[: self.n_b]
 
 

@@ -523,11 +523,223 @@ static double transfer(const oprob *p, int64_t b, int j, int ka, int kb) {
     return ((2.0 * (double)b) * (double)p->layer[F_OUTACT][j - 1]) / E;
 }
 
-int tgo_compose(void *h, const int64_t *cands, int64_t n, const int32_t *order, tgo_plan *plan,
-                double *per_b /* nb x 3: P*, F*, T; may be NULL */) {
+/* Working tables of one b during composition. */
+typedef struct {
+    const oprob *p;
+    const int32_t *order;
+    int L, K, D;
+    int64_t NS;
+    const oentry *ent;
+    int64_t *gstart, *gend; /* [NS*K] entry range of each (slice, position) group */
+    double *V, *Wt;         /* [D+1][L+1][K]: V/W in step (1)-(2), F/G in step (3) */
+    double *Td;             /* [D+1][NS][K] stage table by depth */
+    double *X;              /* [L+1][K][K] link times */
+    int64_t b, m;
+} octx;
+
+#define AT(A, d, i, o) A[((int64_t)(d) * (c->L + 1) + (i)) * c->K + (o)]
+#define TD(d, s, o) c->Td[((int64_t)(d) * c->NS + (s)) * c->K + (o)]
+#define XA(j, o, o2) c->X[((int64_t)(j) * c->K + (o)) * c->K + (o2)]
+
+/* Stage table Td(d, s, o) = least cost of the group's entries that fit at
+   depth d (entries are key-sorted, so the first fitting one), and the link
+   table X(j, o, o') for micro-batch b. */
+static void build_tables(octx *c, int64_t e0, int64_t e1, int bi) {
+    const int L = c->L, K = c->K;
+    const int64_t NS = c->NS;
+    for (int64_t a = 0; a < NS * K; a++) { c->gstart[a] = 0; c->gend[a] = 0; }
+    for (int64_t a = e0; a < e1; a++) {
+        int64_t gk = c->ent[a].gkey % (NS * K);
+        if (c->gend[gk] == 0) c->gstart[gk] = a;
+        c->gend[gk] = a + 1;
+    }
+    (void)bi;
+    for (int d = 1; d <= c->D; d++)
+        for (int64_t s = 0; s < NS; s++)
+            for (int o = 0; o < K; o++) {
+                double v = INFINITY;
+                int64_t gk = s * K + o;
+                for (int64_t a = c->gstart[gk]; a < c->gend[gk]; a++)
+                    if (c->ent[a].dmax >= d) { v = c->ent[a].cost; break; }
+                TD(d, s, o) = v;
+            }
+    for (int j = 1; j < L; j++)
+        for (int o = 0; o < K; o++)
+            for (int o2 = 0; o2 < K; o2++)
+                XA(j, o, o2) = transfer(c->p, c->b, j, c->order[o], c->order[o2]);
+}
+
+/* Steps (1)-(2): least achievable bottleneck.
+   V(d,i,o): best bottleneck covering layers [i, L) with d stages, the first on
+   island position o and the rest on later positions.
+   W(d,j,o): best continuation after a stage on position o ends at j. */
+static double least_bottleneck(octx *c) {
+    const int L = c->L, K = c->K, D = c->D;
+    for (int d = 1; d <= D; d++) {
+        for (int i = 0; i < L; i++)
+            for (int o = 0; o < K; o++) {
+                double v = INFINITY;
+                if (d == 1) v = TD(1, slice_index(L, i, L), o);
+                else
+                    for (int j = i + 1; j <= L - d + 1; j++) {
+                        double x = maxd(TD(d, slice_index(L, i, j), o), AT(c->Wt, d - 1, j, o));
+                        if (x < v) v = x;
+                    }
+                AT(c->V, d, i, o) = v;
+            }
+        for (int j = 1; j < L; j++)
+            for (int o = 0; o < K; o++) {
+                double w = INFINITY;
+                for (int o2 = o + 1; o2 < K; o2++) {
+                    double x = maxd(XA(j, o, o2), AT(c->V, d, j, o2));
+                    if (x < w) w = x;
+                }
+                AT(c->Wt, d, j, o) = w;
+            }
+    }
+    double Pst = INFINITY;
+    for (int d = 1; d <= D; d++)
+        for (int o = 0; o < K; o++)
+            if (AT(c->V, d, 0, o) < Pst) Pst = AT(c->V, d, 0, o);
+    return Pst;
+}
+
+/* Step (3) at bound tau: least fill among plans whose every stage and link
+   stays within tau.  Fill = f1 + (x1 + (f2 + ... + fS)), a right fold; F and G
+   reuse the V and W arrays.  Returns the least root fill; *ro, *rS get its
+   first position (ties to the earliest) and stage count (then fewer). */
+static double least_fill(octx *c, double tau, int *ro, int *rS) {
+    const int L = c->L, K = c->K, D = c->D;
+    for (int d = 1; d <= D; d++) {
+        for (int i = 0; i < L; i++)
+            for (int o = 0; o < K; o++) {
+                double v = INFINITY;
+                if (d == 1) {
+                    double t = TD(1, slice_index(L, i, L), o);
+                    if (t <= tau) v = t;
+                } else
+                    for (int j = i + 1; j <= L - d + 1; j++) {
+                        double t = TD(d, slice_index(L, i, j), o);
+                        if (!(t <= tau)) continue;
+                        double x = t + AT(c->Wt, d - 1, j, o);
+                        if (x < v) v = x;
+                    }
+                AT(c->V, d, i, o) = v;
+            }
+        for (int j = 1; j < L; j++)
+            for (int o = 0; o < K; o++) {
+                double w = INFINITY;
+                for (int o2 = o + 1; o2 < K; o2++) {
+                    double x = XA(j, o, o2);
+                    if (!(x <= tau)) continue;
+                    double y = x + AT(c->V, d, j, o2);
+                    if (y < w) w = y;
+                }
+                AT(c->Wt, d, j, o) = w;
+            }
+    }
+    double Fst = INFINITY;
+    *ro = -1;
+    *rS = -1;
+    for (int o = 0; o < K; o++)
+        for (int d = 1; d <= D; d++)
+            if (AT(c->V, d, 0, o) < Fst) { Fst = AT(c->V, d, 0, o); *ro = o; *rS = d; }
+    return Fst;
+}
+
+/* Walk the argmins of the step-(3) tables at bound tau from root (ro, rS) and
+   fill the plan's stages: smallest j attaining F, then smallest later
+   position attaining G; each stage's candidate is its group's least-key entry
+   fitting at the stage's depth. */
+static void backtrack(octx *c, double tau, int ro, int rS, tgo_plan *plan) {
+    const oprob *p = c->p;
+    const int L = c->L, K = c->K;
+    int i = 0, o = ro;
+    for (int t = 0; t < rS; t++) {
+        int d = rS - t, j, o_next = -1;
+        if (d == 1) j = L;
+        else {
+            for (j = i + 1; j <= L - d + 1; j++) {
+                double tt = TD(d, slice_index(L, i, j), o);
+                if (tt <= tau && tt + AT(c->Wt, d - 1, j, o) == AT(c->V, d, i, o)) break;
+            }
+            for (o_next = o + 1; o_next < K; o_next++) {
+                double x = XA(j, o, o_next);
+                if (x <= tau && x + AT(c->V, d - 1, j, o_next) == AT(c->Wt, d - 1, j, o)) break;
+            }
+        }
+        tgo_stage *st = &plan->stage[t];
+        int64_t s = slice_index(L, i, j);
+        int64_t gk = s * K + o;
+        int64_t rep = -1;
+        for (int64_t a = c->gstart[gk]; a < c->gend[gk]; a++)
+            if (c->ent[a].dmax >= d) { rep = a; break; }
+        const oentry *e = &c->ent[rep];
+        int64_t g = e->idx / c->NS;
+        const ocfg *cf = &p->cfg[g];
+        ocoef co;
+        config_coef(p, cf, &co);
+        double cost, state, A1;
+        int dm;
+        score_candidate(p, &co, &p->slice_sum[s * 6], &cost, &dm, &state, &A1);
+        double inflight = (double)d < co.m_real ? (double)d : co.m_real;
+        st->island = c->order[o]; st->first_layer = i; st->end_layer = j;
+        st->tp = cf->tp; st->dp = cf->dp; st->ep = cf->ep; st->zero = cf->z; st->mb = cf->mb;
+        st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
+        st->mem_bytes = state + (inflight * A1);
+        st->link_out = d > 1 ? XA(j, o, o_next) : 0.0;
+        i = j;
+        o = o_next;
+    }
+}
+
+static int cmp_dbl(const void *a, const void *b) {
+    double x = *(const double *)a, y = *(const double *)b;
+    return (x > y) - (x < y);
+}
+
+/* Step (4): the stage and link costs above P* in ascending order are the
+   relaxed bounds at which the least fill can drop.  Returns them (distinct,
+   ascending) for the bounds whose iteration time could still beat `best`
+   given that no plan fills less than Finf; *nt gets the count. */
+static double *relaxed_bounds(octx *c, double Pst, double Finf, double best, int64_t *nt) {
+    const int L = c->L, K = c->K, D = c->D;
+    const int64_t cap = (int64_t)D * c->NS * K + (int64_t)L * K * K;
+    double *th = (double *)malloc(sizeof(double) * (cap > 0 ? cap : 1));
+    int64_t n = 0;
+    const double mm1 = (double)(c->m - 1);
+    for (int d = 1; d <= D; d++)
+        for (int64_t s = 0; s < c->NS; s++)
+            for (int o = 0; o < K; o++) {
+                double v = TD(d, s, o);
+                if (v > Pst && v < INFINITY && (mm1 * v) + Finf < best) th[n++] = v;
+            }
+    for (int j = 1; j < L; j++)
+        for (int o = 0; o < K; o++)
+            for (int o2 = o + 1; o2 < K; o2++) {
+                double v = XA(j, o, o2);
+                if (v > Pst && v < INFINITY && (mm1 * v) + Finf < best) th[n++] = v;
+            }
+    qsort(th, (size_t)n, sizeof(double), cmp_dbl);
+    int64_t u = 0;
+    for (int64_t a = 0; a < n; a++)
+        if (u == 0 || th[a] != th[u - 1]) th[u++] = th[a];
+    *nt = u;
+    return th;
+}
+
+/* Composition.  relax = 0: steps (1)-(3) per b (least bottleneck, then least
+   fill at it).  relax = 1: also step (4), relaxing the bound over the stage
+   and link costs above P* in ascending order while the iteration time can
+   still improve; per b the least T wins, ties to the smaller bound.
+   per_b (may be NULL): relax = 0: nb x 3 (P*, F*, T); relax = 1: nb x 4
+   (P*, chosen bound, F at it, T). */
+static int compose_impl(void *h, const int64_t *cands, int64_t n, const int32_t *order, tgo_plan *plan,
+                        double *per_b, int relax) {
     oprob *p = (oprob *)h;
     const int L = p->L, K = p->K;
     const int64_t NS = p->NS;
+    const int ncol = relax ? 4 : 3;
     memset(plan, 0, sizeof(tgo_plan));
     plan->status = TGO_ENOPLAN;
     plan->T = INFINITY; plan->P = INFINITY; plan->F = INFINITY;
@@ -547,194 +759,101 @@ int tgo_compose(void *h, const int64_t *cands, int64_t n, const int32_t *order, 
             free(pos); free(ent); return TGO_EINVAL;
         }
         int64_t g = idx / NS, s = idx % NS;
-        const ocfg *c = &p->cfg[g];
-        if (p->B % c->b != 0) { free(pos); free(ent); return TGO_EINVAL; }
+        const ocfg *cf = &p->cfg[g];
+        if (p->B % cf->b != 0) { free(pos); free(ent); return TGO_EINVAL; }
         int bi = 0;
-        while (p->bvals[bi] != c->b) bi++;
+        while (p->bvals[bi] != cf->b) bi++;
         ocoef o;
-        config_coef(p, c, &o);
+        config_coef(p, cf, &o);
         oentry *e = &ent[ne];
         score_candidate(p, &o, &p->slice_sum[s * 6], &e->cost, &e->dmax, NULL, NULL);
         if (e->dmax < 1) continue;
-        e->gkey = ((int64_t)bi * NS + s) * K + pos[c->k];
+        e->gkey = ((int64_t)bi * NS + s) * K + pos[cf->k];
         e->idx = idx;
         ne++;
     }
     qsort(ent, (size_t)ne, sizeof(oentry), cmp_entry);
 
-    const int D = K < L ? K : L; /* a pipeline has at most min(K, L) stages */
+    octx cx;
+    octx *c = &cx;
+    c->p = p; c->order = order; c->L = L; c->K = K; c->NS = NS; c->ent = ent;
+    c->D = K < L ? K : L; /* a pipeline has at most min(K, L) stages */
     const int64_t cell = (int64_t)(L + 1) * K;
-    double *V = (double *)malloc(sizeof(double) * (D + 1) * cell);
-    double *Wt = (double *)malloc(sizeof(double) * (D + 1) * cell);
-    double *Td = (double *)malloc(sizeof(double) * (D + 1) * NS * K); /* Td[d][s][o] */
-    double *X = (double *)malloc(sizeof(double) * (L + 1) * K * K);   /* X[j][o][o'] */
-    int64_t *gstart = (int64_t *)malloc(sizeof(int64_t) * NS * K);
-    int64_t *gend = (int64_t *)malloc(sizeof(int64_t) * NS * K);
-    if (!V || !Wt || !Td || !X || !gstart || !gend) {
-        free(pos); free(ent); free(V); free(Wt); free(Td); free(X); free(gstart); free(gend);
+    c->V = (double *)malloc(sizeof(double) * (c->D + 1) * cell);
+    c->Wt = (double *)malloc(sizeof(double) * (c->D + 1) * cell);
+    c->Td = (double *)malloc(sizeof(double) * (c->D + 1) * NS * K);
+    c->X = (double *)malloc(sizeof(double) * (L + 1) * K * K);
+    c->gstart = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    c->gend = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    if (!c->V || !c->Wt || !c->Td || !c->X || !c->gstart || !c->gend) {
+        free(pos); free(ent); free(c->V); free(c->Wt); free(c->Td); free(c->X); free(c->gstart); free(c->gend);
         return TGO_ENOMEM;
     }
-#define AT(A, d, i, o) A[((int64_t)(d) * (L + 1) + (i)) * K + (o)]
-#define TD(d, s, o) Td[((int64_t)(d) * NS + (s)) * K + (o)]
-#define XA(j, o, o2) X[((int64_t)(j) * K + (o)) * K + (o2)]
 
     double bestT = INFINITY;
-    int best_bi = -1, best_o = -1, best_S = -1;
-    double bestP = INFINITY, bestF = INFINITY;
     int64_t e0 = 0;
     for (int bi = 0; bi < p->nb; bi++) {
-        int64_t b = p->bvals[bi];
-        int64_t m = p->B / b;
-        if (per_b) { per_b[bi * 3] = INFINITY; per_b[bi * 3 + 1] = INFINITY; per_b[bi * 3 + 2] = INFINITY; }
-        /* group ranges of this b */
-        for (int64_t a = 0; a < NS * K; a++) { gstart[a] = 0; gend[a] = 0; }
+        c->b = p->bvals[bi];
+        c->m = p->B / c->b;
+        if (per_b)
+            for (int q = 0; q < ncol; q++) per_b[bi * ncol + q] = INFINITY;
         int64_t e1 = e0;
         while (e1 < ne && ent[e1].gkey / (NS * K) == bi) e1++;
-        for (int64_t a = e0; a < e1; a++) {
-            int64_t gk = ent[a].gkey % (NS * K);
-            if (gend[gk] == 0) gstart[gk] = a;
-            gend[gk] = a + 1;
+        build_tables(c, e0, e1, bi);
+        e0 = e1;
+        double Pst = least_bottleneck(c);
+        if (!(Pst < INFINITY)) continue;
+        int ro, rS;
+        double Fst = least_fill(c, Pst, &ro, &rS);
+        if (ro < 0) continue;
+        const double mm1 = (double)(c->m - 1);
+        double tau = Pst;
+        double Tb = (mm1 * Pst) + Fst;
+        if (relax) {
+            /* step (4): relax the bound while T can still improve */
+            int ro2, rS2;
+            double Finf = least_fill(c, INFINITY, &ro2, &rS2);
+            int64_t nt = 0;
+            double *th = relaxed_bounds(c, Pst, Finf, Tb, &nt);
+            for (int64_t a = 0; a < nt; a++) {
+                if ((mm1 * th[a]) + Finf >= Tb) break; /* no larger bound can improve */
+                double F = least_fill(c, th[a], &ro2, &rS2);
+                double Tt = (mm1 * th[a]) + F;
+                if (Tt < Tb) { Tb = Tt; tau = th[a]; }
+            }
+            free(th);
+            Fst = least_fill(c, tau, &ro, &rS); /* tables at the chosen bound */
         }
-        /* stage table: Td(d, s, o) = least cost of the group's entries that fit
-           at depth d; entries are key-sorted, so the first fitting one. */
-        for (int d = 1; d <= D; d++)
-            for (int64_t s = 0; s < NS; s++)
-                for (int o = 0; o < K; o++) {
-                    double v = INFINITY;
-                    int64_t gk = s * K + o;
-                    for (int64_t a = gstart[gk]; a < gend[gk]; a++)
-                        if (ent[a].dmax >= d) { v = ent[a].cost; break; }
-                    TD(d, s, o) = v;
-                }
-        for (int j = 1; j < L; j++)
-            for (int o = 0; o < K; o++)
-                for (int o2 = 0; o2 < K; o2++)
-                    XA(j, o, o2) = transfer(p, b, j, order[o], order[o2]);
-
-        /* Phase 1, steps (1)-(2): least achievable bottleneck.
-           V(d,i,o): best bottleneck covering layers [i, L) with d stages, the
-           first on island position o and the rest on later positions.
-           W(d,j,o): best continuation after a stage on position o ends at j. */
-        for (int d = 1; d <= D; d++) {
-            for (int i = 0; i < L; i++)
-                for (int o = 0; o < K; o++) {
-                    double v = INFINITY;
-                    if (d == 1) v = TD(1, slice_index(L, i, L), o);
-                    else
-                        for (int j = i + 1; j <= L - d + 1; j++) {
-                            double c = maxd(TD(d, slice_index(L, i, j), o), AT(Wt, d - 1, j, o));
-                            if (c < v) v = c;
-                        }
-                    AT(V, d, i, o) = v;
-                }
-            for (int j = 1; j < L; j++)
-                for (int o = 0; o < K; o++) {
-                    double w = INFINITY;
-                    for (int o2 = o + 1; o2 < K; o2++) {
-                        double c = maxd(XA(j, o, o2), AT(V, d, j, o2));
-                        if (c < w) w = c;
-                    }
-                    AT(Wt, d, j, o) = w;
-                }
-        }
-        double Pst = INFINITY;
-        for (int d = 1; d <= D; d++)
-            for (int o = 0; o < K; o++)
-                if (AT(V, d, 0, o) < Pst) Pst = AT(V, d, 0, o);
-        if (!(Pst < INFINITY)) { e0 = e1; continue; }
-
-        /* Phase 2, step (3): least fill among plans whose every stage and link
-           stays within the bottleneck P*.  Fill = f1 + (x1 + (f2 + ... + fS)),
-           a right fold; F and G reuse the V and W arrays. */
-        for (int d = 1; d <= D; d++) {
-            for (int i = 0; i < L; i++)
-                for (int o = 0; o < K; o++) {
-                    double v = INFINITY;
-                    if (d == 1) {
-                        double t = TD(1, slice_index(L, i, L), o);
-                        if (t <= Pst) v = t;
-                    } else
-                        for (int j = i + 1; j <= L - d + 1; j++) {
-                            double t = TD(d, slice_index(L, i, j), o);
-                            if (!(t <= Pst)) continue;
-                            double c = t + AT(Wt, d - 1, j, o);
-                            if (c < v) v = c;
-                        }
-                    AT(V, d, i, o) = v;
-                }
-            for (int j = 1; j < L; j++)
-                for (int o = 0; o < K; o++) {
-                    double w = INFINITY;
-                    for (int o2 = o + 1; o2 < K; o2++) {
-                        double x = XA(j, o, o2);
-                        if (!(x <= Pst)) continue;
-                        double c = x + AT(V, d, j, o2);
-                        if (c < w) w = c;
-                    }
-                    AT(Wt, d, j, o) = w;
-                }
-        }
-        /* root: least fill, ties to the earliest island position, then fewer stages */
-        double Fst = INFINITY;
-        int ro = -1, rS = -1;
-        for (int o = 0; o < K; o++)
-            for (int d = 1; d <= D; d++)
-                if (AT(V, d, 0, o) < Fst) { Fst = AT(V, d, 0, o); ro = o; rS = d; }
-        if (ro < 0) { e0 = e1; continue; }
-        double Tb = ((double)(m - 1) * Pst) + Fst;
-        if (per_b) { per_b[bi * 3] = Pst; per_b[bi * 3 + 1] = Fst; per_b[bi * 3 + 2] = Tb; }
-        if (Tb < bestT) {
-            /* backtrack now, while this b's tables are live */
-            bestT = Tb; best_bi = bi; best_o = ro; best_S = rS; bestP = Pst; bestF = Fst;
-            plan->status = TGO_OK;
-            plan->b = (int32_t)b; plan->m = (int32_t)m; plan->S = rS;
-            plan->P = Pst; plan->F = Fst; plan->T = Tb;
-            int i = 0, o = ro;
-            for (int t = 0; t < rS; t++) {
-                int d = rS - t, j, o_next = -1;
-                if (d == 1) j = L;
-                else {
-                    /* smallest j attaining F(d, i, o) */
-                    for (j = i + 1; j <= L - d + 1; j++) {
-                        double tt = TD(d, slice_index(L, i, j), o);
-                        if (tt <= Pst && tt + AT(Wt, d - 1, j, o) == AT(V, d, i, o)) break;
-                    }
-                    /* smallest later position attaining G(d-1, j, o) */
-                    for (o_next = o + 1; o_next < K; o_next++) {
-                        double x = XA(j, o, o_next);
-                        if (x <= Pst && x + AT(V, d - 1, j, o_next) == AT(Wt, d - 1, j, o)) break;
-                    }
-                }
-                tgo_stage *st = &plan->stage[t];
-                int64_t s = slice_index(L, i, j);
-                int64_t gk = s * K + o;
-                int64_t rep = -1;
-                for (int64_t a = gstart[gk]; a < gend[gk]; a++)
-                    if (ent[a].dmax >= d) { rep = a; break; }
-                const oentry *e = &ent[rep];
-                int64_t g = e->idx / NS;
-                const ocfg *c = &p->cfg[g];
-                ocoef co;
-                config_coef(p, c, &co);
-                double cost, state, A1;
-                int dm;
-                score_candidate(p, &co, &p->slice_sum[s * 6], &cost, &dm, &state, &A1);
-                double inflight = (double)d < co.m_real ? (double)d : co.m_real;
-                st->island = order[o]; st->first_layer = i; st->end_layer = j;
-                st->tp = c->tp; st->dp = c->dp; st->ep = c->ep; st->zero = c->z; st->mb = c->mb;
-                st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
-                st->mem_bytes = state + (inflight * A1);
-                st->link_out = d > 1 ? XA(j, o, o_next) : 0.0;
-                i = j;
-                o = o_next;
+        if (per_b) {
+            per_b[bi * ncol] = Pst;
+            if (relax) {
+                per_b[bi * ncol + 1] = tau; per_b[bi * ncol + 2] = Fst; per_b[bi * ncol + 3] = Tb;
+            } else {
+                per_b[bi * ncol + 1] = Fst; per_b[bi * ncol + 2] = Tb;
             }
         }
-        e0 = e1;
+        if (Tb < bestT) {
+            /* backtrack now, while this b's tables are live */
+            bestT = Tb;
+            plan->status = TGO_OK;
+            plan->b = (int32_t)c->b; plan->m = (int32_t)c->m; plan->S = rS;
+            plan->P = tau; plan->F = Fst; plan->T = Tb;
+            backtrack(c, tau, ro, rS, plan);
+        }
     }
-    (void)best_bi; (void)best_o; (void)best_S; (void)bestP; (void)bestF;
+    free(pos); free(ent); free(c->V); free(c->Wt); free(c->Td); free(c->X); free(c->gstart); free(c->gend);
+    return plan->status;
+}
 #undef AT
 #undef TD
 #undef XA
-    free(pos); free(ent); free(V); free(Wt); free(Td); free(X); free(gstart); free(gend);
-    return plan->status;
+
+int tgo_compose(void *h, const int64_t *cands, int64_t n, const int32_t *order, tgo_plan *plan,
+                double *per_b /* nb x 3: P*, F*, T; may be NULL */) {
+    return compose_impl(h, cands, n, order, plan, per_b, 0);
+}
+
+int tgo_compose_relaxed(void *h, const int64_t *cands, int64_t n, const int32_t *order, tgo_plan *plan,
+                        double *per_b /* nb x 4: P*, bound, F, T; may be NULL */) {
+    return compose_impl(h, cands, n, order, plan, per_b, 1);
 }

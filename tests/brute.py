@@ -81,8 +81,11 @@ def right_fold(f, x):
     return acc
 
 
-def brute_force_compose(orc, rows, order=None, allowed=None):
-    """Exhaustive composition.  Returns per-b (P*, F*, T) and the optimum.
+def enumerate_plans(orc, rows, order=None, allowed=None):
+    """Every feasible plan per b: dict b -> list of plans, each with its
+    bottleneck P, fill F, lexicographic key (o_1, S, j_1, o_2, j_2, ...) and
+    the chosen candidate per stage (the group's least-key member fitting at
+    the stage's depth).
 
     `allowed`: optional set of candidate indices that may be used (default:
     every compatible candidate)."""
@@ -98,8 +101,7 @@ def brute_force_compose(orc, rows, order=None, allowed=None):
                if r["dmax"] >= d and (allowed is None or r["idx"] in allowed)]
         return min(fit, key=key) if fit else None
 
-    per_b = {}
-    best = None
+    out = {}
     for b in orc.bvalues:
         m = B // b
         plans = []
@@ -130,9 +132,21 @@ def brute_force_compose(orc, rows, order=None, allowed=None):
                         pk += [cuts[t], posn[t + 1]]
                     plans.append({"P": P, "F": F, "key": tuple(pk), "posn": posn, "cuts": cuts,
                                   "picks": picks, "f": f, "x": x, "b": b, "m": m, "L": L})
+        out[b] = plans
+    return out
+
+
+def brute_force_compose(orc, rows, order=None, allowed=None):
+    """Exhaustive composition with the objective of steps (1)-(3): per b the
+    least bottleneck P*, then the least fill among plans attaining it.
+    Returns per-b (P*, F*, T) and the optimum."""
+    per_b = {}
+    best = None
+    for b, plans in enumerate_plans(orc, rows, order, allowed).items():
         if not plans:
             per_b[b] = (math.inf, math.inf, math.inf)
             continue
+        m = plans[0]["m"]
         Pst = min(p["P"] for p in plans)
         at = [p for p in plans if p["P"] == Pst]
         Fst = min(p["F"] for p in at)
@@ -142,6 +156,36 @@ def brute_force_compose(orc, rows, order=None, allowed=None):
         lexmin = min(opt, key=lambda p: p["key"])
         if best is None or T < best["T"]:
             best = {"T": T, "b": b, "P": Pst, "F": Fst, "lexmin": lexmin, "optimal": opt}
+    return per_b, best
+
+
+def brute_force_relaxed(orc, rows, order=None, allowed=None):
+    """Exhaustive composition with the iteration time itself as the objective
+    (step (4) relaxes the bottleneck bound until T stops improving): per b the
+    least T = (m-1) * P + F over every plan; among plans attaining it the
+    least P is the bound tau; the plan is then the least-fill plan among those
+    whose every stage and link is within tau, lexicographically least key.
+    Returns per-b (P*, tau, F, T) and the optimum."""
+    per_b = {}
+    best = None
+    for b, plans in enumerate_plans(orc, rows, order, allowed).items():
+        if not plans:
+            per_b[b] = (math.inf, math.inf, math.inf, math.inf)
+            continue
+        m = plans[0]["m"]
+        Pst = min(p["P"] for p in plans)
+        for p in plans:
+            p["T"] = (float(m - 1) * p["P"]) + p["F"]
+        T = min(p["T"] for p in plans)
+        tau = min(p["P"] for p in plans if p["T"] == T)
+        within = [p for p in plans if p["P"] <= tau]
+        F = min(p["F"] for p in within)
+        opt = [p for p in within if p["F"] == F]
+        assert (float(m - 1) * tau) + F == T
+        per_b[b] = (Pst, tau, F, T)
+        lexmin = min(opt, key=lambda p: p["key"])
+        if best is None or T < best["T"]:
+            best = {"T": T, "b": b, "P": tau, "F": F, "lexmin": lexmin, "optimal": opt}
     return per_b, best
 
 
