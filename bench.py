@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--cpu-islands", type=int, default=24,
                     help="islands of the CPU-baseline sample (first islands of the workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
+    ap.add_argument("--relaxed-steps", type=int, default=5,
+                    help="also time the composition with the step-(4) relaxation this many times "
+                         "(0 skips it); reported beside the main metric, not in it")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, copy BYTES between two device buffers (a plain copy of "
                          "known size that scales profiler byte counters)")
@@ -179,6 +182,22 @@ def main():
     compose_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.steps)]
 
     mean = lambda xs: sum(xs) / len(xs)
+    # composition with the step-(4) relaxation, timed after the main loop on
+    # the same survivors (host clock around the call: it synchronises per round)
+    relaxed = None
+    if args.relaxed_steps > 0:
+        rws = p.compose_relaxed_workspace(int(s.numel()))
+        p.tg_compose_pipeline_relaxed(s, cost, dmax, workspace=rws)  # warm-up
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(args.relaxed_steps):
+            t1 = time.perf_counter()
+            rst, rplan = p.tg_compose_pipeline_relaxed(s, cost, dmax, workspace=rws)
+            times.append((time.perf_counter() - t1) * 1e3)
+        times.sort()
+        relaxed = {"compose_ms_median": times[len(times) // 2], "status": rst, "b": rplan["b"],
+                   "stages": rplan["S"], "P": rplan["P"], "T": rplan["T"]}
+        del rws
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
     traffic = measured_traffic(args.workload, N)
@@ -204,6 +223,7 @@ def main():
         "breakdown_ms": {"score": mean(score_ms), "prune": mean(prune_ms),
                          "compose": mean(compose_ms), "create": t_create * 1e3},
         "score_kernel_pairs_per_s": N / score_s,
+        "relaxed_compose": relaxed,
         "end_to_end_s": elapsed / args.steps,
     }
     if not args.no_cpu:

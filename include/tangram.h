@@ -227,6 +227,28 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
                               const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
                               tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream);
 
+/*
+ * Composition with the relaxation of step (4) of Sec. 5.2: after the least
+ * bottleneck P* and the least fill at it, the bound on every stage and link
+ * is raised over the stage and link costs above P* while the iteration time
+ * can still improve.  Per b the plan minimises T = (m - 1) * tau + F(tau)
+ * over bounds tau >= P*, where F(tau) is the least fill among plans whose
+ * every stage cost and link time is <= tau; ties go to the smallest tau, and
+ * the plan is the one tg_compose_pipeline's rules pick at that bound (least
+ * fill, then earliest first island, fewer stages, earliest cut, earliest next
+ * island).  This is the least T over every plan of that b.  Across b: least
+ * T, ties to the smaller b.  out->P is the chosen bound (the plan's
+ * bottleneck), out->F its fill, out->T = (m - 1) * P + F.  Arguments, list
+ * requirements and errors as for tg_compose_pipeline; d_ws: at least
+ * tg_compose_relaxed_workspace_bytes(p, n_survivors) bytes.  Synchronises the
+ * stream once per search round (a few rounds; each evaluates F at a batch of
+ * bounds on the device).
+ */
+size_t tg_compose_relaxed_workspace_bytes(const tg_problem *p, int64_t n_survivors);
+tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                      const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                                      tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream);
+
 /* Message of the calling thread's last failed call ("" if none). */
 const char *tg_last_error(void);
 

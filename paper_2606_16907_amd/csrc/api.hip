@@ -284,6 +284,9 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.Eidx = (const uint16_t *)(base + parts[15].off);
     pr->bvals = bv;
     pr->n_compat_cfg = (int64_t)row_cfg.size();
+    pr->B = space->global_batch;
+    pr->outact = outact;
+    pr->E.assign(inter_bw, inter_bw + (size_t)K * K);
     // the per-config coefficients are computed on the device
     e = tg::launch_coef(P, (tg::Coef *)(base + parts[4].off), nullptr);
     if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -377,9 +380,17 @@ size_t tg_compose_workspace_bytes(const tg_problem *p, int64_t n_survivors) {
     return tg::compose_ws_bytes(p->P, n_survivors);
 }
 
-tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
-                              const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
-                              tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
+size_t tg_compose_relaxed_workspace_bytes(const tg_problem *p, int64_t n_survivors) {
+    if (!p || n_survivors < 0) return 0;
+    return tg::compose_relaxed_ws_bytes(p->P, n_survivors);
+}
+
+}  // extern "C"
+
+// Argument checks shared by both compositions; uploads the island order.
+static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                               const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                               tg_plan *out, void *d_ws, size_t ws_bytes, size_t need, hipStream_t s) {
     if (!p || !out || !island_order) return fail(TG_EINVAL, "NULL argument");
     std::memset(out, 0, sizeof(*out));
     out->P = out->F = out->T = HUGE_VAL;
@@ -393,21 +404,20 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
     if (n_survivors < 0 || n_survivors > ((int64_t)1 << 30) || (n_survivors > 0 && !d_survivors))
         return fail(TG_EINVAL, "bad survivor list");
     if (n_survivors > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL score arrays");
-    if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31))
-        return fail(TG_EINVAL, "stage table too large");
-    const size_t need = tg::compose_ws_bytes(p->P, n_survivors);
+    if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31)) return fail(TG_EINVAL, "stage table too large");
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (p->P.nb == 0) return fail(TG_ENOPLAN, "no micro-batch size divides the global batch");
-    hipStream_t s = (hipStream_t)stream;
     hipError_t e = hipMemcpyAsync((char *)d_ws + tg::compose_order_offset(p->P, n_survivors), island_order,
                                   sizeof(int32_t) * K, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "order upload");
-    tg::ComposeResult *res_dev = nullptr;
-    e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
-    if (e != hipSuccess) return hip_fail(e, "compose kernels");
+    return TG_OK;
+}
+
+// Reads the device result after the composition kernels.
+static tg_status compose_end(tg::ComposeResult *res_dev, tg_plan *out, hipStream_t s) {
     tg::ComposeResult *res = new (std::nothrow) tg::ComposeResult;
     if (!res) return fail(TG_ENOMEM, "host allocation");
-    e = hipMemcpyAsync(res, res_dev, sizeof(*res), hipMemcpyDeviceToHost, s);
+    hipError_t e = hipMemcpyAsync(res, res_dev, sizeof(*res), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         delete res;
@@ -426,6 +436,39 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
     }
     delete res;
     return st;
+}
+
+extern "C" {
+
+tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                              const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                              tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    hipStream_t s = (hipStream_t)stream;
+    const size_t need = p && n_survivors >= 0 ? tg::compose_ws_bytes(p->P, n_survivors) : 0;
+    tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
+                                 need, s);
+    if (st != TG_OK) return st;
+    tg::ComposeResult *res_dev = nullptr;
+    hipError_t e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
+    if (e != hipSuccess) return hip_fail(e, "compose kernels");
+    return compose_end(res_dev, out, s);
+}
+
+tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                      const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                                      tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    hipStream_t s = (hipStream_t)stream;
+    const size_t need = p && n_survivors >= 0 ? tg::compose_relaxed_ws_bytes(p->P, n_survivors) : 0;
+    tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
+                                 need, s);
+    if (st != TG_OK) return st;
+    const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B};
+    tg::ComposeResult *res_dev = nullptr;
+    int rounds = 0;
+    hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax, d_ws,
+                                              s, &res_dev, &rounds);
+    if (e != hipSuccess) return hip_fail(e, "relaxed compose kernels");
+    return compose_end(res_dev, out, s);
 }
 
 }  // extern "C"

@@ -25,6 +25,8 @@
 // improve it.  This holds whenever the candidate list contains the surviving
 // set, since then T_d equals the least cost over all group members.
 #include <algorithm>
+#include <cmath>
+#include <vector>
 #include <climits>
 #include <type_traits>
 
@@ -751,12 +753,20 @@ __device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
     return v1 < v2 || (v1 == v2 && a1 < a2);
 }
 
-// Phase 2: fill values and argmins at the bottleneck P*.
-template <int KP, int SPLIT>
+// Phase 2: fill values and argmins at a bound on every stage and link (the
+// bottleneck P* of phase 1, or a relaxed bound).  Block (i, b) with b's bound
+// bound[b]; a b whose bound is +inf is skipped.  With kJobs, block (i, job)
+// computes fill values only for job = (job_b, job_tau): its own continuation
+// rows (Gprev/Gnext indexed by job), its least root fill in rootF[job], no
+// argmins.  Several jobs may share one b's table, so the row's table changes
+// are applied by the last of its jobs' blocks to finish reading: each block
+// counts itself on row_cnt[b][i] after its reads (jobs_of_b[b] blocks in all),
+// and the last one writes the changes and resets the counter.
+template <int KP, int SPLIT, bool kJobs>
 __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fill(
     DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
-    const double *T1, const double *Gprev, double *Gnext, const double *EoT, const uint8_t *EiT, const double *Pst,
-    uint16_t *argF,
+    const double *T1, const double *Gprev, double *Gnext, const double *EoT, const uint8_t *EiT, const double *bound,
+    const int32_t *job_b, const double *job_tau, const int32_t *jobs_of_b, int32_t *row_cnt, uint16_t *argF,
     uint8_t *argG, double *rootF, int32_t *root_o, int32_t *root_d) {
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
@@ -766,11 +776,13 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
     __shared__ double xs[kMaxDistinctE];
     __shared__ uint64_t lmask[KP / kWave];
     __shared__ int32_t list[KP];
-    const int i = blockIdx.x, bi = blockIdx.y;
+    __shared__ int32_t last_reader;
+    const int i = blockIdx.x, row = blockIdx.y;  // row: b, or the job
+    const int bi = kJobs ? job_b[row] : row;
     const int L = P.L, K = P.K;
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     const int top = K - d;
-    const double Ps = Pst[bi];
+    const double Ps = kJobs ? job_tau[row] : bound[bi];
     if (!(Ps < kInf)) return;
     RowEvents ev;
     event_bounds(ev, P, d, bi, i, bcnt);
@@ -789,7 +801,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
                 }
             }
         } else {
-            const double *Gp = Gprev + (int64_t)bi * (L + 1) * K + o;
+            const double *Gp = Gprev + (int64_t)row * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
             bool go = true;
@@ -823,7 +835,16 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
     store_links(lr, X, P, i, top, xs, tri_s);
     __syncthreads();
     // every read of this row's table is done
-    load_events(ev, ev_cell, ev_val);
+    // (every read of the block has returned its value before the barrier above,
+    // so counting needs no fence; the next level reads the table after the
+    // kernel boundary)
+    bool apply = true;
+    if (kJobs) {
+        if (threadIdx.x == 0) last_reader = atomicAdd(&row_cnt[(int64_t)bi * L + i], 1) == jobs_of_b[bi] - 1;
+        __syncthreads();
+        apply = last_reader != 0;
+    }
+    if (apply) load_events(ev, ev_cell, ev_val);
     if (sub == 0) {
         double m = part[0][o];
         int a = parg[0][o];
@@ -834,7 +855,8 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
                 a = parg[k][o];
             }
         Fs[o] = m;
-        if (o < K) argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)(m < kInf ? a : 0xFFFF);
+        if (!kJobs && o < K)
+            argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)(m < kInf ? a : 0xFFFF);
         publish_live(o <= top && m < kInf, lmask);
     }
     __syncthreads();
@@ -847,14 +869,17 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
                     m = Fs[t];
                     mo = t;
                 }
-            // lexicographic (fill, position, depth); depths arrive in ascending order
-            if (mo >= 0 && (m < rootF[bi] || (m == rootF[bi] && mo < root_o[bi]))) {
+            if (kJobs) {
+                if (m < rootF[row]) rootF[row] = m;
+            } else if (mo >= 0 && (m < rootF[bi] || (m == rootF[bi] && mo < root_o[bi]))) {
+                // lexicographic (fill, position, depth); depths arrive in ascending order
                 rootF[bi] = m;
                 root_o[bi] = mo;
                 root_d[bi] = d;
             }
         }
-        store_events(ev, ev_cell, ev_val, T);
+        if (apply) store_events(ev, ev_cell, ev_val, T);
+        if (kJobs && apply && threadIdx.x == 0) atomicExch(&row_cnt[(int64_t)bi * L + i], 0);
         return;
     }
     const LiveList lv = build_live<KP>(o, sub, top, lmask, list);
@@ -886,10 +911,11 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
                 m = part[k][o];
                 aa = parg[k][o];
             }
-        Gnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
-        argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)(m < kInf ? aa : 0xFF);
+        Gnext[((int64_t)row * (L + 1) + i) * K + o] = m;
+        if (!kJobs) argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)(m < kInf ? aa : 0xFF);
     }
-    store_events(ev, ev_cell, ev_val, T);
+    if (apply) store_events(ev, ev_cell, ev_val, T);
+    if (kJobs && apply && threadIdx.x == 0) atomicExch(&row_cnt[(int64_t)bi * L + i], 0);
 }
 
 // Threads per cell for a level of `blocks` blocks: the most (up to 4) whose
@@ -905,7 +931,7 @@ struct LevelKernels {
             hipSuccess)
             return INT_MAX;
         int per_cu2 = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu2, level_fill<KP, SPLIT>, SPLIT * KP, lds) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu2, level_fill<KP, SPLIT, false>, SPLIT * KP, lds) !=
             hipSuccess)
             return INT_MAX;
         return std::min(per_cu, per_cu2) * n_cu;
@@ -1072,110 +1098,485 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
     }
 }
 
+// ---------------------------------------------------------------------------
+// host-side sequencing
+// ---------------------------------------------------------------------------
+// Workspace of the relaxed search, after the composition workspace.
+constexpr int kMaxJobs = 128;  // fill evaluations per launch
+
+struct RelaxWs {
+    double *th_val;   // [n_surv] collected stage-cost bounds
+    int32_t *th_b;    // [n_surv] their b
+    int32_t *th_cnt;  // [1]
+    double *lo;       // [nb] P* per b (bounds must exceed it)
+    double *hi;       // [nb] T at P* per b
+    double *mm1;      // [nb] m - 1 per b
+    int32_t *job_b;   // [kMaxJobs]
+    int32_t *jobs_of_b;  // [nb] jobs of each b in the current run
+    int32_t *row_cnt;    // [nb][L] readers done per row (job runs)
+    double *job_tau;  // [kMaxJobs]
+    double *job_F;    // [kMaxJobs]
+    double *job_G;    // [2][kMaxJobs][L+1][K]
+    double *bound;    // [nb]
+    size_t bytes;
+};
+
+static RelaxWs carve_relax(const DevProblem &P, int64_t n, void *base) {
+    RelaxWs r{};
+    char *p = (char *)base;
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> void * {
+        void *x = base ? (void *)(p + off) : nullptr;
+        off += align256(bytes > 0 ? bytes : 1);
+        return x;
+    };
+    const int64_t jrows = (int64_t)kMaxJobs * (P.L + 1) * P.K;
+    r.th_val = (double *)take(sizeof(double) * n);
+    r.th_b = (int32_t *)take(sizeof(int32_t) * n);
+    r.th_cnt = (int32_t *)take(sizeof(int32_t));
+    r.lo = (double *)take(sizeof(double) * P.nb);
+    r.hi = (double *)take(sizeof(double) * P.nb);
+    r.mm1 = (double *)take(sizeof(double) * P.nb);
+    r.job_b = (int32_t *)take(sizeof(int32_t) * kMaxJobs);
+    r.jobs_of_b = (int32_t *)take(sizeof(int32_t) * P.nb);
+    r.row_cnt = (int32_t *)take(sizeof(int32_t) * P.nb * P.L);
+    r.job_tau = (double *)take(sizeof(double) * kMaxJobs);
+    r.job_F = (double *)take(sizeof(double) * kMaxJobs);
+    r.job_G = (double *)take(sizeof(double) * 2 * jrows);
+    r.bound = (double *)take(sizeof(double) * P.nb);
+    r.bytes = off;
+    return r;
+}
+
+size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv) {
+    return compose_ws_bytes(P, n_surv) + carve_relax(P, n_surv, nullptr).bytes;
+}
+
+// Stage costs that can serve as relaxed bounds for their b: above P*_b and
+// with (m-1) * cost below the iteration time at P*_b (a plan bounded by a
+// larger value cannot beat it, its fill being non-negative).  Every entry of
+// every group is a candidate; duplicates are removed on the host.
+__global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_t *__restrict__ gcnt,
+                                                      const double *__restrict__ ent_c, const double *lo,
+                                                      const double *hi, const double *mm1, double *th_val,
+                                                      int32_t *th_b, int32_t *th_cnt, int32_t cap) {
+    const int64_t G = (int64_t)P.nb * P.NS * P.K;
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < G; g += (int64_t)gridDim.x * blockDim.x) {
+        const int bi = (int)((g / P.NS) % P.nb);
+        const double l = lo[bi], h = hi[bi], f = mm1[bi];
+        if (!(l < kInf)) continue;
+        const int32_t st = g ? gcnt[g - 1] : 0, en = gcnt[g];
+        for (int32_t e = st; e < en; ++e) {
+            const double c = ent_c[e];
+            if (c > l && c < kInf && (f * c) < h) {
+                const int32_t slot = atomicAdd(th_cnt, 1);
+                if (slot < cap) {
+                    th_val[slot] = c;
+                    th_b[slot] = bi;
+                }
+            }
+        }
+    }
+}
+
+// Sequencing of the composition kernels on one workspace.
+struct Driver {
+    const DevProblem &P;
+    Ws w;
+    hipStream_t s;
+    int D;
+    int64_t rows;
+    size_t tri_lds;
+    dim3 tgrid;
+    int n_cu = 0;
+
+    Driver(const DevProblem &P_, int64_t n_surv, void *ws, hipStream_t s_)
+        : P(P_), w(carve(P_, n_surv, ws)), s(s_), D(levels(P_)), rows((int64_t)P_.nb * (P_.L + 1) * P_.K) {
+        tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
+        tgrid = dim3((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
+                     (unsigned)P.nb);
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            n_cu = 0;
+    }
+
+    // candidate list -> grouped entries -> per-level table changes
+    void setup(const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax) {
+        const int64_t G = n_groups(P), nbk = n_buckets(P);
+        prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT,
+                                                                                     w.EiT, w.res);
+        fill<int32_t>(w.gcnt, G, 0, s);
+        fill<int32_t>(w.bcnt, nbk + 1, 0, s);
+        fill<double>(w.Pst, P.nb, kInf, s);
+        if (n_surv > 0) {
+            int64_t blocks = (n_surv + 255) / 256;
+            if (blocks > 65536) blocks = 65536;
+            gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, cost, dmax, w.pos, w.rec_g,
+                                                                        w.rec_c, w.rec_d, w.gcnt, w.res);
+            scan_i32(w.gcnt, G, w.tmp, s);
+            scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n_surv, w.rec_g, w.rec_c, w.rec_d,
+                                                                         w.gcnt, w.ent_c, w.ent_d, w.ent_i);
+            const int nch = (int)(((int64_t)P.L * P.K + kEventCells - 1) / kEventCells);
+            const dim3 egrid((unsigned)(P.L * nch), (unsigned)P.nb);
+            group_events<false><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt,
+                                                           w.ev_cell, w.ev_val);
+            scan_i32(w.bcnt, nbk + 1, w.tmp, s);
+            copy_kernel<int32_t><<<dim3((unsigned)((nbk + 1 + 255) / 256)), dim3(256), 0, s>>>(w.bcnt, w.bcur,
+                                                                                              nbk + 1);
+            group_events<true><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcur,
+                                                          w.ev_cell, w.ev_val);
+        } else {
+            scan_i32(w.gcnt, G, w.tmp, s);  // all zeros: offsets stay zero
+        }
+    }
+
+    template <typename F>
+    void with_kp(F f) {
+        if (P.K <= 64)
+            f(std::integral_constant<int, 64>{});
+        else if (P.K <= 128)
+            f(std::integral_constant<int, 128>{});
+        else if (P.K <= 192)
+            f(std::integral_constant<int, 192>{});
+        else
+            f(std::integral_constant<int, 256>{});
+    }
+
+    template <int KP>
+    int split_for(int blocks) {
+        using LK = LevelKernels<KP>;
+        const int cap4 = LK::template capacity<4>(n_cu, tri_lds);
+        if (blocks <= cap4) return 4;
+        const int cap3 = LK::template capacity<3>(n_cu, tri_lds);
+        return blocks <= cap3 ? 3 : 2;
+    }
+
+    void start_tables(double *G0, double *G1, int64_t n) {
+        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
+        fill<double>(G0, n, kInf, s);
+        fill<double>(G1, n, kInf, s);
+    }
+
+    // phase 1: least bottleneck per b into w.Pst
+    void phase1() {
+        with_kp([&](auto kp) {
+            constexpr int KP = decltype(kp)::value;
+            start_tables(w.Wb[0], w.Wb[1], rows);
+            for (int d = 1; d <= D; ++d) {
+                const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
+                const int sp = split_for<KP>((int)(grid.x * grid.y));
+                const double *Wp = w.Wb[(d - 1) & 1];
+                double *Wn = w.Wb[d & 1];
+                auto go = [&](auto spc) {
+                    constexpr int SP = decltype(spc)::value;
+                    level_bottleneck<KP, SP><<<grid, dim3(SP * KP), tri_lds, s>>>(
+                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
+                };
+                if (sp == 4)
+                    go(std::integral_constant<int, 4>{});
+                else if (sp == 3)
+                    go(std::integral_constant<int, 3>{});
+                else
+                    go(std::integral_constant<int, 2>{});
+            }
+        });
+    }
+
+    // phase 2 at bound[b] (+inf skips b): fills, argmins and roots per b
+    void phase2(const double *bound) {
+        fill<double>(w.rootF, P.nb, kInf, s);
+        fill<int32_t>(w.root_o, P.nb, -1, s);
+        fill<int32_t>(w.root_d, P.nb, -1, s);
+        with_kp([&](auto kp) {
+            constexpr int KP = decltype(kp)::value;
+            start_tables(w.Wb[0], w.Wb[1], rows);
+            for (int d = 1; d <= D; ++d) {
+                const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
+                const int sp = split_for<KP>((int)(grid.x * grid.y));
+                const double *Gp = w.Wb[(d - 1) & 1];
+                double *Gn = w.Wb[d & 1];
+                auto go = [&](auto spc) {
+                    constexpr int SP = decltype(spc)::value;
+                    level_fill<KP, SP, false><<<grid, dim3(SP * KP), tri_lds, s>>>(
+                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, bound, nullptr,
+                        nullptr, nullptr, nullptr, w.argF, w.argG, w.rootF, w.root_o, w.root_d);
+                };
+                if (sp == 4)
+                    go(std::integral_constant<int, 4>{});
+                else if (sp == 3)
+                    go(std::integral_constant<int, 3>{});
+                else
+                    go(std::integral_constant<int, 2>{});
+            }
+        });
+    }
+
+    // fill values only, for J <= kMaxJobs (b, bound) jobs staged in r
+    void phase2_jobs(RelaxWs &r, int J) {
+        const int64_t jrows = (int64_t)kMaxJobs * (P.L + 1) * P.K;
+        fill<double>(r.job_F, J, kInf, s);
+        fill<int32_t>(r.row_cnt, (int64_t)P.nb * P.L, 0, s);
+        with_kp([&](auto kp) {
+            constexpr int KP = decltype(kp)::value;
+            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K);
+            for (int d = 1; d <= D; ++d) {
+                const dim3 grid((unsigned)(P.L - d + 1), (unsigned)J);
+                const int sp = split_for<KP>((int)(grid.x * grid.y));
+                const double *Gp = r.job_G + ((d - 1) & 1) * jrows;
+                double *Gn = r.job_G + (d & 1) * jrows;
+                auto go = [&](auto spc) {
+                    constexpr int SP = decltype(spc)::value;
+                    level_fill<KP, SP, true><<<grid, dim3(SP * KP), tri_lds, s>>>(
+                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, nullptr, r.job_b,
+                        r.job_tau, r.jobs_of_b, r.row_cnt, nullptr, nullptr, r.job_F, nullptr, nullptr);
+                };
+                if (sp == 4)
+                    go(std::integral_constant<int, 4>{});
+                else if (sp == 3)
+                    go(std::integral_constant<int, 3>{});
+                else
+                    go(std::integral_constant<int, 2>{});
+            }
+        });
+    }
+
+    void finish(const double *bound) {
+        finish_kernel<<<dim3(1), dim3(kFinishThreads), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT,
+                                                                 bound, w.rootF, w.root_o, w.root_d, w.argF, w.argG,
+                                                                 w.res);
+    }
+};
+
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
                           ComposeResult **result_dev) {
     (void)order_dev;
-    Ws w = carve(P, n_surv, ws);
-    *result_dev = w.res;
-    const int64_t G = n_groups(P), nbk = n_buckets(P);
-    const int D = levels(P);
-    const int64_t rows = (int64_t)P.nb * (P.L + 1) * P.K;
-    prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT, w.EiT, w.res);
-    fill<int32_t>(w.gcnt, G, 0, s);
-    fill<int32_t>(w.bcnt, nbk + 1, 0, s);
-    fill<double>(w.Pst, P.nb, kInf, s);
-    fill<double>(w.rootF, P.nb, kInf, s);
-    fill<int32_t>(w.root_o, P.nb, -1, s);
-    fill<int32_t>(w.root_d, P.nb, -1, s);
-    if (n_surv > 0) {
-        int64_t blocks = (n_surv + 255) / 256;
-        if (blocks > 65536) blocks = 65536;
-        gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, cost, dmax, w.pos, w.rec_g,
-                                                                    w.rec_c, w.rec_d, w.gcnt, w.res);
-        scan_i32(w.gcnt, G, w.tmp, s);
-        scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n_surv, w.rec_g, w.rec_c, w.rec_d,
-                                                                     w.gcnt, w.ent_c, w.ent_d, w.ent_i);
-        const int nch = (int)(((int64_t)P.L * P.K + kEventCells - 1) / kEventCells);
-        const dim3 egrid((unsigned)(P.L * nch), (unsigned)P.nb);
-        group_events<false><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt,
-                                                       w.ev_cell, w.ev_val);
-        scan_i32(w.bcnt, nbk + 1, w.tmp, s);
-        copy_kernel<int32_t><<<dim3((unsigned)((nbk + 1 + 255) / 256)), dim3(256), 0, s>>>(w.bcnt, w.bcur, nbk + 1);
-        group_events<true><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcur,
-                                                      w.ev_cell, w.ev_val);
-    } else {
-        scan_i32(w.gcnt, G, w.tmp, s);  // all zeros: offsets stay zero
-    }
+    Driver dr(P, n_surv, ws, s);
+    *result_dev = dr.w.res;
+    dr.setup(surv, n_surv, cost, dmax);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
-    const dim3 tgrid((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
-                     (unsigned)P.nb);
-    int n_cu = 0, dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        n_cu = 0;
-    auto levels_run = [&](auto kp) {
-        constexpr int KP = decltype(kp)::value;
-        using LK = LevelKernels<KP>;
-        const int cap4 = LK::template capacity<4>(n_cu, tri_lds);
-        const int cap3 = LK::template capacity<3>(n_cu, tri_lds);
-        auto split_for = [&](int blocks) { return blocks <= cap4 ? 4 : (blocks <= cap3 ? 3 : 2); };
-        auto bottleneck = [&](int d) {
-            const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
-            const int sp = split_for((int)(grid.x * grid.y));
-            const double *Wp = w.Wb[(d - 1) & 1];
-            double *Wn = w.Wb[d & 1];
-            if (sp == 4)
-                level_bottleneck<KP, 4><<<grid, dim3(4 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
-                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
-            else if (sp == 3)
-                level_bottleneck<KP, 3><<<grid, dim3(3 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
-                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
-            else
-                level_bottleneck<KP, 2><<<grid, dim3(2 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T,
-                                                                            w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
-        };
-        auto fill_level = [&](int d) {
-            const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
-            const int sp = split_for((int)(grid.x * grid.y));
-            const double *Gp = w.Wb[(d - 1) & 1];
-            double *Gn = w.Wb[d & 1];
-            if (sp == 4)
-                level_fill<KP, 4><<<grid, dim3(4 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
-                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
-                                                                      w.root_o, w.root_d);
-            else if (sp == 3)
-                level_fill<KP, 3><<<grid, dim3(3 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
-                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
-                                                                      w.root_o, w.root_d);
-            else
-                level_fill<KP, 2><<<grid, dim3(2 * KP), tri_lds, s>>>(P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn,
-                                                                      w.EoT, w.EiT, w.Pst, w.argF, w.argG, w.rootF,
-                                                                      w.root_o, w.root_d);
-        };
-        // phase 1: least bottleneck per b
-        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
-        fill<double>(w.Wb[0], rows, kInf, s);
-        fill<double>(w.Wb[1], rows, kInf, s);
-        for (int d = 1; d <= D; ++d) bottleneck(d);
-        // phase 2: least fill at that bottleneck
-        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
-        fill<double>(w.Wb[0], rows, kInf, s);
-        fill<double>(w.Wb[1], rows, kInf, s);
-        for (int d = 1; d <= D; ++d) fill_level(d);
-    };
-    if (P.K <= 64)
-        levels_run(std::integral_constant<int, 64>{});
-    else if (P.K <= 128)
-        levels_run(std::integral_constant<int, 128>{});
-    else if (P.K <= 192)
-        levels_run(std::integral_constant<int, 192>{});
-    else
-        levels_run(std::integral_constant<int, 256>{});
-    finish_kernel<<<dim3(1), dim3(kFinishThreads), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT, w.Pst, w.rootF,
-                                                w.root_o, w.root_d, w.argF, w.argG, w.res);
+    dr.phase1();
+    dr.phase2(dr.w.Pst);
+    dr.finish(dr.w.Pst);
     return hipGetLastError();
+}
+
+// The relaxation of step (4), per b: the bound is raised over the stage and
+// link costs above P* while T = (m-1) * bound + F(bound) can still improve,
+// where F(bound) is the least fill with every stage and link within the
+// bound.  F never increases with the bound, so over an interval of bounds
+// (u, v] the iteration time is at least (m-1) * (its first bound) + F(v): the
+// search evaluates F at up to kSplitWays points per open interval per round
+// (all jobs of a round in one batched run), drops an interval when that lower
+// bound cannot beat the best found (ties go to the smaller bound) or when F is
+// equal at both ends, and splits the rest.  The result is the least T, ties
+// to the smallest bound, as a plain ascending sweep would find.
+constexpr int kSplitWays = 8;
+
+struct BSearch {
+    bool active = false;
+    double Pst = 0, F0 = 0, mm1 = 0, best = 0, tau = 0;
+    std::vector<double> th;  // distinct bounds above P*, ascending
+    std::vector<double> F;   // F at th[k], NaN if unknown
+    std::vector<std::pair<int, int>> iv;  // open intervals (a, c]: F(a) known (a = -1 is P*)
+    double Fat(int k) const { return k < 0 ? F0 : F[k]; }
+    double tat(int k) const { return k < 0 ? Pst : th[k]; }
+};
+
+hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
+                                  const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,
+                                  void *ws, hipStream_t s, ComposeResult **result_dev, int *rounds_out) {
+    Driver dr(P, n_surv, ws, s);
+    RelaxWs r = carve_relax(P, n_surv, (char *)ws + compose_ws_bytes(P, n_surv));
+    *result_dev = dr.w.res;
+    if (rounds_out) *rounds_out = 0;
+    dr.setup(surv, n_surv, cost, dmax);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dr.phase1();
+    dr.phase2(dr.w.Pst);
+    const int nb = P.nb;
+    std::vector<double> Pst(nb), F0(nb);
+    int32_t err = 0;
+    e = hipMemcpyAsync(Pst.data(), dr.w.Pst, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(F0.data(), dr.w.rootF, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&err, &dr.w.res->err, sizeof(err), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    if (err) {  // invalid list: the finish kernel reports it
+        dr.finish(dr.w.Pst);
+        return hipGetLastError();
+    }
+    std::vector<BSearch> bs(nb);
+    std::vector<double> hi(nb, -kInf), mm1(nb, 0.0);
+    bool any = false;
+    for (int bi = 0; bi < nb; ++bi) {
+        BSearch &q = bs[bi];
+        const int64_t m = H.B / H.bvals[bi];
+        q.mm1 = mm1[bi] = (double)(m - 1);
+        if (!(Pst[bi] < kInf) || !(F0[bi] < kInf)) continue;
+        q.active = any = true;
+        q.Pst = Pst[bi];
+        q.F0 = F0[bi];
+        q.best = (q.mm1 * q.Pst) + q.F0;
+        q.tau = q.Pst;
+        hi[bi] = q.best;
+    }
+    if (any) {
+        // candidate bounds: stage costs (device) and link times (host)
+        std::vector<double> lo(Pst);
+        for (int bi = 0; bi < nb; ++bi)
+            if (!bs[bi].active) lo[bi] = kInf;
+        e = hipMemcpyAsync(r.lo, lo.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipMemcpyAsync(r.hi, hi.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipMemcpyAsync(r.mm1, mm1.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return e;
+        fill<int32_t>(r.th_cnt, 1, 0, s);
+        const int64_t G = n_groups(P);
+        int64_t blocks = (G + 255) / 256;
+        if (blocks > 16384) blocks = 16384;
+        collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.gcnt, dr.w.ent_c, r.lo, r.hi, r.mm1,
+                                                                   r.th_val, r.th_b, r.th_cnt,
+                                                                   (int32_t)std::min<int64_t>(n_surv, INT32_MAX));
+        int32_t cnt = 0;
+        e = hipMemcpyAsync(&cnt, r.th_cnt, sizeof(cnt), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return e;
+        cnt = (int32_t)std::min<int64_t>(cnt, n_surv);  // each entry is collected at most once
+        std::vector<double> tv(cnt);
+        std::vector<int32_t> tb(cnt);
+        if (cnt > 0) {
+            e = hipMemcpyAsync(tv.data(), r.th_val, sizeof(double) * cnt, hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess) e = hipMemcpyAsync(tb.data(), r.th_b, sizeof(int32_t) * cnt, hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess) e = hipStreamSynchronize(s);
+            if (e != hipSuccess) return e;
+        }
+        for (int32_t t = 0; t < cnt; ++t) bs[tb[t]].th.push_back(tv[t]);
+        // link times x = (2 b * OA[j-1]) / E over links between positions
+        // o < o2 of the order; x grows with OA, so each distinct E gives one
+        // run of distinct OA values inside the window
+        const int K = P.K, L = P.L;
+        std::vector<double> Es;
+        for (int o = 0; o < K; ++o)
+            for (int o2 = o + 1; o2 < K; ++o2) {
+                const double E = H.E[(int64_t)order_host[o] * K + order_host[o2]];
+                if (E > 0.0) Es.push_back(E);
+            }
+        std::sort(Es.begin(), Es.end());
+        Es.erase(std::unique(Es.begin(), Es.end()), Es.end());
+        std::vector<int64_t> oa(H.outact, H.outact + (L > 1 ? L - 1 : 0));
+        std::sort(oa.begin(), oa.end());
+        oa.erase(std::unique(oa.begin(), oa.end()), oa.end());
+        for (int bi = 0; bi < nb; ++bi) {
+            BSearch &q = bs[bi];
+            if (!q.active) continue;
+            const double two_b = 2.0 * (double)H.bvals[bi];
+            for (double E : Es) {
+                auto x_of = [&](int64_t a) { return (two_b * (double)a) / E; };
+                auto it = std::partition_point(oa.begin(), oa.end(), [&](int64_t a) { return !(x_of(a) > q.Pst); });
+                for (; it != oa.end(); ++it) {
+                    const double x = x_of(*it);
+                    if (!(x < kInf) || !((q.mm1 * x) < q.best)) break;
+                    q.th.push_back(x);
+                }
+            }
+            std::sort(q.th.begin(), q.th.end());
+            q.th.erase(std::unique(q.th.begin(), q.th.end()), q.th.end());
+            q.F.assign(q.th.size(), std::nan(""));
+            if (!q.th.empty()) q.iv.push_back({-1, (int)q.th.size() - 1});
+        }
+        // branch and bound over the bounds, one batched fill run per round
+        for (int round = 0;; ++round) {
+            std::vector<std::pair<int, int>> req;  // (b, index)
+            std::vector<std::vector<int>> pts(nb);
+            for (int bi = 0; bi < nb; ++bi) {
+                BSearch &q = bs[bi];
+                for (auto &ab : q.iv) {
+                    const int a = ab.first, c = ab.second;
+                    const int u = c - a;  // bounds a+1 .. c
+                    const int ways = std::min(kSplitWays, u);
+                    for (int t = 1; t <= ways; ++t) {
+                        const int k = a + (int)(((int64_t)u * t) / ways);
+                        if (std::isnan(q.F[k])) {
+                            q.F[k] = -1.0;  // requested
+                            req.push_back({bi, k});
+                        }
+                    }
+                }
+            }
+            if (req.empty()) break;
+            if (rounds_out) *rounds_out = round + 1;
+            for (size_t c0 = 0; c0 < req.size(); c0 += kMaxJobs) {
+                const int J = (int)std::min<size_t>(kMaxJobs, req.size() - c0);
+                std::vector<int32_t> jb(J), nj(nb, 0);
+                std::vector<double> jt(J), jf(J);
+                for (int t = 0; t < J; ++t) {
+                    jb[t] = req[c0 + t].first;
+                    jt[t] = bs[jb[t]].th[req[c0 + t].second];
+                    ++nj[jb[t]];
+                }
+                e = hipMemcpyAsync(r.job_b, jb.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess) e = hipMemcpyAsync(r.jobs_of_b, nj.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess) e = hipMemcpyAsync(r.job_tau, jt.data(), sizeof(double) * J, hipMemcpyHostToDevice, s);
+                if (e != hipSuccess) return e;
+                dr.phase2_jobs(r, J);
+                e = hipMemcpyAsync(jf.data(), r.job_F, sizeof(double) * J, hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                if (e != hipSuccess) return e;
+                for (int t = 0; t < J; ++t) {
+                    BSearch &q = bs[jb[t]];
+                    const int k = req[c0 + t].second;
+                    q.F[k] = jf[t];
+                    const double Tt = (q.mm1 * q.th[k]) + jf[t];
+                    if (Tt < q.best || (Tt == q.best && q.th[k] < q.tau)) {
+                        q.best = Tt;
+                        q.tau = q.th[k];
+                    }
+                }
+            }
+            for (int bi = 0; bi < nb; ++bi) {
+                BSearch &q = bs[bi];
+                std::vector<std::pair<int, int>> next;
+                for (auto &ab : q.iv) {
+                    // the evaluated points split (a, c] into runs between known F
+                    int u = ab.first;
+                    for (int k = ab.first + 1; k <= ab.second; ++k) {
+                        if (std::isnan(q.F[k])) continue;
+                        const int v = k;
+                        if (v > u + 1 && q.Fat(u) != q.F[v]) {
+                            const double lb = (q.mm1 * q.th[u + 1]) + q.F[v];
+                            if (lb < q.best || (lb == q.best && q.th[u + 1] < q.tau)) next.push_back({u, v});
+                        }
+                        u = v;
+                    }
+                }
+                q.iv.swap(next);
+            }
+        }
+    }
+    // the best b and its bound: reuse the phase-2 argmins when the bound is P*
+    int bstar = -1;
+    double bestT = kInf;
+    for (int bi = 0; bi < nb; ++bi)
+        if (bs[bi].active && bs[bi].best < bestT) {
+            bestT = bs[bi].best;
+            bstar = bi;
+        }
+    if (bstar < 0 || bs[bstar].tau == bs[bstar].Pst) {
+        dr.finish(dr.w.Pst);
+        return hipGetLastError();
+    }
+    std::vector<double> bound(nb, kInf);
+    bound[bstar] = bs[bstar].tau;
+    e = hipMemcpyAsync(r.bound, bound.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    dr.phase2(r.bound);
+    dr.finish(r.bound);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host vectors above must outlive the copies
+    return e;
 }
 
 }  // namespace tg

@@ -129,4 +129,17 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
                           ComposeResult **result_dev);
 size_t compose_order_offset(const DevProblem &P, int64_t n_surv);  // where the order table lives in ws
+
+// Host tables the relaxed search reads (link times are enumerated on the host).
+struct RelaxHost {
+    const int64_t *outact;  // [L] output activation bytes per layer
+    const double *E;        // [K*K] inter-island bandwidth, island ids, row-major
+    const int64_t *bvals;   // [nb] compatible micro-batch sizes, ascending
+    int64_t B;              // global batch
+};
+size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv);
+// Synchronises the stream several times (once per search round).
+hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
+                                  const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,
+                                  void *ws, hipStream_t s, ComposeResult **result_dev, int *rounds_out);
 }  // namespace tg

@@ -11,4 +11,7 @@ struct tg_problem {
     void *dev_block;
     std::vector<int64_t> bvals;  // compatible micro-batch sizes, ascending
     int64_t n_compat_cfg;
+    int64_t B;                    // global batch
+    std::vector<int64_t> outact;  // [L] output activation bytes (host copy)
+    std::vector<double> E;        // [K*K] inter-island bandwidth (host copy)
 };

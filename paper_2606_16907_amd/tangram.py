@@ -72,7 +72,8 @@ class TangramError(RuntimeError):
 
 EXPORTS = ("tg_problem_create", "tg_problem_destroy", "tg_problem_info", "tg_problem_bvalues",
            "tg_enumerate_pairs", "tg_score_pairs", "tg_prune_workspace_bytes", "tg_prune",
-           "tg_compose_workspace_bytes", "tg_compose_pipeline", "tg_last_error")
+           "tg_compose_workspace_bytes", "tg_compose_pipeline", "tg_compose_relaxed_workspace_bytes",
+           "tg_compose_pipeline_relaxed", "tg_last_error")
 
 _lib = None
 
@@ -102,6 +103,9 @@ def load_library(path=LIB_PATH):
     L.tg_compose_workspace_bytes.argtypes = [vp, i64]
     L.tg_compose_workspace_bytes.restype = sz
     L.tg_compose_pipeline.argtypes = [vp, vp, i64, vp, vp, P(i32), P(TgPlan), vp, sz, vp]
+    L.tg_compose_relaxed_workspace_bytes.argtypes = [vp, i64]
+    L.tg_compose_relaxed_workspace_bytes.restype = sz
+    L.tg_compose_pipeline_relaxed.argtypes = [vp, vp, i64, vp, vp, P(i32), P(TgPlan), vp, sz, vp]
     L.tg_last_error.argtypes = []
     L.tg_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -256,6 +260,26 @@ class Problem:
                                      _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline")
+        return st, plan_to_dict(plan)
+
+    def compose_relaxed_workspace(self, n_survivors):
+        n = load_library().tg_compose_relaxed_workspace_bytes(self.h, int(n_survivors))
+        return torch.empty(max(int(n), 1), dtype=torch.uint8, device="cuda")
+
+    def tg_compose_pipeline_relaxed(self, survivors, cost, dmax, island_order=None, workspace=None):
+        """Composition with the step-(4) relaxation.  Returns (status, plan dict)."""
+        lib = load_library()
+        if island_order is None:
+            island_order = self.inst["island_order"]
+        order = (ctypes.c_int32 * self.K)(*[int(x) for x in island_order])
+        n = int(survivors.numel())
+        ws = workspace if workspace is not None else self.compose_relaxed_workspace(n)
+        plan = TgPlan()
+        st = lib.tg_compose_pipeline_relaxed(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
+                                             _dptr(dmax), order, ctypes.byref(plan), _dptr(ws),
+                                             ws.numel(), _stream())
+        if st not in (TG_OK, TG_ENOPLAN):
+            _check(st, "tg_compose_pipeline_relaxed")
         return st, plan_to_dict(plan)
 
     def plan_search(self, island_order=None):
