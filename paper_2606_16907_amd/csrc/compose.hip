@@ -1154,26 +1154,23 @@ size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv) {
 
 // Stage costs that can serve as relaxed bounds for their b: above P*_b and
 // with (m-1) * cost below the iteration time at P*_b (a plan bounded by a
-// larger value cannot beat it, its fill being non-negative).  Every entry of
-// every group is a candidate; duplicates are removed on the host.
-__global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_t *__restrict__ gcnt,
-                                                      const double *__restrict__ ent_c, const double *lo,
-                                                      const double *hi, const double *mm1, double *th_val,
-                                                      int32_t *th_b, int32_t *th_cnt, int32_t cap) {
-    const int64_t G = (int64_t)P.nb * P.NS * P.K;
-    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < G; g += (int64_t)gridDim.x * blockDim.x) {
-        const int bi = (int)((g / P.NS) % P.nb);
-        const double l = lo[bi], h = hi[bi], f = mm1[bi];
-        if (!(l < kInf)) continue;
-        const int32_t st = g ? gcnt[g - 1] : 0, en = gcnt[g];
-        for (int32_t e = st; e < en; ++e) {
-            const double c = ent_c[e];
-            if (c > l && c < kInf && (f * c) < h) {
-                const int32_t slot = atomicAdd(th_cnt, 1);
-                if (slot < cap) {
-                    th_val[slot] = c;
-                    th_b[slot] = bi;
-                }
+// larger value cannot beat it, its fill being non-negative).  Every listed
+// candidate that fits somewhere (a grouped record) is a candidate bound; one
+// thread per record, duplicates removed on the host.
+__global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_t *__restrict__ rec_g,
+                                                      const double *__restrict__ rec_c, int64_t n,
+                                                      const double *lo, const double *hi, const double *mm1,
+                                                      double *th_val, int32_t *th_b, int32_t *th_cnt, int32_t cap) {
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t G = rec_g[r];
+        if (G < 0) continue;
+        const int bi = (int)(((int64_t)G / P.NS) % P.nb);
+        const double c = rec_c[r];
+        if (c > lo[bi] && c < kInf && (mm1[bi] * c) < hi[bi]) {
+            const int32_t slot = atomicAdd(th_cnt, 1);
+            if (slot < cap) {
+                th_val[slot] = c;
+                th_b[slot] = bi;
             }
         }
     }
@@ -1434,11 +1431,11 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         if (e == hipSuccess) e = hipMemcpyAsync(r.mm1, mm1.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
         if (e != hipSuccess) return e;
         fill<int32_t>(r.th_cnt, 1, 0, s);
-        const int64_t G = n_groups(P);
-        int64_t blocks = (G + 255) / 256;
+        int64_t blocks = (n_surv + 255) / 256;
         if (blocks > 16384) blocks = 16384;
-        collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.gcnt, dr.w.ent_c, r.lo, r.hi, r.mm1,
-                                                                   r.th_val, r.th_b, r.th_cnt,
+        if (blocks < 1) blocks = 1;
+        collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.rec_g, dr.w.rec_c, n_surv, r.lo, r.hi,
+                                                                   r.mm1, r.th_val, r.th_b, r.th_cnt,
                                                                    (int32_t)std::min<int64_t>(n_surv, INT32_MAX));
         int32_t cnt = 0;
         e = hipMemcpyAsync(&cnt, r.th_cnt, sizeof(cnt), hipMemcpyDeviceToHost, s);
