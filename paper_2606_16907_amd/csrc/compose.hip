@@ -1157,23 +1157,63 @@ size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv) {
 // larger value cannot beat it, its fill being non-negative).  Every listed
 // candidate that fits somewhere (a grouped record) is a candidate bound; one
 // thread per record, duplicates removed on the host.
+constexpr int kBoundRecs = 8;  // records per thread, loads in flight together
+constexpr int kMaxB = 512;     // b values staged in LDS (more are read from global memory)
+
 __global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_t *__restrict__ rec_g,
                                                       const double *__restrict__ rec_c, int64_t n,
                                                       const double *lo, const double *hi, const double *mm1,
                                                       double *th_val, int32_t *th_b, int32_t *th_cnt, int32_t cap) {
-    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t G = rec_g[r];
-        if (G < 0) continue;
-        const int bi = (int)(((int64_t)G / P.NS) % P.nb);
-        const double c = rec_c[r];
-        if (c > lo[bi] && c < kInf && (mm1[bi] * c) < hi[bi]) {
-            const int32_t slot = atomicAdd(th_cnt, 1);
-            if (slot < cap) {
-                th_val[slot] = c;
-                th_b[slot] = bi;
+    __shared__ double slo[kMaxB], shi[kMaxB], smm[kMaxB];
+    for (int t = threadIdx.x; t < P.nb && t < kMaxB; t += blockDim.x) {
+        slo[t] = lo[t];
+        shi[t] = hi[t];
+        smm[t] = mm1[t];
+    }
+    __syncthreads();
+    const int64_t r0 = ((int64_t)blockIdx.x * blockDim.x * kBoundRecs) + threadIdx.x;
+    int32_t g[kBoundRecs];
+    double c[kBoundRecs];
+#pragma unroll
+    for (int k = 0; k < kBoundRecs; ++k) {
+        const int64_t r = r0 + (int64_t)k * blockDim.x;
+        g[k] = r < n ? rec_g[r] : -1;
+        c[k] = r < n ? rec_c[r] : 0.0;  // unused when the group is -1
+    }
+    int bi[kBoundRecs];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kBoundRecs; ++k) {
+        bi[k] = -1;
+        if (g[k] >= 0) {
+            // G = (position * nb + b) * NS + slice < 2^31 (checked at the boundary)
+            const int b = (int)(((uint32_t)g[k] / (uint32_t)P.NS) % (uint32_t)P.nb);
+            const double l = b < kMaxB ? slo[b] : lo[b];
+            const double h = b < kMaxB ? shi[b] : hi[b];
+            const double f = b < kMaxB ? smm[b] : mm1[b];
+            if (c[k] > l && c[k] < kInf && (f * c[k]) < h) {
+                bi[k] = b;
+                ++cnt;
             }
         }
     }
+    // one counter update per block: same-address atomics serialise
+    __shared__ int32_t scan_lds[256 / kWave + 1];
+    __shared__ int32_t block_base;
+    int32_t total;
+    int32_t slot = block_excl_scan<int32_t>(cnt, scan_lds, &total);
+    if (threadIdx.x == 0) block_base = total ? atomicAdd(th_cnt, total) : 0;
+    __syncthreads();
+    slot += block_base;
+#pragma unroll
+    for (int k = 0; k < kBoundRecs; ++k)
+        if (bi[k] >= 0) {
+            if (slot < cap) {
+                th_val[slot] = c[k];
+                th_b[slot] = bi[k];
+            }
+            ++slot;
+        }
 }
 
 // Sequencing of the composition kernels on one workspace.
@@ -1431,8 +1471,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         if (e == hipSuccess) e = hipMemcpyAsync(r.mm1, mm1.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
         if (e != hipSuccess) return e;
         fill<int32_t>(r.th_cnt, 1, 0, s);
-        int64_t blocks = (n_surv + 255) / 256;
-        if (blocks > 16384) blocks = 16384;
+        int64_t blocks = (n_surv + 256 * kBoundRecs - 1) / (256 * kBoundRecs);
         if (blocks < 1) blocks = 1;
         collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.rec_g, dr.w.rec_c, n_surv, r.lo, r.hi,
                                                                    r.mm1, r.th_val, r.th_b, r.th_cnt,
