@@ -20,7 +20,12 @@ SRC = os.path.join(HERE, "tangram_oracle.c")
 LIB = os.path.join(HERE, "libtg_oracle.so")
 
 LAYER_FIELDS = ("fwd_flops", "dense_params", "expert_params", "act_stash_bytes",
-                "tp_comm_bytes", "a2a_bytes", "out_act_bytes")
+                "tp_comm_bytes", "a2a_bytes", "out_act_bytes", "cp_comm_bytes")
+# instance keys added with context parallelism, recomputation and offloading;
+# instances without them use these values
+LAYER_DEFAULT = 0           # per-layer field absent: zeros
+HOST_BW_DEFAULT = 0.0       # no host link: offloading not admitted
+SPACE_DEFAULTS = {"cp": [1], "recompute": [0], "offload": [0]}
 
 OK, EINVAL, ENOMEM, ECAPACITY, ENOPLAN = 0, -1, -2, -4, -5
 
@@ -39,9 +44,10 @@ def build(force=True):
 
 class Stage(ctypes.Structure):
     _fields_ = [("island", ctypes.c_int32), ("first_layer", ctypes.c_int32),
-                ("end_layer", ctypes.c_int32), ("tp", ctypes.c_int32), ("dp", ctypes.c_int32),
-                ("ep", ctypes.c_int32), ("zero", ctypes.c_int32), ("mb", ctypes.c_int32),
-                ("depth", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("end_layer", ctypes.c_int32), ("tp", ctypes.c_int32), ("cp", ctypes.c_int32),
+                ("dp", ctypes.c_int32), ("ep", ctypes.c_int32), ("zero", ctypes.c_int32),
+                ("recompute", ctypes.c_int32), ("offload", ctypes.c_int32), ("mb", ctypes.c_int32),
+                ("depth", ctypes.c_int32),
                 ("pair_index", ctypes.c_int64), ("cost", ctypes.c_double),
                 ("mem_bytes", ctypes.c_double), ("link_out", ctypes.c_double)]
 
@@ -66,10 +72,11 @@ def lib():
         i32p = ctypes.POINTER(ctypes.c_int32)
         f64p = ctypes.POINTER(ctypes.c_double)
         u8p = ctypes.POINTER(ctypes.c_uint8)
-        L.tgo_create.argtypes = [i64p, ctypes.c_int, i32p, f64p, f64p, f64p, ctypes.c_int, f64p,
-                                 ctypes.c_int64, ctypes.c_int, i32p, ctypes.c_int, i32p,
-                                 ctypes.c_int, i32p, ctypes.c_int, ctypes.c_uint32,
-                                 ctypes.c_double, ctypes.c_double, ctypes.POINTER(vp)]
+        L.tgo_create.argtypes = [i64p, ctypes.c_int, i32p, f64p, f64p, f64p, f64p, ctypes.c_int, f64p,
+                                 ctypes.c_int64, ctypes.c_int, i32p, ctypes.c_int, i32p, ctypes.c_int,
+                                 i32p, ctypes.c_int, i32p, ctypes.c_int, ctypes.c_uint32,
+                                 ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double, ctypes.c_double,
+                                 ctypes.POINTER(vp)]
         L.tgo_destroy.argtypes = [vp]
         L.tgo_counts.argtypes = [vp, i64p]
         L.tgo_bvalues.argtypes = [vp, i64p]
@@ -99,7 +106,9 @@ class Oracle:
 
     def __init__(self, inst):
         self.inst = inst
-        lay = np.array([inst["layers"][f] for f in LAYER_FIELDS], dtype=np.int64)
+        L0 = len(inst["layers"]["fwd_flops"])
+        lay = np.array([inst["layers"].get(f, [LAYER_DEFAULT] * L0) for f in LAYER_FIELDS],
+                       dtype=np.int64)
         self.L = lay.shape[1]
         isl = inst["islands"]
         self.K = len(isl["n_gpus"])
@@ -108,22 +117,29 @@ class Oracle:
         peak = np.array(isl["peak_flops"], dtype=np.float64)
         hbm = np.array(isl["hbm_bytes"], dtype=np.float64)
         intra = np.array(isl["intra_bw"], dtype=np.float64)
+        host = np.array(isl.get("host_bw", [HOST_BW_DEFAULT] * self.K), dtype=np.float64)
         inter = np.ascontiguousarray(np.array(inst["inter_bw"], dtype=np.float64).reshape(-1))
         tp = np.array(sp["tp"], dtype=np.int32)
         ep = np.array(sp["ep"], dtype=np.int32)
         mb = np.array(sp["mb"], dtype=np.int32)
-        zmask = 0
+        cp = np.array(sp.get("cp", SPACE_DEFAULTS["cp"]), dtype=np.int32)
+        zmask = rmask = omask = 0
         for z in sp["zero"]:
             zmask |= 1 << int(z)
-        self._keep = (lay, n_gpus, peak, hbm, intra, inter, tp, ep, mb)
+        for r in sp.get("recompute", SPACE_DEFAULTS["recompute"]):
+            rmask |= 1 << int(r)
+        for r in sp.get("offload", SPACE_DEFAULTS["offload"]):
+            omask |= 1 << int(r)
+        self._keep = (lay, n_gpus, peak, hbm, intra, host, inter, tp, cp, ep, mb)
         h = ctypes.c_void_p()
         st = lib().tgo_create(_ptr(lay, ctypes.c_int64), self.L, _ptr(n_gpus, ctypes.c_int32),
                               _ptr(peak, ctypes.c_double), _ptr(hbm, ctypes.c_double),
-                              _ptr(intra, ctypes.c_double), self.K, _ptr(inter, ctypes.c_double),
-                              int(sp["global_batch"]), int(sp["n_experts"]),
-                              _ptr(tp, ctypes.c_int32), len(tp), _ptr(ep, ctypes.c_int32), len(ep),
-                              _ptr(mb, ctypes.c_int32), len(mb), zmask, float(sp["eta"]),
-                              float(sp["mem_frac"]), ctypes.byref(h))
+                              _ptr(intra, ctypes.c_double), _ptr(host, ctypes.c_double), self.K,
+                              _ptr(inter, ctypes.c_double), int(sp["global_batch"]),
+                              int(sp["n_experts"]), _ptr(tp, ctypes.c_int32), len(tp),
+                              _ptr(cp, ctypes.c_int32), len(cp), _ptr(ep, ctypes.c_int32), len(ep),
+                              _ptr(mb, ctypes.c_int32), len(mb), zmask, rmask, omask,
+                              float(sp["eta"]), float(sp["mem_frac"]), ctypes.byref(h))
         if st != OK:
             raise OracleError(st, "create")
         self.h = h
@@ -142,19 +158,21 @@ class Oracle:
 
     # -- candidate space ---------------------------------------------------
     def decode(self, idx):
-        out = np.zeros(8, dtype=np.int32)
+        out = np.zeros(11, dtype=np.int32)
         st = lib().tgo_decode(self.h, int(idx), _ptr(out, ctypes.c_int32))
         if st != OK:
             raise OracleError(st, "decode")
-        i, j, k, tp, dp, ep, z, mb = (int(x) for x in out)
-        return dict(i=i, j=j, island=k, tp=tp, dp=dp, ep=ep, zero=z, mb=mb)
+        i, j, k, tp, cp, dp, ep, z, rc, of, mb = (int(x) for x in out)
+        return dict(i=i, j=j, island=k, tp=tp, cp=cp, dp=dp, ep=ep, zero=z, recompute=rc,
+                    offload=of, mb=mb)
 
     def coef(self, g):
-        out = np.zeros(10, dtype=np.float64)
+        out = np.zeros(12, dtype=np.float64)
         st = lib().tgo_coef(self.h, int(g), _ptr(out, ctypes.c_double))
         if st != OK:
             raise OracleError(st, "coef")
-        names = ("alpha", "beta", "gamma", "delta_d", "delta_e", "mu_d", "mu_e", "rho", "H", "m_real")
+        names = ("alpha", "beta", "gamma", "delta_d", "delta_e", "mu_d", "mu_e", "rho", "H", "m_real",
+                 "kappa", "omega")
         return dict(zip(names, (float(x) for x in out)))
 
     # -- scoring -----------------------------------------------------------
@@ -222,6 +240,6 @@ def plan_to_dict(plan):
     stages = []
     for t in range(max(plan.S, 0)):
         s = plan.stage[t]
-        stages.append({f: getattr(s, f) for f, _ in Stage._fields_ if f != "pad"})
+        stages.append({f: getattr(s, f) for f, _ in Stage._fields_})
     return {"status": plan.status, "b": plan.b, "m": plan.m, "S": plan.S, "P": plan.P,
             "F": plan.F, "T": plan.T, "stages": stages}

@@ -10,8 +10,11 @@
  * What it computes (every quantity is a plain definition written out):
  *   1. the candidate space: every contiguous layer range [i, j) ("model slice",
  *      Sec. 4.2) times every island (Sec. 4.1) times every intra-island config
- *      (tp, dp, ep, zero stage, micro-batch) -- the model-slice/island pairs
- *      that Sec. 5.1 enumerates and hands to a homogeneous parallelizer;
+ *      (tp, context-parallel degree cp, dp, ep, zero stage, activation
+ *      recomputation, activation offloading, micro-batch) -- the
+ *      model-slice/island pairs that Sec. 5.1 enumerates and hands to a
+ *      homogeneous parallelizer, with the parallelisms and memory-saving
+ *      techniques of Sec. 2.1;
  *   2. per candidate an analytic step-time cost and the deepest 1F1B pipeline
  *      position it fits at (Sec. 5.2: memory depends on the stage's position,
  *      a plan is reused "until it is no longer feasible");
@@ -37,11 +40,12 @@
 #define TGO_ECAPACITY (-4)
 #define TGO_ENOPLAN (-5)
 
-#define NF 7 /* per-layer fields */
-enum { F_FLOPS = 0, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A, F_OUTACT };
+#define NF 8 /* per-layer fields */
+enum { F_FLOPS = 0, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A, F_OUTACT, F_CPCOMM };
+#define NSUM 8 /* slice sums: flops, dparam, eparam, act, tpcomm, a2a, outact, cpcomm */
 
 typedef struct {
-    int32_t island, first_layer, end_layer, tp, dp, ep, zero, mb, depth, pad;
+    int32_t island, first_layer, end_layer, tp, cp, dp, ep, zero, recompute, offload, mb, depth;
     int64_t pair_index;
     double cost, mem_bytes, link_out;
 } tgo_stage;
@@ -53,7 +57,7 @@ typedef struct {
 } tgo_plan;
 
 typedef struct {
-    int k, tp, dp, ep, z, mb;
+    int k, tp, cp, dp, ep, z, rc, of, mb;
     int64_t b;
 } ocfg;
 
@@ -61,10 +65,10 @@ typedef struct {
     int L, K;
     int64_t *layer[NF]; /* [f][L] */
     int32_t *n_gpus;
-    double *peak, *hbm, *intra, *inter; /* inter: K*K row-major */
+    double *peak, *hbm, *intra, *host, *inter; /* inter: K*K row-major */
     int64_t B;
     int n_experts;
-    int ntp, tp[8], nep, ep[8], nmb, mb[8], nz, zs[4];
+    int ntp, tp[8], ncp, cp[8], nep, ep[8], nmb, mb[8], nz, zs[4], nrc, rcs[2], nof, ofs[2];
     double eta, mem_frac;
     /* derived */
     int64_t NS, ncfg, N;
@@ -93,7 +97,7 @@ static void slice_ij(int L, int64_t s, int *pi, int *pj) {
 }
 
 /* ------------------------------------------------------------------------ */
-/* configs of one island: lexicographic (tp, dp, ep, z, mb)                  */
+/* configs of one island: lexicographic (tp, cp, dp, ep, z, rc, of, mb)      */
 /* ------------------------------------------------------------------------ */
 static int ep_admissible(const oprob *p, int ep, int dp) {
     if (dp % ep != 0) return 0;
@@ -101,26 +105,38 @@ static int ep_admissible(const oprob *p, int ep, int dp) {
     return p->n_experts % ep == 0;
 }
 
+/* A config uses tp * cp * dp <= n GPUs of the island; offloading needs a
+   host link (host bandwidth > 0). */
 static int64_t island_configs(const oprob *p, int k, ocfg *out) {
     int64_t c = 0;
     int n = p->n_gpus[k];
     for (int a = 0; a < p->ntp; a++) {
         int tp = p->tp[a];
         if (tp > n) continue;
-        for (int dp = 1; dp <= n / tp; dp++)
-            for (int e = 0; e < p->nep; e++) {
-                if (!ep_admissible(p, p->ep[e], dp)) continue;
-                for (int zi = 0; zi < p->nz; zi++)
-                    for (int mi = 0; mi < p->nmb; mi++) {
-                        if (out) {
-                            ocfg *q = &out[c];
-                            q->k = k; q->tp = tp; q->dp = dp; q->ep = p->ep[e];
-                            q->z = p->zs[zi]; q->mb = p->mb[mi];
-                            q->b = (int64_t)dp * (int64_t)p->mb[mi];
-                        }
-                        c++;
-                    }
-            }
+        for (int ci = 0; ci < p->ncp; ci++) {
+            int cp = p->cp[ci];
+            if ((int64_t)tp * cp > n) continue;
+            int q = tp * cp;
+            for (int dp = 1; dp <= n / q; dp++)
+                for (int e = 0; e < p->nep; e++) {
+                    if (!ep_admissible(p, p->ep[e], dp)) continue;
+                    for (int zi = 0; zi < p->nz; zi++)
+                        for (int ri = 0; ri < p->nrc; ri++)
+                            for (int oi = 0; oi < p->nof; oi++) {
+                                if (p->ofs[oi] && !(p->host[k] > 0.0)) continue;
+                                for (int mi = 0; mi < p->nmb; mi++) {
+                                    if (out) {
+                                        ocfg *g = &out[c];
+                                        g->k = k; g->tp = tp; g->cp = cp; g->dp = dp; g->ep = p->ep[e];
+                                        g->z = p->zs[zi]; g->rc = p->rcs[ri]; g->of = p->ofs[oi];
+                                        g->mb = p->mb[mi];
+                                        g->b = (int64_t)dp * (int64_t)p->mb[mi];
+                                    }
+                                    c++;
+                                }
+                            }
+                }
+        }
     }
     return c;
 }
@@ -143,24 +159,28 @@ void tgo_destroy(void *h) {
     oprob *p = (oprob *)h;
     if (!p) return;
     for (int f = 0; f < NF; f++) free(p->layer[f]);
-    free(p->n_gpus); free(p->peak); free(p->hbm); free(p->intra); free(p->inter);
+    free(p->n_gpus); free(p->peak); free(p->hbm); free(p->intra); free(p->host); free(p->inter);
     free(p->cfg_off); free(p->cfg); free(p->slice_sum); free(p->bvals);
     free(p);
 }
 
-/* layers: NF*L int64, field-major (all fwd_flops, then dense_params, ...). */
+/* layers: NF*L int64, field-major (all fwd_flops, then dense_params, ...).
+   cp: context-parallel degrees (ncp = 0 means {1}); rc_mask / of_mask: bit r
+   admits recomputation / offloading option r (0 means {off}). */
 int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double *peak,
-               const double *hbm, const double *intra, int K, const double *inter,
+               const double *hbm, const double *intra, const double *host_bw, int K, const double *inter,
                int64_t global_batch, int n_experts, const int32_t *tp, int ntp,
-               const int32_t *ep, int nep, const int32_t *mb, int nmb, uint32_t zero_mask,
-               double eta, double mem_frac, void **out) {
+               const int32_t *cp, int ncp, const int32_t *ep, int nep, const int32_t *mb, int nmb,
+               uint32_t zero_mask, uint32_t rc_mask, uint32_t of_mask, double eta, double mem_frac,
+               void **out) {
     *out = NULL;
     if (L < 1 || L > 512 || K < 1 || K > 255) return TGO_EINVAL;
     if (global_batch < 1 || n_experts < 0) return TGO_EINVAL;
     if (!strictly_ascending_pos(tp, ntp) || !strictly_ascending_pos(ep, nep) ||
-        !strictly_ascending_pos(mb, nmb))
+        !strictly_ascending_pos(mb, nmb) || (ncp != 0 && !strictly_ascending_pos(cp, ncp)))
         return TGO_EINVAL;
     if (zero_mask == 0 || (zero_mask & ~0xFu)) return TGO_EINVAL;
+    if ((rc_mask & ~0x3u) || (of_mask & ~0x3u)) return TGO_EINVAL;
     if (!(eta > 0.0) || !isfinite(eta) || !(mem_frac > 0.0) || !isfinite(mem_frac))
         return TGO_EINVAL;
     for (int k = 0; k < K; k++) {
@@ -168,6 +188,7 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
         if (!(peak[k] > 0.0) || !isfinite(peak[k])) return TGO_EINVAL;
         if (!(hbm[k] > 0.0) || !isfinite(hbm[k])) return TGO_EINVAL;
         if (!(intra[k] > 0.0) || !isfinite(intra[k])) return TGO_EINVAL;
+        if (!(host_bw[k] >= 0.0) || !isfinite(host_bw[k])) return TGO_EINVAL;
     }
     for (int a = 0; a < K * K; a++)
         if (!(inter[a] >= 0.0)) return TGO_EINVAL; /* rejects NaN and negatives; +inf allowed */
@@ -192,20 +213,30 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
     p->peak = (double *)malloc(sizeof(double) * K);
     p->hbm = (double *)malloc(sizeof(double) * K);
     p->intra = (double *)malloc(sizeof(double) * K);
+    p->host = (double *)malloc(sizeof(double) * K);
     p->inter = (double *)malloc(sizeof(double) * K * K);
     memcpy(p->n_gpus, n_gpus, sizeof(int32_t) * K);
     memcpy(p->peak, peak, sizeof(double) * K);
     memcpy(p->hbm, hbm, sizeof(double) * K);
     memcpy(p->intra, intra, sizeof(double) * K);
+    memcpy(p->host, host_bw, sizeof(double) * K);
     memcpy(p->inter, inter, sizeof(double) * K * K);
     p->B = global_batch;
     p->n_experts = n_experts;
     p->ntp = ntp; memcpy(p->tp, tp, sizeof(int32_t) * ntp);
+    if (ncp == 0) { p->ncp = 1; p->cp[0] = 1; }
+    else { p->ncp = ncp; memcpy(p->cp, cp, sizeof(int32_t) * ncp); }
     p->nep = nep; memcpy(p->ep, ep, sizeof(int32_t) * nep);
     p->nmb = nmb; memcpy(p->mb, mb, sizeof(int32_t) * nmb);
     p->nz = 0;
     for (int z = 0; z < 4; z++)
         if (zero_mask & (1u << z)) p->zs[p->nz++] = z;
+    p->nrc = 0;
+    for (int r = 0; r < 2; r++)
+        if ((rc_mask ? rc_mask : 1u) & (1u << r)) p->rcs[p->nrc++] = r;
+    p->nof = 0;
+    for (int r = 0; r < 2; r++)
+        if ((of_mask ? of_mask : 1u) & (1u << r)) p->ofs[p->nof++] = r;
     p->eta = eta;
     p->mem_frac = mem_frac;
 
@@ -220,15 +251,15 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
 
     /* Slice sums by running accumulation over the layers of [i, j) (the
        "concatenate" of Tab. 2 for integer per-layer quantities). */
-    p->slice_sum = (int64_t *)malloc(sizeof(int64_t) * 6 * p->NS);
-    const int fmap[6] = {F_FLOPS, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A};
+    p->slice_sum = (int64_t *)malloc(sizeof(int64_t) * NSUM * p->NS);
+    const int fmap[NSUM] = {F_FLOPS, F_DPARAM, F_EPARAM, F_ACT, F_TPCOMM, F_A2A, F_OUTACT, F_CPCOMM};
     int64_t s = 0;
     for (int i = 0; i < L; i++) {
-        int64_t acc[6] = {0, 0, 0, 0, 0, 0};
+        int64_t acc[NSUM] = {0, 0, 0, 0, 0, 0, 0, 0};
         for (int j = i + 1; j <= L; j++, s++)
-            for (int q = 0; q < 6; q++) {
+            for (int q = 0; q < NSUM; q++) {
                 acc[q] += p->layer[fmap[q]][j - 1];
-                p->slice_sum[s * 6 + q] = acc[q];
+                p->slice_sum[s * NSUM + q] = acc[q];
             }
     }
 
@@ -260,7 +291,7 @@ int tgo_bvalues(void *h, int64_t *out) {
     return p->nb;
 }
 
-/* idx = (cfg_off[k] + c) * NS + s  ->  (i, j, k, tp, dp, ep, z, mb) */
+/* idx = (cfg_off[k] + c) * NS + s  ->  (i, j, k, tp, cp, dp, ep, z, rc, of, mb) */
 int tgo_decode(void *h, int64_t idx, int32_t *out) {
     oprob *p = (oprob *)h;
     if (idx < 0 || idx >= p->N) return TGO_EINVAL;
@@ -268,8 +299,8 @@ int tgo_decode(void *h, int64_t idx, int32_t *out) {
     int i, j;
     slice_ij(p->L, s, &i, &j);
     const ocfg *c = &p->cfg[g];
-    out[0] = i; out[1] = j; out[2] = c->k; out[3] = c->tp; out[4] = c->dp;
-    out[5] = c->ep; out[6] = c->z; out[7] = c->mb;
+    out[0] = i; out[1] = j; out[2] = c->k; out[3] = c->tp; out[4] = c->cp; out[5] = c->dp;
+    out[6] = c->ep; out[7] = c->z; out[8] = c->rc; out[9] = c->of; out[10] = c->mb;
     return TGO_OK;
 }
 
@@ -277,7 +308,8 @@ int tgo_decode(void *h, int64_t idx, int32_t *out) {
 /* cost model (stated reading of profile()/parallelize(), Tab. 2)            */
 /* ------------------------------------------------------------------------ */
 typedef struct {
-    double alpha, beta, gamma, delta_d, delta_e, mu_d, mu_e, rho, H, m_real;
+    double alpha, beta, gamma, delta_d, delta_e, mu_d, mu_e, rho, H, m_real, kappa, omega;
+    int rc, of;
 } ocoef;
 
 /* ring collectives over D GPUs move (D-1)/D of the data per phase */
@@ -306,30 +338,55 @@ static double state_bytes(int z, int64_t D) {
 }
 
 static void config_coef(const oprob *p, const ocfg *c, ocoef *o) {
-    double Fk = p->peak[c->k], Wk = p->intra[c->k], Mk = p->hbm[c->k];
-    int64_t Dd = c->dp, De = c->dp / c->ep;
+    double Fk = p->peak[c->k], Wk = p->intra[c->k], Mk = p->hbm[c->k], Hk = p->host[c->k];
+    /* the data-parallel group (gradient sync, ZeRO sharding) spans the dp
+       replicas and the cp ranks of each, which hold the same parameters */
+    int64_t Dd = (int64_t)c->dp * c->cp, De = (int64_t)(c->dp / c->ep) * c->cp;
     double qd = (double)c->tp, qe = (double)((int64_t)c->tp * c->ep);
+    int64_t q = (int64_t)c->tp * c->cp; /* GPUs sharing one micro-batch's tokens */
+    /* forward passes over the data: forward, recomputed forward, backward
+       (= 2 forwards) for compute; forward, recompute, backward for the
+       collectives issued in the forward pass */
+    double nc = c->rc ? 4.0 : 3.0;
+    int nt = c->rc ? 3 : 2;
+    o->rc = c->rc;
+    o->of = c->of;
     o->m_real = (double)p->B / (double)c->b;
-    /* forward + backward = 3x forward FLOPs, split over tp GPUs */
-    o->alpha = (3.0 * (double)c->mb) / (((double)c->tp * Fk) * p->eta);
-    /* two passes of ring all-reduce-equivalent TP collectives, 2(t-1)/t each */
-    o->beta = c->tp > 1 ? ((4.0 * (double)c->mb) * (double)(c->tp - 1)) / ((double)c->tp * Wk) : 0.0;
-    /* all-to-all forward and backward, (e-1)/e leaves the GPU, tokens split by tp */
+    /* compute, split over the tp * cp GPUs of a replica */
+    o->alpha = (nc * (double)c->mb) / (((double)q * Fk) * p->eta);
+    /* ring all-reduce-equivalent TP collectives, 2(t-1)/t per pass, tokens
+       split by cp */
+    o->beta = c->tp > 1 ? (((double)(2 * nt) * (double)c->mb) * (double)(c->tp - 1)) / ((double)q * Wk) : 0.0;
+    /* all-to-all per pass, (e-1)/e leaves the GPU, tokens split by tp and cp */
     o->gamma = c->ep > 1
-                   ? ((2.0 * (double)c->mb) * (double)(c->ep - 1)) / (((double)c->ep * (double)c->tp) * Wk)
+                   ? (((double)nt * (double)c->mb) * (double)(c->ep - 1)) / (((double)c->ep * (double)q) * Wk)
+                   : 0.0;
+    /* ring attention over cp ranks: each receives the other (cp-1)/cp of the
+       keys and values (heads split by tp), once forward and twice backward
+       (keys/values and their gradients), plus once more when recomputing */
+    o->kappa = c->cp > 1
+                   ? (((double)(nt + 1) * (double)c->mb) * (double)(c->cp - 1)) / (((double)c->cp * (double)c->tp) * Wk)
                    : 0.0;
     o->delta_d = ((zero_per_mb(c->z, Dd) / qd) / Wk) + (((zero_per_iter(c->z, Dd) / qd) / Wk) / o->m_real);
     o->delta_e = ((zero_per_mb(c->z, De) / qe) / Wk) + (((zero_per_iter(c->z, De) / qe) / Wk) / o->m_real);
     o->mu_d = state_bytes(c->z, Dd) / qd;
     o->mu_e = state_bytes(c->z, De) / qe;
-    o->rho = (double)c->mb / (double)c->tp;
+    /* stashed activations per GPU: sequence split by tp (sequence
+       parallelism) and cp */
+    o->rho = (double)c->mb / (double)q;
+    /* offloading: the stash goes to host memory after the forward pass and
+       comes back before the backward pass */
+    o->omega = c->of ? (2.0 * (double)c->mb) / ((double)q * Hk) : 0.0;
     o->H = Mk * p->mem_frac;
 }
 
 /* 1F1B: a stage with d stages at or after it holds min(d, m) micro-batches of
-   stashed activations (Sec. 5.2: memory depends on the pipeline position). */
-static int fits(double state, double A1, double H, double m_real, int d) {
-    double inflight = (double)d < m_real ? (double)d : m_real;
+   stashed activations (Sec. 5.2: memory depends on the pipeline position).
+   With offloading only the micro-batch being computed stays on the device,
+   at every depth. */
+static int fits(double state, double A1, double H, double m_real, int d, int of) {
+    double dd = of ? 1.0 : (double)d;
+    double inflight = dd < m_real ? dd : m_real;
     return (state + (inflight * A1)) <= H;
 }
 
@@ -337,20 +394,26 @@ static void score_candidate(const oprob *p, const ocoef *o, const int64_t *sum, 
                             int *dmax, double *state_out, double *A1_out) {
     double Fl = (double)sum[0], Pd = (double)sum[1], Pe = (double)sum[2];
     double Act = (double)sum[3], Tb = (double)sum[4], Ab = (double)sum[5];
+    double Oa = (double)sum[6], Cb = (double)sum[7];
+    /* with recomputation only each layer's boundary activation (its output)
+       is stashed; the rest is recomputed in the backward pass */
+    double S = o->rc ? Oa : Act;
     double c = o->alpha * Fl;
     c = c + (o->beta * Tb);
     c = c + (o->gamma * Ab);
     c = c + (o->delta_d * Pd);
     c = c + (o->delta_e * Pe);
+    c = c + (o->kappa * Cb);
+    c = c + (o->omega * S);
     double state = (o->mu_d * Pd) + (o->mu_e * Pe);
-    double A1 = o->rho * Act;
+    double A1 = o->rho * S;
     /* d_max = largest d in 1..K that fits, 0 if none.  fits() is monotone in d
        (min(d, m) and each rounded operation are non-decreasing), so a binary
        search over d finds exactly the largest fitting depth. */
     int lo = 0, hi = p->K; /* invariant: fits(lo) or lo == 0; !fits(hi+1) */
     while (lo < hi) {
         int mid = lo + (hi - lo + 1) / 2;
-        if (fits(state, A1, o->H, o->m_real, mid)) lo = mid; else hi = mid - 1;
+        if (fits(state, A1, o->H, o->m_real, mid, o->of)) lo = mid; else hi = mid - 1;
     }
     *cost = c;
     *dmax = lo;
@@ -358,13 +421,14 @@ static void score_candidate(const oprob *p, const ocoef *o, const int64_t *sum, 
     if (A1_out) *A1_out = A1;
 }
 
-int tgo_coef(void *h, int64_t g, double *out /* 10 */) {
+int tgo_coef(void *h, int64_t g, double *out /* 12 */) {
     oprob *p = (oprob *)h;
     if (g < 0 || g >= p->ncfg) return TGO_EINVAL;
     ocoef o;
     config_coef(p, &p->cfg[g], &o);
     out[0] = o.alpha; out[1] = o.beta; out[2] = o.gamma; out[3] = o.delta_d; out[4] = o.delta_e;
     out[5] = o.mu_d; out[6] = o.mu_e; out[7] = o.rho; out[8] = o.H; out[9] = o.m_real;
+    out[10] = o.kappa; out[11] = o.omega;
     return TGO_OK;
 }
 
@@ -377,7 +441,7 @@ int tgo_score(void *h, int64_t first, int64_t count, double *cost, uint8_t *dmax
         int64_t idx = first + t, g = idx / p->NS, s = idx % p->NS;
         if (g != prev_g) { config_coef(p, &p->cfg[g], &o); prev_g = g; }
         int dm;
-        score_candidate(p, &o, &p->slice_sum[s * 6], &cost[t], &dm, NULL, NULL);
+        score_candidate(p, &o, &p->slice_sum[s * NSUM], &cost[t], &dm, NULL, NULL);
         dmax[t] = (uint8_t)dm;
     }
     return TGO_OK;
@@ -392,7 +456,7 @@ int tgo_score_list(void *h, const int64_t *idx, int64_t n, double *cost, uint8_t
         ocoef o;
         config_coef(p, &p->cfg[g], &o);
         int dm;
-        score_candidate(p, &o, &p->slice_sum[s * 6], &cost[t], &dm, NULL, NULL);
+        score_candidate(p, &o, &p->slice_sum[s * NSUM], &cost[t], &dm, NULL, NULL);
         dmax[t] = (uint8_t)dm;
     }
     return TGO_OK;
@@ -462,7 +526,7 @@ int tgo_prune(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
                 for (int64_t a = 0; a < nm; a++) {
                     int64_t c = members[a];
                     omember *m = &mem[n++];
-                    score_candidate(p, &coef[c], &p->slice_sum[s * 6], &m->cost, &m->dmax, NULL, NULL);
+                    score_candidate(p, &coef[c], &p->slice_sum[s * NSUM], &m->cost, &m->dmax, NULL, NULL);
                     m->idx = (c0 + c) * p->NS + s;
                 }
                 qsort(mem, (size_t)n, sizeof(omember), cmp_key);
@@ -681,10 +745,12 @@ static void backtrack(octx *c, double tau, int ro, int rS, tgo_plan *plan) {
         config_coef(p, cf, &co);
         double cost, state, A1;
         int dm;
-        score_candidate(p, &co, &p->slice_sum[s * 6], &cost, &dm, &state, &A1);
-        double inflight = (double)d < co.m_real ? (double)d : co.m_real;
+        score_candidate(p, &co, &p->slice_sum[s * NSUM], &cost, &dm, &state, &A1);
+        double dd = cf->of ? 1.0 : (double)d;
+        double inflight = dd < co.m_real ? dd : co.m_real;
         st->island = c->order[o]; st->first_layer = i; st->end_layer = j;
-        st->tp = cf->tp; st->dp = cf->dp; st->ep = cf->ep; st->zero = cf->z; st->mb = cf->mb;
+        st->tp = cf->tp; st->cp = cf->cp; st->dp = cf->dp; st->ep = cf->ep; st->zero = cf->z;
+        st->recompute = cf->rc; st->offload = cf->of; st->mb = cf->mb;
         st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
         st->mem_bytes = state + (inflight * A1);
         st->link_out = d > 1 ? XA(j, o, o_next) : 0.0;
@@ -766,7 +832,7 @@ static int compose_impl(void *h, const int64_t *cands, int64_t n, const int32_t 
         ocoef o;
         config_coef(p, cf, &o);
         oentry *e = &ent[ne];
-        score_candidate(p, &o, &p->slice_sum[s * 6], &e->cost, &e->dmax, NULL, NULL);
+        score_candidate(p, &o, &p->slice_sum[s * NSUM], &e->cost, &e->dmax, NULL, NULL);
         if (e->dmax < 1) continue;
         e->gkey = ((int64_t)bi * NS + s) * K + pos[cf->k];
         e->idx = idx;

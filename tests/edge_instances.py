@@ -27,16 +27,18 @@ def wide_instance(seed, K, L, distinct_links, B=None, tight=False):
         layers["tp_comm_bytes"].append(int(rng.integers(0, 100)) * 10**6)
         layers["a2a_bytes"].append(0)
         layers["out_act_bytes"].append(int(rng.integers(1, 100)) * 10**6)
+        layers["cp_comm_bytes"].append(layers["tp_comm_bytes"][-1])  # no extra draw
     # a few GPU types, so islands repeat specs as in real clusters
     types = [(float(rng.integers(50, 500)) * 1e12, float(rng.integers(4, 64)) * 1e9,
               float(rng.integers(50, 500)) * 1e9) for _ in range(5)]
-    isl = {"n_gpus": [], "peak_flops": [], "hbm_bytes": [], "intra_bw": []}
+    isl = {"n_gpus": [], "peak_flops": [], "hbm_bytes": [], "intra_bw": [], "host_bw": []}
     for _ in range(K):
         t = types[int(rng.integers(0, len(types)))]
         isl["n_gpus"].append(int(rng.integers(1, 5)))
         isl["peak_flops"].append(t[0])
         isl["hbm_bytes"].append(t[1] / (4.0 if tight else 1.0))
         isl["intra_bw"].append(t[2])
+        isl["host_bw"].append(32e9)
     if distinct_links == "few":
         levels = [400e9, 100e9, 25e9]
         E = [[0.0 if a == b else levels[int(rng.integers(0, 3))] for b in range(K)] for a in range(K)]

@@ -35,8 +35,8 @@ import os
 import numpy as np
 
 LAYER_FIELDS = ("fwd_flops", "dense_params", "expert_params", "act_stash_bytes",
-                "tp_comm_bytes", "a2a_bytes", "out_act_bytes")
-ISLAND_FIELDS = ("n_gpus", "peak_flops", "hbm_bytes", "intra_bw")
+                "tp_comm_bytes", "a2a_bytes", "out_act_bytes", "cp_comm_bytes")
+ISLAND_FIELDS = ("n_gpus", "peak_flops", "hbm_bytes", "intra_bw", "host_bw")
 
 FIXTURE_DIR = os.path.join(os.path.dirname(os.path.abspath(__file__)), "fixtures")
 CONFIG_NAMES = ("tiny", "dense8b", "dense70b", "moe", "large")
@@ -67,7 +67,7 @@ def layer_ints(s, h, n_heads, n_kv, ffn, act="gelu", n_experts=0, top_k=0, ffn_e
         a2a = 0
     return {"fwd_flops": fwd, "dense_params": dense_p, "expert_params": expert_p,
             "act_stash_bytes": stash, "tp_comm_bytes": 4 * s * h, "a2a_bytes": a2a,
-            "out_act_bytes": 2 * s * h}
+            "out_act_bytes": 2 * s * h, "cp_comm_bytes": 2 * 2 * s * h_kv}
 
 
 def uniform_layers(n_layers, **shape):
@@ -78,6 +78,13 @@ def uniform_layers(n_layers, **shape):
 # ----------------------------------------------------------------------------
 # islands
 # ----------------------------------------------------------------------------
+def host_link(hbm):
+    """Host (PCIe) bandwidth per GPU, bytes/s, by GPU generation: the
+    large-memory parts sit on PCIe 5 x16, the others on PCIe 4 x16.  A
+    function of the drawn type, so it consumes no random numbers."""
+    return 64e9 if hbm >= 100e9 else 32e9
+
+
 def _draw_gpu_types(rng, n_types):
     types = []
     for _ in range(n_types):
@@ -113,6 +120,7 @@ def random_cluster(rng, n_islands, n_types, max_nodes, one_type_per_island=False
         isl["peak_flops"].append(peak)
         isl["hbm_bytes"].append(hbm)
         isl["intra_bw"].append(intra)
+        isl["host_bw"].append(host_link(hbm))
         inter.append(round(float(rng.uniform(12.5, 50.0)), 2) * 1e9)
     E = [[0.0 if a == b else min(inter[a], inter[b]) for b in range(n_islands)]
          for a in range(n_islands)]
@@ -134,6 +142,7 @@ def fabric_cluster(rng, n_islands, n_types, max_nodes, leaf=4, spine=16,
         isl["peak_flops"].append(peak)
         isl["hbm_bytes"].append(hbm)
         isl["intra_bw"].append(intra)
+        isl["host_bw"].append(host_link(hbm))
     perm = rng.permutation(n_islands)
     slot = [0] * n_islands
     for pos, k in enumerate(perm):
@@ -156,10 +165,25 @@ def fabric_cluster(rng, n_islands, n_types, max_nodes, leaf=4, spine=16,
     return isl, E, leaf_of, spine_of
 
 
-def _space(global_batch, tp, mb, ep=(1,), zero=(0, 1, 2, 3), n_experts=0):
+def _space(global_batch, tp, mb, ep=(1,), zero=(0, 1, 2, 3), n_experts=0, cp=(1,),
+           recompute=(0,), offload=(0,)):
     return {"global_batch": int(global_batch), "n_experts": int(n_experts),
             "tp": list(tp), "ep": list(ep), "mb": list(mb), "zero": list(zero),
+            "cp": list(cp), "recompute": list(recompute), "offload": list(offload),
             "eta": 1.0, "mem_frac": 1.0}
+
+
+def extended(inst, cp=(1, 2, 4), recompute=(0, 1), offload=(0, 1)):
+    """The instance with context parallelism, activation recomputation and
+    offloading added to its configuration space (Sec. 2.1's parallelisms and
+    memory-saving techniques as intra-island config dimensions)."""
+    import copy
+    out = copy.deepcopy(inst)
+    out["space"]["cp"] = list(cp)
+    out["space"]["recompute"] = list(recompute)
+    out["space"]["offload"] = list(offload)
+    out["name"] = inst.get("name", "custom") + "_ext"
+    return out
 
 
 # ----------------------------------------------------------------------------
@@ -263,6 +287,7 @@ def random_tiny(seed, L_range=(2, 6), K_range=(1, 3), tight=False):
         layers["tp_comm_bytes"].append(int(rng.integers(0, 100)) * 10**6)
         layers["a2a_bytes"].append(int(rng.integers(0, 100)) * 10**6 if moe else 0)
         layers["out_act_bytes"].append(int(rng.integers(0, 100)) * 10**6)
+        layers["cp_comm_bytes"].append(layers["tp_comm_bytes"][-1])  # no extra draw
     isl = {f: [] for f in ISLAND_FIELDS}
     for _ in range(K):
         isl["n_gpus"].append(int(rng.integers(1, 5)))
@@ -272,6 +297,7 @@ def random_tiny(seed, L_range=(2, 6), K_range=(1, 3), tight=False):
             mem = mem / 4.0
         isl["hbm_bytes"].append(mem)
         isl["intra_bw"].append(float(rng.integers(50, 500)) * 1e9)
+        isl["host_bw"].append(16e9)  # no extra draw
     E = [[0.0] * K for _ in range(K)]
     for a in range(K):
         for b in range(K):
