@@ -4,7 +4,9 @@
  * The library computes the search at the core of Tangram's heterogeneous
  * planner (arXiv 2606.16907): every model slice (a contiguous layer range,
  * Sec. 4.2) is paired with every GPU island (Sec. 4.1) and every intra-island
- * parallel configuration; each pair gets an analytic step-time cost and the
+ * parallel configuration (tensor, context, data and expert parallelism, ZeRO,
+ * activation recomputation and offloading, micro-batch size; Sec. 2.1); each
+ * pair gets an analytic step-time cost and the
  * deepest 1F1B pipeline position it fits at (Sec. 5.2); incompatible,
  * infeasible and dominated pairs are pruned (Sec. 5.1); the survivors are
  * composed into a work-balanced pipeline across islands, lowest bottleneck
@@ -59,23 +61,31 @@ typedef struct {
     int64_t tp_comm_bytes;   /* bytes per sample in the layer's tensor-parallel collectives, one pass */
     int64_t a2a_bytes;       /* bytes per sample moved by the layer's all-to-alls, one pass */
     int64_t out_act_bytes;   /* bytes per sample of the layer's output activation */
+    int64_t cp_comm_bytes;   /* key and value bytes per sample of the layer's attention (whole
+                                sequence), circulated by ring attention under context parallelism */
 } tg_layer;
 
 /* One GPU island (Sec. 4.1): nodes of identical GPUs.  n_gpus in [1, 65536];
-   the three rates are finite and > 0. */
+   peak_flops, hbm_bytes and intra_bw are finite and > 0; host_bw is finite
+   and >= 0 (0: no host link, activation offloading is not admitted). */
 typedef struct {
     int32_t n_gpus;
     int32_t reserved; /* must be 0 */
     double peak_flops; /* FLOP/s per GPU */
     double hbm_bytes;  /* memory per GPU */
     double intra_bw;   /* bytes/s per GPU for intra-island collectives */
+    double host_bw;    /* bytes/s per GPU to host memory (activation offloading) */
 } tg_island;
 
 /* The intra-island configuration space.  Each set holds 1..8 strictly
-   ascending entries >= 1.  zero_mask: bit z set admits ZeRO stage z (0..3);
-   it must be non-zero.  n_experts = 0 describes a dense model (then only
-   ep = 1 is admitted); otherwise ep must divide n_experts.  eta scales peak
-   FLOP/s (efficiency), mem_frac scales usable memory; both finite and > 0. */
+   ascending entries >= 1 (cp may be empty: n_cp = 0 means {1}).  zero_mask:
+   bit z set admits ZeRO stage z (0..3); it must be non-zero.  recompute_mask
+   and offload_mask: bit 0 admits "off", bit 1 "on" (0 means {off}).
+   n_experts = 0 describes a dense model (then only ep = 1 is admitted);
+   otherwise ep must divide n_experts.  eta scales peak FLOP/s (efficiency),
+   mem_frac scales usable memory; both finite and > 0.  A zero-filled tail
+   (n_cp, masks) keeps the space without context parallelism, recomputation
+   and offloading. */
 typedef struct {
     int64_t global_batch; /* samples per iteration, >= 1 */
     int32_t n_experts;
@@ -89,19 +99,24 @@ typedef struct {
     int32_t reserved; /* must be 0 */
     double eta;
     double mem_frac;
+    int32_t n_cp;
+    int32_t cp[8];           /* context-parallel degrees */
+    uint32_t recompute_mask; /* activation recomputation (Sec. 2.1 RC) */
+    uint32_t offload_mask;   /* activation offloading to host memory (Sec. 2.1 OF) */
+    int32_t reserved2;       /* must be 0 */
 } tg_space;
 
 /* A decoded candidate: layers [i, j) on island `island` with the given
-   degrees, ZeRO stage and micro-batch size (samples per DP rank). */
+   degrees (tensor, context, data, expert), ZeRO stage, recomputation and
+   offloading flags (0/1) and micro-batch size (samples per DP rank). */
 typedef struct {
-    int32_t i, j, island, tp, dp, ep, zero, mb;
+    int32_t i, j, island, tp, cp, dp, ep, zero, recompute, offload, mb, reserved;
 } tg_pair;
 
 /* One pipeline stage of a plan; stage 0 is the pipeline front. */
 typedef struct {
-    int32_t island, first_layer, end_layer, tp, dp, ep, zero, mb;
+    int32_t island, first_layer, end_layer, tp, cp, dp, ep, zero, recompute, offload, mb;
     int32_t depth; /* stages from this one to the pipeline end, inclusive */
-    int32_t reserved;
     int64_t pair_index; /* candidate index of the chosen pair */
     double cost;        /* seconds per micro-batch (step-time cost of the pair) */
     double mem_bytes;   /* per-GPU memory at this depth */
@@ -142,7 +157,10 @@ typedef struct tg_problem tg_problem;
  *   lexicographically over (tp, dp, ep, zero, mb) with tp in space.tp,
  *   tp <= n_gpus, dp in 1..floor(n_gpus / tp), ep admitted and dividing dp,
  *   zero in zero_mask, mb in space.mb; cfg_off is the running count over
- *   islands in input order.
+ *   islands in input order.  With context parallelism, recomputation or
+ *   offloading the order is lexicographic over (tp, cp, dp, ep, zero,
+ *   recompute, offload, mb), tp * cp * dp <= n_gpus, and offloading needs
+ *   host_bw > 0; with their defaults it is the order above.
  * Returns TG_EINVAL on any invalid value, TG_ENOMEM / TG_EDEVICE on device
  * failures; *out is NULL on failure.
  */
@@ -171,19 +189,31 @@ tg_status tg_enumerate_pairs(const tg_problem *p, int64_t *n_candidates, int64_t
  *   d_dmax[idx - first]: the largest pipeline depth d in 1..K at which the
  *                        pair fits in memory when min(d, m) micro-batches of
  *                        activations are in flight (1F1B, Sec. 5.2), or 0.
- * With b = dp*mb, m = B/b, r(D) = (D-1)/D, De = dp/ep, W the island's intra
- * bandwidth, F its peak, and slice sums Fl, Tb, Ab, Pd, Pe, Act of the
- * tg_layer fields over [i, j):
- *   cost  = alpha*Fl + beta*Tb + gamma*Ab + dd*Pd + de*Pe   (summed left to right)
- *   alpha = 3 mb / (tp F eta)                    forward + backward compute
- *   beta  = 4 mb (tp-1) / (tp W)                 TP collectives, 2 passes x 2r
- *   gamma = 2 mb (ep-1) / (ep tp W)              all-to-all, 2 passes
- *   dd/de = (zm/q)/W + ((zi/q)/W)/m with q = tp (dense) or tp*ep (expert),
- *           D = dp (dense) or De (expert), and per-parameter bf16 traffic
+ * With b = dp*mb, m = B/b, r(D) = (D-1)/D, q = tp*cp, Dd = dp*cp (the
+ * data-parallel group), De = (dp/ep)*cp, W the island's intra bandwidth, F
+ * its peak, Hb its host bandwidth, nc = 3 (4 with recomputation: the forward
+ * pass runs twice), nt = 2 (3 with recomputation: forward collectives run
+ * twice), and slice sums Fl, Tb, Ab, Pd, Pe, Act, Oa, Cb of the tg_layer
+ * fields fwd_flops, tp_comm, a2a, dense_params, expert_params, act_stash,
+ * out_act and cp_comm over [i, j); S = Oa with recomputation (only layer
+ * boundaries are stashed), else Act:
+ *   cost  = alpha*Fl + beta*Tb + gamma*Ab + dd*Pd + de*Pe + kappa*Cb + omega*S
+ *           (summed left to right)
+ *   alpha = nc mb / (q F eta)                    compute over tp*cp GPUs
+ *   beta  = 2 nt mb (tp-1) / (q W)               TP collectives, nt passes x 2r
+ *   gamma = nt mb (ep-1) / (ep q W)              all-to-all, nt passes
+ *   kappa = (nt+1) mb (cp-1) / (cp tp W)         ring attention: keys/values once
+ *                                                forward, twice backward
+ *   omega = 2 mb / (q Hb) with offloading, else 0   stash to host and back
+ *   dd/de = (zm/qd)/W + ((zi/qd)/W)/m with qd = tp (dense) or tp*ep (expert),
+ *           D = Dd (dense) or De (expert), and per-parameter bf16 traffic
  *           zm = {0, 0, 2r, 6r} per micro-batch, zi = {4r, 4r, 2r, 0} per
  *           iteration for ZeRO stage 0..3
- *   state = (w(dp)/tp)*Pd + (w(De)/(tp ep))*Pe, w(D) = {16, 4+12/D, 2+14/D, 16/D}
- *   fits(d) <=> state + min(d, m) * (mb/tp) * Act <= hbm * mem_frac
+ *   state = (w(Dd)/tp)*Pd + (w(De)/(tp ep))*Pe, w(D) = {16, 4+12/D, 2+14/D, 16/D}
+ *   fits(d) <=> state + n(d) * (mb/q) * S <= hbm * mem_frac, n(d) = min(d, m),
+ *           or min(1, m) at every depth with offloading
+ * cp = 1, no recomputation and no offloading reduce this exactly to the
+ * model without them (the added terms are +0).
  * Asynchronous.  TG_EINVAL if the range leaves [0, N).
  */
 tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, double *d_cost,

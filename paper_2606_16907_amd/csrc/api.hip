@@ -61,6 +61,10 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     if (!ascending_set(sp.ep, sp.n_ep)) return fail(TG_EINVAL, "ep set invalid");
     if (!ascending_set(sp.mb, sp.n_mb)) return fail(TG_EINVAL, "mb set invalid");
     if (sp.zero_mask == 0 || (sp.zero_mask & ~0xFu)) return fail(TG_EINVAL, "zero_mask invalid");
+    if (sp.n_cp != 0 && !ascending_set(sp.cp, sp.n_cp)) return fail(TG_EINVAL, "cp set invalid");
+    if (sp.recompute_mask & ~0x3u) return fail(TG_EINVAL, "recompute_mask invalid");
+    if (sp.offload_mask & ~0x3u) return fail(TG_EINVAL, "offload_mask invalid");
+    if (sp.reserved2 != 0) return fail(TG_EINVAL, "space reserved2 field not 0");
     if (!(sp.eta > 0.0) || !std::isfinite(sp.eta)) return fail(TG_EINVAL, "eta invalid");
     if (!(sp.mem_frac > 0.0) || !std::isfinite(sp.mem_frac)) return fail(TG_EINVAL, "mem_frac invalid");
     for (int k = 0; k < K; ++k) {
@@ -70,60 +74,75 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         if (!(is.peak_flops > 0.0) || !std::isfinite(is.peak_flops)) return fail(TG_EINVAL, "island %d: peak", k);
         if (!(is.hbm_bytes > 0.0) || !std::isfinite(is.hbm_bytes)) return fail(TG_EINVAL, "island %d: hbm", k);
         if (!(is.intra_bw > 0.0) || !std::isfinite(is.intra_bw)) return fail(TG_EINVAL, "island %d: intra", k);
+        if (!(is.host_bw >= 0.0) || !std::isfinite(is.host_bw)) return fail(TG_EINVAL, "island %d: host_bw", k);
     }
     for (int a = 0; a < K * K; ++a)
         if (!(inter_bw[a] >= 0.0)) return fail(TG_EINVAL, "inter_bw[%d] negative or NaN", a);
 
-    // prefix sums of the six summed layer fields; every whole-model sum < 2^62
+    // prefix sums of the eight summed layer fields; every whole-model sum < 2^62
     const int64_t Lp = L + 1;
-    std::vector<int64_t> pre(6 * Lp, 0), outact(L);
+    std::vector<int64_t> pre(8 * Lp, 0), outact(L);
     const int64_t lim = (int64_t)1 << 62;
     for (int l = 0; l < L; ++l) {
         const tg_layer &y = layers[l];
-        const int64_t f[6] = {y.fwd_flops, y.dense_params, y.expert_params, y.act_stash_bytes, y.tp_comm_bytes,
-                              y.a2a_bytes};
-        for (int q = 0; q < 6; ++q) {
+        const int64_t f[8] = {y.fwd_flops,     y.dense_params, y.expert_params, y.act_stash_bytes,
+                              y.tp_comm_bytes, y.a2a_bytes,    y.out_act_bytes, y.cp_comm_bytes};
+        for (int q = 0; q < 8; ++q) {
             if (f[q] < 0 || f[q] >= lim - pre[q * Lp + l]) return fail(TG_EINVAL, "layer %d field %d", l, q);
             pre[q * Lp + l + 1] = pre[q * Lp + l] + f[q];
         }
-        if (y.out_act_bytes < 0) return fail(TG_EINVAL, "layer %d out_act_bytes", l);
         outact[l] = y.out_act_bytes;
-    }
-    int64_t oa_sum = 0;
-    for (int l = 0; l < L; ++l) {
-        if (outact[l] >= lim - oa_sum) return fail(TG_EINVAL, "out_act_bytes sum too large");
-        oa_sum += outact[l];
     }
     const int dense = (pre[2 * Lp + L] == 0 && pre[5 * Lp + L] == 0) ? 1 : 0;
 
-    // the config list of every island: lexicographic (tp, dp, ep, z, mb)
+    // the config list of every island: lexicographic (tp, cp, dp, ep, z, rc,
+    // of, mb) with tp * cp * dp <= n; offloading needs a host link
     std::vector<tg::Coef> cfg;
-    std::vector<int> zs;
+    std::vector<int> zs, cps, rcs, ofs;
     for (int z = 0; z < 4; ++z)
         if (sp.zero_mask & (1u << z)) zs.push_back(z);
+    if (sp.n_cp == 0) cps.push_back(1);
+    for (int a = 0; a < sp.n_cp; ++a) cps.push_back(sp.cp[a]);
+    for (int r = 0; r < 2; ++r) {
+        if ((sp.recompute_mask ? sp.recompute_mask : 1u) & (1u << r)) rcs.push_back(r);
+        if ((sp.offload_mask ? sp.offload_mask : 1u) & (1u << r)) ofs.push_back(r);
+    }
+    int ext = 0;
     for (int k = 0; k < K; ++k) {
         const int n = islands[k].n_gpus;
         for (int a = 0; a < sp.n_tp; ++a) {
             const int tp = sp.tp[a];
             if (tp > n) continue;
-            for (int dp = 1; dp <= n / tp; ++dp)
-                for (int e = 0; e < sp.n_ep; ++e) {
-                    const int ep = sp.ep[e];
-                    if (dp % ep) continue;
-                    if (sp.n_experts == 0 ? ep != 1 : (sp.n_experts % ep) != 0) continue;
-                    for (int z : zs)
-                        for (int mi = 0; mi < sp.n_mb; ++mi) {
-                            tg::Coef c;
-                            std::memset(&c, 0, sizeof(c));
-                            c.k = k;
-                            c.tp = tp;
-                            c.dp = dp;
-                            c.ep = ep;
-                            c.z = z;
-                            c.mb = sp.mb[mi];
-                            cfg.push_back(c);
-                        }
-                }
+            for (int cp : cps) {
+                if ((int64_t)tp * cp > n) continue;
+                const int q = tp * cp;
+                for (int dp = 1; dp <= n / q; ++dp)
+                    for (int e = 0; e < sp.n_ep; ++e) {
+                        const int ep = sp.ep[e];
+                        if (dp % ep) continue;
+                        if (sp.n_experts == 0 ? ep != 1 : (sp.n_experts % ep) != 0) continue;
+                        for (int z : zs)
+                            for (int rc : rcs)
+                                for (int of : ofs) {
+                                    if (of && !(islands[k].host_bw > 0.0)) continue;
+                                    for (int mi = 0; mi < sp.n_mb; ++mi) {
+                                        tg::Coef c;
+                                        std::memset(&c, 0, sizeof(c));
+                                        c.k = k;
+                                        c.tp = tp;
+                                        c.cp = cp;
+                                        c.dp = dp;
+                                        c.ep = ep;
+                                        c.z = z;
+                                        c.rc = rc;
+                                        c.of = of;
+                                        c.mb = sp.mb[mi];
+                                        if (cp > 1 || rc || of) ext = 1;
+                                        cfg.push_back(c);
+                                    }
+                                }
+                    }
+            }
         }
     }
     const int64_t ncfg = (int64_t)cfg.size();
@@ -199,11 +218,12 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         size_t bytes;
         size_t off;
     };
-    std::vector<double> peak(K), hbm(K), intra(K);
+    std::vector<double> peak(K), hbm(K), intra(K), host(K);
     for (int k = 0; k < K; ++k) {
         peak[k] = islands[k].peak_flops;
         hbm[k] = islands[k].hbm_bytes;
         intra[k] = islands[k].intra_bw;
+        host[k] = islands[k].host_bw;
     }
     Part parts[] = {
         {pre.data(), pre.size() * 8, 0},
@@ -222,6 +242,7 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         {intra.data(), (size_t)K * 8, 0},
         {ev.data(), ev.size() * 8, 0},
         {eidx.data(), eidx.size() * 2, 0},
+        {host.data(), (size_t)K * 8, 0},
     };
     size_t total = 0;
     for (auto &p : parts) {
@@ -255,6 +276,7 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.K = K;
     P.nb = nb;
     P.dense = dense;
+    P.ext = ext;
     P.NS = NS;
     P.ncfg = ncfg;
     P.N = NS * ncfg;
@@ -282,6 +304,7 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.n_ev = e_table ? (int32_t)ev.size() : 0;
     P.Ev = (const double *)(base + parts[14].off);
     P.Eidx = (const uint16_t *)(base + parts[15].off);
+    P.host = (const double *)(base + parts[16].off);
     pr->bvals = bv;
     pr->n_compat_cfg = (int64_t)row_cfg.size();
     pr->B = space->global_batch;

@@ -1072,23 +1072,28 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
         const int64_t Lp = L + 1;
         const double Pd = (double)(P.pre[Lp + j] - P.pre[Lp + i]);
         const double Pe = (double)(P.pre[2 * Lp + j] - P.pre[2 * Lp + i]);
-        const double Act = (double)(P.pre[3 * Lp + j] - P.pre[3 * Lp + i]);
+        // stash per sample: layer outputs with recomputation, else all activations
+        const int sq = c.rc ? 6 : 3;
+        const double S = (double)(P.pre[sq * Lp + j] - P.pre[sq * Lp + i]);
         const double state = (c.mud * Pd) + (c.mue * Pe);
-        const double A1 = c.rho * Act;
+        const double A1 = c.rho * S;
         tg_stage &sg = plan.stage[t];
         sg.island = order[o];
         sg.first_layer = i;
         sg.end_layer = j;
         sg.tp = c.tp;
+        sg.cp = c.cp;
         sg.dp = c.dp;
         sg.ep = c.ep;
         sg.zero = c.z;
+        sg.recompute = c.rc;
+        sg.offload = c.of;
         sg.mb = c.mb;
         sg.depth = d;
-        sg.reserved = 0;
         sg.pair_index = best;
         sg.cost = bc;
-        sg.mem_bytes = state + (fmin((double)d, c.m_real) * A1);
+        // in flight: min(d, m) micro-batches, one when offloaded
+        sg.mem_bytes = state + (fmin(c.of ? 1.0 : (double)d, c.m_real) * A1);
         if (d > 1) {
             const double E = EoT[(int64_t)o_next * K + o];
             sg.link_out = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;

@@ -9,6 +9,8 @@
 // config writes one coalesced 512-byte row of costs and 64 bytes of depths
 // with streaming (nontemporal) stores.  The kernel is bound by HBM writes
 // (9 bytes per candidate).
+#include <type_traits>
+
 #include "tg_device.h"
 
 #pragma clang fp contract(off)
@@ -42,25 +44,36 @@ __device__ inline double state_per_param(int z, int64_t D) {
     return 16.0 / (double)D;
 }
 
+// q = tp * cp GPUs share a micro-batch's tokens; the data-parallel group
+// (gradient sync, ZeRO sharding) is dp * cp; recomputation runs the forward
+// pass twice (compute passes nc = 4, forward-collective passes nt = 3).
 __global__ __launch_bounds__(256) void coef_kernel(DevProblem P, Coef *coef) {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= P.ncfg) return;
     Coef c = coef[g];
-    const double F = P.peak[c.k], W = P.intra[c.k], M = P.hbm[c.k];
+    const double F = P.peak[c.k], W = P.intra[c.k], M = P.hbm[c.k], Hb = P.host[c.k];
     const int64_t b = (int64_t)c.dp * c.mb;
-    const int64_t Dd = c.dp, De = c.dp / c.ep;
+    const int64_t Dd = (int64_t)c.dp * c.cp, De = (int64_t)(c.dp / c.ep) * c.cp;
     const double qd = (double)c.tp, qe = (double)((int64_t)c.tp * c.ep);
+    const int64_t q = (int64_t)c.tp * c.cp;
+    const double nc = c.rc ? 4.0 : 3.0;
+    const int nt = c.rc ? 3 : 2;
     c.m_real = (double)P.B / (double)b;
-    c.alpha = (3.0 * (double)c.mb) / (((double)c.tp * F) * P.eta);
-    c.beta = c.tp > 1 ? ((4.0 * (double)c.mb) * (double)(c.tp - 1)) / ((double)c.tp * W) : 0.0;
-    c.gamma = c.ep > 1 ? ((2.0 * (double)c.mb) * (double)(c.ep - 1)) / (((double)c.ep * (double)c.tp) * W) : 0.0;
+    c.alpha = (nc * (double)c.mb) / (((double)q * F) * P.eta);
+    c.beta = c.tp > 1 ? (((double)(2 * nt) * (double)c.mb) * (double)(c.tp - 1)) / ((double)q * W) : 0.0;
+    c.gamma = c.ep > 1 ? (((double)nt * (double)c.mb) * (double)(c.ep - 1)) / (((double)c.ep * (double)q) * W)
+                       : 0.0;
+    c.kappa = c.cp > 1 ? (((double)(nt + 1) * (double)c.mb) * (double)(c.cp - 1)) /
+                             (((double)c.cp * (double)c.tp) * W)
+                       : 0.0;
     c.dd = ((sync_per_microbatch(c.z, Dd) / qd) / W) + (((sync_per_iteration(c.z, Dd) / qd) / W) / c.m_real);
     c.de = ((sync_per_microbatch(c.z, De) / qe) / W) + (((sync_per_iteration(c.z, De) / qe) / W) / c.m_real);
     c.mud = state_per_param(c.z, Dd) / qd;
     c.mue = state_per_param(c.z, De) / qe;
-    c.rho = (double)c.mb / (double)c.tp;
+    c.rho = (double)c.mb / (double)q;
+    c.omega = c.of ? (2.0 * (double)c.mb) / ((double)q * Hb) : 0.0;
     c.H = M * P.mem_frac;
-    c.inv_rho = (double)c.tp / (double)c.mb;
+    c.inv_rho = (double)q / (double)c.mb;
     coef[g] = c;
 }
 
@@ -110,10 +123,13 @@ constexpr int kXcds = 8;
 // every iteration (the coefficient table falls out of L2 under the streaming
 // writes, and scalar misses would stall each iteration).
 struct StagedCoef {
-    double alpha, beta, gamma, dd, de, mud, mue, rho, H, m_real, inv_rho;
+    double alpha, beta, gamma, dd, de, mud, mue, rho, H, m_real, inv_rho, kappa, omega;
+    int32_t rc, of;
 };
 
-template <bool kDense>
+// kExt: the space has context parallelism, recomputation or offloading
+// (two more slice sums, two more cost terms, the stash and depth rules).
+template <bool kDense, bool kExt>
 __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first, int64_t last, int64_t g_lo,
                                                     int64_t g_hi, int64_t n_stiles, int64_t n_tiles,
                                                     double *__restrict__ cost, uint8_t *__restrict__ dmax) {
@@ -132,7 +148,25 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
     const int ng = (int)(min(g_beg + kScoreConfigs, g_hi + 1) - g_beg);
     if (lane < ng) {
         const Coef &c = P.coef[g_beg + lane];
-        cs[wv][lane] = StagedCoef{c.alpha, c.beta, c.gamma, c.dd, c.de, c.mud, c.mue, c.rho, c.H, c.m_real, c.inv_rho};
+        StagedCoef x;
+        x.alpha = c.alpha;
+        x.beta = c.beta;
+        x.gamma = c.gamma;
+        x.dd = c.dd;
+        x.de = c.de;
+        x.mud = c.mud;
+        x.mue = c.mue;
+        x.rho = c.rho;
+        x.H = c.H;
+        x.m_real = c.m_real;
+        x.inv_rho = c.inv_rho;
+        if (kExt) {  // read only by the extended variant
+            x.kappa = c.kappa;
+            x.omega = c.omega;
+            x.rc = c.rc;
+            x.of = c.of;
+        }
+        cs[wv][lane] = x;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -140,6 +174,7 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
 
     // slice sums: exact int64 prefix differences, then one rounding to binary64
     double Fl = 0.0, Pd = 0.0, Pe = 0.0, Act = 0.0, Tb = 0.0, Ab = 0.0, inv_act = 0.0;
+    double Oa = 0.0, Cb = 0.0, inv_oa = 0.0;
     if (sv) {
         const uint32_t ij = P.sij[s];
         const int i = (int)(ij & 0xFFFFu), j = (int)(ij >> 16);
@@ -154,20 +189,37 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
             Ab = (double)(pre[5 * Lp + j] - pre[5 * Lp + i]);
         }
         inv_act = 1.0 / Act;
+        if (kExt) {
+            Oa = (double)(pre[6 * Lp + j] - pre[6 * Lp + i]);
+            Cb = (double)(pre[7 * Lp + j] - pre[7 * Lp + i]);
+            inv_oa = 1.0 / Oa;
+        }
     }
     const int K = P.K;
     const int64_t NS = P.NS;
     for (int t = 0; t < ng; ++t) {
         const StagedCoef &c = cs[wv][t];
+        // with recomputation only the layer boundaries (outputs) are stashed
+        const double S = (kExt && c.rc) ? Oa : Act;
         double v = c.alpha * Fl;
         v = v + c.beta * Tb;
         if (!kDense) v = v + c.gamma * Ab;
         v = v + c.dd * Pd;
         if (!kDense) v = v + c.de * Pe;
+        if (kExt) {
+            v = v + c.kappa * Cb;
+            v = v + c.omega * S;
+        }
         double state = c.mud * Pd;
         if (!kDense) state = state + c.mue * Pe;
-        const double A1 = c.rho * Act;
-        const int dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * inv_act, K);
+        const double A1 = c.rho * S;
+        int dm;
+        if (kExt && c.of) {
+            // offloaded: one micro-batch on the device at every depth
+            dm = (state + (fmin(1.0, c.m_real) * A1)) <= c.H ? K : 0;
+        } else {
+            dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * ((kExt && c.rc) ? inv_oa : inv_act), K);
+        }
         const int64_t idx = (g_beg + t) * NS + s;
         if (sv && idx >= first && idx < last) {
             // streaming stores: the arrays are far larger than the caches
@@ -188,12 +240,20 @@ hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, doubl
     int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
     blocks = (blocks + kXcds - 1) / kXcds * kXcds;  // whole rounds over the XCDs
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    if (P.dense)
-        score_kernel<true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi, n_stiles,
-                                                                         n_tiles, cost, dmax);
+    auto go = [&](auto dense, auto ext) {
+        score_kernel<decltype(dense)::value, decltype(ext)::value><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
+            P, first, last, g_lo, g_hi, n_stiles, n_tiles, cost, dmax);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    if (P.dense && !P.ext)
+        go(T_{}, F_{});
+    else if (!P.dense && !P.ext)
+        go(F_{}, F_{});
+    else if (P.dense)
+        go(T_{}, T_{});
     else
-        score_kernel<false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi, n_stiles,
-                                                                          n_tiles, cost, dmax);
+        go(F_{}, T_{});
     return hipGetLastError();
 }
 
@@ -212,10 +272,14 @@ __global__ __launch_bounds__(256) void enumerate_kernel(DevProblem P, int64_t fi
     p.j = (int32_t)(ij >> 16);
     p.island = c.k;
     p.tp = c.tp;
+    p.cp = c.cp;
     p.dp = c.dp;
     p.ep = c.ep;
     p.zero = c.z;
+    p.recompute = c.rc;
+    p.offload = c.of;
     p.mb = c.mb;
+    p.reserved = 0;
     out[t] = p;
 }
 

@@ -14,30 +14,33 @@ namespace tg {
 constexpr int kWave = 64;
 constexpr double kInf = __builtin_huge_val();
 
-// Per-config coefficients of the step-time and memory model.  One 128-byte
-// row per config so a wave reads its config with two scalar loads.
-struct alignas(128) Coef {
+// Per-config coefficients of the step-time and memory model, one row per
+// config.
+struct alignas(64) Coef {
     double alpha, beta, gamma, dd, de;  // cost = alpha Fl + beta Tb + gamma Ab + dd Pd + de Pe
     double mud, mue;                    // state = mud Pd + mue Pe
-    double rho;                         // A1 = rho Act (stash of one micro-batch)
+    double rho;                         // A1 = rho S (stash of one micro-batch)
     double H;                           // usable bytes per GPU
     double m_real;                      // B / b
     double inv_rho;                     // 1 / rho, only for the d_max first guess
-    int32_t k, tp, dp, ep, z, mb;       // the config tuple
+    double kappa, omega;                // + kappa Cb + omega S (ring attention, offload traffic)
+    int32_t k, tp, cp, dp, ep, z, rc, of, mb;  // the config tuple
     int32_t b_idx;                      // index of b in the compatible list, -1 if B mod b != 0
     int32_t row;                        // bitmap row of a compatible config, -1 otherwise
 };
-static_assert(sizeof(Coef) == 128, "Coef row must be 128 bytes");
+static_assert(sizeof(Coef) == 192, "Coef row must be 192 bytes");
 
 // All device tables of one problem.  Passed to kernels by value.
 struct DevProblem {
     int32_t L, K, nb, dense;
+    int32_t ext;          // some config has cp > 1, recomputation or offloading
+    int32_t pad0_;
     int64_t NS, ncfg, N, B;
     int32_t n_kb;         // (island, b) groups with at least one compatible config
     int32_t max_members;  // largest group
     int32_t n_rows;       // compatible configs = bitmap rows
     int32_t words;        // 64-bit bitmap words per row = ceil(NS / 64)
-    const int64_t *pre;   // [6][L+1] prefix sums: flops, dparam, eparam, act, tpcomm, a2a
+    const int64_t *pre;   // [8][L+1] prefix sums: flops, dparam, eparam, act, tpcomm, a2a, outact, cpcomm
     const int64_t *outact;  // [L]
     const double *E;        // [K*K] inter-island bytes/s
     const uint32_t *sij;    // [NS] slice -> i | j << 16
@@ -48,7 +51,7 @@ struct DevProblem {
     const int32_t *kb_island;   // [n_kb]
     const int32_t *kb_bidx;     // [n_kb]
     const int32_t *row_cfg;     // [n_rows] config id of each bitmap row
-    const double *peak, *hbm, *intra;  // [K] island rates
+    const double *peak, *hbm, *intra, *host;  // [K] island rates
     double eta, mem_frac;
     int32_t n_ev;            // distinct inter-island bandwidth values (<= kMaxDistinctE), else 0
     int32_t pad_;

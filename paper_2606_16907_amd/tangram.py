@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libtangram_hip.so")
 
 TG_OK, TG_EINVAL, TG_ENOMEM, TG_EDEVICE, TG_ECAPACITY, TG_ENOPLAN = 0, -1, -2, -3, -4, -5
 LAYER_FIELDS = ("fwd_flops", "dense_params", "expert_params", "act_stash_bytes",
-                "tp_comm_bytes", "a2a_bytes", "out_act_bytes")
+                "tp_comm_bytes", "a2a_bytes", "out_act_bytes", "cp_comm_bytes")
 
 
 class TgLayer(ctypes.Structure):
@@ -27,7 +27,7 @@ class TgLayer(ctypes.Structure):
 class TgIsland(ctypes.Structure):
     _fields_ = [("n_gpus", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("peak_flops", ctypes.c_double), ("hbm_bytes", ctypes.c_double),
-                ("intra_bw", ctypes.c_double)]
+                ("intra_bw", ctypes.c_double), ("host_bw", ctypes.c_double)]
 
 
 class TgSpace(ctypes.Structure):
@@ -36,18 +36,25 @@ class TgSpace(ctypes.Structure):
                 ("n_ep", ctypes.c_int32), ("ep", ctypes.c_int32 * 8),
                 ("n_mb", ctypes.c_int32), ("mb", ctypes.c_int32 * 8),
                 ("zero_mask", ctypes.c_uint32), ("reserved", ctypes.c_int32),
-                ("eta", ctypes.c_double), ("mem_frac", ctypes.c_double)]
+                ("eta", ctypes.c_double), ("mem_frac", ctypes.c_double),
+                ("n_cp", ctypes.c_int32), ("cp", ctypes.c_int32 * 8),
+                ("recompute_mask", ctypes.c_uint32), ("offload_mask", ctypes.c_uint32),
+                ("reserved2", ctypes.c_int32)]
+
+
+PAIR_FIELDS = ("i", "j", "island", "tp", "cp", "dp", "ep", "zero", "recompute", "offload", "mb")
 
 
 class TgPair(ctypes.Structure):
-    _fields_ = [(f, ctypes.c_int32) for f in ("i", "j", "island", "tp", "dp", "ep", "zero", "mb")]
+    _fields_ = [(f, ctypes.c_int32) for f in PAIR_FIELDS + ("reserved",)]
 
 
 class TgStage(ctypes.Structure):
     _fields_ = [("island", ctypes.c_int32), ("first_layer", ctypes.c_int32),
-                ("end_layer", ctypes.c_int32), ("tp", ctypes.c_int32), ("dp", ctypes.c_int32),
-                ("ep", ctypes.c_int32), ("zero", ctypes.c_int32), ("mb", ctypes.c_int32),
-                ("depth", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("end_layer", ctypes.c_int32), ("tp", ctypes.c_int32), ("cp", ctypes.c_int32),
+                ("dp", ctypes.c_int32), ("ep", ctypes.c_int32), ("zero", ctypes.c_int32),
+                ("recompute", ctypes.c_int32), ("offload", ctypes.c_int32), ("mb", ctypes.c_int32),
+                ("depth", ctypes.c_int32),
                 ("pair_index", ctypes.c_int64), ("cost", ctypes.c_double),
                 ("mem_bytes", ctypes.c_double), ("link_out", ctypes.c_double)]
 
@@ -143,7 +150,7 @@ class Problem:
         layers = (TgLayer * L)()
         for l in range(L):
             for f in LAYER_FIELDS:
-                setattr(layers[l], f, int(lay[f][l]))
+                setattr(layers[l], f, int(lay[f][l]) if f in lay else 0)
         isl = inst["islands"]
         K = len(isl["n_gpus"])
         islands = (TgIsland * K)()
@@ -152,6 +159,7 @@ class Problem:
             islands[k].peak_flops = float(isl["peak_flops"][k])
             islands[k].hbm_bytes = float(isl["hbm_bytes"][k])
             islands[k].intra_bw = float(isl["intra_bw"][k])
+            islands[k].host_bw = float(isl["host_bw"][k]) if "host_bw" in isl else 0.0
         inter = (ctypes.c_double * (K * K))(*[float(x) for row in inst["inter_bw"] for x in row])
         sp = inst["space"]
         space = TgSpace()
@@ -164,6 +172,12 @@ class Problem:
             for a, v in enumerate(vals[:8]):
                 arr[a] = int(v)
         space.zero_mask = sum(1 << int(z) for z in sp["zero"])
+        cps = list(sp.get("cp", [1]))
+        space.n_cp = len(cps)
+        for a, v in enumerate(cps[:8]):
+            space.cp[a] = int(v)
+        space.recompute_mask = sum(1 << int(r) for r in sp.get("recompute", [0]))
+        space.offload_mask = sum(1 << int(r) for r in sp.get("offload", [0]))
         space.eta = float(sp["eta"])
         space.mem_frac = float(sp["mem_frac"])
         h = ctypes.c_void_p()
@@ -193,8 +207,9 @@ class Problem:
 
     # --- entry points -----------------------------------------------------
     def tg_enumerate_pairs(self, first=0, count=None, out=None):
-        """Decode candidates [first, first+count) into an int32 [count, 8]
-        device tensor (i, j, island, tp, dp, ep, zero, mb)."""
+        """Decode candidates [first, first+count) into an int32 [count, 12]
+        device tensor (i, j, island, tp, cp, dp, ep, zero, recompute, offload,
+        mb, 0)."""
         lib = load_library()
         n = ctypes.c_int64(0)
         if count is None:
@@ -202,7 +217,7 @@ class Problem:
                    "tg_enumerate_pairs")
             count = n.value - first
         if out is None:
-            out = torch.empty((count, 8), dtype=torch.int32, device="cuda")
+            out = torch.empty((count, 12), dtype=torch.int32, device="cuda")
         _check(lib.tg_enumerate_pairs(self.h, ctypes.byref(n), int(first), int(count), _dptr(out),
                                       _stream()), "tg_enumerate_pairs")
         return out

@@ -1,0 +1,95 @@
+"""GPU parity over the extended configuration space (context parallelism,
+activation recomputation, activation offloading): decoding, every score bit
+for bit, the surviving set and both compositions against the live oracle."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from oracle.oracle import Oracle  # noqa: E402
+from workloads import extended, load_instance, random_tiny  # noqa: E402
+from tests.inst_util import instance  # noqa: E402
+from tests.test_gpu_parity import bits, plan_equal  # noqa: E402
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2606_16907_amd import tangram as T  # noqa: E402
+
+
+def _closed_form():
+    lay = {"dense_params": 2 ** 30, "act_stash_bytes": 2 ** 22, "out_act_bytes": 2 ** 20,
+           "fwd_flops": 2 ** 41, "tp_comm_bytes": 2 ** 30, "cp_comm_bytes": 2 ** 30}
+    return instance(L=3, K=2, layer=lay, n_gpus=[4, 8], hbm=2.0 ** 32 + 5 * 2.0 ** 22, B=64,
+                    tp=(1, 2), cp=(1, 2, 4), mb=(1, 2), zero=(0, 3), recompute=(0, 1),
+                    offload=(0, 1), host=[2.0 ** 30, 0.0], peak=2.0 ** 40, intra=2.0 ** 30)
+
+
+def _no_offload_island():
+    inst = extended(random_tiny(3, L_range=(4, 4), K_range=(3, 3)), cp=(1, 2), recompute=(0, 1),
+                    offload=(0, 1))
+    inst["islands"]["host_bw"][1] = 0.0
+    return inst
+
+
+CASES = ([("closed_form", _closed_form), ("tiny_ext", lambda: extended(load_instance("tiny"))),
+          ("dense8b_ext", lambda: extended(load_instance("dense8b"))),
+          ("no_offload_island", _no_offload_island)]
+         + [(f"rand_ext{s}", lambda s=s: extended(random_tiny(s, tight=(s % 2 == 1)), cp=(1, 2, 4),
+                                                   recompute=(0, 1), offload=(0, 1)))
+            for s in range(12)])
+
+
+@pytest.mark.parametrize("name,make", CASES, ids=[n for n, _ in CASES])
+def test_extended_parity(name, make):
+    inst = make()
+    print("case", name, flush=True)
+    sys.stdout.flush()
+    o = Oracle(inst)
+    p = T.Problem(inst)
+    assert (p.N, p.NS, p.n_configs, p.n_b) == (o.N, o.NS, o.n_configs, o.n_b)
+    pairs = p.tg_enumerate_pairs().cpu().numpy()
+    for idx in range(0, o.N, max(1, o.N // 1999)):
+        d = o.decode(idx)
+        assert tuple(pairs[idx]) == (d["i"], d["j"], d["island"], d["tp"], d["cp"], d["dp"], d["ep"],
+                                     d["zero"], d["recompute"], d["offload"], d["mb"], 0)
+    cost, dmax = p.tg_score_pairs()
+    oc, od = o.score()
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(cost.cpu().numpy()), bits(oc))
+    assert np.array_equal(dmax.cpu().numpy(), od)
+    surv = p.tg_prune(cost, dmax)
+    osurv = o.prune()
+    assert np.array_equal(surv.cpu().numpy(), osurv)
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax)
+    ost, oplan, _ = o.compose(osurv)
+    assert st == ost
+    if st == 0:
+        plan_equal(plan, oplan)
+    st, plan = p.tg_compose_pipeline_relaxed(surv, cost, dmax)
+    ost, oplan, _ = o.compose_relaxed(osurv)
+    assert st == ost
+    if st == 0:
+        plan_equal(plan, oplan)
+
+
+def test_extended_plans_use_the_new_dimensions():
+    # on the extended 8B instance the chosen plan is no slower than the
+    # original and the space really contains cp > 1, recomputed and offloaded
+    # candidates that survive
+    base = load_instance("dense8b")
+    p0 = T.Problem(base)
+    c0, d0 = p0.tg_score_pairs()
+    s0 = p0.tg_prune(c0, d0)
+    t0 = p0.tg_compose_pipeline(s0, c0, d0)[1]["T"]
+    p = T.Problem(extended(base))
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    plan = p.tg_compose_pipeline(surv, cost, dmax)[1]
+    assert plan["T"] <= t0
+    pairs = p.tg_enumerate_pairs().cpu().numpy()[surv.cpu().numpy()]
+    assert (pairs[:, 4] > 1).any() and (pairs[:, 8] == 1).any() and (pairs[:, 9] == 1).any()

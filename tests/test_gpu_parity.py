@@ -30,6 +30,10 @@ if not torch.cuda.is_available():
 from paper_2606_16907_amd import tangram as T  # noqa: E402
 
 
+# decoded pair columns (tg_pair), named like the oracle's decode
+PAIR_COLS = ("i", "j", "island", "tp", "cp", "dp", "ep", "zero", "recompute", "offload", "mb")
+
+
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
@@ -49,6 +53,8 @@ def plan_equal(gpu_plan, orc_plan):
     for a, b in zip(gpu_plan["stages"], orc_plan["stages"]):
         for f in ("island", "first_layer", "end_layer", "tp", "dp", "ep", "zero", "mb", "depth",
                   "pair_index"):
+            assert a[f] == b[f], (f, a, b)
+        for f in ("cp", "recompute", "offload"):
             assert a[f] == b[f], (f, a, b)
         for f in ("cost", "mem_bytes", "link_out"):
             assert bits(a[f]) == bits(b[f]), (f, a[f], b[f])
@@ -82,8 +88,7 @@ def test_full_path_parity(name, make):
     pairs = p.tg_enumerate_pairs().cpu().numpy()
     for idx in range(0, o.N, max(1, o.N // 997)):
         d = o.decode(idx)
-        assert tuple(pairs[idx]) == (d["i"], d["j"], d["island"], d["tp"], d["dp"], d["ep"],
-                                     d["zero"], d["mb"])
+        assert tuple(pairs[idx]) == tuple(d[f] for f in PAIR_COLS) + (0,)
     # score
     cost, dmax = p.tg_score_pairs()
     oc, od = o.score()
@@ -148,8 +153,7 @@ def test_score_windows(first, count):
     pairs = p.tg_enumerate_pairs(first, count).cpu().numpy()
     for t in range(0, count, max(1, count // 50)):
         d = o.decode(first + t)
-        assert tuple(pairs[t]) == (d["i"], d["j"], d["island"], d["tp"], d["dp"], d["ep"],
-                                   d["zero"], d["mb"])
+        assert tuple(pairs[t]) == tuple(d[f] for f in PAIR_COLS) + (0,)
 
 
 def test_prune_safety_on_gpu():
@@ -159,7 +163,8 @@ def test_prune_safety_on_gpu():
     surv = p.tg_prune(cost, dmax)
     B = inst["space"]["global_batch"]
     pairs = p.tg_enumerate_pairs().cpu().numpy()
-    compatible = (B % (pairs[:, 4] * pairs[:, 7]) == 0)
+    col = {f: c for c, f in enumerate(PAIR_COLS)}
+    compatible = (B % (pairs[:, col["dp"]] * pairs[:, col["mb"]]) == 0)
     allc = torch.from_numpy(np.nonzero(compatible)[0].astype(np.int64)).cuda()
     a = p.tg_compose_pipeline(surv, cost, dmax)
     b = p.tg_compose_pipeline(allc, cost, dmax)

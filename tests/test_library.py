@@ -39,12 +39,12 @@ def test_binding_declares_every_export():
 
 def test_binding_struct_layouts_match_header_sizes():
     from paper_2606_16907_amd import tangram as T
-    assert ctypes.sizeof(T.TgLayer) == 56
-    assert ctypes.sizeof(T.TgIsland) == 32
-    assert ctypes.sizeof(T.TgSpace) == 144
-    assert ctypes.sizeof(T.TgPair) == 32
-    assert ctypes.sizeof(T.TgStage) == 72
-    assert ctypes.sizeof(T.TgPlan) == 16 + 24 + 255 * 72
+    assert ctypes.sizeof(T.TgLayer) == 64
+    assert ctypes.sizeof(T.TgIsland) == 40
+    assert ctypes.sizeof(T.TgSpace) == 192
+    assert ctypes.sizeof(T.TgPair) == 48
+    assert ctypes.sizeof(T.TgStage) == 80
+    assert ctypes.sizeof(T.TgPlan) == 16 + 24 + 255 * 80
 
 
 def test_struct_sizes_agree_with_the_c_compiler(tmp_path):
