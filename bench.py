@@ -1,6 +1,7 @@
 """Benchmark of the plan search on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large]
+                    [--space named|extended] [--other-steps 10]
 
 A step is one whole plan search over a resident instance: score every
 model-slice/island/config candidate (tg_score_pairs), prune to the surviving
@@ -14,6 +15,10 @@ before the timed region.  Prints one JSON line:
                the 8 TB/s HBM peak
   cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
                workload (the same 128 layers on the first islands only)
+  workloads    the same plan search timed on each of the five synthetic
+               clusters (fewer steps), after the main measurement
+--space extended adds context parallelism {1,2,4}, recomputation and
+offloading to the chosen workload's config space.
 """
 from __future__ import annotations
 
@@ -37,6 +42,9 @@ WORKLOADS = {
     "large": "128-layer dense decoder (h 12288, FFN 49152 GeLU, 96 heads, s 8192, global batch "
              "4096) on 128 islands of 8-64 GPUs, 5 GPU types, 3-level fabric 400/100/25 GB/s; "
              "TP{1,2,4,8} x DP 1..n/tp x ZeRO 0-3 x MB{1,2,4,8}",
+    "tiny": "8-layer dense (h 1024, 16 heads, s 2048, global batch 64) on 2 islands of 4 GPUs",
+    "dense8b": "32-layer dense (h 4096, FFN 14336 SwiGLU, GQA 32/8, s 4096, global batch 512) "
+               "on 4 islands of 8 GPUs",
     "dense70b": "80-layer dense (h 8192, FFN 28672 SwiGLU, GQA 64/8, s 8192, global batch 1024) "
                 "on 16 islands of 8-64 GPUs",
     "moe": "48-layer MoE (h 6144, 64 experts top-2, expert FFN 4096, s 4096, global batch 2048) "
@@ -56,6 +64,11 @@ def parse():
     ap.add_argument("--relaxed-steps", type=int, default=5,
                     help="also time the composition with the step-(4) relaxation this many times "
                          "(0 skips it); reported beside the main metric, not in it")
+    ap.add_argument("--space", default="named", choices=("named", "extended"),
+                    help="config space: the workload's own, or extended with context parallelism "
+                         "{1,2,4}, recomputation and offloading")
+    ap.add_argument("--other-steps", type=int, default=10,
+                    help="timed plan searches per workload in the five-workload table (0 skips it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, copy BYTES between two device buffers (a plain copy of "
                          "known size that scales profiler byte counters)")
@@ -82,10 +95,95 @@ def cpu_baseline(inst, n_islands):
     del cost, dmax
     el = t3 - t0
     return {"value": o.N / el, "unit": "pairs/s", "cores": 1, "kind": "oracle",
-            "sample": f"same 128-layer workload on its first {n_islands} of 128 islands "
+            "sample": f"same workload on its first {n_islands} of {len(inst['island_order'])} islands "
                       f"(N={o.N} candidates): score all, prune, compose; single thread",
             "seconds": round(el, 3), "score_s": round(t1 - t0, 3), "prune_s": round(t2 - t1, 3),
             "compose_s": round(t3 - t2, 3), "candidates": o.N, "plan_status": st}
+
+
+def time_search(torch, T, inst, steps, warmup):
+    """Create the problem, size the buffers (untimed), then run `warmup` and
+    `steps` whole plan searches (score, prune, compose with the plan on the
+    host), with HIP events between the three calls of every timed step."""
+    t_create = time.perf_counter()
+    p = T.Problem(inst)
+    torch.cuda.synchronize()
+    t_create = time.perf_counter() - t_create
+    N = p.N
+    cost = torch.empty(N, dtype=torch.float64, device="cuda")
+    dmax = torch.empty(N, dtype=torch.uint8, device="cuda")
+    pws = p.prune_workspace()
+
+    # size the survivor buffer and composition workspace once (untimed)
+    p.tg_score_pairs(0, N, cost, dmax)
+    surv0 = p.tg_prune(cost, dmax, workspace=pws)
+    n_surv = int(surv0.numel())
+    surv_buf = torch.empty(max(n_surv, 1), dtype=torch.int64, device="cuda")
+    cws = p.compose_workspace(n_surv)
+    del surv0
+
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record(stream)
+        p.tg_score_pairs(0, N, cost, dmax)
+        if e:
+            e[1].record(stream)
+        s = p.tg_prune(cost, dmax, survivors=surv_buf, workspace=pws)
+        if e:
+            e[2].record(stream)
+        st, plan = p.tg_compose_pipeline(s, cost, dmax, workspace=cws)
+        if e:
+            e[3].record(stream)
+        return st, plan, s
+
+    for _ in range(warmup):
+        st, plan, s = step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        st, plan, s = step(ev[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    return {"problem": p, "N": N, "cost": cost, "dmax": dmax, "survivors": s, "status": st,
+            "plan": plan, "elapsed": elapsed, "create_s": t_create,
+            "score_ms": [ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)],
+            "prune_ms": [ev[k][1].elapsed_time(ev[k][2]) for k in range(steps)],
+            "compose_ms": [ev[k][2].elapsed_time(ev[k][3]) for k in range(steps)]}
+
+
+def five_workloads(torch, T, load_instance, space, steps, main_name, main_row):
+    """The plan search on each synthetic cluster: candidates, survivors,
+    milliseconds per whole search, candidates per second, the score kernel's
+    share of the HBM peak, the chosen plan's b, stages and T."""
+    out = {}
+    for name in ("tiny", "dense8b", "dense70b", "moe", "large"):
+        if name == main_name:
+            out[name] = main_row
+            continue
+        inst = load_instance(name)
+        if space == "extended":
+            from workloads import extended
+            inst = extended(inst)
+        run = time_search(torch, T, inst, steps, 2)
+        out[name] = workload_row(run, steps)
+        del run
+        torch.cuda.empty_cache()
+    return out
+
+
+def workload_row(run, steps):
+    sc = sum(run["score_ms"]) / steps
+    return {"candidates": run["N"], "survivors": int(run["survivors"].numel()),
+            "ms_per_step": run["elapsed"] / steps * 1e3,
+            "pairs_per_s": run["N"] * steps / run["elapsed"],
+            "score_ms": sc, "prune_ms": sum(run["prune_ms"]) / steps,
+            "compose_ms": sum(run["compose_ms"]) / steps,
+            "score_hbm_frac": SCORE_BYTES_PER_CANDIDATE * run["N"] / (sc / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "plan": {"status": run["status"], "b": run["plan"]["b"], "stages": run["plan"]["S"],
+                     "T": run["plan"]["T"]}}
 
 
 def score_source_digest():
@@ -129,57 +227,20 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     inst = load_instance(args.workload)
+    if args.space == "extended":
+        from workloads import extended
+        inst = extended(inst)
     if args.copy_calibration > 0:
         a = torch.ones(args.copy_calibration // 8, dtype=torch.float64, device="cuda")
         b = torch.empty_like(a)
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    t_create = time.perf_counter()
-    p = T.Problem(inst)
-    torch.cuda.synchronize()
-    t_create = time.perf_counter() - t_create
-    N = p.N
-    cost = torch.empty(N, dtype=torch.float64, device="cuda")
-    dmax = torch.empty(N, dtype=torch.uint8, device="cuda")
-    pws = p.prune_workspace()
-
-    # size the survivor buffer and composition workspace once (untimed)
-    p.tg_score_pairs(0, N, cost, dmax)
-    surv0 = p.tg_prune(cost, dmax, workspace=pws)
-    n_surv = int(surv0.numel())
-    surv_buf = torch.empty(max(n_surv, 1), dtype=torch.int64, device="cuda")
-    cws = p.compose_workspace(n_surv)
-    del surv0
-
-    stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-
-    def step(e=None):
-        if e:
-            e[0].record(stream)
-        p.tg_score_pairs(0, N, cost, dmax)
-        if e:
-            e[1].record(stream)
-        s = p.tg_prune(cost, dmax, survivors=surv_buf, workspace=pws)
-        if e:
-            e[2].record(stream)
-        st, plan = p.tg_compose_pipeline(s, cost, dmax, workspace=cws)
-        if e:
-            e[3].record(stream)
-        return st, plan, s
-
-    for _ in range(args.warmup):
-        st, plan, s = step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        st, plan, s = step(ev[k])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    score_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
-    prune_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
-    compose_ms = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.steps)]
+    run = time_search(torch, T, inst, args.steps, args.warmup)
+    p, N, s, st, plan = run["problem"], run["N"], run["survivors"], run["status"], run["plan"]
+    cost, dmax = run["cost"], run["dmax"]
+    elapsed, t_create = run["elapsed"], run["create_s"]
+    score_ms, prune_ms, compose_ms = run["score_ms"], run["prune_ms"], run["compose_ms"]
 
     mean = lambda xs: sum(xs) / len(xs)
     # composition with the step-(4) relaxation, timed after the main loop on
@@ -200,7 +261,7 @@ def main():
         del rws
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
-    traffic = measured_traffic(args.workload, N)
+    traffic = measured_traffic(args.workload if args.space == "named" else args.workload + "+extended", N)
     out = {
         "metric": METRIC,
         "value": N * args.steps / elapsed,
@@ -214,7 +275,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}",
+        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}"
+                               + ("" if args.space == "named" else
+                                  "; extended with CP{1,2,4} x recomputation x offloading"),
                    "candidates": N, "survivors": int(s.numel()), "islands": p.K, "layers": p.L,
                    "plan": {"status": st, "b": plan["b"], "stages": plan["S"], "T": plan["T"]}},
         "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": achieved,
@@ -226,6 +289,12 @@ def main():
         "relaxed_compose": relaxed,
         "end_to_end_s": elapsed / args.steps,
     }
+    if args.other_steps > 0:
+        main_row = workload_row(run, args.steps)
+        del run, cost, dmax, s
+        torch.cuda.empty_cache()
+        out["workloads"] = five_workloads(torch, T, load_instance, args.space, args.other_steps,
+                                          args.workload, main_row)
     if not args.no_cpu:
         cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
         out["cpu_baseline"] = cb
