@@ -57,19 +57,24 @@ __global__ __launch_bounds__(256) void frontier_kernel(DevProblem P, const doubl
             double bc = kInf;
             int bd = 0, bm = -1, mx = 0;
             // members in batches of eight loads in flight; they come in ascending
-            // idx, so equal (cost, d_max) keeps the earlier one
+            // idx, so equal (cost, d_max) keeps the earlier one.  Depths are
+            // read first and a cost only where the member reaches past the
+            // previous rep: after the first pass most members do not, so the
+            // later passes move about one byte per member instead of nine.
             for (int mb = 0; mb < nm; mb += 8) {
                 double c[8];
                 int d[8];
+                int64_t idx[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    d[u] = 0;
+                    idx[u] = (int64_t)P.kb_members[m0 + min(mb + u, nm - 1)] * NS + s;
+                    if (mb + u < nm && live) d[u] = dmax[idx[u]];
+                }
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
                     c[u] = kInf;
-                    d[u] = 0;
-                    if (mb + u < nm && live) {
-                        const int64_t idx = (int64_t)P.kb_members[m0 + mb + u] * NS + s;
-                        c[u] = cost[idx];
-                        d[u] = dmax[idx];
-                    }
+                    if (d[u] > prev) c[u] = cost[idx[u]];
                 }
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
