@@ -711,12 +711,40 @@ static double least_fill(octx *c, double tau, int *ro, int *rS) {
     return Fst;
 }
 
+/* Fill one plan stage: layers [i, j) on island position o at depth d; the
+   candidate is the group's least-key entry fitting at d; `link` is the
+   transfer to the next stage (0 for the last). */
+static void emit_stage(octx *c, tgo_stage *st, int i, int j, int o, int d, double link) {
+    const oprob *p = c->p;
+    const int K = c->K;
+    int64_t s = slice_index(c->L, i, j);
+    int64_t gk = s * K + o;
+    int64_t rep = -1;
+    for (int64_t a = c->gstart[gk]; a < c->gend[gk]; a++)
+        if (c->ent[a].dmax >= d) { rep = a; break; }
+    const oentry *e = &c->ent[rep];
+    int64_t g = e->idx / c->NS;
+    const ocfg *cf = &p->cfg[g];
+    ocoef co;
+    config_coef(p, cf, &co);
+    double cost, state, A1;
+    int dm;
+    score_candidate(p, &co, &p->slice_sum[s * NSUM], &cost, &dm, &state, &A1);
+    double dd = cf->of ? 1.0 : (double)d;
+    double inflight = dd < co.m_real ? dd : co.m_real;
+    st->island = c->order[o]; st->first_layer = i; st->end_layer = j;
+    st->tp = cf->tp; st->cp = cf->cp; st->dp = cf->dp; st->ep = cf->ep; st->zero = cf->z;
+    st->recompute = cf->rc; st->offload = cf->of; st->mb = cf->mb;
+    st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
+    st->mem_bytes = state + (inflight * A1);
+    st->link_out = link;
+}
+
 /* Walk the argmins of the step-(3) tables at bound tau from root (ro, rS) and
    fill the plan's stages: smallest j attaining F, then smallest later
    position attaining G; each stage's candidate is its group's least-key entry
    fitting at the stage's depth. */
 static void backtrack(octx *c, double tau, int ro, int rS, tgo_plan *plan) {
-    const oprob *p = c->p;
     const int L = c->L, K = c->K;
     int i = 0, o = ro;
     for (int t = 0; t < rS; t++) {
@@ -732,28 +760,7 @@ static void backtrack(octx *c, double tau, int ro, int rS, tgo_plan *plan) {
                 if (x <= tau && x + AT(c->V, d - 1, j, o_next) == AT(c->Wt, d - 1, j, o)) break;
             }
         }
-        tgo_stage *st = &plan->stage[t];
-        int64_t s = slice_index(L, i, j);
-        int64_t gk = s * K + o;
-        int64_t rep = -1;
-        for (int64_t a = c->gstart[gk]; a < c->gend[gk]; a++)
-            if (c->ent[a].dmax >= d) { rep = a; break; }
-        const oentry *e = &c->ent[rep];
-        int64_t g = e->idx / c->NS;
-        const ocfg *cf = &p->cfg[g];
-        ocoef co;
-        config_coef(p, cf, &co);
-        double cost, state, A1;
-        int dm;
-        score_candidate(p, &co, &p->slice_sum[s * NSUM], &cost, &dm, &state, &A1);
-        double dd = cf->of ? 1.0 : (double)d;
-        double inflight = dd < co.m_real ? dd : co.m_real;
-        st->island = c->order[o]; st->first_layer = i; st->end_layer = j;
-        st->tp = cf->tp; st->cp = cf->cp; st->dp = cf->dp; st->ep = cf->ep; st->zero = cf->z;
-        st->recompute = cf->rc; st->offload = cf->of; st->mb = cf->mb;
-        st->depth = d; st->pair_index = e->idx; st->cost = e->cost;
-        st->mem_bytes = state + (inflight * A1);
-        st->link_out = d > 1 ? XA(j, o, o_next) : 0.0;
+        emit_stage(c, &plan->stage[t], i, j, o, d, d > 1 ? XA(j, o, o_next) : 0.0);
         i = j;
         o = o_next;
     }
@@ -910,6 +917,239 @@ static int compose_impl(void *h, const int64_t *cands, int64_t n, const int32_t 
     free(pos); free(ent); free(c->V); free(c->Wt); free(c->Td); free(c->X); free(c->gstart); free(c->gend);
     return plan->status;
 }
+/* ------------------------------------------------------------------------ */
+/* composition over every island order: the subset dynamic program           */
+/* ------------------------------------------------------------------------ */
+/* A plan uses a set U of islands, each at most once, in any order (Sec. 5.2
+   builds the pipeline from any islands; Sec. 6.2 shows that their order
+   changes the plan).  With U the set of islands from a stage to the pipeline
+   end, the stage's depth is |U|, so the island order needs no input:
+     V(U,k,i)  least bottleneck covering [i, L) with the stages on the islands
+               of U, the first on k (k in U);
+     W(U',k,j) least bottleneck of a continuation on the islands of U' after a
+               stage on k (k not in U') ends at j.
+   Every proper subset of U is numerically smaller than U, so visiting the
+   sets in ascending order computes each continuation before it is used.
+   The arrays are indexed [U][k][i], (2^K x K x (L+1)), so K <= 16. */
+#define SV(A, U, k, i) A[(((int64_t)(U) * c->K) + (k)) * (c->L + 1) + (i)]
+
+static int popcount32(uint32_t x) {
+    int n = 0;
+    while (x) { n += (int)(x & 1u); x >>= 1; }
+    return n;
+}
+
+static double least_bottleneck_sets(octx *c, double *V, double *W) {
+    const int L = c->L, K = c->K, D = c->D;
+    const uint32_t full = 1u << K;
+    for (uint32_t U = 1; U < full; U++) {
+        const int d = popcount32(U);
+        for (int k = 0; k < K; k++) {
+            if (!(U >> k & 1u)) continue;
+            const uint32_t Up = U & ~(1u << k);
+            for (int i = 0; i <= L; i++) {
+                double v = INFINITY;
+                if (d > D || i == L) v = INFINITY;
+                else if (d == 1) v = TD(1, slice_index(L, i, L), k);
+                else
+                    for (int j = i + 1; j <= L - d + 1; j++) {
+                        double x = maxd(TD(d, slice_index(L, i, j), k), SV(W, Up, k, j));
+                        if (x < v) v = x;
+                    }
+                SV(V, U, k, i) = v;
+            }
+        }
+        /* continuations on exactly the islands of U, after a stage on k0 */
+        for (int k0 = 0; k0 < K; k0++) {
+            if (U >> k0 & 1u) continue;
+            for (int j = 0; j <= L; j++) {
+                double w = INFINITY;
+                if (j >= 1 && j < L)
+                    for (int k = 0; k < K; k++) {
+                        if (!(U >> k & 1u)) continue;
+                        double x = maxd(XA(j, k0, k), SV(V, U, k, j));
+                        if (x < w) w = x;
+                    }
+                SV(W, U, k0, j) = w;
+            }
+        }
+    }
+    double Pst = INFINITY;
+    for (uint32_t U = 1; U < full; U++)
+        for (int k = 0; k < K; k++)
+            if ((U >> k & 1u) && SV(V, U, k, 0) < Pst) Pst = SV(V, U, k, 0);
+    return Pst;
+}
+
+/* Step (3) over sets at bound tau: least fill with every stage and link
+   within tau, ties to the least cut j and then the least next island.  The
+   root is the least F(U, k, 0); ties go to the least first island k, then
+   fewer stages |U|, then the numerically least set U. */
+static double least_fill_sets(octx *c, double tau, double *F, double *G, int *rk, uint32_t *rU) {
+    const int L = c->L, K = c->K, D = c->D;
+    const uint32_t full = 1u << K;
+    for (uint32_t U = 1; U < full; U++) {
+        const int d = popcount32(U);
+        for (int k = 0; k < K; k++) {
+            if (!(U >> k & 1u)) continue;
+            const uint32_t Up = U & ~(1u << k);
+            for (int i = 0; i <= L; i++) {
+                double v = INFINITY;
+                if (d > D || i == L) v = INFINITY;
+                else if (d == 1) {
+                    double t = TD(1, slice_index(L, i, L), k);
+                    if (t <= tau) v = t;
+                } else
+                    for (int j = i + 1; j <= L - d + 1; j++) {
+                        double t = TD(d, slice_index(L, i, j), k);
+                        if (!(t <= tau)) continue;
+                        double x = t + SV(G, Up, k, j);
+                        if (x < v) v = x;
+                    }
+                SV(F, U, k, i) = v;
+            }
+        }
+        for (int k0 = 0; k0 < K; k0++) {
+            if (U >> k0 & 1u) continue;
+            for (int j = 0; j <= L; j++) {
+                double g = INFINITY;
+                if (j >= 1 && j < L)
+                    for (int k = 0; k < K; k++) {
+                        if (!(U >> k & 1u)) continue;
+                        double x = XA(j, k0, k);
+                        if (!(x <= tau)) continue;
+                        double y = x + SV(F, U, k, j);
+                        if (y < g) g = y;
+                    }
+                SV(G, U, k0, j) = g;
+            }
+        }
+    }
+    double Fst = INFINITY;
+    *rk = -1;
+    *rU = 0;
+    for (int k = 0; k < K; k++)
+        for (int d = 1; d <= D; d++)
+            for (uint32_t U = 1; U < full; U++) {
+                if (!(U >> k & 1u) || popcount32(U) != d) continue;
+                if (SV(F, U, k, 0) < Fst) { Fst = SV(F, U, k, 0); *rk = k; *rU = U; }
+            }
+    return Fst;
+}
+
+/* Walk the step-(3) set tables from root (rk, rU): least j attaining F, then
+   least next island attaining G. */
+static void backtrack_sets(octx *c, double tau, const double *F, const double *G, int rk, uint32_t rU,
+                           tgo_plan *plan) {
+    const int L = c->L, K = c->K;
+    const int S = popcount32(rU);
+    int i = 0, k = rk;
+    uint32_t U = rU;
+    for (int t = 0; t < S; t++) {
+        int d = S - t, j, k_next = -1;
+        const uint32_t Up = U & ~(1u << k);
+        if (d == 1) j = L;
+        else {
+            for (j = i + 1; j <= L - d + 1; j++) {
+                double tt = TD(d, slice_index(L, i, j), k);
+                if (tt <= tau && tt + SV(G, Up, k, j) == SV(F, U, k, i)) break;
+            }
+            for (k_next = 0; k_next < K; k_next++) {
+                if (!(Up >> k_next & 1u)) continue;
+                double x = XA(j, k, k_next);
+                if (x <= tau && x + SV(F, Up, k_next, j) == SV(G, Up, k, j)) break;
+            }
+        }
+        emit_stage(c, &plan->stage[t], i, j, k, d, d > 1 ? XA(j, k, k_next) : 0.0);
+        i = j;
+        k = k_next;
+        U = Up;
+    }
+}
+#undef SV
+
+/* Composition over every island subset and order, steps (1)-(3) per b.
+   per_b (may be NULL): nb x 3 (P*, F*, T).  K <= 16. */
+int tgo_compose_sets(void *h, const int64_t *cands, int64_t n, tgo_plan *plan, double *per_b) {
+    oprob *p = (oprob *)h;
+    const int L = p->L, K = p->K;
+    const int64_t NS = p->NS;
+    memset(plan, 0, sizeof(tgo_plan));
+    plan->status = TGO_ENOPLAN;
+    plan->T = INFINITY; plan->P = INFINITY; plan->F = INFINITY;
+    if (K > 16) return TGO_EINVAL;
+    int32_t *ident = (int32_t *)malloc(sizeof(int32_t) * K);
+    for (int k = 0; k < K; k++) ident[k] = k;
+    oentry *ent = (oentry *)malloc(sizeof(oentry) * (n > 0 ? n : 1));
+    int64_t ne = 0;
+    for (int64_t t = 0; t < n; t++) {
+        int64_t idx = cands[t];
+        if (idx < 0 || idx >= p->N || (t > 0 && idx <= cands[t - 1])) {
+            free(ident); free(ent); return TGO_EINVAL;
+        }
+        int64_t g = idx / NS, s = idx % NS;
+        const ocfg *cf = &p->cfg[g];
+        if (p->B % cf->b != 0) { free(ident); free(ent); return TGO_EINVAL; }
+        int bi = 0;
+        while (p->bvals[bi] != cf->b) bi++;
+        ocoef o;
+        config_coef(p, cf, &o);
+        oentry *e = &ent[ne];
+        score_candidate(p, &o, &p->slice_sum[s * NSUM], &e->cost, &e->dmax, NULL, NULL);
+        if (e->dmax < 1) continue;
+        e->gkey = ((int64_t)bi * NS + s) * K + cf->k;
+        e->idx = idx;
+        ne++;
+    }
+    qsort(ent, (size_t)ne, sizeof(oentry), cmp_entry);
+
+    octx cx;
+    octx *c = &cx;
+    c->p = p; c->order = ident; c->L = L; c->K = K; c->NS = NS; c->ent = ent;
+    c->D = K < L ? K : L;
+    const int64_t sets = ((int64_t)1 << K) * K * (L + 1);
+    double *V = (double *)malloc(sizeof(double) * sets);
+    double *W = (double *)malloc(sizeof(double) * sets);
+    c->V = NULL; c->Wt = NULL;
+    c->Td = (double *)malloc(sizeof(double) * (c->D + 1) * NS * K);
+    c->X = (double *)malloc(sizeof(double) * (L + 1) * K * K);
+    c->gstart = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    c->gend = (int64_t *)malloc(sizeof(int64_t) * NS * K);
+    if (!V || !W || !c->Td || !c->X || !c->gstart || !c->gend) {
+        free(ident); free(ent); free(V); free(W); free(c->Td); free(c->X); free(c->gstart); free(c->gend);
+        return TGO_ENOMEM;
+    }
+    double bestT = INFINITY;
+    int64_t e0 = 0;
+    for (int bi = 0; bi < p->nb; bi++) {
+        c->b = p->bvals[bi];
+        c->m = p->B / c->b;
+        if (per_b)
+            for (int q = 0; q < 3; q++) per_b[bi * 3 + q] = INFINITY;
+        int64_t e1 = e0;
+        while (e1 < ne && ent[e1].gkey / (NS * K) == bi) e1++;
+        build_tables(c, e0, e1, bi);
+        e0 = e1;
+        double Pst = least_bottleneck_sets(c, V, W);
+        if (!(Pst < INFINITY)) continue;
+        int rk;
+        uint32_t rU;
+        double Fst = least_fill_sets(c, Pst, V, W, &rk, &rU);
+        if (rk < 0) continue;
+        double Tb = ((double)(c->m - 1) * Pst) + Fst;
+        if (per_b) { per_b[bi * 3] = Pst; per_b[bi * 3 + 1] = Fst; per_b[bi * 3 + 2] = Tb; }
+        if (Tb < bestT) {
+            bestT = Tb;
+            plan->status = TGO_OK;
+            plan->b = (int32_t)c->b; plan->m = (int32_t)c->m; plan->S = popcount32(rU);
+            plan->P = Pst; plan->F = Fst; plan->T = Tb;
+            backtrack_sets(c, Pst, V, W, rk, rU, plan);
+        }
+    }
+    free(ident); free(ent); free(V); free(W); free(c->Td); free(c->X); free(c->gstart); free(c->gend);
+    return plan->status;
+}
+
 #undef AT
 #undef TD
 #undef XA

@@ -228,3 +228,81 @@ def linear_partition_minmax(values, parts):
         else:
             lo = mid + 1
     return lo
+
+
+def enumerate_plans_all_orders(orc, rows, allowed=None):
+    """Every feasible plan per b over every island subset and order: dict
+    b -> list of plans with P, F and the key (k_1, S, set mask, j_1, k_2, j_2,
+    ..., k_S) that orders ties (first island, stage count, set, then cuts and
+    islands front to back)."""
+    inst = orc.inst
+    L, K = orc.L, orc.K
+    B = inst["space"]["global_batch"]
+    groups = groups_of(rows)
+
+    def stage_choice(i, j, k, b, d):
+        fit = [r for r in groups.get((i, j, k, b), [])
+               if r["dmax"] >= d and (allowed is None or r["idx"] in allowed)]
+        return min(fit, key=key) if fit else None
+
+    out = {}
+    for b in orc.bvalues:
+        m = B // b
+        plans = []
+        for S in range(1, min(K, L) + 1):
+            for isl in itertools.permutations(range(K), S):
+                mask = sum(1 << k for k in isl)
+                for cuts in itertools.combinations(range(1, L), S - 1):
+                    bounds = (0,) + cuts + (L,)
+                    f, x, picks = [], [], []
+                    ok = True
+                    for t in range(S):
+                        pick = stage_choice(bounds[t], bounds[t + 1], isl[t], b, S - t)
+                        if pick is None:
+                            ok = False
+                            break
+                        f.append(pick["cost"])
+                        picks.append(pick)
+                        if t < S - 1:
+                            x.append(transfer(inst, b, bounds[t + 1], isl[t], isl[t + 1]))
+                    if not ok:
+                        continue
+                    P = max(f + x)
+                    if P == math.inf:
+                        continue
+                    pk = [isl[0], S, mask]
+                    for t in range(S - 1):
+                        pk += [cuts[t], isl[t + 1]]
+                    plans.append({"P": P, "F": right_fold(f, x), "key": tuple(pk), "islands": isl,
+                                  "cuts": cuts, "picks": picks, "f": f, "x": x, "b": b, "m": m, "L": L})
+        out[b] = plans
+    return out
+
+
+def brute_force_compose_sets(orc, rows, allowed=None):
+    """Exhaustive steps (1)-(3) over every island subset and order: per b the
+    least bottleneck, then the least fill at it.  Returns per-b (P*, F*, T)
+    and the optimum with its optimal plans and the least-key one."""
+    per_b = {}
+    best = None
+    for b, plans in enumerate_plans_all_orders(orc, rows, allowed).items():
+        if not plans:
+            per_b[b] = (math.inf, math.inf, math.inf)
+            continue
+        m = plans[0]["m"]
+        Pst = min(p["P"] for p in plans)
+        at = [p for p in plans if p["P"] == Pst]
+        Fst = min(p["F"] for p in at)
+        opt = [p for p in at if p["F"] == Fst]
+        T = (float(m - 1) * Pst) + Fst
+        per_b[b] = (Pst, Fst, T)
+        if best is None or T < best["T"]:
+            best = {"T": T, "b": b, "P": Pst, "F": Fst, "lexmin": min(opt, key=lambda p: p["key"]),
+                    "optimal": opt}
+    return per_b, best
+
+
+def sets_signature(p):
+    S = len(p["islands"])
+    bounds = (0,) + p["cuts"] + (p["L"],)
+    return tuple((p["islands"][t], bounds[t], bounds[t + 1], S - t, p["picks"][t]["idx"]) for t in range(S))

@@ -19,8 +19,8 @@ def instance(L=1, K=1, layer=None, layers=None, n_gpus=1, peak=2.0**40, hbm=2.0*
         base.update(layer or {})
         layers = {f: [int(base[f])] * L for f in LAYER_FIELDS}
     else:
-        layers = {f: [int(v) for v in layers.get(f, [0] * L)] for f in LAYER_FIELDS}
         L = len(layers["fwd_flops"])
+        layers = {f: [int(v) for v in layers.get(f, [0] * L)] for f in LAYER_FIELDS}
 
     def per(v, cast):
         return [cast(x) for x in v] if isinstance(v, (list, tuple)) else [cast(v)] * K

@@ -1,0 +1,248 @@
+"""Pins of the oracle's composition over every island subset and order (the
+set dynamic program): Sec. 5.2 composes a pipeline from any islands, and
+Sec. 6.2 shows that the order in which islands are stacked changes the plan,
+so the order is searched instead of taken as an input.
+
+Objective and ties as for a fixed order (steps (1)-(3) per b): least
+bottleneck, then least fill at it; across b least T, ties to the smaller b.
+Plan ties: least first island, then fewer stages, then the numerically least
+island set, then the least cut and the least next island, stage by stage.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+from oracle.oracle import Oracle, ENOPLAN, EINVAL
+from workloads import make_instance, random_tiny
+from tests import brute
+from tests.inst_util import instance, tiny_tight
+
+
+def _random(seed):
+    if seed % 5 == 4:  # a few with four islands on short models
+        return random_tiny(seed, L_range=(2, 4), K_range=(4, 4), tight=(seed % 2 == 1))
+    return random_tiny(seed, tight=(seed % 2 == 1))
+
+
+def _check_against_brute(o, rows):
+    surv = o.prune()
+    st, plan, per_b = o.compose_sets(surv)
+    bf_per_b, best = brute.brute_force_compose_sets(o, rows)
+    for bi, b in enumerate(o.bvalues):
+        P, F, T = bf_per_b[b]
+        if math.isinf(P):
+            assert math.isinf(per_b[bi][0])
+        else:
+            assert tuple(per_b[bi]) == (P, F, T), (b, per_b[bi], (P, F, T))
+    if best is None:
+        assert st == ENOPLAN
+        return "noplan"
+    assert st == 0
+    assert (plan["b"], plan["P"], plan["F"], plan["T"]) == (best["b"], best["P"], best["F"], best["T"])
+    sig = brute.plan_signature(plan)
+    optimal = {brute.sets_signature(p): p for p in best["optimal"]}
+    assert sig in optimal, "oracle plan is not among the optimal plans"
+    lex = brute.sets_signature(best["lexmin"])
+    if sig == lex:
+        return "lexmin"
+    # differs only through floating-point absorption: where the two plans
+    # part, their suffix fills differ although both totals tie
+    mine, other = optimal[sig], best["lexmin"]
+    t = next(t for t in range(min(len(sig), len(lex))) if sig[t] != lex[t])
+    if t == 0:  # the first stage differs: same root (island, count, set), other cut
+        assert (mine["key"][:3] == other["key"][:3])
+    assert brute.suffix_values(mine)[t] != brute.suffix_values(other)[t]
+    return "absorbed"
+
+
+@pytest.mark.parametrize("seed", range(80))
+def test_sets_equal_exhaustive_search(seed):
+    o = Oracle(_random(seed))
+    _check_against_brute(o, brute.candidate_table(o))
+
+
+def test_sets_exhaustive_tiny_and_tight():
+    outcomes = []
+    for inst in (make_instance("tiny"), tiny_tight()):
+        o = Oracle(inst)
+        outcomes.append(_check_against_brute(o, brute.candidate_table(o)))
+    assert outcomes[0] == "lexmin"
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_sets_are_the_best_over_every_order(seed):
+    # per b, (P*, F*) over sets = the lexicographic least (P*, F*) that the
+    # fixed-order composition reaches over all K! island orders
+    o = Oracle(_random(seed))
+    s = o.prune()
+    st, plan, per_b = o.compose_sets(s)
+    best = None
+    for order in itertools.permutations(range(o.K)):
+        _, _, pb = o.compose(s, list(order))
+        cur = [tuple(r[:2]) for r in pb]
+        best = cur if best is None else [min(a, c) for a, c in zip(best, cur)]
+    for bi in range(o.n_b):
+        assert tuple(per_b[bi][:2]) == best[bi], (bi, per_b[bi], best[bi])
+
+
+def test_one_island_equals_the_fixed_order():
+    for seed in range(20):
+        o = Oracle(random_tiny(seed, K_range=(1, 1), tight=(seed % 2 == 1)))
+        s = o.prune()
+        a = o.compose(s)
+        b = o.compose_sets(s)
+        assert a[0] == b[0]
+        assert np.array_equal(a[2], b[2])
+        assert brute.plan_signature(a[1]) == brute.plan_signature(b[1])
+
+
+@pytest.mark.parametrize("seed", [0, 3, 7, 11])
+def test_island_relabelling_leaves_the_values(seed):
+    inst = random_tiny(seed, L_range=(4, 6), K_range=(3, 3))
+    o = Oracle(inst)
+    _, plan, per_b = o.compose_sets(o.prune())
+    perm = [2, 0, 1]  # new island t is old island perm[t]
+    inst2 = dict(inst)
+    inst2["islands"] = {f: [v[perm[t]] for t in range(3)] for f, v in inst["islands"].items()}
+    inst2["inter_bw"] = [[inst["inter_bw"][perm[a]][perm[b]] for b in range(3)] for a in range(3)]
+    inv = {perm[t]: t for t in range(3)}
+    inst2["island_order"] = [inv[k] for k in inst["island_order"]]
+    o2 = Oracle(inst2)
+    _, plan2, per_b2 = o2.compose_sets(o2.prune())
+    assert np.array_equal(per_b, per_b2)
+    assert (plan["b"], plan["P"], plan["F"], plan["T"]) == (plan2["b"], plan2["P"], plan2["F"], plan2["T"])
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_sets_prune_safety(seed):
+    o = Oracle(_random(seed))
+    cost, dmax = o.score()
+    B = o.inst["space"]["global_batch"]
+    compatible = [idx for idx in range(o.N)
+                  if B % (o.decode(idx)["dp"] * o.decode(idx)["mb"]) == 0]
+    a = o.compose_sets(o.prune())
+    b = o.compose_sets(compatible)
+    assert a[0] == b[0] and np.array_equal(a[2], b[2])
+    assert brute.plan_signature(a[1]) == brute.plan_signature(b[1])
+
+
+def test_bad_input_order_is_repaired():
+    # the memory-rich island must hold the deep (first) stage; a fixed order
+    # that puts it last finds a worse plan or none, the set search does not
+    # depend on the order
+    # island 1 holds one layer's state (2^30 B) plus one stashed micro-batch
+    # (2^29 B) but not two, so it can only run the last stage
+    lay = {"fwd_flops": 2 ** 40, "dense_params": 2 ** 26, "act_stash_bytes": 2 ** 29,
+           "out_act_bytes": 2 ** 20}
+    inst = instance(K=2, L=4, layer=lay, n_gpus=1, hbm=[2.0 ** 40, 1.75 * 2.0 ** 30], B=8, tp=(1,),
+                    mb=(1,), zero=(0,), inter=2.0 ** 40)
+    o = Oracle(inst)
+    s = o.prune()
+    fixed = {tuple(order): o.compose(s, order)[1] for order in ([0, 1], [1, 0])}
+    assert [x["island"] for x in fixed[(0, 1)]["stages"]] == [0, 1]
+    assert [x["island"] for x in fixed[(1, 0)]["stages"]] == [0]  # island 1 unusable first
+    assert fixed[(0, 1)]["T"] < fixed[(1, 0)]["T"]
+    st, plan, _ = o.compose_sets(s)
+    assert st == 0 and plan["T"] == fixed[(0, 1)]["T"]
+    assert brute.plan_signature(plan) == brute.plan_signature(fixed[(0, 1)])
+
+
+def test_uniform_layers_any_order_closed_form():
+    # identical islands, free links, equal layers: ceil(L / min(K, L)) layers
+    # on the bottleneck stage whatever the order
+    for L, K in ((6, 3), (7, 3), (5, 4), (3, 4)):
+        lay = {"fwd_flops": 2 ** 40}
+        inst = instance(K=K, L=L, layer=lay, n_gpus=1, B=1, tp=(1,), mb=(1,), zero=(0,),
+                        inter=math.inf)
+        o = Oracle(inst)
+        st, plan, _ = o.compose_sets(o.prune())
+        per_layer = o.score_list([0])[0][0]  # slice [0, 1) on island 0
+        assert plan["P"] == per_layer * math.ceil(L / min(K, L))
+
+
+def check_set_plan_invariants(o, plan, survivors):
+    inst = o.inst
+    B = inst["space"]["global_batch"]
+    st = plan["stages"]
+    assert plan["S"] == len(st) >= 1
+    assert B % plan["b"] == 0 and plan["m"] == B // plan["b"]
+    assert st[0]["first_layer"] == 0 and st[-1]["end_layer"] == o.L
+    for a, c in zip(st, st[1:]):
+        assert a["end_layer"] == c["first_layer"]
+    islands = [s["island"] for s in st]
+    assert len(set(islands)) == len(islands)
+    surv = set(int(x) for x in survivors)
+    costs, dms = o.score_list([s["pair_index"] for s in st])
+    for t, s in enumerate(st):
+        assert s["depth"] == plan["S"] - t and s["pair_index"] in surv
+        d = o.decode(s["pair_index"])
+        assert (d["i"], d["j"], d["island"]) == (s["first_layer"], s["end_layer"], s["island"])
+        assert costs[t] == s["cost"] and dms[t] >= s["depth"]
+        assert s["mem_bytes"] <= inst["islands"]["hbm_bytes"][s["island"]] * inst["space"]["mem_frac"]
+    f = [s["cost"] for s in st]
+    x = [s["link_out"] for s in st[:-1]]
+    for t in range(len(x)):
+        assert x[t] == brute.transfer(inst, plan["b"], st[t]["end_layer"], st[t]["island"], st[t + 1]["island"])
+    assert plan["P"] == max(f + x)
+    assert plan["F"] == brute.right_fold(f, x)
+    assert plan["T"] == (float(plan["m"] - 1) * plan["P"]) + plan["F"]
+
+
+@pytest.mark.parametrize("name", ["tiny", "dense8b"])
+def test_named_instance_set_plans(name):
+    o = Oracle(make_instance(name))
+    s = o.prune()
+    st, plan, per_b = o.compose_sets(s)
+    assert st == 0
+    check_set_plan_invariants(o, plan, s)
+    assert plan["T"] == min(per_b[:, 2])
+    # never worse than any fixed order's plan
+    for order in itertools.permutations(range(o.K)):
+        assert plan["T"] <= o.compose(s, list(order))[1]["T"]
+
+
+def test_more_than_16_islands_rejected():
+    inst = make_instance("moe")  # 32 islands
+    o = Oracle(inst)
+    st, plan, _ = o.compose_sets([])
+    assert st == EINVAL
+
+
+def _symmetric(seed):
+    """Identical islands, equal links and power-of-two layer values: many
+    plans tie exactly, so only the stated tie rules pick the plan."""
+    rng = np.random.default_rng(1000 + seed)
+    L = int(rng.integers(3, 6))
+    K = int(rng.integers(2, 4)) if seed % 3 else 4
+    layers = {"fwd_flops": [int(2 ** rng.integers(38, 41)) for _ in range(L)],
+              "dense_params": [int(2 ** rng.integers(24, 27)) for _ in range(L)],
+              "act_stash_bytes": [int(2 ** rng.integers(26, 29)) for _ in range(L)],
+              "tp_comm_bytes": [int(2 ** rng.integers(20, 24)) for _ in range(L)],
+              "out_act_bytes": [2 ** 20] * L}
+    hbm = 2.0 ** 32 if seed % 2 else 2.0 ** 40
+    return instance(K=K, layers=layers, n_gpus=2, hbm=hbm, B=8, tp=(1, 2), mb=(1, 2), zero=(0, 3),
+                    inter=2.0 ** 34, order=list(range(K))[::-1])
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_exact_ties_follow_the_stated_rule(seed):
+    o = Oracle(_symmetric(seed))
+    assert _check_against_brute(o, brute.candidate_table(o)) in ("lexmin", "noplan")
+
+
+def test_root_tie_prefers_the_least_first_island_over_fewer_stages():
+    # Two optimal plans, equal P and F: layer 0 on island 0 then the free
+    # layer 1 on island 1 (first island 0, two stages), or both layers on
+    # island 1 (first island 1, one stage).  Island 0 cannot hold layer 1.
+    layers = {"fwd_flops": [2 ** 40, 0], "dense_params": [2 ** 20, 2 ** 30],
+              "act_stash_bytes": [2 ** 20, 0], "out_act_bytes": [0, 0]}
+    inst = instance(K=2, layers=layers, n_gpus=1, hbm=[2.0 ** 30, 2.0 ** 40], B=4, inter=2.0 ** 34)
+    o = Oracle(inst)
+    rows = brute.candidate_table(o)
+    _, best = brute.brute_force_compose_sets(o, rows)
+    assert sorted(p["key"][:2] for p in best["optimal"]) == [(0, 2), (1, 1)]
+    st, plan, _ = o.compose_sets(o.prune())
+    assert [s["island"] for s in plan["stages"]] == [0, 1]
+    assert _check_against_brute(o, rows) == "lexmin"
