@@ -16,7 +16,9 @@ before the timed region.  Prints one JSON line:
   cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
                workload (the same 128 layers on the first islands only)
   workloads    the same plan search timed on each of the five synthetic
-               clusters (fewer steps), after the main measurement
+               clusters (fewer steps), after the main measurement; for those
+               with at most 16 islands also the composition over every
+               island order (tg_compose_pipeline_all_orders)
 --space extended adds context parallelism {1,2,4}, recomputation and
 offloading to the chosen workload's config space.
 """
@@ -147,7 +149,24 @@ def time_search(torch, T, inst, steps, warmup):
         st, plan, s = step(ev[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    return {"problem": p, "N": N, "cost": cost, "dmax": dmax, "survivors": s, "status": st,
+    orders = None
+    if p.K <= 16 and steps > 0:
+        # composition over every island order on the same survivors (host
+        # clock around each call: it synchronises once)
+        ows = p.compose_all_orders_workspace(int(s.numel()))
+        p.tg_compose_pipeline_all_orders(s, cost, dmax, workspace=ows)  # warm-up
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(min(steps, 5)):
+            t1 = time.perf_counter()
+            ost, oplan = p.tg_compose_pipeline_all_orders(s, cost, dmax, workspace=ows)
+            times.append((time.perf_counter() - t1) * 1e3)
+        times.sort()
+        orders = {"compose_ms_median": times[len(times) // 2], "status": ost, "b": oplan["b"],
+                  "stages": oplan["S"], "T": oplan["T"],
+                  "islands": [x["island"] for x in oplan["stages"]]}
+        del ows
+    return {"problem": p, "all_orders": orders, "N": N, "cost": cost, "dmax": dmax, "survivors": s, "status": st,
             "plan": plan, "elapsed": elapsed, "create_s": t_create,
             "score_ms": [ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)],
             "prune_ms": [ev[k][1].elapsed_time(ev[k][2]) for k in range(steps)],
@@ -183,7 +202,8 @@ def workload_row(run, steps):
             "compose_ms": sum(run["compose_ms"]) / steps,
             "score_hbm_frac": SCORE_BYTES_PER_CANDIDATE * run["N"] / (sc / 1e3) / 1e9 / HBM_PEAK_GBS,
             "plan": {"status": run["status"], "b": run["plan"]["b"], "stages": run["plan"]["S"],
-                     "T": run["plan"]["T"]}}
+                     "T": run["plan"]["T"]},
+            "all_orders_compose": run["all_orders"]}
 
 
 def score_source_digest():

@@ -279,6 +279,28 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
                                       const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
                                       tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream);
 
+/*
+ * Composition over every island subset and order (Sec. 5.2 builds the
+ * pipeline from any islands, each used at most once; Sec. 6.2 shows that the
+ * order in which islands are stacked changes the plan): the island order is
+ * searched instead of given.  For each b the plan minimises the bottleneck P,
+ * then the fill F at it, over all plans on any ordered subset of islands;
+ * across b it minimises T = (m - 1) P + F, ties to the smaller b.  Ties inside
+ * a b go to the least first island id, then fewer stages, then the least set
+ * of islands (as a bit mask, island k = bit k), then the earliest cut, then
+ * the least next island id, stage by stage.  The set dynamic program has
+ * K 2^(K-1) states per first layer and b, so K <= 16 (TG_EINVAL otherwise,
+ * and the workspace query returns 0); at most 65535 distinct b.  List
+ * requirements, scores and errors as for tg_compose_pipeline (no island
+ * order).  d_ws: at least tg_compose_all_orders_workspace_bytes(p,
+ * n_survivors) bytes, about nb K 2^(K-1) (3L + 8) bytes for the argmin and
+ * root tables plus two level buffers.  Synchronises the stream once.
+ */
+size_t tg_compose_all_orders_workspace_bytes(const tg_problem *p, int64_t n_survivors);
+tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                         const double *d_cost, const uint8_t *d_dmax, tg_plan *out, void *d_ws,
+                                         size_t ws_bytes, tg_stream stream);
+
 /* Message of the calling thread's last failed call ("" if none). */
 const char *tg_last_error(void);
 

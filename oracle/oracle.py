@@ -87,7 +87,7 @@ def lib():
         L.tgo_prune.argtypes = [vp, i64p, ctypes.c_int64, i64p]
         L.tgo_compose.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
         L.tgo_compose_relaxed.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
-        L.tgo_compose_sets.argtypes = [vp, i64p, ctypes.c_int64, ctypes.POINTER(Plan), f64p]
+        L.tgo_compose_all_orders.argtypes = [vp, i64p, ctypes.c_int64, ctypes.POINTER(Plan), f64p]
         _lib = L
     return _lib
 
@@ -236,14 +236,14 @@ class Oracle:
                                        _ptr(per_b, ctypes.c_double))
         return st, plan_to_dict(plan), per_b[: self.n_b]
 
-    def compose_sets(self, candidates):
+    def compose_all_orders(self, candidates):
         """Composition over every island subset and order (steps (1)-(3); no
         order input; K <= 16).  Returns (status, plan dict, per-b array [n_b, 3]
         of P*, F*, T)."""
         cands = np.ascontiguousarray(np.asarray(candidates, dtype=np.int64))
         plan = Plan()
         per_b = np.full((max(self.n_b, 1), 3), np.inf)
-        st = lib().tgo_compose_sets(self.h, _ptr(cands, ctypes.c_int64), len(cands), ctypes.byref(plan),
+        st = lib().tgo_compose_all_orders(self.h, _ptr(cands, ctypes.c_int64), len(cands), ctypes.byref(plan),
                                     _ptr(per_b, ctypes.c_double))
         return st, plan_to_dict(plan), per_b[: self.n_b]
 

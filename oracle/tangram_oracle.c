@@ -1070,7 +1070,7 @@ static void backtrack_sets(octx *c, double tau, const double *F, const double *G
 
 /* Composition over every island subset and order, steps (1)-(3) per b.
    per_b (may be NULL): nb x 3 (P*, F*, T).  K <= 16. */
-int tgo_compose_sets(void *h, const int64_t *cands, int64_t n, tgo_plan *plan, double *per_b) {
+int tgo_compose_all_orders(void *h, const int64_t *cands, int64_t n, tgo_plan *plan, double *per_b) {
     oprob *p = (oprob *)h;
     const int L = p->L, K = p->K;
     const int64_t NS = p->NS;

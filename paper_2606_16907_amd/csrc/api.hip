@@ -408,18 +408,23 @@ size_t tg_compose_relaxed_workspace_bytes(const tg_problem *p, int64_t n_survivo
     return tg::compose_relaxed_ws_bytes(p->P, n_survivors);
 }
 
+size_t tg_compose_all_orders_workspace_bytes(const tg_problem *p, int64_t n_survivors) {
+    if (!p || n_survivors < 0 || p->P.K > 16) return 0;
+    return tg::compose_orders_ws_bytes(p->P, n_survivors);
+}
+
 }  // extern "C"
 
 // Argument checks shared by both compositions; uploads the island order.
 static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
                                const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
                                tg_plan *out, void *d_ws, size_t ws_bytes, size_t need, hipStream_t s) {
-    if (!p || !out || !island_order) return fail(TG_EINVAL, "NULL argument");
+    if (!p || !out) return fail(TG_EINVAL, "NULL argument");
     std::memset(out, 0, sizeof(*out));
     out->P = out->F = out->T = HUGE_VAL;
     const int K = p->P.K;
     std::vector<int> seen(K, 0);
-    for (int o = 0; o < K; ++o) {
+    for (int o = 0; island_order && o < K; ++o) {
         const int k = island_order[o];
         if (k < 0 || k >= K || seen[k]) return fail(TG_EINVAL, "island_order is not a permutation");
         seen[k] = 1;
@@ -430,6 +435,7 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
     if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31)) return fail(TG_EINVAL, "stage table too large");
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (p->P.nb == 0) return fail(TG_ENOPLAN, "no micro-batch size divides the global batch");
+    if (!island_order) return TG_OK;
     hipError_t e = hipMemcpyAsync((char *)d_ws + tg::compose_order_offset(p->P, n_survivors), island_order,
                                   sizeof(int32_t) * K, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "order upload");
@@ -467,6 +473,7 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
                               const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
                               tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
     hipStream_t s = (hipStream_t)stream;
+    if (!island_order) return fail(TG_EINVAL, "NULL argument");
     const size_t need = p && n_survivors >= 0 ? tg::compose_ws_bytes(p->P, n_survivors) : 0;
     tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
                                  need, s);
@@ -481,6 +488,7 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
                                       const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
                                       tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
     hipStream_t s = (hipStream_t)stream;
+    if (!island_order) return fail(TG_EINVAL, "NULL argument");
     const size_t need = p && n_survivors >= 0 ? tg::compose_relaxed_ws_bytes(p->P, n_survivors) : 0;
     tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
                                  need, s);
@@ -491,6 +499,21 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
     hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax, d_ws,
                                               s, &res_dev, &rounds);
     if (e != hipSuccess) return hip_fail(e, "relaxed compose kernels");
+    return compose_end(res_dev, out, s);
+}
+
+tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                         const double *d_cost, const uint8_t *d_dmax, tg_plan *out, void *d_ws,
+                                         size_t ws_bytes, tg_stream stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (p && p->P.K > 16) return fail(TG_EINVAL, "composition over all island orders takes at most 16 islands");
+    if (p && p->P.nb > 65535) return fail(TG_EINVAL, "more than 65535 micro-batch sizes");
+    const size_t need = p && n_survivors >= 0 ? tg::compose_orders_ws_bytes(p->P, n_survivors) : 0;
+    tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, nullptr, out, d_ws, ws_bytes, need, s);
+    if (st != TG_OK) return st;
+    tg::ComposeResult *res_dev = nullptr;
+    hipError_t e = tg::launch_compose_orders(p->P, d_survivors, n_survivors, d_cost, d_dmax, d_ws, s, &res_dev);
+    if (e != hipSuccess) return hip_fail(e, "all-orders compose kernels");
     return compose_end(res_dev, out, s);
 }
 

@@ -30,7 +30,7 @@
 #include <climits>
 #include <type_traits>
 
-#include "tg_device.h"
+#include "compose_util.h"
 
 #pragma clang fp contract(off)
 
@@ -203,13 +203,7 @@ size_t compose_order_offset(const DevProblem &P, int64_t n_surv) {
     return align256(sizeof(ComposeResult));
 }
 
-// Groups (slice, island position, b) are numbered position-major, then b,
-// then slice: the candidate list runs through each config's slices in
-// ascending order, so building the groups touches consecutive counters.  The
-// stage table keeps the DP's layout [b][slice][position].
-__host__ __device__ inline int64_t group_id(const DevProblem &P, int64_t o, int64_t bi, int64_t s) {
-    return (o * P.nb + bi) * P.NS + s;
-}
+// The stage table keeps the DP's layout [b][slice][position].
 __host__ __device__ inline int64_t cell_id(const DevProblem &P, int64_t bi, int64_t s, int64_t o) {
     return (bi * P.NS + s) * P.K + o;
 }
@@ -277,6 +271,26 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int64_t *surv, int64
         ent_c[slot] = rec_c[r];
         ent_d[slot] = rec_d[r];
         ent_i[slot] = surv[r];
+    }
+}
+
+int64_t group_scan_tiles(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
+
+void launch_grouping(const DevProblem &P, const int64_t *surv, int64_t n, const double *cost,
+                     const uint8_t *dmax, const int32_t *pos, const Groups &g, ComposeResult *res,
+                     hipStream_t s) {
+    const int64_t G = n_groups(P);
+    fill<int32_t>(g.gcnt, G, 0, s);
+    if (n > 0) {
+        int64_t blocks = (n + 255) / 256;
+        if (blocks > 65536) blocks = 65536;
+        gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n, cost, dmax, pos, g.rec_g, g.rec_c,
+                                                                    g.rec_d, g.gcnt, res);
+        scan_i32(g.gcnt, G, g.tmp, s);
+        scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n, g.rec_g, g.rec_c, g.rec_d, g.gcnt,
+                                                                     g.ent_c, g.ent_d, g.ent_i);
+    } else {
+        scan_i32(g.gcnt, G, g.tmp, s);  // all zeros: offsets stay zero
     }
 }
 
@@ -946,13 +960,6 @@ struct LevelKernels {
 // wave per stage finds the stage's candidate in its group.
 constexpr int kFinishThreads = 256;
 
-// Candidate order within a group: least cost, then deepest fit, then least
-// index; idx < 0 marks "none".
-__device__ inline bool cand_less(double c1, int d1, int64_t i1, double c2, int d2, int64_t i2) {
-    if (i1 < 0) return false;
-    if (i2 < 0) return true;
-    return c1 < c2 || (c1 == c2 && (d1 > d2 || (d1 == d2 && i1 < i2)));
-}
 
 __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, const int32_t *gcnt,
                                                                 const double *ent_c, const uint8_t *ent_d,
@@ -1031,75 +1038,15 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
     if (S == 0) return;
     const int bb = sh_bb;
     const int64_t b = P.bvals[bb];
-    const int wv = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int wv = threadIdx.x / kWave;
     for (int t = wv; t < S; t += kFinishThreads / kWave) {
         const int d = S - t, i = st_i[t], j = st_j[t], o = st_o[t], o_next = st_on[t];
-        const int64_t s = slice_of(L, i, j);
-        const int64_t G = group_id(P, o, bb, s);
-        const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
-        int64_t best = -1;
-        double bc = kInf;
-        int bd = 0;
-        for (int32_t e = st + lane; e < en; e += kWave) {
-            const int dd = ent_d[e];
-            if (dd < d) continue;
-            const double c = ent_c[e];
-            const int64_t ie = ent_i[e];
-            if (cand_less(c, dd, ie, bc, bd, best)) {
-                best = ie;
-                bc = c;
-                bd = dd;
-            }
-        }
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-            const double c2 = __shfl_xor(bc, off);
-            const int d2 = __shfl_xor(bd, off);
-            const int64_t i2 = __shfl_xor(best, off);
-            if (cand_less(c2, d2, i2, bc, bd, best)) {
-                best = i2;
-                bc = c2;
-                bd = d2;
-            }
-        }
-        if (lane != 0) continue;
-        if (best < 0) {  // the stage table said a candidate fits here
-            res->err = 4;
-            res->status = TG_ENOPLAN;
-            continue;
-        }
-        const int64_t g = best / P.NS;
-        const Coef &c = P.coef[g];
-        const int64_t Lp = L + 1;
-        const double Pd = (double)(P.pre[Lp + j] - P.pre[Lp + i]);
-        const double Pe = (double)(P.pre[2 * Lp + j] - P.pre[2 * Lp + i]);
-        // stash per sample: layer outputs with recomputation, else all activations
-        const int sq = c.rc ? 6 : 3;
-        const double S = (double)(P.pre[sq * Lp + j] - P.pre[sq * Lp + i]);
-        const double state = (c.mud * Pd) + (c.mue * Pe);
-        const double A1 = c.rho * S;
-        tg_stage &sg = plan.stage[t];
-        sg.island = order[o];
-        sg.first_layer = i;
-        sg.end_layer = j;
-        sg.tp = c.tp;
-        sg.cp = c.cp;
-        sg.dp = c.dp;
-        sg.ep = c.ep;
-        sg.zero = c.z;
-        sg.recompute = c.rc;
-        sg.offload = c.of;
-        sg.mb = c.mb;
-        sg.depth = d;
-        sg.pair_index = best;
-        sg.cost = bc;
-        // in flight: min(d, m) micro-batches, one when offloaded
-        sg.mem_bytes = state + (fmin(c.of ? 1.0 : (double)d, c.m_real) * A1);
+        double link = 0.0;
         if (d > 1) {
             const double E = EoT[(int64_t)o_next * K + o];
-            sg.link_out = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;
-        } else {
-            sg.link_out = 0.0;
+            link = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;
         }
+        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, i, j, o, order[o], d, bb, link, plan.stage[t], res);
     }
 }
 
@@ -1245,20 +1192,14 @@ struct Driver {
 
     // candidate list -> grouped entries -> per-level table changes
     void setup(const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax) {
-        const int64_t G = n_groups(P), nbk = n_buckets(P);
+        const int64_t nbk = n_buckets(P);
         prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT,
                                                                                      w.EiT, w.res);
-        fill<int32_t>(w.gcnt, G, 0, s);
         fill<int32_t>(w.bcnt, nbk + 1, 0, s);
         fill<double>(w.Pst, P.nb, kInf, s);
+        const Groups g{w.rec_g, w.rec_c, w.rec_d, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.tmp};
+        launch_grouping(P, surv, n_surv, cost, dmax, w.pos, g, w.res, s);
         if (n_surv > 0) {
-            int64_t blocks = (n_surv + 255) / 256;
-            if (blocks > 65536) blocks = 65536;
-            gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n_surv, cost, dmax, w.pos, w.rec_g,
-                                                                        w.rec_c, w.rec_d, w.gcnt, w.res);
-            scan_i32(w.gcnt, G, w.tmp, s);
-            scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n_surv, w.rec_g, w.rec_c, w.rec_d,
-                                                                         w.gcnt, w.ent_c, w.ent_d, w.ent_i);
             const int nch = (int)(((int64_t)P.L * P.K + kEventCells - 1) / kEventCells);
             const dim3 egrid((unsigned)(P.L * nch), (unsigned)P.nb);
             group_events<false><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt,
@@ -1268,8 +1209,6 @@ struct Driver {
                                                                                               nbk + 1);
             group_events<true><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcur,
                                                           w.ev_cell, w.ev_val);
-        } else {
-            scan_i32(w.gcnt, G, w.tmp, s);  // all zeros: offsets stay zero
         }
     }
 

@@ -1,0 +1,503 @@
+// compose_orders.hip -- pipeline composition over every island subset and
+// order (Sec. 5.2 builds the pipeline from any islands, each used at most
+// once; Sec. 6.2 shows that the order in which islands are stacked changes
+// the plan), for K <= 16 islands.
+//
+// With U the set of islands from a stage to the pipeline end, the stage's
+// depth is |U|, so no island order is needed.  Per micro-batch size b:
+//   V_d(i, k, U)  least bottleneck covering [i, L) with the stages on the
+//                 islands of U (|U| = d), the first on k in U;
+//   W_d(j, k, U)  least bottleneck of a continuation on U \ {k} after a stage
+//                 on k ends at j: min over k' in U \ {k} of
+//                 max(X(j, k, k'), V_{d-1}(j, k', U \ {k}));
+//   F_d, G_d      the same for the fill, with every stage and link within the
+//                 least bottleneck P* (step (3)), ties to the least cut j and
+//                 the least next island k'.
+// The levels are the set sizes d = 1..min(K, L), one launch per level and
+// phase.  The states of level d are the pairs (k, U), k in U, |U| = d,
+// numbered r * d + t: r is the rank of U among the d-sets in ascending
+// numeric order (the combinatorial number system), t the position of k among
+// U's islands.  Block (state, b) first writes its continuation row W_d(., k,
+// U) to LDS, reading one coalesced row of V_{d-1} per island of U \ {k}; then
+// one thread per first layer i scans the cuts j.  As in the fixed-order
+// composition, T_d(i, j, k) never decreases with j, so a scan stops at the
+// first stage cost that cannot improve the running best.
+#include <algorithm>
+#include <vector>
+
+#include "compose_util.h"
+
+#pragma clang fp contract(off)
+
+namespace tg {
+
+constexpr int kMaxSetIslands = 16;
+constexpr int kMaxLayers = 512;
+constexpr int kOrderFinishThreads = 256;
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Level bookkeeping, passed by value.
+struct SetLevels {
+    int32_t D;                            // levels 1..D = min(K, L)
+    int32_t moff[kMaxSetIslands + 2];     // masks of popcount d start at moff[d]
+    int32_t n[kMaxSetIslands + 2];        // states of level d: C(K, d) * d
+    int64_t soff[kMaxSetIslands + 2];     // global number of level d's first state
+    int64_t total;                        // states of all levels
+    int32_t maxn;                         // largest level
+};
+
+static int64_t binom(int n, int k) {
+    if (k < 0 || k > n) return 0;
+    int64_t r = 1;
+    for (int q = 1; q <= k; ++q) r = r * (n - k + q) / q;
+    return r;
+}
+
+static SetLevels set_levels(const DevProblem &P) {
+    SetLevels v{};
+    v.D = std::min(P.K, P.L);
+    int32_t mo = 0;
+    int64_t so = 0;
+    for (int d = 0; d <= P.K + 1 && d <= kMaxSetIslands + 1; ++d) {
+        v.moff[d] = mo;
+        v.soff[d] = so;
+        const int64_t c = d <= P.K ? binom(P.K, d) : 0;
+        v.n[d] = (d >= 1 && d <= v.D) ? (int32_t)(c * d) : 0;
+        mo += (int32_t)c;
+        so += v.n[d];
+        v.maxn = std::max(v.maxn, v.n[d]);
+    }
+    v.total = v.soff[v.D + 1];
+    return v;
+}
+
+struct OrdersWs {
+    ComposeResult *res;
+    int32_t *pos;       // [K] identity: groups are numbered by island id
+    Groups g;
+    int32_t *masks;     // [2^K] the d-sets of each level, ascending
+    uint16_t *rank;     // [2^K] rank of a set among the sets of its size
+    double *T;          // [D][nb][K][NS] least cost of group (s, k, b) fitting at depth d
+    double *X;          // [nb][K][K][L+1] link time after layer j-1 from island k to k'
+    double *Vb[2];      // [nb][maxn][L+1] level values, double-buffered
+    double *root;       // [nb][total] value at i = 0 of every state
+    uint16_t *argF;     // [nb][total][L] least cut j of F
+    uint8_t *argG;      // [nb][total][L+1] least next island of G (255: none)
+    double *Pst;        // [nb]
+    double *rootF;      // [nb]
+    uint32_t *rootKey;  // [nb] (k << 24 | d << 16 | U) of the chosen root
+    size_t bytes;
+};
+
+static OrdersWs carve_orders(const DevProblem &P, int64_t n, void *base) {
+    OrdersWs w{};
+    char *p = (char *)base;
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> void * {
+        void *r = base ? (void *)(p + off) : nullptr;
+        off += align256(bytes > 0 ? bytes : 1);
+        return r;
+    };
+    const SetLevels lv = set_levels(P);
+    const int64_t G = (int64_t)P.nb * P.NS * P.K, nb = P.nb, L = P.L, K = P.K;
+    w.res = (ComposeResult *)take(sizeof(ComposeResult));
+    w.pos = (int32_t *)take(sizeof(int32_t) * K);
+    w.g.rec_g = (int32_t *)take(sizeof(int32_t) * n);
+    w.g.rec_c = (double *)take(sizeof(double) * n);
+    w.g.rec_d = (uint8_t *)take(n);
+    w.g.gcnt = (int32_t *)take(sizeof(int32_t) * G);
+    w.g.ent_c = (double *)take(sizeof(double) * n);
+    w.g.ent_d = (uint8_t *)take(n);
+    w.g.ent_i = (int64_t *)take(sizeof(int64_t) * n);
+    w.g.tmp = (int64_t *)take(sizeof(int64_t) * group_scan_tiles(G));
+    w.masks = (int32_t *)take(sizeof(int32_t) << K);
+    w.rank = (uint16_t *)take(sizeof(uint16_t) << K);
+    w.T = (double *)take(sizeof(double) * lv.D * nb * K * P.NS);
+    w.X = (double *)take(sizeof(double) * nb * K * K * (L + 1));
+    w.Vb[0] = (double *)take(sizeof(double) * nb * lv.maxn * (L + 1));
+    w.Vb[1] = (double *)take(sizeof(double) * nb * lv.maxn * (L + 1));
+    w.root = (double *)take(sizeof(double) * nb * lv.total);
+    w.argF = (uint16_t *)take(sizeof(uint16_t) * nb * lv.total * L);
+    w.argG = (uint8_t *)take(sizeof(uint8_t) * nb * lv.total * (L + 1));
+    w.Pst = (double *)take(sizeof(double) * nb);
+    w.rootF = (double *)take(sizeof(double) * nb);
+    w.rootKey = (uint32_t *)take(sizeof(uint32_t) * nb);
+    w.bytes = off;
+    return w;
+}
+
+size_t compose_orders_ws_bytes(const DevProblem &P, int64_t n_surv) { return carve_orders(P, n_surv, nullptr).bytes; }
+
+// ---------------------------------------------------------------------------
+// setup
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void orders_init(int K, int32_t *pos, ComposeResult *res) {
+    const int t = threadIdx.x;
+    if (t < K) pos[t] = t;
+    if (t == 0) {
+        res->err = 0;
+        res->status = TG_ENOPLAN;
+    }
+}
+
+// C(n, k) for the small arguments of the set numbering.
+__device__ inline int32_t dbinom(int n, int k) {
+    if (k < 0 || k > n) return 0;
+    int32_t r = 1;
+    for (int q = 1; q <= k; ++q) r = r * (n - k + q) / q;
+    return r;
+}
+
+// Every nonempty set U of islands: its rank among the sets of its size (sum
+// over its islands c_1 < c_2 < ... of C(c_t, t), ascending numeric order) and
+// its slot in the level's list.
+__global__ __launch_bounds__(256) void orders_masks(int K, SetLevels lv, int32_t *masks, uint16_t *rank) {
+    const uint32_t U = blockIdx.x * blockDim.x + threadIdx.x;
+    if (U == 0 || U >= (1u << K)) return;
+    int r = 0, t = 0;
+    for (uint32_t u = U; u; u &= u - 1) r += dbinom(__builtin_ctz(u), ++t);
+    masks[lv.moff[t] + r] = (int32_t)U;
+    rank[U] = (uint16_t)r;
+}
+
+// Stage tables: one thread per group (slice s, island k, b) writes the least
+// cost of its entries fitting at each depth d.
+__global__ __launch_bounds__(256) void orders_stage_table(DevProblem P, int D, const int32_t *__restrict__ gcnt,
+                                                          const double *__restrict__ ent_c,
+                                                          const uint8_t *__restrict__ ent_d, double *T) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t per_b = (int64_t)P.K * P.NS;
+    if (e >= (int64_t)P.nb * per_b) return;
+    const int64_t bb = e / per_b, r = e - bb * per_b;
+    const int64_t k = r / P.NS, s = r - k * P.NS;
+    const int64_t G = group_id(P, k, bb, s);
+    const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+    for (int d = 1; d <= D; ++d) {
+        double v = kInf;
+        for (int32_t a = st; a < en; ++a)
+            if (ent_d[a] >= d && ent_c[a] < v) v = ent_c[a];
+        T[(int64_t)(d - 1) * P.nb * per_b + e] = v;
+    }
+}
+
+// Link times X[b][k][k'][j]: activations forward and gradients backward of one
+// micro-batch across the boundary after layer j-1; no link (E = 0) is +inf.
+__global__ __launch_bounds__(256) void orders_links(DevProblem P, double *X) {
+    const int L = P.L, K = P.K;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t n = (int64_t)P.nb * K * K * (L + 1);
+    if (e >= n) return;
+    const int64_t j = e % (L + 1), q = e / (L + 1);
+    const int64_t k2 = q % K, k = (q / K) % K, bb = q / ((int64_t)K * K);
+    double x = kInf;
+    if (j >= 1 && j < L) {
+        const double E = P.E[k * K + k2];
+        x = E == 0.0 ? kInf : ((2.0 * (double)P.bvals[bb]) * (double)P.outact[j - 1]) / E;
+    }
+    X[e] = x;
+}
+
+// ---------------------------------------------------------------------------
+// levels
+// ---------------------------------------------------------------------------
+// Level 1: one stage on island k covering [i, L).
+template <bool kFill>
+__global__ __launch_bounds__(256) void orders_level1(DevProblem P, SetLevels lv, const double *__restrict__ T,
+                                                     const double *__restrict__ Pst, double *cur, double *root) {
+    const int L = P.L, K = P.K, bb = blockIdx.y;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= (int64_t)K * (L + 1)) return;
+    const int k = (int)(e / (L + 1)), i = (int)(e - (int64_t)k * (L + 1));
+    double v = kInf;
+    if (i < L) {
+        v = T[((int64_t)bb * K + k) * P.NS + slice_of(L, i, L)];
+        if (kFill && !(v <= Pst[bb])) v = kInf;
+    }
+    cur[((int64_t)bb * lv.n[1] + k) * (L + 1) + i] = v;
+    if (i == 0) root[(int64_t)bb * lv.total + lv.soff[1] + k] = v;
+}
+
+// Level d >= 2, block (state, b).  kFill: the fill phase at bound P*, with
+// argmins; otherwise the bottleneck phase.
+template <int NT, bool kFill>
+__global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, const int32_t *__restrict__ masks,
+                                                   const uint16_t *__restrict__ rank, const double *__restrict__ T,
+                                                   const double *__restrict__ X, const double *__restrict__ prev,
+                                                   double *cur, double *root, const double *__restrict__ Pst,
+                                                   uint16_t *argF, uint8_t *argG) {
+    __shared__ double Wl[kMaxLayers + 1];
+    const int L = P.L, K = P.K;
+    const int st = blockIdx.x, bb = blockIdx.y;
+    const int r = st / d, t = st - r * d;
+    const uint32_t U = (uint32_t)masks[lv.moff[d] + r];
+    uint32_t u = U;
+    for (int q = 0; q < t; ++q) u &= u - 1;
+    const int k = __builtin_ctz(u);
+    const uint32_t Up = U & ~(1u << k);
+    const int rp = rank[Up];
+    const int jmax = L - d + 1;
+    const double bound = kFill ? Pst[bb] : 0.0;
+    const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
+    // continuation row: X[b][k][k'][.] and V_{d-1}(., k', Up) for k' in Up
+    const double *Xr = X + ((int64_t)bb * K + k) * K * (L + 1);
+    const double *Vp = prev + ((int64_t)bb * lv.n[d - 1] + (int64_t)rp * (d - 1)) * (L + 1);
+    for (int j = threadIdx.x + 1; j <= jmax; j += NT) {
+        double w = kInf;
+        int arg = 255;
+        int tp = 0;
+        for (uint32_t rest = Up; rest; rest &= rest - 1, ++tp) {
+            const int k2 = __builtin_ctz(rest);
+            const double x = Xr[(int64_t)k2 * (L + 1) + j];
+            const double v = Vp[(int64_t)tp * (L + 1) + j];
+            if (kFill) {
+                if (x <= bound) {
+                    const double y = x + v;
+                    if (y < w) {
+                        w = y;
+                        arg = k2;
+                    }
+                }
+            } else {
+                const double y = x > v ? x : v;
+                if (y < w) w = y;
+            }
+        }
+        Wl[j] = w;
+        if (kFill) argG[gst * (L + 1) + j] = (uint8_t)arg;
+    }
+    __syncthreads();
+    const double *Tr = T + (((int64_t)(d - 1) * P.nb + bb) * K + k) * P.NS;
+    double *out = cur + ((int64_t)bb * lv.n[d] + st) * (L + 1);
+    for (int i = threadIdx.x; i <= L; i += NT) {
+        double best = kInf;
+        int bj = 0;
+        if (i <= L - d) {
+            const int64_t base = slice_of(L, i, i + 1) - (i + 1);  // T_d(i, j, k) = Tr[base + j]
+            for (int j = i + 1; j <= jmax; ++j) {
+                const double tv = Tr[base + j];
+                if (kFill) {
+                    if (tv > bound || tv >= best) break;
+                    const double y = tv + Wl[j];
+                    if (y < best) {
+                        best = y;
+                        bj = j;
+                    }
+                } else {
+                    if (tv >= best) break;
+                    const double y = tv > Wl[j] ? tv : Wl[j];
+                    if (y < best) best = y;
+                }
+            }
+        }
+        out[i] = best;
+        if (kFill && i < L) argF[gst * L + i] = (uint16_t)bj;
+        if (i == 0) root[gst] = best;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// roots and the plan
+// ---------------------------------------------------------------------------
+// Decodes global state number q of b's states into (k, d, U).
+__device__ inline void state_of(const SetLevels &lv, const int32_t *masks, int64_t q, int *k, int *d, uint32_t *U) {
+    int dd = 1;
+    while (dd < lv.D && q >= lv.soff[dd + 1]) ++dd;
+    const int64_t st = q - lv.soff[dd];
+    const int r = (int)(st / dd), t = (int)(st - (int64_t)r * dd);
+    uint32_t u = (uint32_t)masks[lv.moff[dd] + r];
+    *U = u;
+    for (int a = 0; a < t; ++a) u &= u - 1;
+    *k = __builtin_ctz(u);
+    *d = dd;
+}
+
+// Per b: P* = least root bottleneck (kRoot = false), or the root of the fill:
+// least F, ties to the least first island k, then fewer stages d, then the
+// least set U (kRoot = true).  Block b, 256 threads.
+template <bool kRoot>
+__global__ __launch_bounds__(256) void orders_reduce(SetLevels lv, const int32_t *__restrict__ masks,
+                                                     const double *__restrict__ root, double *out_v,
+                                                     uint32_t *out_key) {
+    __shared__ double sv[256];
+    __shared__ uint32_t sk[256];
+    const int bb = blockIdx.x;
+    const double *rv = root + (int64_t)bb * lv.total;
+    double bv = kInf;
+    uint32_t bk = kNoKey;
+    for (int64_t q = threadIdx.x; q < lv.total; q += blockDim.x) {
+        const double v = rv[q];
+        if (!kRoot) {
+            if (v < bv) bv = v;
+            continue;
+        }
+        if (!(v < kInf) || v > bv) continue;
+        int k, d;
+        uint32_t U;
+        state_of(lv, masks, q, &k, &d, &U);
+        const uint32_t key = ((uint32_t)k << 24) | ((uint32_t)d << 16) | U;
+        if (v < bv || key < bk) {
+            bv = v;
+            bk = key;
+        }
+    }
+    sv[threadIdx.x] = bv;
+    sk[threadIdx.x] = bk;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) {
+            const double v2 = sv[threadIdx.x + h];
+            const uint32_t k2 = sk[threadIdx.x + h];
+            if (v2 < sv[threadIdx.x] || (v2 == sv[threadIdx.x] && k2 < sk[threadIdx.x])) {
+                sv[threadIdx.x] = v2;
+                sk[threadIdx.x] = k2;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        out_v[bb] = sv[0];
+        if (kRoot) out_key[bb] = sk[0];
+    }
+}
+
+// Choose b, walk the argmins from the root (one thread), then one wave per
+// stage resolves its candidate.
+__global__ __launch_bounds__(kOrderFinishThreads) void orders_finish(
+    DevProblem P, SetLevels lv, const int32_t *__restrict__ masks, const uint16_t *__restrict__ rank,
+    const int32_t *gcnt, const double *ent_c, const uint8_t *ent_d, const int64_t *ent_i, const double *X,
+    const double *Pst, const double *rootF, const uint32_t *rootKey, const uint16_t *argF, const uint8_t *argG,
+    ComposeResult *res) {
+    __shared__ int32_t st_i[kMaxSetIslands], st_j[kMaxSetIslands], st_k[kMaxSetIslands], st_kn[kMaxSetIslands];
+    __shared__ int32_t sh_S, sh_bb;
+    const int L = P.L, K = P.K;
+    tg_plan &plan = res->plan;
+    if (threadIdx.x == 0) {
+        sh_S = 0;
+        plan.b = 0;
+        plan.m = 0;
+        plan.S = 0;
+        plan.reserved = 0;
+        plan.P = kInf;
+        plan.F = kInf;
+        plan.T = kInf;
+        double bestT = kInf;
+        int bb = -1;
+        if (!res->err)
+            for (int bi = 0; bi < P.nb; ++bi) {
+                if (!(Pst[bi] < kInf) || rootKey[bi] == kNoKey) continue;
+                const int64_t m = P.B / P.bvals[bi];
+                const double T = ((double)(m - 1) * Pst[bi]) + rootF[bi];
+                if (T < bestT) {
+                    bestT = T;
+                    bb = bi;
+                }
+            }
+        if (bb >= 0) {
+            const int64_t b = P.bvals[bb];
+            const uint32_t key = rootKey[bb];
+            int k = (int)(key >> 24);
+            const int S = (int)((key >> 16) & 0xFF);
+            uint32_t U = key & 0xFFFFu;
+            plan.b = (int32_t)b;
+            plan.m = (int32_t)(P.B / b);
+            plan.S = S;
+            plan.P = Pst[bb];
+            plan.F = rootF[bb];
+            plan.T = bestT;
+            res->status = TG_OK;
+            int i = 0;
+            bool ok = S >= 1 && S <= lv.D && (U >> k & 1u);
+            for (int t = 0; ok && t < S; ++t) {
+                const int d = S - t;
+                int j = L, kn = -1;
+                if (d > 1) {
+                    const int tk = __builtin_popcount(U & ((1u << k) - 1u));
+                    const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + (int64_t)rank[U] * d + tk;
+                    j = argF[gst * L + i];
+                    // an argmin on the optimal path is always set
+                    ok = j > i && j <= L - d + 1;
+                    if (ok) {
+                        kn = argG[gst * (L + 1) + j];
+                        ok = kn < K && kn != k && (U >> kn & 1u);
+                    }
+                }
+                st_i[t] = i;
+                st_j[t] = j;
+                st_k[t] = k;
+                st_kn[t] = kn;
+                U &= ~(1u << k);
+                i = j;
+                k = kn;
+            }
+            if (ok) {
+                sh_S = S;
+                sh_bb = bb;
+            } else {
+                res->err = 4;
+                res->status = TG_ENOPLAN;
+            }
+        }
+    }
+    __syncthreads();
+    const int S = sh_S;
+    if (S == 0) return;
+    const int bb = sh_bb;
+    const int wv = threadIdx.x / kWave;
+    for (int t = wv; t < S; t += kOrderFinishThreads / kWave) {
+        const int d = S - t, i = st_i[t], j = st_j[t], k = st_k[t], kn = st_kn[t];
+        const double link = d > 1 ? X[(((int64_t)bb * K + k) * K + kn) * (L + 1) + j] : 0.0;
+        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, i, j, k, k, d, bb, link, plan.stage[t], res);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host-side sequencing
+// ---------------------------------------------------------------------------
+template <bool kFill>
+static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs &w, hipStream_t s) {
+    const int L = P.L;
+    const dim3 g1((unsigned)(((int64_t)P.K * (L + 1) + 255) / 256), (unsigned)P.nb);
+    orders_level1<kFill><<<g1, dim3(256), 0, s>>>(P, lv, w.T, w.Pst, w.Vb[1], w.root);
+    for (int d = 2; d <= lv.D; ++d) {
+        const dim3 grid((unsigned)lv.n[d], (unsigned)P.nb);
+        const double *prev = w.Vb[(d - 1) & 1];
+        double *cur = w.Vb[d & 1];
+        if (L < 64)
+            orders_level<64, kFill><<<grid, dim3(64), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur, w.root,
+                                                             w.Pst, w.argF, w.argG);
+        else if (L < 128)
+            orders_level<128, kFill><<<grid, dim3(128), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur,
+                                                               w.root, w.Pst, w.argF, w.argG);
+        else
+            orders_level<256, kFill><<<grid, dim3(256), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur,
+                                                               w.root, w.Pst, w.argF, w.argG);
+    }
+}
+
+hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
+                                 const uint8_t *dmax, void *ws, hipStream_t s, ComposeResult **result_dev) {
+    if (P.K > kMaxSetIslands || P.L > kMaxLayers || P.nb > 65535) return hipErrorInvalidValue;
+    const SetLevels lv = set_levels(P);
+    const OrdersWs w = carve_orders(P, n_surv, ws);
+    *result_dev = w.res;
+    orders_init<<<dim3(1), dim3(64), 0, s>>>(P.K, w.pos, w.res);
+    orders_masks<<<dim3((unsigned)(((1u << P.K) + 255) / 256)), dim3(256), 0, s>>>(P.K, lv, w.masks, w.rank);
+    launch_grouping(P, surv, n_surv, cost, dmax, w.pos, w.g, w.res, s);
+    const int64_t ngroups = (int64_t)P.nb * P.K * P.NS;
+    orders_stage_table<<<dim3((unsigned)((ngroups + 255) / 256)), dim3(256), 0, s>>>(P, lv.D, w.g.gcnt, w.g.ent_c,
+                                                                                    w.g.ent_d, w.T);
+    const int64_t nx = (int64_t)P.nb * P.K * P.K * (P.L + 1);
+    orders_links<<<dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s>>>(P, w.X);
+    run_levels<false>(P, lv, w, s);
+    orders_reduce<false><<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(lv, w.masks, w.root, w.Pst, nullptr);
+    run_levels<true>(P, lv, w, s);
+    orders_reduce<true><<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(lv, w.masks, w.root, w.rootF, w.rootKey);
+    orders_finish<<<dim3(1), dim3(kOrderFinishThreads), 0, s>>>(P, lv, w.masks, w.rank, w.g.gcnt, w.g.ent_c,
+                                                                w.g.ent_d, w.g.ent_i, w.X, w.Pst, w.rootF,
+                                                                w.rootKey, w.argF, w.argG, w.res);
+    return hipGetLastError();
+}
+
+}  // namespace tg

@@ -141,6 +141,10 @@ struct RelaxHost {
     int64_t B;              // global batch
 };
 size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv);
+// Composition over every island subset and order (K <= 16).
+size_t compose_orders_ws_bytes(const DevProblem &P, int64_t n_surv);
+hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
+                                 const uint8_t *dmax, void *ws, hipStream_t s, ComposeResult **result_dev);
 // Synchronises the stream several times (once per search round).
 hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
                                   const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,

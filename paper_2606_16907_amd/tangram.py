@@ -80,7 +80,8 @@ class TangramError(RuntimeError):
 EXPORTS = ("tg_problem_create", "tg_problem_destroy", "tg_problem_info", "tg_problem_bvalues",
            "tg_enumerate_pairs", "tg_score_pairs", "tg_prune_workspace_bytes", "tg_prune",
            "tg_compose_workspace_bytes", "tg_compose_pipeline", "tg_compose_relaxed_workspace_bytes",
-           "tg_compose_pipeline_relaxed", "tg_last_error")
+           "tg_compose_pipeline_relaxed", "tg_compose_all_orders_workspace_bytes",
+           "tg_compose_pipeline_all_orders", "tg_last_error")
 
 _lib = None
 
@@ -113,6 +114,9 @@ def load_library(path=LIB_PATH):
     L.tg_compose_relaxed_workspace_bytes.argtypes = [vp, i64]
     L.tg_compose_relaxed_workspace_bytes.restype = sz
     L.tg_compose_pipeline_relaxed.argtypes = [vp, vp, i64, vp, vp, P(i32), P(TgPlan), vp, sz, vp]
+    L.tg_compose_all_orders_workspace_bytes.argtypes = [vp, i64]
+    L.tg_compose_all_orders_workspace_bytes.restype = sz
+    L.tg_compose_pipeline_all_orders.argtypes = [vp, vp, i64, vp, vp, P(TgPlan), vp, sz, vp]
     L.tg_last_error.argtypes = []
     L.tg_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -295,6 +299,24 @@ class Problem:
                                              ws.numel(), _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline_relaxed")
+        return st, plan_to_dict(plan)
+
+    def compose_all_orders_workspace(self, n_survivors):
+        n = load_library().tg_compose_all_orders_workspace_bytes(self.h, int(n_survivors))
+        return torch.empty(max(int(n), 1), dtype=torch.uint8, device="cuda")
+
+    def tg_compose_pipeline_all_orders(self, survivors, cost, dmax, workspace=None):
+        """Composition over every island subset and order (K <= 16).  Returns
+        (status, plan dict)."""
+        lib = load_library()
+        n = int(survivors.numel())
+        ws = workspace if workspace is not None else self.compose_all_orders_workspace(n)
+        plan = TgPlan()
+        st = lib.tg_compose_pipeline_all_orders(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
+                                                _dptr(dmax), ctypes.byref(plan), _dptr(ws), ws.numel(),
+                                                _stream())
+        if st not in (TG_OK, TG_ENOPLAN):
+            _check(st, "tg_compose_pipeline_all_orders")
         return st, plan_to_dict(plan)
 
     def plan_search(self, island_order=None):

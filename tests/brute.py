@@ -279,7 +279,7 @@ def enumerate_plans_all_orders(orc, rows, allowed=None):
     return out
 
 
-def brute_force_compose_sets(orc, rows, allowed=None):
+def brute_force_all_orders(orc, rows, allowed=None):
     """Exhaustive steps (1)-(3) over every island subset and order: per b the
     least bottleneck, then the least fill at it.  Returns per-b (P*, F*, T)
     and the optimum with its optimal plans and the least-key one."""
@@ -302,7 +302,7 @@ def brute_force_compose_sets(orc, rows, allowed=None):
     return per_b, best
 
 
-def sets_signature(p):
+def all_orders_signature(p):
     S = len(p["islands"])
     bounds = (0,) + p["cuts"] + (p["L"],)
     return tuple((p["islands"][t], bounds[t], bounds[t + 1], S - t, p["picks"][t]["idx"]) for t in range(S))

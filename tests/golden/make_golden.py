@@ -4,8 +4,9 @@ Every stored value comes from the CPU oracle (oracle/tangram_oracle.c) and
 nothing else: counts, the surviving set (count, SHA-256 of the ascending int64
 little-endian index list, and its first/last entries), the per-b (P*, F*, T)
 table, the chosen plan, the plan and per-b (P*, bound, F, T) table of the
-composition with the step-(4) relaxation, and a seeded sample of
-per-candidate scores.
+composition with the step-(4) relaxation, for instances of at most 16 islands
+the plan and per-b (P*, F*, T) table of the composition over every island
+order, and a seeded sample of per-candidate scores.
 
 Run from the repository root:  python -m tests.golden.make_golden [names...]
 """
@@ -55,6 +56,11 @@ def golden(name):
     t2 = time.time()
     rst, rplan, rper_b = o.compose_relaxed(surv)
     t3 = time.time()
+    all_orders = None
+    if o.K <= 16:
+        ast, aplan, aper_b = o.compose_all_orders(surv)
+        all_orders = {"status": ast, "plan": aplan, "per_b": [[float(v) for v in row] for row in aper_b]}
+    t4 = time.time()
     idx = sample_indices(o.N, o.NS)
     cost, dmax = o.score_list(idx)
     return {
@@ -68,10 +74,11 @@ def golden(name):
         "per_b": [[float(v) for v in row] for row in per_b],
         "relaxed": {"status": rst, "plan": rplan,
                     "per_b": [[float(v) for v in row] for row in rper_b]},
+        "all_orders": all_orders,
         "sample": {"idx": [int(x) for x in idx], "cost": [float(x) for x in cost],
                    "dmax": [int(x) for x in dmax]},
         "oracle_seconds": {"prune": round(t1 - t0, 3), "compose": round(t2 - t1, 3),
-                           "compose_relaxed": round(t3 - t2, 3)},
+                           "compose_relaxed": round(t3 - t2, 3), "compose_all_orders": round(t4 - t3, 3)},
     }
 
 

@@ -28,8 +28,8 @@ def _random(seed):
 
 def _check_against_brute(o, rows):
     surv = o.prune()
-    st, plan, per_b = o.compose_sets(surv)
-    bf_per_b, best = brute.brute_force_compose_sets(o, rows)
+    st, plan, per_b = o.compose_all_orders(surv)
+    bf_per_b, best = brute.brute_force_all_orders(o, rows)
     for bi, b in enumerate(o.bvalues):
         P, F, T = bf_per_b[b]
         if math.isinf(P):
@@ -42,9 +42,9 @@ def _check_against_brute(o, rows):
     assert st == 0
     assert (plan["b"], plan["P"], plan["F"], plan["T"]) == (best["b"], best["P"], best["F"], best["T"])
     sig = brute.plan_signature(plan)
-    optimal = {brute.sets_signature(p): p for p in best["optimal"]}
+    optimal = {brute.all_orders_signature(p): p for p in best["optimal"]}
     assert sig in optimal, "oracle plan is not among the optimal plans"
-    lex = brute.sets_signature(best["lexmin"])
+    lex = brute.all_orders_signature(best["lexmin"])
     if sig == lex:
         return "lexmin"
     # differs only through floating-point absorption: where the two plans
@@ -77,7 +77,7 @@ def test_sets_are_the_best_over_every_order(seed):
     # fixed-order composition reaches over all K! island orders
     o = Oracle(_random(seed))
     s = o.prune()
-    st, plan, per_b = o.compose_sets(s)
+    st, plan, per_b = o.compose_all_orders(s)
     best = None
     for order in itertools.permutations(range(o.K)):
         _, _, pb = o.compose(s, list(order))
@@ -92,7 +92,7 @@ def test_one_island_equals_the_fixed_order():
         o = Oracle(random_tiny(seed, K_range=(1, 1), tight=(seed % 2 == 1)))
         s = o.prune()
         a = o.compose(s)
-        b = o.compose_sets(s)
+        b = o.compose_all_orders(s)
         assert a[0] == b[0]
         assert np.array_equal(a[2], b[2])
         assert brute.plan_signature(a[1]) == brute.plan_signature(b[1])
@@ -102,7 +102,7 @@ def test_one_island_equals_the_fixed_order():
 def test_island_relabelling_leaves_the_values(seed):
     inst = random_tiny(seed, L_range=(4, 6), K_range=(3, 3))
     o = Oracle(inst)
-    _, plan, per_b = o.compose_sets(o.prune())
+    _, plan, per_b = o.compose_all_orders(o.prune())
     perm = [2, 0, 1]  # new island t is old island perm[t]
     inst2 = dict(inst)
     inst2["islands"] = {f: [v[perm[t]] for t in range(3)] for f, v in inst["islands"].items()}
@@ -110,7 +110,7 @@ def test_island_relabelling_leaves_the_values(seed):
     inv = {perm[t]: t for t in range(3)}
     inst2["island_order"] = [inv[k] for k in inst["island_order"]]
     o2 = Oracle(inst2)
-    _, plan2, per_b2 = o2.compose_sets(o2.prune())
+    _, plan2, per_b2 = o2.compose_all_orders(o2.prune())
     assert np.array_equal(per_b, per_b2)
     assert (plan["b"], plan["P"], plan["F"], plan["T"]) == (plan2["b"], plan2["P"], plan2["F"], plan2["T"])
 
@@ -122,8 +122,8 @@ def test_sets_prune_safety(seed):
     B = o.inst["space"]["global_batch"]
     compatible = [idx for idx in range(o.N)
                   if B % (o.decode(idx)["dp"] * o.decode(idx)["mb"]) == 0]
-    a = o.compose_sets(o.prune())
-    b = o.compose_sets(compatible)
+    a = o.compose_all_orders(o.prune())
+    b = o.compose_all_orders(compatible)
     assert a[0] == b[0] and np.array_equal(a[2], b[2])
     assert brute.plan_signature(a[1]) == brute.plan_signature(b[1])
 
@@ -144,7 +144,7 @@ def test_bad_input_order_is_repaired():
     assert [x["island"] for x in fixed[(0, 1)]["stages"]] == [0, 1]
     assert [x["island"] for x in fixed[(1, 0)]["stages"]] == [0]  # island 1 unusable first
     assert fixed[(0, 1)]["T"] < fixed[(1, 0)]["T"]
-    st, plan, _ = o.compose_sets(s)
+    st, plan, _ = o.compose_all_orders(s)
     assert st == 0 and plan["T"] == fixed[(0, 1)]["T"]
     assert brute.plan_signature(plan) == brute.plan_signature(fixed[(0, 1)])
 
@@ -157,7 +157,7 @@ def test_uniform_layers_any_order_closed_form():
         inst = instance(K=K, L=L, layer=lay, n_gpus=1, B=1, tp=(1,), mb=(1,), zero=(0,),
                         inter=math.inf)
         o = Oracle(inst)
-        st, plan, _ = o.compose_sets(o.prune())
+        st, plan, _ = o.compose_all_orders(o.prune())
         per_layer = o.score_list([0])[0][0]  # slice [0, 1) on island 0
         assert plan["P"] == per_layer * math.ceil(L / min(K, L))
 
@@ -194,19 +194,22 @@ def check_set_plan_invariants(o, plan, survivors):
 def test_named_instance_set_plans(name):
     o = Oracle(make_instance(name))
     s = o.prune()
-    st, plan, per_b = o.compose_sets(s)
+    st, plan, per_b = o.compose_all_orders(s)
     assert st == 0
     check_set_plan_invariants(o, plan, s)
     assert plan["T"] == min(per_b[:, 2])
-    # never worse than any fixed order's plan
+    # per b, (P*, F*) is never worse than any fixed order's (T itself can be:
+    # the objective of steps (1)-(3) puts the bottleneck first)
     for order in itertools.permutations(range(o.K)):
-        assert plan["T"] <= o.compose(s, list(order))[1]["T"]
+        fixed = o.compose(s, list(order))[2]
+        for bi in range(o.n_b):
+            assert tuple(per_b[bi][:2]) <= tuple(fixed[bi][:2])
 
 
 def test_more_than_16_islands_rejected():
     inst = make_instance("moe")  # 32 islands
     o = Oracle(inst)
-    st, plan, _ = o.compose_sets([])
+    st, plan, _ = o.compose_all_orders([])
     assert st == EINVAL
 
 
@@ -241,8 +244,8 @@ def test_root_tie_prefers_the_least_first_island_over_fewer_stages():
     inst = instance(K=2, layers=layers, n_gpus=1, hbm=[2.0 ** 30, 2.0 ** 40], B=4, inter=2.0 ** 34)
     o = Oracle(inst)
     rows = brute.candidate_table(o)
-    _, best = brute.brute_force_compose_sets(o, rows)
+    _, best = brute.brute_force_all_orders(o, rows)
     assert sorted(p["key"][:2] for p in best["optimal"]) == [(0, 2), (1, 1)]
-    st, plan, _ = o.compose_sets(o.prune())
+    st, plan, _ = o.compose_all_orders(o.prune())
     assert [s["island"] for s in plan["stages"]] == [0, 1]
     assert _check_against_brute(o, rows) == "lexmin"
