@@ -17,11 +17,15 @@
 // phase.  The states of level d are the pairs (k, U), k in U, |U| = d,
 // numbered r * d + t: r is the rank of U among the d-sets in ascending
 // numeric order (the combinatorial number system), t the position of k among
-// U's islands.  Block (state, b) first writes its continuation row W_d(., k,
-// U) to LDS, reading one coalesced row of V_{d-1} per island of U \ {k}; then
-// one thread per first layer i scans the cuts j.  As in the fixed-order
-// composition, T_d(i, j, k) never decreases with j, so a scan stops at the
-// first stage cost that cannot improve the running best.
+// U's islands.  Every state (k, U) reads the rows V_{d-1}(., k', U \ {k}) of
+// the same smaller set for each k' in it, so a block owns one (d-1)-set U'
+// (and b) and runs the states (k, U' + {k}) for the islands k outside U' one
+// after the other: the rows come from HBM once and from the cache after that.
+// Where a level has few sets, the islands outside U' are split over several
+// blocks.  Per state the block writes its continuation row W_d(., k, U) to
+// LDS, then one thread per first layer i scans the cuts j.  As in the
+// fixed-order composition, T_d(i, j, k) never decreases with j, so a scan
+// stops at the first stage cost that cannot improve the running best.
 #include <algorithm>
 #include <vector>
 
@@ -35,6 +39,8 @@ constexpr int kMaxSetIslands = 16;
 constexpr int kMaxLayers = 512;
 constexpr int kOrderFinishThreads = 256;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+constexpr int64_t kTargetBlocks = 8192;  // blocks per level launch worth splitting for
+constexpr int kReduceChunks = 64;        // partials per b in the root reductions
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -79,7 +85,8 @@ struct OrdersWs {
     Groups g;
     int32_t *masks;     // [2^K] the d-sets of each level, ascending
     uint16_t *rank;     // [2^K] rank of a set among the sets of its size
-    double *T;          // [D][nb][K][NS] least cost of group (s, k, b) fitting at depth d
+    double *T;          // [D][nb][K][L][L] least cost of group ((i, j), k, b) fitting at depth d,
+                        // by diagonal: [j - i - 1][i], so threads i read along a row
     double *X;          // [nb][K][K][L+1] link time after layer j-1 from island k to k'
     double *Vb[2];      // [nb][maxn][L+1] level values, double-buffered
     double *root;       // [nb][total] value at i = 0 of every state
@@ -88,6 +95,8 @@ struct OrdersWs {
     double *Pst;        // [nb]
     double *rootF;      // [nb]
     uint32_t *rootKey;  // [nb] (k << 24 | d << 16 | U) of the chosen root
+    double *part_v;     // [nb][kReduceChunks] partial reductions
+    uint32_t *part_k;   // [nb][kReduceChunks]
     size_t bytes;
 };
 
@@ -114,7 +123,7 @@ static OrdersWs carve_orders(const DevProblem &P, int64_t n, void *base) {
     w.g.tmp = (int64_t *)take(sizeof(int64_t) * group_scan_tiles(G));
     w.masks = (int32_t *)take(sizeof(int32_t) << K);
     w.rank = (uint16_t *)take(sizeof(uint16_t) << K);
-    w.T = (double *)take(sizeof(double) * lv.D * nb * K * P.NS);
+    w.T = (double *)take(sizeof(double) * lv.D * nb * K * L * L);
     w.X = (double *)take(sizeof(double) * nb * K * K * (L + 1));
     w.Vb[0] = (double *)take(sizeof(double) * nb * lv.maxn * (L + 1));
     w.Vb[1] = (double *)take(sizeof(double) * nb * lv.maxn * (L + 1));
@@ -124,6 +133,8 @@ static OrdersWs carve_orders(const DevProblem &P, int64_t n, void *base) {
     w.Pst = (double *)take(sizeof(double) * nb);
     w.rootF = (double *)take(sizeof(double) * nb);
     w.rootKey = (uint32_t *)take(sizeof(uint32_t) * nb);
+    w.part_v = (double *)take(sizeof(double) * nb * kReduceChunks);
+    w.part_k = (uint32_t *)take(sizeof(uint32_t) * nb * kReduceChunks);
     w.bytes = off;
     return w;
 }
@@ -162,18 +173,25 @@ __global__ __launch_bounds__(256) void orders_masks(int K, SetLevels lv, int32_t
     rank[U] = (uint16_t)r;
 }
 
-// Stage tables: one thread per group (slice s, island k, b) writes the least
-// cost of its entries fitting at each depth d.
+// Stage tables: one thread per cell (diagonal j - i - 1, first layer i) of
+// (island k, b) writes the least cost of group ((i, j), k, b)'s entries
+// fitting at each depth d (+inf off the triangle).
 __global__ __launch_bounds__(256) void orders_stage_table(DevProblem P, int D, const int32_t *__restrict__ gcnt,
                                                           const double *__restrict__ ent_c,
                                                           const uint8_t *__restrict__ ent_d, double *T) {
+    const int64_t L = P.L;
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t per_b = (int64_t)P.K * P.NS;
+    const int64_t per_b = (int64_t)P.K * L * L;
     if (e >= (int64_t)P.nb * per_b) return;
     const int64_t bb = e / per_b, r = e - bb * per_b;
-    const int64_t k = r / P.NS, s = r - k * P.NS;
-    const int64_t G = group_id(P, k, bb, s);
-    const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+    const int64_t k = r / (L * L), c = r - k * L * L;
+    const int64_t len = c / L + 1, i = c - (len - 1) * L;
+    int32_t st = 0, en = 0;
+    if (i + len <= L) {
+        const int64_t G = group_id(P, k, bb, slice_of(L, i, i + len));
+        st = G ? gcnt[G - 1] : 0;
+        en = gcnt[G];
+    }
     for (int d = 1; d <= D; ++d) {
         double v = kInf;
         for (int32_t a = st; a < en; ++a)
@@ -212,88 +230,138 @@ __global__ __launch_bounds__(256) void orders_level1(DevProblem P, SetLevels lv,
     const int k = (int)(e / (L + 1)), i = (int)(e - (int64_t)k * (L + 1));
     double v = kInf;
     if (i < L) {
-        v = T[((int64_t)bb * K + k) * P.NS + slice_of(L, i, L)];
+        v = T[((int64_t)bb * K + k) * L * L + (int64_t)(L - i - 1) * L + i];
         if (kFill && !(v <= Pst[bb])) v = kInf;
     }
     cur[((int64_t)bb * lv.n[1] + k) * (L + 1) + i] = v;
     if (i == 0) root[(int64_t)bb * lv.total + lv.soff[1] + k] = v;
 }
 
-// Level d >= 2, block (state, b).  kFill: the fill phase at bound P*, with
-// argmins; otherwise the bottleneck phase.
+// Level d >= 2, block (part of the islands outside a (d-1)-set U', b).  kFill:
+// the fill phase at bound P*, with argmins; otherwise the bottleneck phase.
 template <int NT, bool kFill>
-__global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, const int32_t *__restrict__ masks,
+__global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, int nsplit,
+                                                   const int32_t *__restrict__ masks,
                                                    const uint16_t *__restrict__ rank, const double *__restrict__ T,
                                                    const double *__restrict__ X, const double *__restrict__ prev,
                                                    double *cur, double *root, const double *__restrict__ Pst,
                                                    uint16_t *argF, uint8_t *argG) {
-    __shared__ double Wl[kMaxLayers + 1];
+    __shared__ double Wl[2][kMaxLayers + 1];
     const int L = P.L, K = P.K;
-    const int st = blockIdx.x, bb = blockIdx.y;
-    const int r = st / d, t = st - r * d;
-    const uint32_t U = (uint32_t)masks[lv.moff[d] + r];
-    uint32_t u = U;
-    for (int q = 0; q < t; ++q) u &= u - 1;
-    const int k = __builtin_ctz(u);
-    const uint32_t Up = U & ~(1u << k);
-    const int rp = rank[Up];
+    const int rp = blockIdx.x / nsplit, part = blockIdx.x - rp * nsplit;
+    const int bb = blockIdx.y;
+    const uint32_t Up = (uint32_t)masks[lv.moff[d - 1] + rp];
+    const int nk = K - (d - 1);
+    const int per = (nk + nsplit - 1) / nsplit;
+    const int q0 = part * per, q1 = min(nk, q0 + per);
+    uint32_t rest = ((1u << K) - 1u) & ~Up;  // islands outside U', ascending
+    for (int q = 0; q < q0; ++q) rest &= rest - 1;
     const int jmax = L - d + 1;
     const double bound = kFill ? Pst[bb] : 0.0;
-    const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
-    // continuation row: X[b][k][k'][.] and V_{d-1}(., k', Up) for k' in Up
-    const double *Xr = X + ((int64_t)bb * K + k) * K * (L + 1);
     const double *Vp = prev + ((int64_t)bb * lv.n[d - 1] + (int64_t)rp * (d - 1)) * (L + 1);
-    for (int j = threadIdx.x + 1; j <= jmax; j += NT) {
-        double w = kInf;
-        int arg = 255;
-        int tp = 0;
-        for (uint32_t rest = Up; rest; rest &= rest - 1, ++tp) {
-            const int k2 = __builtin_ctz(rest);
-            const double x = Xr[(int64_t)k2 * (L + 1) + j];
-            const double v = Vp[(int64_t)tp * (L + 1) + j];
-            if (kFill) {
-                if (x <= bound) {
-                    const double y = x + v;
-                    if (y < w) {
-                        w = y;
-                        arg = k2;
-                    }
-                }
-            } else {
-                const double y = x > v ? x : v;
-                if (y < w) w = y;
-            }
+    // the islands of U' in ascending order (the same for every thread)
+    int ks[kMaxSetIslands];
+    {
+        uint32_t r2 = Up;
+#pragma unroll
+        for (int q = 0; q < kMaxSetIslands; ++q) {
+            ks[q] = r2 ? __builtin_ctz(r2) : 0;
+            r2 &= r2 - 1;
         }
-        Wl[j] = w;
-        if (kFill) argG[gst * (L + 1) + j] = (uint8_t)arg;
     }
-    __syncthreads();
-    const double *Tr = T + (((int64_t)(d - 1) * P.nb + bb) * K + k) * P.NS;
-    double *out = cur + ((int64_t)bb * lv.n[d] + st) * (L + 1);
-    for (int i = threadIdx.x; i <= L; i += NT) {
-        double best = kInf;
-        int bj = 0;
-        if (i <= L - d) {
-            const int64_t base = slice_of(L, i, i + 1) - (i + 1);  // T_d(i, j, k) = Tr[base + j]
-            for (int j = i + 1; j <= jmax; ++j) {
-                const double tv = Tr[base + j];
-                if (kFill) {
-                    if (tv > bound || tv >= best) break;
-                    const double y = tv + Wl[j];
-                    if (y < best) {
-                        best = y;
-                        bj = j;
+    const int nu = d - 1;
+    constexpr int NJ = NT >= 256 ? 2 : 1;  // cuts per thread (j <= L < 2 NT)
+    int buf = 0;  // continuation rows alternate between two LDS rows, so one
+                  // barrier per state separates writers from readers
+    for (int q = q0; q < q1; ++q, rest &= rest - 1, buf ^= 1) {
+        const int k = __builtin_ctz(rest);
+        const uint32_t U = Up | (1u << k);
+        const int st = (int)rank[U] * d + __builtin_popcount(U & ((1u << k) - 1u));
+        const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
+        double *Wrow = Wl[buf];
+        // continuation row from X[b][k][k'][.] and V_{d-1}(., k', U'), four
+        // islands' loads in flight
+        const double *Xr = X + ((int64_t)bb * K + k) * K * (L + 1);
+        for (int c = 0; c < NJ; ++c) {
+            const int j = threadIdx.x + 1 + c * NT;
+            if (j > jmax) continue;
+            double w = kInf;
+            int arg = 255;
+            for (int t0 = 0; t0 < nu; t0 += 4) {
+                double x[4], vv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int t = min(t0 + u, nu - 1);
+                    x[u] = Xr[(int64_t)ks[t] * (L + 1) + j];
+                    vv[u] = Vp[(int64_t)t * (L + 1) + j];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int t = t0 + u;
+                    const double v = vv[u];
+                    if (t >= nu) {
+                    } else if (kFill) {
+                        if (x[u] <= bound) {
+                            const double y = x[u] + v;
+                            if (y < w) {
+                                w = y;
+                                arg = ks[t];
+                            }
+                        }
+                    } else {
+                        const double y = x[u] > v ? x[u] : v;
+                        if (y < w) w = y;
                     }
-                } else {
-                    if (tv >= best) break;
-                    const double y = tv > Wl[j] ? tv : Wl[j];
-                    if (y < best) best = y;
                 }
             }
+            Wrow[j] = w;
+            if (kFill) argG[gst * (L + 1) + j] = (uint8_t)arg;
         }
-        out[i] = best;
-        if (kFill && i < L) argF[gst * L + i] = (uint16_t)bj;
-        if (i == 0) root[gst] = best;
+        __syncthreads();
+        const double *Tr = T + (((int64_t)(d - 1) * P.nb + bb) * K + k) * L * L;
+        double *out = cur + ((int64_t)bb * lv.n[d] + st) * (L + 1);
+        for (int i = threadIdx.x; i <= L; i += NT) {
+            double best = kInf;
+            int bj = 0;
+            if (i <= L - d) {
+                // T_d(i, j, k) = Tr[(j - i - 1) * L + i]: the threads of a wave
+                // read consecutive first layers
+                const double *Ti = Tr + i;
+                bool go = true;
+                // four cuts' stage costs in flight at a time (clamped to the row)
+                for (int j0 = i + 1; go && j0 <= jmax; j0 += 4) {
+                    double tv[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) tv[u] = Ti[(int64_t)(min(j0 + u, jmax) - i - 1) * L];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int j = j0 + u;
+                        if (!go || j > jmax) {
+                        } else if (kFill) {
+                            if (tv[u] > bound || tv[u] >= best) {
+                                go = false;
+                            } else {
+                                const double y = tv[u] + Wrow[j];
+                                if (y < best) {
+                                    best = y;
+                                    bj = j;
+                                }
+                            }
+                        } else {
+                            if (tv[u] >= best) {
+                                go = false;
+                            } else {
+                                const double y = tv[u] > Wrow[j] ? tv[u] : Wrow[j];
+                                if (y < best) best = y;
+                            }
+                        }
+                    }
+                }
+            }
+            out[i] = best;
+            if (kFill && i < L) argF[gst * L + i] = (uint16_t)bj;
+            if (i == 0) root[gst] = best;
+        }
     }
 }
 
@@ -315,18 +383,38 @@ __device__ inline void state_of(const SetLevels &lv, const int32_t *masks, int64
 
 // Per b: P* = least root bottleneck (kRoot = false), or the root of the fill:
 // least F, ties to the least first island k, then fewer stages d, then the
-// least set U (kRoot = true).  Block b, 256 threads.
+// least set U (kRoot = true).  Two passes: block (chunk, b) reduces a chunk of
+// b's states to a partial, then block b reduces its partials.
+
+__device__ inline bool key_less(double v1, uint32_t k1, double v2, uint32_t k2) {
+    return v1 < v2 || (v1 == v2 && k1 < k2);
+}
+
+// Reduces (sv, sk) over the block (256 threads) into entry 0.
+__device__ inline void block_argmin(double *sv, uint32_t *sk) {
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h && key_less(sv[threadIdx.x + h], sk[threadIdx.x + h], sv[threadIdx.x], sk[threadIdx.x])) {
+            sv[threadIdx.x] = sv[threadIdx.x + h];
+            sk[threadIdx.x] = sk[threadIdx.x + h];
+        }
+        __syncthreads();
+    }
+}
+
 template <bool kRoot>
-__global__ __launch_bounds__(256) void orders_reduce(SetLevels lv, const int32_t *__restrict__ masks,
-                                                     const double *__restrict__ root, double *out_v,
-                                                     uint32_t *out_key) {
+__global__ __launch_bounds__(256) void orders_reduce_part(SetLevels lv, const int32_t *__restrict__ masks,
+                                                          const double *__restrict__ root, double *part_v,
+                                                          uint32_t *part_k) {
     __shared__ double sv[256];
     __shared__ uint32_t sk[256];
-    const int bb = blockIdx.x;
+    const int c = blockIdx.x, bb = blockIdx.y;
+    const int64_t per = (lv.total + kReduceChunks - 1) / kReduceChunks;
+    const int64_t q0 = (int64_t)c * per, q1 = min(lv.total, q0 + per);
     const double *rv = root + (int64_t)bb * lv.total;
     double bv = kInf;
     uint32_t bk = kNoKey;
-    for (int64_t q = threadIdx.x; q < lv.total; q += blockDim.x) {
+    for (int64_t q = q0 + threadIdx.x; q < q1; q += blockDim.x) {
         const double v = rv[q];
         if (!kRoot) {
             if (v < bv) bv = v;
@@ -337,28 +425,33 @@ __global__ __launch_bounds__(256) void orders_reduce(SetLevels lv, const int32_t
         uint32_t U;
         state_of(lv, masks, q, &k, &d, &U);
         const uint32_t key = ((uint32_t)k << 24) | ((uint32_t)d << 16) | U;
-        if (v < bv || key < bk) {
+        if (key_less(v, key, bv, bk)) {
             bv = v;
             bk = key;
         }
     }
     sv[threadIdx.x] = bv;
     sk[threadIdx.x] = bk;
-    __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-        if (threadIdx.x < h) {
-            const double v2 = sv[threadIdx.x + h];
-            const uint32_t k2 = sk[threadIdx.x + h];
-            if (v2 < sv[threadIdx.x] || (v2 == sv[threadIdx.x] && k2 < sk[threadIdx.x])) {
-                sv[threadIdx.x] = v2;
-                sk[threadIdx.x] = k2;
-            }
-        }
-        __syncthreads();
+    block_argmin(sv, sk);
+    if (threadIdx.x == 0) {
+        part_v[(int64_t)bb * kReduceChunks + c] = sv[0];
+        part_k[(int64_t)bb * kReduceChunks + c] = sk[0];
     }
+}
+
+__global__ __launch_bounds__(256) void orders_reduce_final(const double *__restrict__ part_v,
+                                                           const uint32_t *__restrict__ part_k, double *out_v,
+                                                           uint32_t *out_key) {
+    __shared__ double sv[256];
+    __shared__ uint32_t sk[256];
+    const int bb = blockIdx.x;
+    const bool in = threadIdx.x < kReduceChunks;
+    sv[threadIdx.x] = in ? part_v[(int64_t)bb * kReduceChunks + threadIdx.x] : kInf;
+    sk[threadIdx.x] = in ? part_k[(int64_t)bb * kReduceChunks + threadIdx.x] : kNoKey;
+    block_argmin(sv, sk);
     if (threadIdx.x == 0) {
         out_v[bb] = sv[0];
-        if (kRoot) out_key[bb] = sk[0];
+        if (out_key) out_key[bb] = sk[0];
     }
 }
 
@@ -461,18 +554,23 @@ static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs 
     const dim3 g1((unsigned)(((int64_t)P.K * (L + 1) + 255) / 256), (unsigned)P.nb);
     orders_level1<kFill><<<g1, dim3(256), 0, s>>>(P, lv, w.T, w.Pst, w.Vb[1], w.root);
     for (int d = 2; d <= lv.D; ++d) {
-        const dim3 grid((unsigned)lv.n[d], (unsigned)P.nb);
+        // blocks: the (d-1)-sets times b, each split over the islands outside
+        // the set until there are enough blocks to fill the device
+        const int64_t sets = binom(P.K, d - 1) * P.nb;
+        const int nk = P.K - (d - 1);
+        const int nsplit = (int)std::max<int64_t>(1, std::min<int64_t>(nk, (kTargetBlocks + sets - 1) / sets));
+        const dim3 grid((unsigned)(binom(P.K, d - 1) * nsplit), (unsigned)P.nb);
         const double *prev = w.Vb[(d - 1) & 1];
         double *cur = w.Vb[d & 1];
         if (L < 64)
-            orders_level<64, kFill><<<grid, dim3(64), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur, w.root,
-                                                             w.Pst, w.argF, w.argG);
+            orders_level<64, kFill><<<grid, dim3(64), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev, cur,
+                                                             w.root, w.Pst, w.argF, w.argG);
         else if (L < 128)
-            orders_level<128, kFill><<<grid, dim3(128), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur,
-                                                               w.root, w.Pst, w.argF, w.argG);
+            orders_level<128, kFill><<<grid, dim3(128), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev,
+                                                               cur, w.root, w.Pst, w.argF, w.argG);
         else
-            orders_level<256, kFill><<<grid, dim3(256), 0, s>>>(P, lv, d, w.masks, w.rank, w.T, w.X, prev, cur,
-                                                               w.root, w.Pst, w.argF, w.argG);
+            orders_level<256, kFill><<<grid, dim3(256), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev,
+                                                               cur, w.root, w.Pst, w.argF, w.argG);
     }
 }
 
@@ -485,15 +583,18 @@ hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64
     orders_init<<<dim3(1), dim3(64), 0, s>>>(P.K, w.pos, w.res);
     orders_masks<<<dim3((unsigned)(((1u << P.K) + 255) / 256)), dim3(256), 0, s>>>(P.K, lv, w.masks, w.rank);
     launch_grouping(P, surv, n_surv, cost, dmax, w.pos, w.g, w.res, s);
-    const int64_t ngroups = (int64_t)P.nb * P.K * P.NS;
-    orders_stage_table<<<dim3((unsigned)((ngroups + 255) / 256)), dim3(256), 0, s>>>(P, lv.D, w.g.gcnt, w.g.ent_c,
-                                                                                    w.g.ent_d, w.T);
+    const int64_t ncells = (int64_t)P.nb * P.K * P.L * P.L;
+    orders_stage_table<<<dim3((unsigned)((ncells + 255) / 256)), dim3(256), 0, s>>>(P, lv.D, w.g.gcnt, w.g.ent_c,
+                                                                                   w.g.ent_d, w.T);
     const int64_t nx = (int64_t)P.nb * P.K * P.K * (P.L + 1);
     orders_links<<<dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s>>>(P, w.X);
+    const dim3 rgrid(kReduceChunks, (unsigned)P.nb);
     run_levels<false>(P, lv, w, s);
-    orders_reduce<false><<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(lv, w.masks, w.root, w.Pst, nullptr);
+    orders_reduce_part<false><<<rgrid, dim3(256), 0, s>>>(lv, w.masks, w.root, w.part_v, w.part_k);
+    orders_reduce_final<<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.Pst, nullptr);
     run_levels<true>(P, lv, w, s);
-    orders_reduce<true><<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(lv, w.masks, w.root, w.rootF, w.rootKey);
+    orders_reduce_part<true><<<rgrid, dim3(256), 0, s>>>(lv, w.masks, w.root, w.part_v, w.part_k);
+    orders_reduce_final<<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.rootF, w.rootKey);
     orders_finish<<<dim3(1), dim3(kOrderFinishThreads), 0, s>>>(P, lv, w.masks, w.rank, w.g.gcnt, w.g.ent_c,
                                                                 w.g.ent_d, w.g.ent_i, w.X, w.Pst, w.rootF,
                                                                 w.rootKey, w.argF, w.argG, w.res);
