@@ -25,7 +25,7 @@ LAYER_FIELDS = ("fwd_flops", "dense_params", "expert_params", "act_stash_bytes",
 # instances without them use these values
 LAYER_DEFAULT = 0           # per-layer field absent: zeros
 HOST_BW_DEFAULT = 0.0       # no host link: offloading not admitted
-SPACE_DEFAULTS = {"cp": [1], "recompute": [0], "offload": [0]}
+SPACE_DEFAULTS = {"cp": [1], "recompute": [0], "offload": [0], "imbalance_eps": 0.0}
 
 OK, EINVAL, ENOMEM, ECAPACITY, ENOPLAN = 0, -1, -2, -4, -5
 
@@ -76,7 +76,7 @@ def lib():
                                  ctypes.c_int64, ctypes.c_int, i32p, ctypes.c_int, i32p, ctypes.c_int,
                                  i32p, ctypes.c_int, i32p, ctypes.c_int, ctypes.c_uint32,
                                  ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double, ctypes.c_double,
-                                 ctypes.POINTER(vp)]
+                                 ctypes.c_double, ctypes.POINTER(vp)]
         L.tgo_destroy.argtypes = [vp]
         L.tgo_counts.argtypes = [vp, i64p]
         L.tgo_bvalues.argtypes = [vp, i64p]
@@ -88,6 +88,7 @@ def lib():
         L.tgo_compose.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
         L.tgo_compose_relaxed.argtypes = [vp, i64p, ctypes.c_int64, i32p, ctypes.POINTER(Plan), f64p]
         L.tgo_compose_all_orders.argtypes = [vp, i64p, ctypes.c_int64, ctypes.POINTER(Plan), f64p]
+        L.tgo_balanced.argtypes = [vp, ctypes.c_int64, ctypes.c_int]
         _lib = L
     return _lib
 
@@ -140,7 +141,8 @@ class Oracle:
                               int(sp["n_experts"]), _ptr(tp, ctypes.c_int32), len(tp),
                               _ptr(cp, ctypes.c_int32), len(cp), _ptr(ep, ctypes.c_int32), len(ep),
                               _ptr(mb, ctypes.c_int32), len(mb), zmask, rmask, omask,
-                              float(sp["eta"]), float(sp["mem_frac"]), ctypes.byref(h))
+                              float(sp["eta"]), float(sp["mem_frac"]),
+                              float(sp.get("imbalance_eps", SPACE_DEFAULTS["imbalance_eps"])), ctypes.byref(h))
         if st != OK:
             raise OracleError(st, "create")
         self.h = h
@@ -199,6 +201,14 @@ class Oracle:
         return cost, dmax
 
     # -- pruning -----------------------------------------------------------
+    def balanced(self, i, j, island):
+        """Whether slice [i, j) on `island` passes imbalance pruning."""
+        s = i * self.L - (i * (i - 1)) // 2 + (j - i - 1)
+        r = lib().tgo_balanced(self.h, s, int(island))
+        if r < 0:
+            raise OracleError(r, "balanced")
+        return bool(r)
+
     def prune(self):
         n = ctypes.c_int64(0)
         lib().tgo_prune(self.h, None, 0, ctypes.byref(n))

@@ -70,6 +70,7 @@ typedef struct {
     int n_experts;
     int ntp, tp[8], ncp, cp[8], nep, ep[8], nmb, mb[8], nz, zs[4], nrc, rcs[2], nof, ofs[2];
     double eta, mem_frac;
+    double imb_eps; /* imbalance-pruning tolerance, 0 = off */
     /* derived */
     int64_t NS, ncfg, N;
     int64_t *cfg_off; /* K+1 */
@@ -77,6 +78,7 @@ typedef struct {
     int64_t *slice_sum; /* NS x 6: flops, dparam, eparam, act, tpcomm, a2a */
     int nb;
     int64_t *bvals; /* distinct compatible b, ascending */
+    double *cap_share; /* [K] island's share of the cluster's compute */
 } oprob;
 
 /* ------------------------------------------------------------------------ */
@@ -160,19 +162,20 @@ void tgo_destroy(void *h) {
     if (!p) return;
     for (int f = 0; f < NF; f++) free(p->layer[f]);
     free(p->n_gpus); free(p->peak); free(p->hbm); free(p->intra); free(p->host); free(p->inter);
-    free(p->cfg_off); free(p->cfg); free(p->slice_sum); free(p->bvals);
+    free(p->cfg_off); free(p->cfg); free(p->slice_sum); free(p->bvals); free(p->cap_share);
     free(p);
 }
 
 /* layers: NF*L int64, field-major (all fwd_flops, then dense_params, ...).
    cp: context-parallel degrees (ncp = 0 means {1}); rc_mask / of_mask: bit r
-   admits recomputation / offloading option r (0 means {off}). */
+   admits recomputation / offloading option r (0 means {off}).  imb_eps: the
+   imbalance-pruning tolerance (0 = off; otherwise finite and > 0). */
 int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double *peak,
                const double *hbm, const double *intra, const double *host_bw, int K, const double *inter,
                int64_t global_batch, int n_experts, const int32_t *tp, int ntp,
                const int32_t *cp, int ncp, const int32_t *ep, int nep, const int32_t *mb, int nmb,
                uint32_t zero_mask, uint32_t rc_mask, uint32_t of_mask, double eta, double mem_frac,
-               void **out) {
+               double imb_eps, void **out) {
     *out = NULL;
     if (L < 1 || L > 512 || K < 1 || K > 255) return TGO_EINVAL;
     if (global_batch < 1 || n_experts < 0) return TGO_EINVAL;
@@ -183,6 +186,7 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
     if ((rc_mask & ~0x3u) || (of_mask & ~0x3u)) return TGO_EINVAL;
     if (!(eta > 0.0) || !isfinite(eta) || !(mem_frac > 0.0) || !isfinite(mem_frac))
         return TGO_EINVAL;
+    if (!(imb_eps >= 0.0) || !isfinite(imb_eps)) return TGO_EINVAL;
     for (int k = 0; k < K; k++) {
         if (n_gpus[k] < 1 || n_gpus[k] > 65536) return TGO_EINVAL;
         if (!(peak[k] > 0.0) || !isfinite(peak[k])) return TGO_EINVAL;
@@ -239,6 +243,13 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
         if ((of_mask ? of_mask : 1u) & (1u << r)) p->ofs[p->nof++] = r;
     p->eta = eta;
     p->mem_frac = mem_frac;
+    p->imb_eps = imb_eps;
+    /* an island's compute capacity is n_k F_k; its share of the cluster's is
+       the capacity over the sum of all islands' (summed in island order) */
+    p->cap_share = (double *)malloc(sizeof(double) * K);
+    double cap_sum = 0.0;
+    for (int k = 0; k < K; k++) cap_sum = cap_sum + ((double)n_gpus[k] * peak[k]);
+    for (int k = 0; k < K; k++) p->cap_share[k] = ((double)n_gpus[k] * peak[k]) / cap_sum;
 
     p->NS = (int64_t)L * (L + 1) / 2;
     p->cfg_off = (int64_t *)malloc(sizeof(int64_t) * (K + 1));
@@ -463,6 +474,29 @@ int tgo_score_list(void *h, const int64_t *idx, int64_t n, double *cost, uint8_t
 }
 
 /* ------------------------------------------------------------------------ */
+/* imbalance pruning (Sec. 5.1 (ii))                                         */
+/* ------------------------------------------------------------------------ */
+/* A slice demands its share q of the model's forward FLOPs; an island offers
+   its share c of the cluster's compute.  With tolerance eps the pair is kept
+   iff q <= c (1 + eps) (the island does not stall) and q (1 + eps) >= c (it is
+   not left underused).  Off when eps = 0 or the model has no FLOPs. */
+static int balanced(const oprob *p, int64_t s, int k) {
+    if (p->imb_eps == 0.0) return 1;
+    int64_t total = p->slice_sum[slice_index(p->L, 0, p->L) * NSUM + 0];
+    if (total == 0) return 1;
+    double q = (double)p->slice_sum[s * NSUM + 0] / (double)total;
+    double r = 1.0 + p->imb_eps;
+    double c = p->cap_share[k];
+    return q <= c * r && q * r >= c;
+}
+
+int tgo_balanced(void *h, int64_t s, int k) {
+    oprob *p = (oprob *)h;
+    if (s < 0 || s >= p->NS || k < 0 || k >= p->K) return -1;
+    return balanced(p, s, k);
+}
+
+/* ------------------------------------------------------------------------ */
 /* pruning: the surviving set                                                */
 /* ------------------------------------------------------------------------ */
 /* A group is (slice, island, b).  Preference key (cost, -d_max, idx) ascending.
@@ -470,7 +504,9 @@ int tgo_score_list(void *h, const int64_t *idx, int64_t n, double *cost, uint8_t
    rep(G, d) over d = 1..K.  Equivalently p survives iff p is compatible,
    d_max_p >= 1 and no member q has key_q < key_p with d_max_q >= d_max_p, i.e.
    d_max_p exceeds the largest d_max among all members preceding p in key
-   order.  Sorting by key and sweeping a running maximum evaluates exactly that. */
+   order.  Sorting by key and sweeping a running maximum evaluates exactly that.
+   With imbalance pruning on, groups of unbalanced (slice, island) pairs have
+   no survivors. */
 typedef struct {
     double cost;
     int dmax;
@@ -522,6 +558,7 @@ int tgo_prune(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
                 if (p->cfg[c0 + c].b == b) members[nm++] = c;
             if (nm == 0) continue;
             for (int64_t s = 0; s < p->NS; s++) {
+                if (!balanced(p, s, k)) continue;
                 int64_t n = 0;
                 for (int64_t a = 0; a < nm; a++) {
                     int64_t c = members[a];
@@ -833,7 +870,7 @@ static int compose_impl(void *h, const int64_t *cands, int64_t n, const int32_t 
         }
         int64_t g = idx / NS, s = idx % NS;
         const ocfg *cf = &p->cfg[g];
-        if (p->B % cf->b != 0) { free(pos); free(ent); return TGO_EINVAL; }
+        if (p->B % cf->b != 0 || !balanced(p, s, cf->k)) { free(pos); free(ent); return TGO_EINVAL; }
         int bi = 0;
         while (p->bvals[bi] != cf->b) bi++;
         ocoef o;
@@ -1089,7 +1126,7 @@ int tgo_compose_all_orders(void *h, const int64_t *cands, int64_t n, tgo_plan *p
         }
         int64_t g = idx / NS, s = idx % NS;
         const ocfg *cf = &p->cfg[g];
-        if (p->B % cf->b != 0) { free(ident); free(ent); return TGO_EINVAL; }
+        if (p->B % cf->b != 0 || !balanced(p, s, cf->k)) { free(ident); free(ent); return TGO_EINVAL; }
         int bi = 0;
         while (p->bvals[bi] != cf->b) bi++;
         ocoef o;
