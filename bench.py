@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--space", default="named", choices=("named", "extended"),
                     help="config space: the workload's own, or extended with context parallelism "
                          "{1,2,4}, recomputation and offloading")
+    ap.add_argument("--imbalance-eps", type=float, default=0.0,
+                    help="imbalance-pruning tolerance for every workload (0: off)")
     ap.add_argument("--other-steps", type=int, default=10,
                     help="timed plan searches per workload in the five-workload table (0 skips it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -173,7 +175,7 @@ def time_search(torch, T, inst, steps, warmup):
             "compose_ms": [ev[k][2].elapsed_time(ev[k][3]) for k in range(steps)]}
 
 
-def five_workloads(torch, T, load_instance, space, steps, main_name, main_row):
+def five_workloads(torch, T, load_instance, space, steps, main_name, main_row, imbalance_eps=0.0):
     """The plan search on each synthetic cluster: candidates, survivors,
     milliseconds per whole search, candidates per second, the score kernel's
     share of the HBM peak, the chosen plan's b, stages and T."""
@@ -186,6 +188,7 @@ def five_workloads(torch, T, load_instance, space, steps, main_name, main_row):
         if space == "extended":
             from workloads import extended
             inst = extended(inst)
+        inst["space"]["imbalance_eps"] = imbalance_eps
         run = time_search(torch, T, inst, steps, 2)
         out[name] = workload_row(run, steps)
         del run
@@ -250,6 +253,7 @@ def main():
     if args.space == "extended":
         from workloads import extended
         inst = extended(inst)
+    inst["space"]["imbalance_eps"] = args.imbalance_eps
     if args.copy_calibration > 0:
         a = torch.ones(args.copy_calibration // 8, dtype=torch.float64, device="cuda")
         b = torch.empty_like(a)
@@ -282,6 +286,8 @@ def main():
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
     traffic = measured_traffic(args.workload if args.space == "named" else args.workload + "+extended", N)
+    if args.imbalance_eps > 0:
+        traffic = None  # the counters were taken without imbalance pruning
     out = {
         "metric": METRIC,
         "value": N * args.steps / elapsed,
@@ -297,7 +303,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}"
                                + ("" if args.space == "named" else
-                                  "; extended with CP{1,2,4} x recomputation x offloading"),
+                                  "; extended with CP{1,2,4} x recomputation x offloading")
+                               + ("" if args.imbalance_eps == 0 else
+                                  f"; imbalance pruning eps {args.imbalance_eps}"),
                    "candidates": N, "survivors": int(s.numel()), "islands": p.K, "layers": p.L,
                    "plan": {"status": st, "b": plan["b"], "stages": plan["S"], "T": plan["T"]}},
         "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": achieved,
@@ -314,7 +322,7 @@ def main():
         del run, cost, dmax, s
         torch.cuda.empty_cache()
         out["workloads"] = five_workloads(torch, T, load_instance, args.space, args.other_steps,
-                                          args.workload, main_row)
+                                          args.workload, main_row, args.imbalance_eps)
     if not args.no_cpu:
         cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
         out["cpu_baseline"] = cb

@@ -84,8 +84,17 @@ typedef struct {
    n_experts = 0 describes a dense model (then only ep = 1 is admitted);
    otherwise ep must divide n_experts.  eta scales peak FLOP/s (efficiency),
    mem_frac scales usable memory; both finite and > 0.  A zero-filled tail
-   (n_cp, masks) keeps the space without context parallelism, recomputation
-   and offloading. */
+   (n_cp, masks, imbalance_eps) keeps the space without context parallelism,
+   recomputation, offloading and imbalance pruning.
+
+   imbalance_eps (Sec. 5.1 (ii), imbalance pruning; finite, >= 0, 0 = off):
+   with q = Fl(i, j) / Fl(0, L) the slice's share of the model's forward FLOPs
+   and c_k = (n_k F_k) / sum_k' (n_k' F_k') the island's share of the
+   cluster's compute (the sum taken in island order), the pair (slice, island)
+   is kept iff q <= c_k (1 + eps) and q (1 + eps) >= c_k, each operation one
+   binary64 rounding in that order.  Unbalanced pairs are scored but never
+   survive, and the compositions reject them.  A model with no FLOPs is never
+   pruned. */
 typedef struct {
     int64_t global_batch; /* samples per iteration, >= 1 */
     int32_t n_experts;
@@ -104,6 +113,7 @@ typedef struct {
     uint32_t recompute_mask; /* activation recomputation (Sec. 2.1 RC) */
     uint32_t offload_mask;   /* activation offloading to host memory (Sec. 2.1 OF) */
     int32_t reserved2;       /* must be 0 */
+    double imbalance_eps;    /* imbalance-pruning tolerance, 0 = off */
 } tg_space;
 
 /* A decoded candidate: layers [i, j) on island `island` with the given

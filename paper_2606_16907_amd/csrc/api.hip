@@ -67,6 +67,8 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     if (sp.reserved2 != 0) return fail(TG_EINVAL, "space reserved2 field not 0");
     if (!(sp.eta > 0.0) || !std::isfinite(sp.eta)) return fail(TG_EINVAL, "eta invalid");
     if (!(sp.mem_frac > 0.0) || !std::isfinite(sp.mem_frac)) return fail(TG_EINVAL, "mem_frac invalid");
+    if (!(sp.imbalance_eps >= 0.0) || !std::isfinite(sp.imbalance_eps))
+        return fail(TG_EINVAL, "imbalance_eps invalid");
     for (int k = 0; k < K; ++k) {
         const tg_island &is = islands[k];
         if (is.n_gpus < 1 || is.n_gpus > 65536) return fail(TG_EINVAL, "island %d: n_gpus", k);
@@ -212,6 +214,30 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
             for (int j = i + 1; j <= L; ++j) sij[s++] = (uint32_t)i | ((uint32_t)j << 16);
     }
 
+    // imbalance pruning: each island's share of the cluster's compute (summed
+    // in island order) and, per island and first layer, the first balanced cut
+    // (a slice's FLOP share only grows with its end, so the balanced cuts of a
+    // first layer are one interval)
+    const int64_t total_flops = pre[L] - pre[0];
+    const int imb = (sp.imbalance_eps > 0.0 && total_flops > 0) ? 1 : 0;
+    const double imb_r = 1.0 + sp.imbalance_eps;
+    std::vector<double> cap(K);
+    {
+        double cap_sum = 0.0;
+        for (int k = 0; k < K; ++k) cap_sum = cap_sum + ((double)islands[k].n_gpus * islands[k].peak_flops);
+        for (int k = 0; k < K; ++k) cap[k] = ((double)islands[k].n_gpus * islands[k].peak_flops) / cap_sum;
+    }
+    std::vector<int32_t> jlo(imb ? (size_t)K * L : 0);
+    for (int k = 0; imb && k < K; ++k)
+        for (int i = 0; i < L; ++i) {
+            int j = i + 1;
+            for (; j <= L; ++j) {
+                const double q = (double)(pre[j] - pre[i]) / (double)total_flops;
+                if (q <= cap[k] * imb_r && q * imb_r >= cap[k]) break;
+            }
+            jlo[(size_t)k * L + i] = j;
+        }
+
     // one device block for all tables
     struct Part {
         const void *src;
@@ -243,6 +269,8 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         {ev.data(), ev.size() * 8, 0},
         {eidx.data(), eidx.size() * 2, 0},
         {host.data(), (size_t)K * 8, 0},
+        {cap.data(), (size_t)K * 8, 0},
+        {jlo.data(), jlo.size() * 4, 0},
     };
     size_t total = 0;
     for (auto &p : parts) {
@@ -305,6 +333,12 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.Ev = (const double *)(base + parts[14].off);
     P.Eidx = (const uint16_t *)(base + parts[15].off);
     P.host = (const double *)(base + parts[16].off);
+    P.imb = imb;
+    P.imb_r = imb_r;
+    P.total_flops = total_flops;
+    P.cap = (const double *)(base + parts[17].off);
+    P.jlo = imb ? (const int32_t *)(base + parts[18].off) : nullptr;
+    P.jlo_pos = nullptr;
     pr->bvals = bv;
     pr->n_compat_cfg = (int64_t)row_cfg.size();
     pr->B = space->global_batch;

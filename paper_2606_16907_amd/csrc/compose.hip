@@ -137,6 +137,7 @@ struct Ws {
     double *T;         // [n_groups] current stage table, layout [b][s][o]
     double *T1;        // [nb][L][K] depth-1 table of the slices (i, L)
     int32_t *bcur;     // [n_buckets + 1] per-bucket write cursors
+    int32_t *jlo_pos;  // [K][L] first balanced cut by island position (imbalance pruning)
     double *Wb[2];     // [nb][L+1][K] continuation rows, double-buffered by level
     uint16_t *argF;    // [D][nb][L][K]
     uint8_t *argG;     // [D][nb][L+1][K]
@@ -183,6 +184,7 @@ static Ws carve(const DevProblem &P, int64_t n, void *base) {
     w.T = (double *)take(sizeof(double) * G);
     w.T1 = (double *)take(sizeof(double) * P.nb * P.L * P.K);
     w.bcur = (int32_t *)take(sizeof(int32_t) * (nbk + 1));
+    w.jlo_pos = (int32_t *)take(P.imb ? sizeof(int32_t) * P.K * P.L : 1);
     w.Wb[0] = (double *)take(sizeof(double) * rows);
     w.Wb[1] = (double *)take(sizeof(double) * rows);
     w.argF = (uint16_t *)take(sizeof(uint16_t) * D * P.nb * P.L * P.K);
@@ -228,6 +230,14 @@ __global__ __launch_bounds__(256) void prep_kernel(DevProblem P, const int32_t *
     }
 }
 
+// First balanced cut of each first layer, by island position of this call.
+__global__ __launch_bounds__(256) void jlo_kernel(DevProblem P, const int32_t *order, int32_t *jlo_pos) {
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= P.K * P.L) return;
+    const int o = t / P.L, i = t - o * P.L;
+    jlo_pos[t] = P.jlo[order[o] * P.L + i];
+}
+
 // ---------------------------------------------------------------------------
 // grouping: candidate list -> per-group entry records -> per-level events
 // ---------------------------------------------------------------------------
@@ -245,7 +255,8 @@ __global__ __launch_bounds__(256) void gather_kernel(DevProblem P, const int64_t
         } else {
             const int64_t g = idx / P.NS, s = idx - g * P.NS;
             const Coef &c = P.coef[g];
-            if (c.b_idx < 0) {
+            const uint32_t ij = P.sij[s];
+            if (c.b_idx < 0 || !slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), c.k)) {
                 atomicOr(&res->err, 2);
             } else {
                 const uint8_t d = dmax[idx];
@@ -700,8 +711,11 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bot
             const double *Wp = Wprev + (int64_t)bi * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
+            // with imbalance pruning the cuts before the first balanced one have no
+            // stage; from there on T again never decreases in j
+            const int js = P.jlo_pos ? max(i + 1, P.jlo_pos[o * L + i]) : i + 1;
             bool go = true;
-            for (int j0 = i + 1 + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
+            for (int j0 = js + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
                 double t[kAhead], w[kAhead];
 #pragma unroll
                 for (int u = 0; u < kAhead; ++u) {  // unconditional loads, all in flight at once
@@ -818,8 +832,9 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
             const double *Gp = Gprev + (int64_t)row * (L + 1) * K + o;
             const double *Tp = T + srow * K + o;
             const int jmax = L - d + 1;
+            const int js = P.jlo_pos ? max(i + 1, P.jlo_pos[o * L + i]) : i + 1;
             bool go = true;
-            for (int j0 = i + 1 + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
+            for (int j0 = js + sub; go && j0 <= jmax; j0 += kAhead * SPLIT) {
                 double t[kAhead], g[kAhead];
 #pragma unroll
                 for (int u = 0; u < kAhead; ++u) {  // unconditional loads, all in flight at once
@@ -1170,7 +1185,7 @@ __global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_
 
 // Sequencing of the composition kernels on one workspace.
 struct Driver {
-    const DevProblem &P;
+    DevProblem P;  // this call's copy: carries the table of first balanced cuts by position
     Ws w;
     hipStream_t s;
     int D;
@@ -1182,6 +1197,7 @@ struct Driver {
     Driver(const DevProblem &P_, int64_t n_surv, void *ws, hipStream_t s_)
         : P(P_), w(carve(P_, n_surv, ws)), s(s_), D(levels(P_)), rows((int64_t)P_.nb * (P_.L + 1) * P_.K) {
         tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
+        P.jlo_pos = P.imb ? w.jlo_pos : nullptr;
         tgrid = dim3((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
                      (unsigned)P.nb);
         int dev = 0;
@@ -1195,6 +1211,8 @@ struct Driver {
         const int64_t nbk = n_buckets(P);
         prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT,
                                                                                      w.EiT, w.res);
+        if (P.imb)
+            jlo_kernel<<<dim3((unsigned)((P.K * P.L + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.jlo_pos);
         fill<int32_t>(w.bcnt, nbk + 1, 0, s);
         fill<double>(w.Pst, P.nb, kInf, s);
         const Groups g{w.rec_g, w.rec_c, w.rec_d, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.tmp};

@@ -328,8 +328,10 @@ __global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, i
                 // read consecutive first layers
                 const double *Ti = Tr + i;
                 bool go = true;
+                // with imbalance pruning the scan starts at the first balanced cut
+                const int js = P.jlo ? max(i + 1, P.jlo[k * L + i]) : i + 1;
                 // four cuts' stage costs in flight at a time (clamped to the row)
-                for (int j0 = i + 1; go && j0 <= jmax; j0 += 4) {
+                for (int j0 = js; go && j0 <= jmax; j0 += 4) {
                     double tv[4];
 #pragma unroll
                     for (int u = 0; u < 4; ++u) tv[u] = Ti[(int64_t)(min(j0 + u, jmax) - i - 1) * L];

@@ -2,7 +2,8 @@
 // dominance pruning (Sec. 5.1), as a frontier pass plus a stream compaction.
 //
 // Group G = (slice s, island k, micro-batch b).  A member p survives iff b
-// divides the global batch, d_max_p >= 1 and p has the least key
+// divides the global batch, (s, k) passes imbalance pruning when it is on,
+// d_max_p >= 1 and p has the least key
 // (cost, -d_max, idx) among members whose d_max reaches d_max_p.  Equivalently
 // the survivors are rep(G, d) for d = 1..K, the least-key member fitting at
 // depth d.  The frontier pass finds those reps depth band by depth band: pass t
@@ -51,6 +52,10 @@ __global__ __launch_bounds__(256) void frontier_kernel(DevProblem P, const doubl
         const int64_t NS = P.NS;
         const int K = P.K;
         bool live = s < NS;
+        if (live && P.imb) {  // an unbalanced (slice, island) group has no survivors
+            const uint32_t ij = P.sij[s];
+            live = slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), P.kb_island[q]);
+        }
         int prev = 0;   // d_max of the previous rep of this lane's group
         int top = -1;   // the group's largest d_max, known after the first pass
         while (__ballot(live) != 0) {

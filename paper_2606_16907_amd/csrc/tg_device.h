@@ -54,10 +54,24 @@ struct DevProblem {
     const double *peak, *hbm, *intra, *host;  // [K] island rates
     double eta, mem_frac;
     int32_t n_ev;            // distinct inter-island bandwidth values (<= kMaxDistinctE), else 0
-    int32_t pad_;
+    int32_t imb;             // imbalance pruning on
     const double *Ev;        // [n_ev] the distinct values, ascending
     const uint16_t *Eidx;    // [K*K] index of E[a][b] in Ev
+    double imb_r;            // 1 + eps
+    int64_t total_flops;     // forward FLOPs of the whole model
+    const double *cap;       // [K] island's share of the cluster's compute
+    const int32_t *jlo;      // [K][L] first balanced cut j of slices starting at i (L + 1: none)
+    const int32_t *jlo_pos;  // the same by island position of one composition call, or null
 };
+
+// Imbalance pruning: the slice's share of the model's FLOPs against the
+// island's share of the cluster's compute, within a factor imb_r either way.
+__host__ __device__ inline bool slice_balanced(const DevProblem &P, const int64_t *pre, int i, int j, int k) {
+    if (!P.imb) return true;
+    const double q = (double)(pre[j] - pre[i]) / (double)P.total_flops;
+    const double c = P.cap[k];
+    return q <= c * P.imb_r && q * P.imb_r >= c;
+}
 
 // Link times use one division per distinct bandwidth when there are few.
 constexpr int kMaxDistinctE = 256;

@@ -39,7 +39,7 @@ class TgSpace(ctypes.Structure):
                 ("eta", ctypes.c_double), ("mem_frac", ctypes.c_double),
                 ("n_cp", ctypes.c_int32), ("cp", ctypes.c_int32 * 8),
                 ("recompute_mask", ctypes.c_uint32), ("offload_mask", ctypes.c_uint32),
-                ("reserved2", ctypes.c_int32)]
+                ("reserved2", ctypes.c_int32), ("imbalance_eps", ctypes.c_double)]
 
 
 PAIR_FIELDS = ("i", "j", "island", "tp", "cp", "dp", "ep", "zero", "recompute", "offload", "mb")
@@ -182,6 +182,7 @@ class Problem:
             space.cp[a] = int(v)
         space.recompute_mask = sum(1 << int(r) for r in sp.get("recompute", [0]))
         space.offload_mask = sum(1 << int(r) for r in sp.get("offload", [0]))
+        space.imbalance_eps = float(sp.get("imbalance_eps", 0.0))
         space.eta = float(sp["eta"])
         space.mem_frac = float(sp["mem_frac"])
         h = ctypes.c_void_p()

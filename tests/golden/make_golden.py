@@ -8,7 +8,11 @@ composition with the step-(4) relaxation, for instances of at most 16 islands
 the plan and per-b (P*, F*, T) table of the composition over every island
 order, and a seeded sample of per-candidate scores.
 
-Run from the repository root:  python -m tests.golden.make_golden [names...]
+With --imbalance the same records (survivors, plan, per-b table) are
+written for the instance with imbalance pruning at IMBALANCE_EPS, to
+<name>_imbalance.json.
+
+Run from the repository root:  python -m tests.golden.make_golden [--imbalance] [names...]
 """
 from __future__ import annotations
 
@@ -29,6 +33,7 @@ from workloads import CONFIG_NAMES, load_instance  # noqa: E402
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 N_SAMPLE = 4096
+IMBALANCE_EPS = 1.0
 
 
 def sample_indices(N, NS, seed=1234):
@@ -82,6 +87,24 @@ def golden(name):
     }
 
 
+def golden_imbalance(name):
+    inst = load_instance(name)
+    inst["space"]["imbalance_eps"] = IMBALANCE_EPS
+    o = Oracle(inst)
+    t0 = time.time()
+    surv = o.prune()
+    t1 = time.time()
+    st, plan, per_b = o.compose(surv)
+    t2 = time.time()
+    return {
+        "name": name, "imbalance_eps": IMBALANCE_EPS,
+        "survivors": {"count": int(len(surv)), "sha256": survivors_digest(surv),
+                      "head": [int(x) for x in surv[:16]], "tail": [int(x) for x in surv[-16:]]},
+        "status": st, "plan": plan, "per_b": [[float(v) for v in row] for row in per_b],
+        "oracle_seconds": {"prune": round(t1 - t0, 3), "compose": round(t2 - t1, 3)},
+    }
+
+
 def path(name):
     return os.path.join(HERE, f"{name}.json")
 
@@ -93,6 +116,15 @@ def load(name):
 
 def main(names):
     build(force=False)
+    if names and names[0] == "--imbalance":
+        for name in names[1:] or list(CONFIG_NAMES):
+            g = golden_imbalance(name)
+            with open(path(name + "_imbalance"), "w") as fh:
+                json.dump(g, fh, indent=1, sort_keys=True)
+                fh.write("\n")
+            print(name, "imbalance", "survivors", g["survivors"]["count"], "T", g["plan"]["T"],
+                  g["oracle_seconds"], flush=True)
+        return
     for name in names:
         g = golden(name)
         with open(path(name), "w") as fh:

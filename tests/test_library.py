@@ -41,7 +41,7 @@ def test_binding_struct_layouts_match_header_sizes():
     from paper_2606_16907_amd import tangram as T
     assert ctypes.sizeof(T.TgLayer) == 64
     assert ctypes.sizeof(T.TgIsland) == 40
-    assert ctypes.sizeof(T.TgSpace) == 192
+    assert ctypes.sizeof(T.TgSpace) == 200
     assert ctypes.sizeof(T.TgPair) == 48
     assert ctypes.sizeof(T.TgStage) == 80
     assert ctypes.sizeof(T.TgPlan) == 16 + 24 + 255 * 80
