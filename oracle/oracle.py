@@ -265,3 +265,41 @@ def plan_to_dict(plan):
         stages.append({f: getattr(s, f) for f, _ in Stage._fields_})
     return {"status": plan.status, "b": plan.b, "m": plan.m, "S": plan.S, "P": plan.P,
             "F": plan.F, "T": plan.T, "stages": stages}
+
+
+def build_islands(cluster):
+    """Island construction (Sec. 4.1) of a node-level cluster: dict with
+    "nodes" (gpus, peak_flops, hbm_bytes, intra_bw, host_bw per node),
+    "node_bw" (n x n bytes/s, row = source) and "eps" (compute, memory,
+    intra).  Returns island_of (per node), K, islands (the tg_island fields)
+    and inter_bw (K x K)."""
+    nd = cluster["nodes"]
+    n = len(nd["gpus"])
+    gpus = np.ascontiguousarray(np.array(nd["gpus"], dtype=np.int32))
+    cols = [np.ascontiguousarray(np.array(nd[f], dtype=np.float64))
+            for f in ("peak_flops", "hbm_bytes", "intra_bw", "host_bw")]
+    e = np.ascontiguousarray(np.array(cluster["node_bw"], dtype=np.float64).reshape(-1))
+    eps = cluster["eps"]
+    isl = np.zeros(n, dtype=np.int32)
+    K = ctypes.c_int32(0)
+    og = np.zeros(n, dtype=np.int32)
+    out = [np.zeros(n, dtype=np.float64) for _ in range(4)]
+    oe = np.zeros(n * n, dtype=np.float64)
+    L_ = lib()
+    f = L_.tgo_build_islands
+    f.argtypes = [ctypes.POINTER(ctypes.c_int32)] + [ctypes.POINTER(ctypes.c_double)] * 4 + [
+        ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.c_double, ctypes.c_double, ctypes.c_double,
+        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)] + [
+        ctypes.POINTER(ctypes.c_double)] * 5
+    st = f(_ptr(gpus, ctypes.c_int32), *[_ptr(x, ctypes.c_double) for x in cols], n,
+           _ptr(e, ctypes.c_double), float(eps["compute"]), float(eps["memory"]), float(eps["intra"]),
+           _ptr(isl, ctypes.c_int32), ctypes.byref(K), _ptr(og, ctypes.c_int32),
+           *[_ptr(x, ctypes.c_double) for x in out], _ptr(oe, ctypes.c_double))
+    if st != OK:
+        raise OracleError(st, "build_islands")
+    k = K.value
+    return {"island_of": isl.tolist(), "K": k,
+            "islands": {"n_gpus": og[:k].tolist(), "peak_flops": out[0][:k].tolist(),
+                        "hbm_bytes": out[1][:k].tolist(), "intra_bw": out[2][:k].tolist(),
+                        "host_bw": out[3][:k].tolist()},
+            "inter_bw": oe[:k * k].reshape(k, k).tolist()}

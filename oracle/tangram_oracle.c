@@ -1200,3 +1200,176 @@ int tgo_compose_relaxed(void *h, const int64_t *cands, int64_t n, const int32_t 
                         double *per_b /* nb x 4: P*, bound, F, T; may be NULL */) {
     return compose_impl(h, cands, n, order, plan, per_b, 1);
 }
+
+/* ------------------------------------------------------------------------ */
+/* island construction (Sec. 4.1)                                            */
+/* ------------------------------------------------------------------------ */
+/* Nodes: gpus[u] GPUs of compute c[u], memory m[u] and intra-node bandwidth
+   bi[u] each (host[u]: host-link bandwidth); e[u*n + v] is the bandwidth from
+   node u to node v.  An island I must hold nodes with the same GPU count and
+   pairwise ratios max/min <= 1 + eps of compute and memory (Eq. 1) and of
+   intra-node bandwidth (Eq. 2), and every member's links inside I must be at
+   least as fast as its links leaving I (Eq. 3).  Steps (1)-(2): split the
+   nodes by GPU count, then by compute, memory and intra-node bandwidth, each
+   split a sweep over the values in ascending order that opens a new group at
+   the first value above the group's smallest times (1 + eps).  Step (3):
+   agglomerative clustering inside each group: repeatedly take the pair of
+   clusters with the highest complete linkage (least bandwidth between their
+   nodes, each node pair counted by its slower direction), ties to the least
+   pair of smallest node ids; merge it if the union satisfies Eq. 3, else mark
+   the pair and go on; stop when every remaining pair is marked.  Islands are
+   numbered by smallest node id; an island has the sum of its members' GPUs,
+   the least of their compute, memory, intra and host bandwidth, and the
+   island-to-island bandwidth is the least over node pairs. */
+static const double *node_cmp_val = NULL;
+static const int64_t *node_cmp_grp = NULL;
+
+static int cmp_nodes(const void *a, const void *b) {
+    int x = *(const int *)a, y = *(const int *)b;
+    if (node_cmp_grp[x] != node_cmp_grp[y]) return node_cmp_grp[x] < node_cmp_grp[y] ? -1 : 1;
+    if (node_cmp_val[x] != node_cmp_val[y]) return node_cmp_val[x] < node_cmp_val[y] ? -1 : 1;
+    return (x > y) - (x < y);
+}
+
+/* Refine groups grp[] by a sweep over val[] within each group (tolerance eps):
+   new group numbers are dense, in (old group, value, node id) order. */
+static void split_by(int n, int64_t *grp, const double *val, double eps, int *ord) {
+    for (int u = 0; u < n; u++) ord[u] = u;
+    node_cmp_val = val;
+    node_cmp_grp = grp;
+    qsort(ord, (size_t)n, sizeof(int), cmp_nodes);
+    int64_t *ng = (int64_t *)malloc(sizeof(int64_t) * (n > 0 ? n : 1));
+    int64_t g = -1;
+    double v0 = 0.0;
+    int64_t prev = -1;
+    for (int t = 0; t < n; t++) {
+        int u = ord[t];
+        if (t == 0 || grp[u] != prev || !(val[u] <= v0 * (1.0 + eps))) {
+            g++;
+            v0 = val[u];
+        }
+        prev = grp[u];
+        ng[u] = g;
+    }
+    for (int u = 0; u < n; u++) grp[u] = ng[u];
+    free(ng);
+}
+
+/* Eq. 3 for the node set given by in_set[]: every member's least link to
+   another member is at least its greatest link to a non-member. */
+static int eq3_holds(int n, const double *e, const unsigned char *in_set) {
+    for (int u = 0; u < n; u++) {
+        if (!in_set[u]) continue;
+        double in = INFINITY, out = -INFINITY;
+        for (int w = 0; w < n; w++) {
+            if (w == u) continue;
+            double x = e[(int64_t)u * n + w];
+            if (in_set[w]) { if (x < in) in = x; }
+            else if (x > out) out = x;
+        }
+        if (!(in >= out)) return 0;
+    }
+    return 1;
+}
+
+int tgo_build_islands(const int32_t *gpus, const double *c, const double *m, const double *bi,
+                      const double *host, int n, const double *e, double eps_c, double eps_m,
+                      double eps_i, int32_t *island_of, int32_t *n_islands, int32_t *isl_gpus,
+                      double *isl_peak, double *isl_hbm, double *isl_intra, double *isl_host,
+                      double *isl_e /* n*n, K*K used */) {
+    if (n < 1) return TGO_EINVAL;
+    if (!(eps_c >= 0.0) || !(eps_m >= 0.0) || !(eps_i >= 0.0) || !isfinite(eps_c) || !isfinite(eps_m) ||
+        !isfinite(eps_i))
+        return TGO_EINVAL;
+    for (int u = 0; u < n; u++) {
+        if (gpus[u] < 1 || !(c[u] > 0.0) || !(m[u] > 0.0) || !(bi[u] > 0.0) || !(host[u] >= 0.0) ||
+            !isfinite(c[u]) || !isfinite(m[u]) || !isfinite(bi[u]) || !isfinite(host[u]))
+            return TGO_EINVAL;
+        for (int v = 0; v < n; v++)
+            if (!(e[(int64_t)u * n + v] >= 0.0) || !isfinite(e[(int64_t)u * n + v])) return TGO_EINVAL;
+    }
+    int64_t *grp = (int64_t *)malloc(sizeof(int64_t) * n);
+    int *ord = (int *)malloc(sizeof(int) * n);
+    double *gd = (double *)malloc(sizeof(double) * n);
+    /* step (1): GPU count (exact), compute, memory; step (2): intra-node bandwidth */
+    for (int u = 0; u < n; u++) { grp[u] = 0; gd[u] = (double)gpus[u]; }
+    split_by(n, grp, gd, 0.0, ord);
+    split_by(n, grp, c, eps_c, ord);
+    split_by(n, grp, m, eps_m, ord);
+    split_by(n, grp, bi, eps_i, ord);
+    /* step (3): clusters start as single nodes; cl[u] = cluster (its smallest node) */
+    int *cl = (int *)malloc(sizeof(int) * n);
+    unsigned char *marked = (unsigned char *)calloc((size_t)n * n, 1); /* [a][b] by cluster ids */
+    unsigned char *in_set = (unsigned char *)calloc((size_t)n, 1);
+    for (int u = 0; u < n; u++) cl[u] = u;
+    /* members of each cluster, listed by cluster id: start[a], then members */
+    int *mstart = (int *)malloc(sizeof(int) * (n + 1));
+    int *mlist = (int *)malloc(sizeof(int) * n);
+    for (;;) {
+        int pos = 0;
+        for (int a = 0; a < n; a++) {
+            mstart[a] = pos;
+            for (int u = 0; u < n; u++) if (cl[u] == a) mlist[pos++] = u;
+        }
+        mstart[n] = pos;
+        double best = -INFINITY;
+        int ba = -1, bb = -1;
+        for (int a = 0; a < n; a++) {
+            if (cl[a] != a) continue; /* a is a cluster id */
+            for (int b = a + 1; b < n; b++) {
+                if (cl[b] != b || grp[a] != grp[b] || marked[(int64_t)a * n + b]) continue;
+                double l = INFINITY;
+                for (int p = mstart[a]; p < mstart[a + 1]; p++)
+                    for (int q = mstart[b]; q < mstart[b + 1]; q++) {
+                        int u = mlist[p], v = mlist[q];
+                        double x = e[(int64_t)u * n + v], y = e[(int64_t)v * n + u];
+                        double xy = x < y ? x : y;
+                        if (xy < l) l = xy;
+                    }
+                if (l > best) { best = l; ba = a; bb = b; }
+            }
+        }
+        if (ba < 0) break;
+        for (int u = 0; u < n; u++) in_set[u] = (cl[u] == ba || cl[u] == bb);
+        if (eq3_holds(n, e, in_set)) {
+            for (int u = 0; u < n; u++) if (cl[u] == bb) cl[u] = ba;
+            /* pairs involving the grown cluster are new pairs */
+            for (int x = 0; x < n; x++) {
+                marked[(int64_t)ba * n + x] = 0; marked[(int64_t)x * n + ba] = 0;
+            }
+        } else {
+            marked[(int64_t)ba * n + bb] = 1;
+        }
+    }
+    /* number islands by smallest node id (= cluster id) */
+    int K = 0;
+    int *isl_id = (int *)malloc(sizeof(int) * n);
+    for (int u = 0; u < n; u++) isl_id[u] = -1;
+    for (int u = 0; u < n; u++)
+        if (cl[u] == u) isl_id[u] = K++;
+    for (int u = 0; u < n; u++) island_of[u] = isl_id[cl[u]];
+    *n_islands = K;
+    for (int k = 0; k < K; k++) {
+        isl_gpus[k] = 0; isl_peak[k] = INFINITY; isl_hbm[k] = INFINITY; isl_intra[k] = INFINITY;
+        isl_host[k] = INFINITY;
+    }
+    for (int u = 0; u < n; u++) {
+        int k = island_of[u];
+        isl_gpus[k] += gpus[u];
+        if (c[u] < isl_peak[k]) isl_peak[k] = c[u];
+        if (m[u] < isl_hbm[k]) isl_hbm[k] = m[u];
+        if (bi[u] < isl_intra[k]) isl_intra[k] = bi[u];
+        if (host[u] < isl_host[k]) isl_host[k] = host[u];
+    }
+    for (int a = 0; a < K; a++)
+        for (int b = 0; b < K; b++) isl_e[a * K + b] = a == b ? 0.0 : INFINITY;
+    for (int u = 0; u < n; u++)
+        for (int v = 0; v < n; v++) {
+            int a = island_of[u], b = island_of[v];
+            if (a == b) continue;
+            double x = e[(int64_t)u * n + v];
+            if (x < isl_e[a * K + b]) isl_e[a * K + b] = x;
+        }
+    free(grp); free(ord); free(gd); free(cl); free(marked); free(in_set); free(isl_id); free(mstart); free(mlist);
+    return TGO_OK;
+}

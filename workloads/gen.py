@@ -165,6 +165,49 @@ def fabric_cluster(rng, n_islands, n_types, max_nodes, leaf=4, spine=16,
     return isl, E, leaf_of, spine_of
 
 
+def node_cluster(seed, n_nodes, n_types=5, leaf=8, pod=4, run=(4, 48), jitter=0.02,
+                 bw=(400e9, 100e9, 25e9), asym=0.0, eps=(0.1, 0.1, 0.1)):
+    """Node-level cluster for island construction (Sec. 4.1): nodes bought in
+    batches (contiguous runs of `run` nodes of one GPU type, 8 GPUs per node),
+    each node's measured compute and intra-node bandwidth within +-`jitter` of
+    its type's; a leaf/pod fabric of `leaf` nodes per leaf switch and `pod`
+    leaves per pod, bandwidth bw[0] inside a leaf, bw[1] inside a pod, bw[2]
+    across pods, each direction of each node pair scaled by 1 + asym U[-1, 1]
+    (links need not be symmetric; the default keeps each fabric level exact,
+    since Eq. 3 compares link speeds without tolerance).  eps = (compute,
+    memory, intra)."""
+    rng = np.random.default_rng(seed)
+    types = _draw_gpu_types(rng, n_types)
+    t_of = []
+    while len(t_of) < n_nodes:
+        t = int(rng.integers(0, n_types))
+        t_of += [t] * int(rng.integers(run[0], run[1] + 1))
+    t_of = t_of[:n_nodes]
+    nodes = {"gpus": [], "peak_flops": [], "hbm_bytes": [], "intra_bw": [], "host_bw": []}
+    for u in range(n_nodes):
+        peak, hbm, intra = types[t_of[u]]
+        nodes["gpus"].append(8)
+        nodes["peak_flops"].append(round(peak * (1.0 + jitter * float(rng.uniform(-1.0, 1.0))), -6))
+        nodes["hbm_bytes"].append(hbm)
+        nodes["intra_bw"].append(round(intra * (1.0 + jitter * float(rng.uniform(-1.0, 1.0))), -3))
+        nodes["host_bw"].append(host_link(hbm))
+    noise = rng.uniform(-1.0, 1.0, size=(n_nodes, n_nodes))
+    e = []
+    for u in range(n_nodes):
+        row = []
+        for v in range(n_nodes):
+            if u == v:
+                row.append(0.0)
+                continue
+            base = bw[0] if u // leaf == v // leaf else (bw[1] if u // (leaf * pod) == v // (leaf * pod) else bw[2])
+            row.append(round(base * (1.0 + asym * float(noise[u, v])), -3))
+        e.append(row)
+    return {"name": f"nodes{n_nodes}_s{seed}", "nodes": nodes, "node_bw": e,
+            "eps": {"compute": eps[0], "memory": eps[1], "intra": eps[2]},
+            "meta": {"seed": seed, "types": [list(t) for t in types], "type_of": t_of,
+                     "leaf": leaf, "pod": pod}}
+
+
 def _space(global_batch, tp, mb, ep=(1,), zero=(0, 1, 2, 3), n_experts=0, cp=(1,),
            recompute=(0,), offload=(0,)):
     return {"global_batch": int(global_batch), "n_experts": int(n_experts),
