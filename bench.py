@@ -19,6 +19,8 @@ before the timed region.  Prints one JSON line:
                clusters (fewer steps), after the main measurement; for those
                with at most 16 islands also the composition over every
                island order (tg_compose_pipeline_all_orders)
+  island_construction  tg_build_islands on node clusters of 1024 and 4096
+               nodes (the oracle beside it at 1024)
 --space extended adds context parallelism {1,2,4}, recomputation and
 offloading to the chosen workload's config space.
 """
@@ -73,6 +75,9 @@ def parse():
                     help="imbalance-pruning tolerance for every workload (0: off)")
     ap.add_argument("--other-steps", type=int, default=10,
                     help="timed plan searches per workload in the five-workload table (0 skips it)")
+    ap.add_argument("--island-nodes", type=int, nargs="*", default=[1024, 4096],
+                    help="time island construction (tg_build_islands) on generated node clusters of "
+                         "these sizes (none: skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, copy BYTES between two device buffers (a plain copy of "
                          "known size that scales profiler byte counters)")
@@ -209,6 +214,35 @@ def workload_row(run, steps):
             "all_orders_compose": run["all_orders"]}
 
 
+def island_construction(T, sizes, with_cpu):
+    """Island construction on generated node clusters (GPU types bought in
+    runs on a leaf/pod fabric): milliseconds per call (host arrays in and
+    out, so the node bandwidth matrix upload is inside), islands found, and
+    the oracle on the clusters of at most 1024 nodes."""
+    from workloads import node_cluster
+    out = []
+    for n in sizes:
+        cl = node_cluster(11, n)
+        ws = None
+        r = T.build_islands(cl)  # warm-up
+        times = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            r = T.build_islands(cl, workspace=ws)
+            times.append((time.perf_counter() - t0) * 1e3)
+        times.sort()
+        row = {"nodes": n, "islands": r["K"], "gpu_ms_median": times[1]}
+        if with_cpu and n <= 1024:
+            from oracle.oracle import build_islands
+            t0 = time.perf_counter()
+            o = build_islands(cl)
+            row["oracle_s"] = round(time.perf_counter() - t0, 3)
+            row["oracle_cores"] = 1
+            row["same_islands"] = o["island_of"] == r["island_of"]
+        out.append(row)
+    return out
+
+
 def score_source_digest():
     import hashlib
     h = hashlib.sha256()
@@ -323,6 +357,8 @@ def main():
         torch.cuda.empty_cache()
         out["workloads"] = five_workloads(torch, T, load_instance, args.space, args.other_steps,
                                           args.workload, main_row, args.imbalance_eps)
+    if args.island_nodes:
+        out["island_construction"] = island_construction(T, args.island_nodes, not args.no_cpu)
     if not args.no_cpu:
         cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
         out["cpu_baseline"] = cb

@@ -311,6 +311,41 @@ tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_s
                                          const double *d_cost, const uint8_t *d_dmax, tg_plan *out, void *d_ws,
                                          size_t ws_bytes, tg_stream stream);
 
+/*
+ * Island construction (Sec. 4.1): groups the nodes of a cluster into GPU
+ * islands that a homogeneous parallelizer accepts, the input of
+ * tg_problem_create.  nodes (host, n_nodes entries in [1, 4096]): one
+ * tg_island per node, its n_gpus the GPUs of the node and the other fields
+ * per GPU as for islands.  node_bw (host, n_nodes x n_nodes, row = source
+ * node, finite and >= 0; the diagonal is ignored): bytes/s between nodes.
+ * eps_compute, eps_memory, eps_intra (finite, >= 0): the tolerances of Eq. 1
+ * (compute, memory) and Eq. 2 (intra-node bandwidth).
+ *   An island holds nodes with the same GPU count whose compute, memory and
+ * intra-node bandwidth differ pairwise by at most a factor 1 + eps, and every
+ * member's links to the other members are at least as fast as its links to
+ * any node outside (Eq. 3).  Steps (1)-(2) split the nodes by GPU count, then
+ * compute, memory and intra-node bandwidth, each split a sweep over ascending
+ * values (ties by node index) that opens a new group at the first value
+ * above the group's smallest times (1 + eps), each operation one binary64
+ * rounding.  Step (3) runs agglomerative clustering inside each group: take
+ * the pair of clusters with the highest complete linkage (least bandwidth
+ * over their node pairs, each pair counted by its slower direction), ties to
+ * the least pair of smallest node indices; merge it if the union satisfies
+ * Eq. 3 against every node outside it, else set the pair aside until one of
+ * its clusters grows; stop when no pair is left.
+ *   Outputs (host): island_of[n_nodes] the island of each node, islands
+ * numbered by their smallest node index; islands[K] (capacity n_nodes) with
+ * n_gpus the sum over members and the other fields the least over members;
+ * inter_bw[K * K] (capacity n_nodes^2, row-major) the least node-to-node
+ * bandwidth from island a to island b, 0 on the diagonal; *n_islands = K.
+ * d_ws: at least tg_build_islands_workspace_bytes(n_nodes) device bytes
+ * (about 25 n_nodes^2).  Synchronises the stream.
+ */
+size_t tg_build_islands_workspace_bytes(int32_t n_nodes);
+tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double *node_bw, double eps_compute,
+                           double eps_memory, double eps_intra, int32_t *island_of, tg_island *islands,
+                           double *inter_bw, int32_t *n_islands, void *d_ws, size_t ws_bytes, tg_stream stream);
+
 /* Message of the calling thread's last failed call ("" if none). */
 const char *tg_last_error(void);
 

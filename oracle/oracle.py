@@ -209,6 +209,34 @@ class Oracle:
             raise OracleError(r, "balanced")
         return bool(r)
 
+    def slice_classes(self):
+        """Class of every slice (equal per-slice sums), numbered by first slice."""
+        cls = np.zeros(self.NS, dtype=np.int32)
+        n = ctypes.c_int64(0)
+        L_ = lib()
+        L_.tgo_slice_classes.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                                         ctypes.POINTER(ctypes.c_int64)]
+        st = L_.tgo_slice_classes(self.h, _ptr(cls, ctypes.c_int32), ctypes.byref(n))
+        if st != OK:
+            raise OracleError(st, "slice_classes")
+        return cls, n.value
+
+    def prune_classes(self):
+        """The surviving set computed with redundancy pruning (one staircase
+        per slice class, copied to the class's slices)."""
+        L_ = lib()
+        L_.tgo_prune_classes.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64), ctypes.c_int64,
+                                         ctypes.POINTER(ctypes.c_int64)]
+        n = ctypes.c_int64(0)
+        st = L_.tgo_prune_classes(self.h, None, 0, ctypes.byref(n))
+        if st not in (OK, ECAPACITY):
+            raise OracleError(st, "prune_classes")
+        out = np.zeros(max(n.value, 1), dtype=np.int64)
+        st = L_.tgo_prune_classes(self.h, _ptr(out, ctypes.c_int64), n.value, ctypes.byref(n))
+        if st != OK:
+            raise OracleError(st, "prune_classes")
+        return out[: n.value]
+
     def prune(self):
         n = ctypes.c_int64(0)
         lib().tgo_prune(self.h, None, 0, ctypes.byref(n))

@@ -592,6 +592,116 @@ int tgo_prune(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
 }
 
 /* ------------------------------------------------------------------------ */
+/* redundancy pruning (Sec. 5.1 (i))                                         */
+/* ------------------------------------------------------------------------ */
+/* Slices with the same composition are the same work: here two slices are
+   equivalent when all eight of their per-slice sums are equal, so every
+   config scores them alike (the score reads nothing else of the slice).
+   Classes are numbered in the order of their first slice. */
+static const int64_t *cls_sums = NULL;
+
+static int cmp_slice_sums(const void *a, const void *b) {
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    for (int q = 0; q < NSUM; q++) {
+        int64_t u = cls_sums[x * NSUM + q], v = cls_sums[y * NSUM + q];
+        if (u != v) return u < v ? -1 : 1;
+    }
+    return (x > y) - (x < y);
+}
+
+int tgo_slice_classes(void *h, int32_t *cls, int64_t *n_classes) {
+    oprob *p = (oprob *)h;
+    const int64_t NS = p->NS;
+    int64_t *ord = (int64_t *)malloc(sizeof(int64_t) * NS);
+    int64_t *first = (int64_t *)malloc(sizeof(int64_t) * NS);
+    for (int64_t s = 0; s < NS; s++) ord[s] = s;
+    cls_sums = p->slice_sum;
+    qsort(ord, (size_t)NS, sizeof(int64_t), cmp_slice_sums);
+    /* first[s] = the smallest slice with the same sums as s (runs of equal
+       sums are sorted by slice index, so a run's head is its smallest) */
+    int64_t head = 0;
+    for (int64_t t = 0; t < NS; t++) {
+        if (t == 0 ||
+            memcmp(&p->slice_sum[ord[t - 1] * NSUM], &p->slice_sum[ord[t] * NSUM], sizeof(int64_t) * NSUM) != 0)
+            head = ord[t];
+        first[ord[t]] = head;
+    }
+    int64_t nc = 0;
+    for (int64_t s = 0; s < NS; s++) {
+        if (first[s] == s) cls[s] = (int32_t)nc++;
+        else cls[s] = cls[first[s]];
+    }
+    *n_classes = nc;
+    free(ord);
+    free(first);
+    return TGO_OK;
+}
+
+/* The surviving set with redundancy pruning: each group's staircase is found
+   once per (island, b, slice class) at the class's first slice, scoring only
+   that slice, and copied to the other slices of the class.  Equal to
+   tgo_prune's set: a group's members score alike on equivalent slices and
+   their candidate indices keep the same order. */
+int tgo_prune_classes(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
+    oprob *p = (oprob *)h;
+    const int64_t NS = p->NS;
+    int32_t *cls = (int32_t *)malloc(sizeof(int32_t) * NS);
+    int64_t nc = 0;
+    tgo_slice_classes(h, cls, &nc);
+    int64_t *rep = (int64_t *)malloc(sizeof(int64_t) * (nc > 0 ? nc : 1));
+    for (int64_t s = NS - 1; s >= 0; s--) rep[cls[s]] = s; /* first slice of each class */
+    ivec surv = {0, 0, 0};
+    int64_t maxc = 0;
+    for (int k = 0; k < p->K; k++)
+        if (p->cfg_off[k + 1] - p->cfg_off[k] > maxc) maxc = p->cfg_off[k + 1] - p->cfg_off[k];
+    omember *mem = (omember *)malloc(sizeof(omember) * (maxc > 0 ? maxc : 1));
+    ocoef *coef = (ocoef *)malloc(sizeof(ocoef) * (maxc > 0 ? maxc : 1));
+    int64_t *members = (int64_t *)malloc(sizeof(int64_t) * (maxc > 0 ? maxc : 1));
+    /* kept[c * maxc + a] = member a survives on class c */
+    unsigned char *kept = (unsigned char *)malloc((size_t)(nc > 0 ? nc : 1) * (size_t)(maxc > 0 ? maxc : 1));
+    for (int k = 0; k < p->K; k++) {
+        int64_t c0 = p->cfg_off[k], nc0 = p->cfg_off[k + 1] - c0;
+        for (int64_t c = 0; c < nc0; c++) config_coef(p, &p->cfg[c0 + c], &coef[c]);
+        for (int bi = 0; bi < p->nb; bi++) {
+            int64_t b = p->bvals[bi];
+            int64_t nm = 0;
+            for (int64_t c = 0; c < nc0; c++)
+                if (p->cfg[c0 + c].b == b) members[nm++] = c;
+            if (nm == 0) continue;
+            for (int64_t q = 0; q < nc; q++) {
+                int64_t s = rep[q];
+                for (int64_t a = 0; a < nm; a++) kept[q * maxc + a] = 0;
+                if (!balanced(p, s, k)) continue;
+                for (int64_t a = 0; a < nm; a++) {
+                    omember *m = &mem[a];
+                    score_candidate(p, &coef[members[a]], &p->slice_sum[s * NSUM], &m->cost, &m->dmax, NULL, NULL);
+                    m->idx = a; /* member order = candidate index order on every slice */
+                }
+                qsort(mem, (size_t)nm, sizeof(omember), cmp_key);
+                int run = 0;
+                for (int64_t a = 0; a < nm; a++)
+                    if (mem[a].dmax > run) { kept[q * maxc + mem[a].idx] = 1; run = mem[a].dmax; }
+            }
+            for (int64_t s = 0; s < NS; s++)
+                for (int64_t a = 0; a < nm; a++)
+                    if (kept[(int64_t)cls[s] * maxc + a] &&
+                        ivec_push(&surv, (c0 + members[a]) * NS + s) != TGO_OK) {
+                        free(mem); free(coef); free(members); free(kept); free(cls); free(rep); free(surv.v);
+                        return TGO_ENOMEM;
+                    }
+        }
+    }
+    free(mem); free(coef); free(members); free(kept); free(cls); free(rep);
+    qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64);
+    *n_out = surv.n;
+    int rc = TGO_OK;
+    if (surv.n > cap) rc = TGO_ECAPACITY;
+    else if (out) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
+    free(surv.v);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
 /* composition (Sec. 5.2)                                                    */
 /* ------------------------------------------------------------------------ */
 /* An entry is one usable candidate of the list handed to composition. */

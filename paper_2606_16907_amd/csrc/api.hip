@@ -536,6 +536,37 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
     return compose_end(res_dev, out, s);
 }
 
+size_t tg_build_islands_workspace_bytes(int32_t n_nodes) {
+    if (n_nodes < 1 || n_nodes > 4096) return 0;
+    return tg::islands_ws_bytes(n_nodes);
+}
+
+tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double *node_bw, double eps_compute,
+                           double eps_memory, double eps_intra, int32_t *island_of, tg_island *islands,
+                           double *inter_bw, int32_t *n_islands, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    if (!nodes || !node_bw || !island_of || !islands || !inter_bw || !n_islands)
+        return fail(TG_EINVAL, "NULL argument");
+    if (n_nodes < 1 || n_nodes > 4096) return fail(TG_EINVAL, "n_nodes %d outside [1, 4096]", n_nodes);
+    for (double x : {eps_compute, eps_memory, eps_intra})
+        if (!(x >= 0.0) || !std::isfinite(x)) return fail(TG_EINVAL, "tolerance invalid");
+    for (int u = 0; u < n_nodes; ++u) {
+        const tg_island &v = nodes[u];
+        if (v.n_gpus < 1 || v.n_gpus > 65536 || v.reserved != 0) return fail(TG_EINVAL, "node %d GPU count", u);
+        if (!(v.peak_flops > 0.0) || !std::isfinite(v.peak_flops) || !(v.hbm_bytes > 0.0) ||
+            !std::isfinite(v.hbm_bytes) || !(v.intra_bw > 0.0) || !std::isfinite(v.intra_bw) ||
+            !(v.host_bw >= 0.0) || !std::isfinite(v.host_bw))
+            return fail(TG_EINVAL, "node %d specs", u);
+    }
+    for (int64_t t = 0; t < (int64_t)n_nodes * n_nodes; ++t)
+        if (!(node_bw[t] >= 0.0) || !std::isfinite(node_bw[t])) return fail(TG_EINVAL, "node_bw[%lld]", (long long)t);
+    const size_t need = tg::islands_ws_bytes(n_nodes);
+    if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    hipError_t e = tg::launch_build_islands(n_nodes, nodes, node_bw, eps_compute, eps_memory, eps_intra, d_ws,
+                                            (hipStream_t)stream, island_of, islands, inter_bw, n_islands);
+    if (e != hipSuccess) return hip_fail(e, "island construction kernels");
+    return TG_OK;
+}
+
 tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
                                          const double *d_cost, const uint8_t *d_dmax, tg_plan *out, void *d_ws,
                                          size_t ws_bytes, tg_stream stream) {

@@ -81,7 +81,8 @@ EXPORTS = ("tg_problem_create", "tg_problem_destroy", "tg_problem_info", "tg_pro
            "tg_enumerate_pairs", "tg_score_pairs", "tg_prune_workspace_bytes", "tg_prune",
            "tg_compose_workspace_bytes", "tg_compose_pipeline", "tg_compose_relaxed_workspace_bytes",
            "tg_compose_pipeline_relaxed", "tg_compose_all_orders_workspace_bytes",
-           "tg_compose_pipeline_all_orders", "tg_last_error")
+           "tg_compose_pipeline_all_orders", "tg_build_islands_workspace_bytes", "tg_build_islands",
+           "tg_last_error")
 
 _lib = None
 
@@ -117,6 +118,10 @@ def load_library(path=LIB_PATH):
     L.tg_compose_all_orders_workspace_bytes.argtypes = [vp, i64]
     L.tg_compose_all_orders_workspace_bytes.restype = sz
     L.tg_compose_pipeline_all_orders.argtypes = [vp, vp, i64, vp, vp, P(TgPlan), vp, sz, vp]
+    L.tg_build_islands_workspace_bytes.argtypes = [i32]
+    L.tg_build_islands_workspace_bytes.restype = sz
+    L.tg_build_islands.argtypes = [P(TgIsland), i32, P(ctypes.c_double), ctypes.c_double, ctypes.c_double,
+                                   ctypes.c_double, P(i32), P(TgIsland), P(ctypes.c_double), P(i32), vp, sz, vp]
     L.tg_last_error.argtypes = []
     L.tg_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -335,3 +340,43 @@ def plan_to_dict(plan):
         stages.append({f: getattr(s, f) for f, _ in TgStage._fields_ if f != "reserved"})
     return {"b": plan.b, "m": plan.m, "S": plan.S, "P": plan.P, "F": plan.F, "T": plan.T,
             "stages": stages}
+
+
+def build_islands(cluster, workspace=None):
+    """Island construction (Sec. 4.1) of a node-level cluster (dict with
+    "nodes": gpus, peak_flops, hbm_bytes, intra_bw, host_bw per node;
+    "node_bw": n x n bytes/s; "eps": compute, memory, intra).  Returns
+    island_of, K, islands (tg_island fields) and inter_bw (K x K)."""
+    lib = load_library()
+    nd = cluster["nodes"]
+    n = len(nd["gpus"])
+    nodes = (TgIsland * n)()
+    for u in range(n):
+        nodes[u].n_gpus = int(nd["gpus"][u])
+        nodes[u].peak_flops = float(nd["peak_flops"][u])
+        nodes[u].hbm_bytes = float(nd["hbm_bytes"][u])
+        nodes[u].intra_bw = float(nd["intra_bw"][u])
+        nodes[u].host_bw = float(nd["host_bw"][u])
+    import numpy as np
+    e_arr = np.ascontiguousarray(np.asarray(cluster["node_bw"], dtype=np.float64).reshape(n * n))
+    e = e_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    ws = workspace
+    if ws is None:
+        ws = torch.empty(max(int(lib.tg_build_islands_workspace_bytes(n)), 1), dtype=torch.uint8, device="cuda")
+    isl_of = (ctypes.c_int32 * n)()
+    isl = (TgIsland * n)()
+    inter_arr = np.zeros(n * n, dtype=np.float64)
+    inter = inter_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    K = ctypes.c_int32(0)
+    eps = cluster["eps"]
+    st = lib.tg_build_islands(nodes, n, e, float(eps["compute"]), float(eps["memory"]), float(eps["intra"]),
+                              isl_of, isl, inter, ctypes.byref(K), _dptr(ws), ws.numel(), _stream())
+    _check(st, "tg_build_islands")
+    k = K.value
+    return {"island_of": list(isl_of), "K": k,
+            "islands": {"n_gpus": [isl[a].n_gpus for a in range(k)],
+                        "peak_flops": [isl[a].peak_flops for a in range(k)],
+                        "hbm_bytes": [isl[a].hbm_bytes for a in range(k)],
+                        "intra_bw": [isl[a].intra_bw for a in range(k)],
+                        "host_bw": [isl[a].host_bw for a in range(k)]},
+            "inter_bw": inter_arr[:k * k].reshape(k, k).tolist()}

@@ -1,0 +1,108 @@
+"""Parity of the HIP island construction (tg_build_islands, through the C ABI)
+with the CPU oracle's: the island of every node, the island count, the
+island attributes and the island-to-island bandwidth, bit for bit.  Cases:
+generated node clusters from 8 to 1024 nodes (GPU types bought in runs on a
+leaf/pod fabric, some with direction-dependent links), the hand-built
+fabrics of the oracle's pins, one node, and the 4096-node limit against the
+oracle's stored digests; inputs outside the limits are rejected."""
+import hashlib
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from oracle.oracle import build_islands as oracle_islands  # noqa: E402
+from workloads import node_cluster  # noqa: E402
+from tests.test_oracle_islands import cluster, fabric  # noqa: E402
+from tests.golden.make_islands_golden import CASE, PATH, digests  # noqa: E402
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2606_16907_amd import tangram as T  # noqa: E402
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def same(g, o):
+    assert g["K"] == o["K"]
+    assert g["island_of"] == o["island_of"]
+    for f in ("n_gpus", "peak_flops", "hbm_bytes", "intra_bw", "host_bw"):
+        assert g["islands"][f] == o["islands"][f], f
+    assert np.array_equal(np.array(g["inter_bw"]).view(np.uint64), np.array(o["inter_bw"]).view(np.uint64))
+
+
+GEN = ([(f"n{n}_s{s}", lambda n=n, s=s: node_cluster(s, n, n_types=4, leaf=4, pod=2, run=(2, 12),
+                                                     asym=0.01 if s % 3 == 2 else 0.0))
+        for n in (8, 24, 63, 130) for s in range(3)]
+       + [(f"fabric{n}_s{s}", lambda n=n, s=s: node_cluster(s, n)) for n in (256, 1024) for s in (1, 2)])
+
+PEAKS_INTERLEAVED = [100e12 if u % 4 < 2 else 200e12 for u in range(8)]
+HAND = [("homogeneous", lambda: cluster([8] * 16, [300e12] * 16, fabric(16, 4, 2))),
+        ("tolerance", lambda: cluster([8] * 4, [100e12, 112e12, 105e12, 120e12], fabric(4, 4, 1))),
+        ("gpu_counts", lambda: cluster([8, 4, 8, 4], [100e12] * 4, fabric(4, 4, 1))),
+        ("interleaved", lambda: cluster([8] * 8, PEAKS_INTERLEAVED, fabric(8, 4, 2))),
+        ("merge_order", lambda: cluster([8] * 4, [100e12, 100e12, 100e12, 400e12],
+                                        [[0, 400e9, 100e9, 300e9], [400e9, 0, 400e9, 50e9],
+                                         [100e9, 450e9, 0, 50e9], [300e9, 50e9, 50e9, 0]])),
+        ("one_node", lambda: cluster([8], [100e12], [[0.0]]))]
+
+
+@pytest.mark.parametrize("name,make", GEN + HAND, ids=[n for n, _ in GEN + HAND])
+def test_islands_parity(name, make):
+    cl = make()
+    say("case", name, len(cl["nodes"]["gpus"]), "nodes")
+    o = oracle_islands(cl)
+    g = T.build_islands(cl)
+    same(g, o)
+
+
+def test_islands_at_the_node_limit_against_stored():
+    import json
+    with open(PATH) as fh:
+        want = json.load(fh)
+    cl = node_cluster(CASE["seed"], CASE["n_nodes"])
+    say("case", CASE)
+    g = T.build_islands(cl)
+    assert g["K"] == want["K"]
+    assert digests(g) == (want["island_of_sha256"], want["inter_bw_sha256"])
+    for f in ("n_gpus", "peak_flops", "hbm_bytes", "intra_bw", "host_bw"):
+        assert g["islands"][f] == want["islands"][f], f
+
+
+def test_islands_then_plan_search():
+    # the islands of a node cluster are a problem the plan search takes
+    from workloads import make_instance
+    cl = node_cluster(5, 64)
+    r = T.build_islands(cl)
+    inst = make_instance("dense8b")
+    inst["islands"] = r["islands"]
+    inst["inter_bw"] = r["inter_bw"]
+    inst["island_order"] = list(range(r["K"]))
+    p = T.Problem(inst)
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax)
+    assert st == 0 and plan["S"] >= 1
+
+
+@pytest.mark.parametrize("bad", ["too_many", "eps", "bw"])
+def test_islands_invalid_rejected(bad):
+    cl = cluster([8, 8], [1e14, 1e14], [[0, 1e11], [1e11, 0]])
+    if bad == "too_many":
+        assert T.load_library().tg_build_islands_workspace_bytes(4097) == 0
+        return
+    if bad == "eps":
+        cl["eps"]["memory"] = float("inf")
+    else:
+        cl["node_bw"][1][0] = -1.0
+    with pytest.raises(T.TangramError) as e:
+        T.build_islands(cl, workspace=torch.empty(1 << 20, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == T.TG_EINVAL

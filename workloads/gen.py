@@ -192,16 +192,12 @@ def node_cluster(seed, n_nodes, n_types=5, leaf=8, pod=4, run=(4, 48), jitter=0.
         nodes["intra_bw"].append(round(intra * (1.0 + jitter * float(rng.uniform(-1.0, 1.0))), -3))
         nodes["host_bw"].append(host_link(hbm))
     noise = rng.uniform(-1.0, 1.0, size=(n_nodes, n_nodes))
-    e = []
-    for u in range(n_nodes):
-        row = []
-        for v in range(n_nodes):
-            if u == v:
-                row.append(0.0)
-                continue
-            base = bw[0] if u // leaf == v // leaf else (bw[1] if u // (leaf * pod) == v // (leaf * pod) else bw[2])
-            row.append(round(base * (1.0 + asym * float(noise[u, v])), -3))
-        e.append(row)
+    u = np.arange(n_nodes)
+    same_leaf = (u[:, None] // leaf) == (u[None, :] // leaf)
+    same_pod = (u[:, None] // (leaf * pod)) == (u[None, :] // (leaf * pod))
+    base = np.where(same_leaf, bw[0], np.where(same_pod, bw[1], bw[2]))
+    e = np.round(base * (1.0 + asym * noise), -3)
+    np.fill_diagonal(e, 0.0)
     return {"name": f"nodes{n_nodes}_s{seed}", "nodes": nodes, "node_bw": e,
             "eps": {"compute": eps[0], "memory": eps[1], "intra": eps[2]},
             "meta": {"seed": seed, "types": [list(t) for t in types], "type_of": t_of,
