@@ -151,6 +151,7 @@ typedef struct {
     int64_t n_configs;  /* intra-island configs summed over islands */
     int64_t N;          /* candidates = NS * n_configs */
     int64_t n_compatible_configs;
+    int64_t n_slice_classes; /* NC: classes of slices with equal per-slice sums (redundancy pruning) */
 } tg_info;
 
 typedef struct tg_problem tg_problem;
@@ -244,6 +245,33 @@ tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, doub
 size_t tg_prune_workspace_bytes(const tg_problem *p);
 tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
                    int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream);
+
+/*
+ * Redundancy pruning (Sec. 5.1 (i): slices of the same composition are one
+ * query).  Two slices are equivalent when all eight of their per-slice sums
+ * (the tg_layer fields summed over the slice) are equal; every config scores
+ * them alike.  Classes c = 0..NC-1 are numbered by their first slice (the
+ * slice order of tg_score_pairs).  A class candidate is idx_c = (cfg_off[k] +
+ * c_cfg) * NC + c, config-major like the candidate index.
+ *   tg_score_classes: as tg_score_pairs over class candidates [first, first +
+ * count) of [0, n_configs * NC): the score of each class's first slice.
+ *   tg_prune_classes: the surviving set from class scores (d_cost, d_dmax over
+ * all n_configs * NC class candidates), found once per (island, b, class) and
+ * copied to the class's slices: writes exactly tg_prune's survivor list (full
+ * candidate indices, ascending) under tg_prune's capacity rules.  d_ws: at
+ * least tg_prune_classes_workspace_bytes(p) bytes.  Synchronises once.
+ *   tg_compose_pipeline_classes: tg_compose_pipeline with class scores: the
+ * list is tg_prune_classes' (or tg_prune's) output, d_cost / d_dmax are
+ * tg_score_classes' arrays; same plan, workspace and errors.
+ */
+tg_status tg_score_classes(const tg_problem *p, int64_t first, int64_t count, double *d_cost, uint8_t *d_dmax,
+                           tg_stream stream);
+size_t tg_prune_classes_workspace_bytes(const tg_problem *p);
+tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                           int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream);
+tg_status tg_compose_pipeline_classes(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                      const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                                      tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream);
 
 /*
  * Composition (Sec. 5.2): builds the pipeline from the candidates listed in

@@ -238,6 +238,41 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
             jlo[(size_t)k * L + i] = j;
         }
 
+    // redundancy pruning: slices with equal per-slice sums form a class,
+    // classes numbered by their first slice
+    std::vector<uint32_t> cls(NS), cls_ij;
+    {
+        auto sums = [&](int64_t s, int q) {
+            const uint32_t ij = sij[s];
+            return pre[(size_t)q * Lp + (ij >> 16)] - pre[(size_t)q * Lp + (ij & 0xFFFFu)];
+        };
+        std::vector<int64_t> ord(NS);
+        for (int64_t s = 0; s < NS; ++s) ord[s] = s;
+        std::sort(ord.begin(), ord.end(), [&](int64_t x, int64_t y) {
+            for (int q = 0; q < 8; ++q) {
+                const int64_t u = sums(x, q), v = sums(y, q);
+                if (u != v) return u < v;
+            }
+            return x < y;
+        });
+        std::vector<int64_t> first(NS);
+        int64_t head = 0;
+        for (int64_t t = 0; t < NS; ++t) {
+            bool same = t > 0;
+            for (int q = 0; same && q < 8; ++q) same = sums(ord[t - 1], q) == sums(ord[t], q);
+            if (!same) head = ord[t];
+            first[ord[t]] = head;
+        }
+        for (int64_t s = 0; s < NS; ++s) {
+            if (first[s] == s) {
+                cls[s] = (uint32_t)cls_ij.size();
+                cls_ij.push_back(sij[s]);
+            } else {
+                cls[s] = cls[first[s]];
+            }
+        }
+    }
+
     // one device block for all tables
     struct Part {
         const void *src;
@@ -271,6 +306,8 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         {host.data(), (size_t)K * 8, 0},
         {cap.data(), (size_t)K * 8, 0},
         {jlo.data(), jlo.size() * 4, 0},
+        {cls.data(), cls.size() * 4, 0},
+        {cls_ij.data(), cls_ij.size() * 4, 0},
     };
     size_t total = 0;
     for (auto &p : parts) {
@@ -339,6 +376,10 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.cap = (const double *)(base + parts[17].off);
     P.jlo = imb ? (const int32_t *)(base + parts[18].off) : nullptr;
     P.jlo_pos = nullptr;
+    P.NC = (int64_t)cls_ij.size();
+    P.cls = (const uint32_t *)(base + parts[19].off);
+    P.cls_ij = (const uint32_t *)(base + parts[20].off);
+    P.class_scores = 0;
     pr->bvals = bv;
     pr->n_compat_cfg = (int64_t)row_cfg.size();
     pr->B = space->global_batch;
@@ -376,6 +417,7 @@ tg_status tg_problem_info(const tg_problem *p, tg_info *out) {
     out->n_configs = p->P.ncfg;
     out->N = p->P.N;
     out->n_compatible_configs = p->n_compat_cfg;
+    out->n_slice_classes = p->P.NC;
     return TG_OK;
 }
 
@@ -411,6 +453,20 @@ tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, doub
 
 size_t tg_prune_workspace_bytes(const tg_problem *p) { return p ? tg::prune_ws_bytes(p->P) : 0; }
 
+tg_status tg_score_classes(const tg_problem *p, int64_t first, int64_t count, double *d_cost, uint8_t *d_dmax,
+                           tg_stream stream) {
+    if (!p) return fail(TG_EINVAL, "NULL problem");
+    const tg::DevProblem C = tg::class_view(p->P);
+    if (first < 0 || count < 0 || first > C.N || count > C.N - first)
+        return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
+                    (long long)C.N);
+    if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
+    hipError_t e = tg::launch_score(C, first, count, d_cost, d_dmax, (hipStream_t)stream);
+    return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
+}
+
+size_t tg_prune_classes_workspace_bytes(const tg_problem *p) { return p ? tg::prune_classes_ws_bytes(p->P) : 0; }
+
 tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
                    int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream) {
     if (!p || !n_survivors) return fail(TG_EINVAL, "NULL argument");
@@ -421,6 +477,27 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
+    if (e != hipSuccess) return hip_fail(e, "prune kernels");
+    int64_t total = 0;
+    e = hipMemcpyAsync(&total, d_total, sizeof(total), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "prune count");
+    *n_survivors = total;
+    if (total > capacity)
+        return fail(TG_ECAPACITY, "%lld survivors exceed capacity %lld", (long long)total, (long long)capacity);
+    return TG_OK;
+}
+
+tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                           int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    if (!p || !n_survivors) return fail(TG_EINVAL, "NULL argument");
+    if (!d_cost || !d_dmax) return fail(TG_EINVAL, "NULL score arrays");
+    if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
+    const size_t need = tg::prune_classes_ws_bytes(p->P);
+    if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    int64_t *d_total = nullptr;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = tg::launch_prune_classes(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
     if (e != hipSuccess) return hip_fail(e, "prune kernels");
     int64_t total = 0;
     e = hipMemcpyAsync(&total, d_total, sizeof(total), hipMemcpyDeviceToHost, s);
@@ -514,6 +591,23 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
     if (st != TG_OK) return st;
     tg::ComposeResult *res_dev = nullptr;
     hipError_t e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
+    if (e != hipSuccess) return hip_fail(e, "compose kernels");
+    return compose_end(res_dev, out, s);
+}
+
+tg_status tg_compose_pipeline_classes(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
+                                      const double *d_cost, const uint8_t *d_dmax, const int32_t *island_order,
+                                      tg_plan *out, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (!island_order) return fail(TG_EINVAL, "NULL argument");
+    const size_t need = p && n_survivors >= 0 ? tg::compose_ws_bytes(p->P, n_survivors) : 0;
+    tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
+                                 need, s);
+    if (st != TG_OK) return st;
+    tg::DevProblem P = p->P;
+    P.class_scores = 1;
+    tg::ComposeResult *res_dev = nullptr;
+    hipError_t e = tg::launch_compose(P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
     if (e != hipSuccess) return hip_fail(e, "compose kernels");
     return compose_end(res_dev, out, s);
 }

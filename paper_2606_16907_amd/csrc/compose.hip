@@ -259,10 +259,13 @@ __global__ __launch_bounds__(256) void gather_kernel(DevProblem P, const int64_t
             if (c.b_idx < 0 || !slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), c.k)) {
                 atomicOr(&res->err, 2);
             } else {
-                const uint8_t d = dmax[idx];
+                // scores by candidate, or by class candidate (equal on every
+                // slice of the class)
+                const int64_t si = P.class_scores ? g * P.NC + P.cls[s] : idx;
+                const uint8_t d = dmax[si];
                 if (d > 0) {
                     G = (int32_t)group_id(P, pos[c.k], c.b_idx, s);
-                    rec_c[r] = cost[idx];
+                    rec_c[r] = cost[si];
                     rec_d[r] = d;
                     atomicAdd(&gcnt[G], 1);
                 }

@@ -19,6 +19,8 @@
 // whole 64-bit words of a bitmap with one row per compatible config.
 // Compaction: popcount per tile, scan of tile counts, then each thread writes
 // the candidate indices of its words' set bits in ascending order.
+#include <algorithm>
+
 #include "tg_device.h"
 
 namespace tg {
@@ -171,6 +173,25 @@ __global__ __launch_bounds__(kCountThreads) void emit_kernel(DevProblem P, const
     }
 }
 
+// Redundancy pruning: bit s of a row of the slice bitmap is bit cls[s] of
+// the same row of the class bitmap (a class's staircase holds on every slice
+// of the class).
+__global__ __launch_bounds__(256) void expand_kernel(DevProblem P, const uint64_t *__restrict__ cbits,
+                                                     int32_t cwords, uint64_t *bits, int64_t n_words) {
+    const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= n_words) return;
+    const int64_t row = w / P.words, sw = w - row * P.words;
+    const uint64_t *crow = cbits + row * cwords;
+    uint64_t out = 0;
+    for (int b = 0; b < kWave; ++b) {
+        const int64_t s = sw * kWave + b;
+        if (s >= P.NS) break;
+        const uint32_t c = P.cls[s];
+        out |= ((crow[c >> 6] >> (c & 63)) & 1ull) << b;
+    }
+    bits[w] = out;
+}
+
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static int64_t bitmap_words(const DevProblem &P) { return (int64_t)P.n_rows * P.words; }
@@ -182,8 +203,21 @@ size_t prune_ws_bytes(const DevProblem &P) {
            align256(sizeof(int64_t));
 }
 
-hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
-                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out) {
+static hipError_t launch_frontier(const DevProblem &P, const double *cost, const uint8_t *dmax, uint64_t *bitmap,
+                                  hipStream_t s) {
+    const int64_t n_front = (int64_t)P.n_kb * P.words;
+    if (n_front > 0) {
+        const int64_t blocks = (n_front + kFrontWaves - 1) / kFrontWaves;
+        const size_t lds = sizeof(uint64_t) * (size_t)kFrontWaves * (size_t)P.max_members;
+        frontier_kernel<<<dim3((unsigned)blocks), dim3(kFrontWaves * kWave), lds, s>>>(P, cost, dmax, bitmap,
+                                                                                       n_front);
+    }
+    return hipGetLastError();
+}
+
+// Survivor bitmap (at the start of ws) -> ascending candidate indices.
+static hipError_t launch_compact(const DevProblem &P, int64_t *surv, int64_t capacity, void *ws, hipStream_t s,
+                                 int64_t **d_total_out) {
     const int64_t nw = bitmap_words(P);
     const int64_t nt = (nw + kTileWords - 1) / kTileWords;
     char *p = (char *)ws;
@@ -193,23 +227,38 @@ hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *
     p += align256(sizeof(int64_t) * (size_t)(nt + 1));
     int64_t *total = (int64_t *)p;
     *d_total_out = total;
-    const int64_t n_front = (int64_t)P.n_kb * P.words;
-    if (n_front > 0) {
-        const int64_t blocks = (n_front + kFrontWaves - 1) / kFrontWaves;
-        const size_t lds = sizeof(uint64_t) * (size_t)kFrontWaves * (size_t)P.max_members;
-        frontier_kernel<<<dim3((unsigned)blocks), dim3(kFrontWaves * kWave), lds, s>>>(P, cost, dmax, bitmap,
-                                                                                       n_front);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (nt > 0) {
-        count_kernel<<<dim3((unsigned)nt), dim3(kCountThreads), 0, s>>>(bitmap, nw, tiles);
-    }
+    if (nt > 0) count_kernel<<<dim3((unsigned)nt), dim3(kCountThreads), 0, s>>>(bitmap, nw, tiles);
     scan_small_i64<<<dim3(1), dim3(1024), 0, s>>>(tiles, nt, total);
-    if (nt > 0) {
+    if (nt > 0)
         emit_kernel<<<dim3((unsigned)nt), dim3(kCountThreads), 0, s>>>(P, bitmap, nw, tiles, surv, capacity);
-    }
     return hipGetLastError();
+}
+
+hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
+                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out) {
+    hipError_t e = launch_frontier(P, cost, dmax, (uint64_t *)ws, s);
+    if (e != hipSuccess) return e;
+    return launch_compact(P, surv, capacity, ws, s, d_total_out);
+}
+
+// Class bitmap after the slice-level workspace of launch_prune.
+size_t prune_classes_ws_bytes(const DevProblem &P) {
+    const DevProblem C = class_view(P);
+    return prune_ws_bytes(P) + align256(sizeof(uint64_t) * (size_t)std::max<int64_t>(1, bitmap_words(C)));
+}
+
+hipError_t launch_prune_classes(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
+                                int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out) {
+    const DevProblem C = class_view(P);
+    uint64_t *cbits = (uint64_t *)((char *)ws + prune_ws_bytes(P));
+    hipError_t e = launch_frontier(C, cost, dmax, cbits, s);
+    if (e != hipSuccess) return e;
+    const int64_t nw = bitmap_words(P);
+    if (nw > 0)
+        expand_kernel<<<dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s>>>(P, cbits, C.words, (uint64_t *)ws, nw);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_compact(P, surv, capacity, ws, s, d_total_out);
 }
 
 }  // namespace tg

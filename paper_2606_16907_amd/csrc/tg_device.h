@@ -62,7 +62,23 @@ struct DevProblem {
     const double *cap;       // [K] island's share of the cluster's compute
     const int32_t *jlo;      // [K][L] first balanced cut j of slices starting at i (L + 1: none)
     const int32_t *jlo_pos;  // the same by island position of one composition call, or null
+    int64_t NC;              // slice classes (equal per-slice sums)
+    const uint32_t *cls;     // [NS] class of each slice
+    const uint32_t *cls_ij;  // [NC] first slice of each class, i | j << 16
+    int32_t class_scores;    // composition reads scores by class candidate (g * NC + cls[s])
+    int32_t pad2_;
 };
+
+// The problem seen through its slice classes: class c stands for its first
+// slice, so the score and frontier kernels run unchanged on NC "slices".
+inline DevProblem class_view(const DevProblem &P) {
+    DevProblem C = P;
+    C.NS = P.NC;
+    C.sij = P.cls_ij;
+    C.N = P.ncfg * P.NC;
+    C.words = (int32_t)((P.NC + 63) / 64);
+    return C;
+}
 
 // Imbalance pruning: the slice's share of the model's FLOPs against the
 // island's share of the cluster's compute, within a factor imb_r either way.
@@ -130,6 +146,9 @@ hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, doubl
 hipError_t launch_enumerate(const DevProblem &P, int64_t first, int64_t count, tg_pair *out, hipStream_t s);
 
 size_t prune_ws_bytes(const DevProblem &P);
+size_t prune_classes_ws_bytes(const DevProblem &P);
+hipError_t launch_prune_classes(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
+                                int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
 hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
                         int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
 

@@ -68,7 +68,8 @@ class TgPlan(ctypes.Structure):
 class TgInfo(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int32), ("K", ctypes.c_int32), ("n_b", ctypes.c_int32),
                 ("dense", ctypes.c_int32), ("NS", ctypes.c_int64), ("n_configs", ctypes.c_int64),
-                ("N", ctypes.c_int64), ("n_compatible_configs", ctypes.c_int64)]
+                ("N", ctypes.c_int64), ("n_compatible_configs", ctypes.c_int64),
+                ("n_slice_classes", ctypes.c_int64)]
 
 
 class TangramError(RuntimeError):
@@ -82,6 +83,8 @@ EXPORTS = ("tg_problem_create", "tg_problem_destroy", "tg_problem_info", "tg_pro
            "tg_compose_workspace_bytes", "tg_compose_pipeline", "tg_compose_relaxed_workspace_bytes",
            "tg_compose_pipeline_relaxed", "tg_compose_all_orders_workspace_bytes",
            "tg_compose_pipeline_all_orders", "tg_build_islands_workspace_bytes", "tg_build_islands",
+           "tg_score_classes", "tg_prune_classes_workspace_bytes", "tg_prune_classes",
+           "tg_compose_pipeline_classes",
            "tg_last_error")
 
 _lib = None
@@ -118,6 +121,11 @@ def load_library(path=LIB_PATH):
     L.tg_compose_all_orders_workspace_bytes.argtypes = [vp, i64]
     L.tg_compose_all_orders_workspace_bytes.restype = sz
     L.tg_compose_pipeline_all_orders.argtypes = [vp, vp, i64, vp, vp, P(TgPlan), vp, sz, vp]
+    L.tg_score_classes.argtypes = [vp, i64, i64, vp, vp, vp]
+    L.tg_prune_classes_workspace_bytes.argtypes = [vp]
+    L.tg_prune_classes_workspace_bytes.restype = sz
+    L.tg_prune_classes.argtypes = [vp, vp, vp, vp, i64, P(i64), vp, sz, vp]
+    L.tg_compose_pipeline_classes.argtypes = [vp, vp, i64, vp, vp, P(i32), P(TgPlan), vp, sz, vp]
     L.tg_build_islands_workspace_bytes.argtypes = [i32]
     L.tg_build_islands_workspace_bytes.restype = sz
     L.tg_build_islands.argtypes = [P(TgIsland), i32, P(ctypes.c_double), ctypes.c_double, ctypes.c_double,
@@ -200,6 +208,7 @@ class Problem:
         self.L, self.K, self.n_b, self.dense = info.L, info.K, info.n_b, bool(info.dense)
         self.NS, self.n_configs, self.N = info.NS, info.n_configs, info.N
         self.n_compatible_configs = info.n_compatible_configs
+        self.NC = info.n_slice_classes
         bv = (ctypes.c_int64 * max(self.n_b, 1))()
         _check(lib.tg_problem_bvalues(self.h, bv, max(self.n_b, 1)), "tg_problem_bvalues")
         self.bvalues = [int(bv[a]) for a in range(self.n_b)]
@@ -242,6 +251,54 @@ class Problem:
         _check(load_library().tg_score_pairs(self.h, int(first), int(count), _dptr(cost), _dptr(dmax),
                                              _stream()), "tg_score_pairs")
         return cost, dmax
+
+    # -- redundancy pruning: scores by slice class --------------------------
+    def tg_score_classes(self, first=0, count=None, cost=None, dmax=None):
+        if count is None:
+            count = self.n_configs * self.NC - first
+        if cost is None:
+            cost = torch.empty(count, dtype=torch.float64, device="cuda")
+        if dmax is None:
+            dmax = torch.empty(count, dtype=torch.uint8, device="cuda")
+        _check(load_library().tg_score_classes(self.h, int(first), int(count), _dptr(cost), _dptr(dmax),
+                                               _stream()), "tg_score_classes")
+        return cost, dmax
+
+    def prune_classes_workspace(self):
+        n = load_library().tg_prune_classes_workspace_bytes(self.h)
+        return torch.empty(max(int(n), 1), dtype=torch.uint8, device="cuda")
+
+    def tg_prune_classes(self, cost, dmax, survivors=None, workspace=None):
+        """Surviving set from class scores: tg_prune's ascending list."""
+        lib = load_library()
+        ws = workspace if workspace is not None else self.prune_classes_workspace()
+        n = ctypes.c_int64(0)
+        if survivors is None:
+            st = lib.tg_prune_classes(self.h, _dptr(cost), _dptr(dmax), None, 0, ctypes.byref(n),
+                                      _dptr(ws), ws.numel(), _stream())
+            if st not in (TG_OK, TG_ECAPACITY):
+                _check(st, "tg_prune_classes")
+            survivors = torch.empty(max(n.value, 1), dtype=torch.int64, device="cuda")
+        st = lib.tg_prune_classes(self.h, _dptr(cost), _dptr(dmax), _dptr(survivors), survivors.numel(),
+                                  ctypes.byref(n), _dptr(ws), ws.numel(), _stream())
+        _check(st, "tg_prune_classes")
+        return survivors[: n.value]
+
+    def tg_compose_pipeline_classes(self, survivors, cost, dmax, island_order=None, workspace=None):
+        """tg_compose_pipeline with class scores.  Returns (status, plan dict)."""
+        lib = load_library()
+        if island_order is None:
+            island_order = self.inst["island_order"]
+        order = (ctypes.c_int32 * self.K)(*[int(x) for x in island_order])
+        n = int(survivors.numel())
+        ws = workspace if workspace is not None else self.compose_workspace(n)
+        plan = TgPlan()
+        st = lib.tg_compose_pipeline_classes(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
+                                             _dptr(dmax), order, ctypes.byref(plan), _dptr(ws), ws.numel(),
+                                             _stream())
+        if st not in (TG_OK, TG_ENOPLAN):
+            _check(st, "tg_compose_pipeline_classes")
+        return st, plan_to_dict(plan)
 
     def prune_workspace(self):
         n = load_library().tg_prune_workspace_bytes(self.h)
