@@ -19,6 +19,8 @@ before the timed region.  Prints one JSON line:
                clusters (fewer steps), after the main measurement; for those
                with at most 16 islands also the composition over every
                island order (tg_compose_pipeline_all_orders)
+  redundancy_pruned  the same plan search with redundancy pruning: each
+               (config, slice class) scored once, survivors expanded to slices
   island_construction  tg_build_islands on node clusters of 1024 and 4096
                nodes (the oracle beside it at 1024)
 --space extended adds context parallelism {1,2,4}, recomputation and
@@ -75,6 +77,9 @@ def parse():
                     help="imbalance-pruning tolerance for every workload (0: off)")
     ap.add_argument("--other-steps", type=int, default=10,
                     help="timed plan searches per workload in the five-workload table (0 skips it)")
+    ap.add_argument("--redundancy-steps", type=int, default=10,
+                    help="also time the plan search with redundancy pruning (scores per slice class) this "
+                         "many times (0 skips it); reported beside the main metric")
     ap.add_argument("--island-nodes", type=int, nargs="*", default=[1024, 4096],
                     help="time island construction (tg_build_islands) on generated node clusters of "
                          "these sizes (none: skip)")
@@ -212,6 +217,45 @@ def workload_row(run, steps):
             "plan": {"status": run["status"], "b": run["plan"]["b"], "stages": run["plan"]["S"],
                      "T": run["plan"]["T"]},
             "all_orders_compose": run["all_orders"]}
+
+
+def redundancy_search(torch, T, p, steps, order=None):
+    """The plan search with redundancy pruning on a created problem: score
+    each (config, slice class) once, the surviving set from class scores,
+    composition reading them; HIP events between the three calls."""
+    nc = p.n_configs * p.NC
+    cost = torch.empty(max(nc, 1), dtype=torch.float64, device="cuda")
+    dmax = torch.empty(max(nc, 1), dtype=torch.uint8, device="cuda")
+    pws = p.prune_classes_workspace()
+    p.tg_score_classes(0, nc, cost, dmax)
+    s0 = p.tg_prune_classes(cost, dmax, workspace=pws)
+    surv_buf = torch.empty(max(int(s0.numel()), 1), dtype=torch.int64, device="cuda")
+    cws = p.compose_workspace(int(s0.numel()))
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for k in range(-2, steps):
+        e = ev[k] if k >= 0 else None
+        if e:
+            e[0].record(stream)
+        p.tg_score_classes(0, nc, cost, dmax)
+        if e:
+            e[1].record(stream)
+        s = p.tg_prune_classes(cost, dmax, survivors=surv_buf, workspace=pws)
+        if e:
+            e[2].record(stream)
+        st, plan = p.tg_compose_pipeline_classes(s, cost, dmax, workspace=cws)
+        if e:
+            e[3].record(stream)
+        if k == -1:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    mean = lambda a, b: sum(ev[k][a].elapsed_time(ev[k][b]) for k in range(steps)) / steps
+    return {"slice_classes": p.NC, "class_candidates": nc, "survivors": int(s.numel()),
+            "ms_per_step": elapsed / steps * 1e3,
+            "breakdown_ms": {"score_classes": mean(0, 1), "prune_classes": mean(1, 2), "compose": mean(2, 3)},
+            "plan": {"status": st, "b": plan["b"], "stages": plan["S"], "T": plan["T"]}}
 
 
 def island_construction(T, sizes, with_cpu):
@@ -357,6 +401,8 @@ def main():
         torch.cuda.empty_cache()
         out["workloads"] = five_workloads(torch, T, load_instance, args.space, args.other_steps,
                                           args.workload, main_row, args.imbalance_eps)
+    if args.redundancy_steps > 0:
+        out["redundancy_pruned"] = redundancy_search(torch, T, p, args.redundancy_steps)
     if args.island_nodes:
         out["island_construction"] = island_construction(T, args.island_nodes, not args.no_cpu)
     if not args.no_cpu:

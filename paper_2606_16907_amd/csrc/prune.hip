@@ -175,21 +175,33 @@ __global__ __launch_bounds__(kCountThreads) void emit_kernel(DevProblem P, const
 
 // Redundancy pruning: bit s of a row of the slice bitmap is bit cls[s] of
 // the same row of the class bitmap (a class's staircase holds on every slice
-// of the class).
+// of the class).  A wave builds kExpandWords consecutive 64-bit words, lane b
+// testing slice 64 w + b of each, the loads of all its words in flight.
+constexpr int kExpandWords = 8;
+
 __global__ __launch_bounds__(256) void expand_kernel(DevProblem P, const uint64_t *__restrict__ cbits,
                                                      int32_t cwords, uint64_t *bits, int64_t n_words) {
-    const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (w >= n_words) return;
-    const int64_t row = w / P.words, sw = w - row * P.words;
-    const uint64_t *crow = cbits + row * cwords;
-    uint64_t out = 0;
-    for (int b = 0; b < kWave; ++b) {
-        const int64_t s = sw * kWave + b;
-        if (s >= P.NS) break;
-        const uint32_t c = P.cls[s];
-        out |= ((crow[c >> 6] >> (c & 63)) & 1ull) << b;
+    const int64_t w0 = ((int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * kExpandWords;
+    if (w0 >= n_words) return;  // whole waves leave together
+    const int lane = threadIdx.x & (kWave - 1);
+    uint32_t c[kExpandWords];
+    int64_t row[kExpandWords];
+#pragma unroll
+    for (int t = 0; t < kExpandWords; ++t) {
+        const int64_t w = min(w0 + t, n_words - 1);
+        row[t] = w / P.words;
+        const int64_t s = (w - row[t] * P.words) * kWave + lane;
+        c[t] = s < P.NS ? P.cls[s] : 0xFFFFFFFFu;
     }
-    bits[w] = out;
+    uint64_t x[kExpandWords];
+#pragma unroll
+    for (int t = 0; t < kExpandWords; ++t)
+        x[t] = c[t] != 0xFFFFFFFFu ? cbits[row[t] * cwords + (c[t] >> 6)] : 0ull;
+#pragma unroll
+    for (int t = 0; t < kExpandWords; ++t) {
+        const uint64_t word = __ballot(c[t] != 0xFFFFFFFFu && ((x[t] >> (c[t] & 63)) & 1ull));
+        if (lane == 0 && w0 + t < n_words) bits[w0 + t] = word;
+    }
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -255,7 +267,8 @@ hipError_t launch_prune_classes(const DevProblem &P, const double *cost, const u
     if (e != hipSuccess) return e;
     const int64_t nw = bitmap_words(P);
     if (nw > 0)
-        expand_kernel<<<dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s>>>(P, cbits, C.words, (uint64_t *)ws, nw);
+        expand_kernel<<<dim3((unsigned)((nw + 4 * kExpandWords - 1) / (4 * kExpandWords))), dim3(256), 0, s>>>(
+            P, cbits, C.words, (uint64_t *)ws, nw);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_compact(P, surv, capacity, ws, s, d_total_out);
