@@ -10,9 +10,12 @@ order, and a seeded sample of per-candidate scores.
 
 With --imbalance the same records (survivors, plan, per-b table) are
 written for the instance with imbalance pruning at IMBALANCE_EPS, to
-<name>_imbalance.json.
+<name>_imbalance.json; with --extended for the instance with the extended
+config space (context parallelism {1, 2, 4}, recomputation, offloading), to
+<name>_extended.json, plus a seeded sample of candidate scores.
 
-Run from the repository root:  python -m tests.golden.make_golden [--imbalance] [names...]
+Run from the repository root:
+    python -m tests.golden.make_golden [--imbalance | --extended] [names...]
 """
 from __future__ import annotations
 
@@ -105,6 +108,29 @@ def golden_imbalance(name):
     }
 
 
+def golden_extended(name):
+    from workloads import extended
+    inst = extended(load_instance(name))
+    o = Oracle(inst)
+    t0 = time.time()
+    surv = o.prune()
+    t1 = time.time()
+    st, plan, per_b = o.compose(surv)
+    t2 = time.time()
+    idx = sample_indices(o.N, o.NS)
+    cost, dmax = o.score_list(idx)
+    return {
+        "name": name, "space": "extended",
+        "counts": {"NS": o.NS, "n_configs": o.n_configs, "N": o.N, "n_b": o.n_b},
+        "survivors": {"count": int(len(surv)), "sha256": survivors_digest(surv),
+                      "head": [int(x) for x in surv[:16]], "tail": [int(x) for x in surv[-16:]]},
+        "status": st, "plan": plan, "per_b": [[float(v) for v in row] for row in per_b],
+        "sample": {"idx": [int(x) for x in idx], "cost": [float(x) for x in cost],
+                   "dmax": [int(x) for x in dmax]},
+        "oracle_seconds": {"prune": round(t1 - t0, 3), "compose": round(t2 - t1, 3)},
+    }
+
+
 def path(name):
     return os.path.join(HERE, f"{name}.json")
 
@@ -116,6 +142,15 @@ def load(name):
 
 def main(names):
     build(force=False)
+    if names and names[0] == "--extended":
+        for name in names[1:] or list(CONFIG_NAMES):
+            g = golden_extended(name)
+            with open(path(name + "_extended"), "w") as fh:
+                json.dump(g, fh, indent=1, sort_keys=True)
+                fh.write("\n")
+            print(name, "extended", g["counts"], "survivors", g["survivors"]["count"], "T", g["plan"]["T"],
+                  g["oracle_seconds"], flush=True)
+        return
     if names and names[0] == "--imbalance":
         for name in names[1:] or list(CONFIG_NAMES):
             g = golden_imbalance(name)
