@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 from oracle.oracle import Oracle  # noqa: E402
 from workloads import extended, load_instance, random_tiny  # noqa: E402
-from tests.inst_util import tiny_tight  # noqa: E402
+from tests.inst_util import scaled, tiny_tight  # noqa: E402
 from tests.golden.make_golden import load as load_golden  # noqa: E402
 from tests.test_gpu_parity import plan_equal  # noqa: E402
 from tests.test_oracle_all_orders import _symmetric  # noqa: E402
@@ -42,6 +42,7 @@ CASES = ([("tiny", lambda: load_instance("tiny")), ("tiny_tight", tiny_tight),
             for s in range(6)]
          + [("long70", lambda: random_tiny(3000, L_range=(70, 70), K_range=(3, 3))),
             ("long140", lambda: random_tiny(3001, L_range=(140, 140), K_range=(2, 2), tight=True)),
+            ("long300", lambda: scaled(random_tiny(3006, L_range=(300, 300), K_range=(3, 3)), memory=64.0)),
             ("few_layers", lambda: random_tiny(3002, L_range=(2, 3), K_range=(5, 6))),
             ("one_island", lambda: random_tiny(3003, L_range=(5, 5), K_range=(1, 1)))])
 

@@ -93,3 +93,31 @@ def test_extended_plans_use_the_new_dimensions():
     assert plan["T"] <= t0
     pairs = p.tg_enumerate_pairs().cpu().numpy()[surv.cpu().numpy()]
     assert (pairs[:, 4] > 1).any() and (pairs[:, 8] == 1).any() and (pairs[:, 9] == 1).any()
+
+
+@pytest.mark.parametrize("name", ["dense70b", "moe", "large"])
+def test_extended_named_against_stored(name):
+    """The extended named instances against the oracle's stored results: on
+    the 128-island one N = 7,881,904,128 candidates (more than 2^32, 71 GB of
+    scores) in the launch configuration bench.py times."""
+    import hashlib
+    from tests.golden.make_golden import load as load_golden
+    g = load_golden(name + "_extended")
+    print("case", name, "extended", g["counts"], flush=True)
+    p = T.Problem(extended(load_instance(name)))
+    assert (p.N, p.NS, p.n_configs) == (g["counts"]["N"], g["counts"]["NS"], g["counts"]["n_configs"])
+    cost, dmax = p.tg_score_pairs()
+    idx = torch.tensor(g["sample"]["idx"], dtype=torch.int64, device="cuda")
+    assert np.array_equal(bits(cost[idx].cpu().numpy()), bits(g["sample"]["cost"]))
+    assert np.array_equal(dmax[idx].cpu().numpy(), np.array(g["sample"]["dmax"], dtype=np.uint8))
+    surv = p.tg_prune(cost, dmax)
+    s = surv.cpu().numpy()
+    assert len(s) == g["survivors"]["count"]
+    assert s[:16].tolist() == g["survivors"]["head"] and s[-16:].tolist() == g["survivors"]["tail"]
+    assert hashlib.sha256(np.ascontiguousarray(s, dtype="<i8").tobytes()).hexdigest() == g["survivors"]["sha256"]
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax)
+    assert st == g["status"] == 0
+    g["plan"]["status"] = 0
+    plan_equal(plan, g["plan"])
+    del cost, dmax, surv
+    torch.cuda.empty_cache()
