@@ -6,17 +6,25 @@
 // d_max_p >= 1 and p has the least key
 // (cost, -d_max, idx) among members whose d_max reaches d_max_p.  Equivalently
 // the survivors are rep(G, d) for d = 1..K, the least-key member fitting at
-// depth d.  The frontier pass finds those reps depth band by depth band: pass t
-// takes the least-key member whose d_max exceeds the previous rep's d_max.
+// depth d: a member survives iff no other member at least as deep has a
+// smaller key.
 //
 // Frontier: a wave owns 64 consecutive slices of one (island, b) group list;
-// every lane walks the same members (a scalar loop), reading one coalesced
-// 512-byte row of costs and 64 bytes of depths per member, eight members in
-// flight.  The first pass also finds the group's largest d_max, so a lane
-// stops as soon as its rep reaches it instead of spending a pass to find
-// nothing deeper.  Survivors are
-// recorded in an LDS bit mask per member (lane bit = slice) and written as
-// whole 64-bit words of a bitmap with one row per compatible config.
+// every lane walks the same members (a scalar loop) in ascending idx, reading
+// one coalesced 64-byte row of depths per member and, where the depth can
+// still matter, one 512-byte row of costs, eight members in flight.  Each
+// lane keeps the staircase of its group in registers (up to kStair entries of
+// strictly increasing depth and key): a member is dropped when an entry at
+// least as deep costs no more; otherwise it removes the entries it beats and
+// takes a slot.  When the slots are full the shallowest of them and the
+// newcomer leaves and the pass ignores every member at or above its depth
+// from then on: survival of a member depends only on members at least as
+// deep, so the entries kept are exactly the survivors deeper than that depth.
+// A further pass (rare: more than kStair survivors in one group) settles the
+// shallower ones, with the least kept entry as a cost cap.  Each pass
+// records its entries in an LDS bit mask per member (lane bit = slice), 512
+// members at a time, written as whole 64-bit words of a bitmap with one row
+// per compatible config (a later pass ORs into the words it wrote).
 // Compaction: popcount per tile, scan of tile counts, then each thread writes
 // the candidate indices of its words' set bits in ascending order.
 #include <algorithm>
@@ -26,92 +34,160 @@
 namespace tg {
 
 constexpr int kFrontWaves = 4;
+// Staircase entries a lane keeps per pass: 4 for groups of up to 64 members
+// (60 VGPRs, 8 waves per SIMD), 8 above (82 VGPRs, 5 waves per SIMD), where
+// staircases grow longer and a second pass would cost more than occupancy.
+constexpr int kSmallGroup = 64;
+constexpr int kMaskChunk = 512;   // members per LDS mask round when a pass is recorded
+constexpr int kMemberBits = 23;   // an entry packs depth << kMemberBits | member
+constexpr uint32_t kMemberMask = (1u << kMemberBits) - 1u;
 constexpr int kCountThreads = 256;
 constexpr int kWordsPerThread = 4;
 constexpr int kTileWords = kCountThreads * kWordsPerThread;
 
+// Offer member m (cost c, depth d >= 1, later in idx than every entry) to a
+// lane's staircase.  Entry e beats m when d_e >= d and c_e <= c (equal cost:
+// the deeper key is smaller, and equal depth: the earlier idx).
+template <int R>
+__device__ inline void stair_offer(double (&cv)[R], uint32_t (&pk)[R], double c, int d, int m, int &floor) {
+    const uint32_t dk = (uint32_t)d << kMemberBits;
+    bool beaten = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) beaten = beaten || (pk[r] >= dk && cv[r] <= c);  // empty slots hold 0
+    if (beaten) return;
+    const uint32_t dk1 = (uint32_t)(d + 1) << kMemberBits;
+    const uint32_t x = dk | (uint32_t)m;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        if (pk[r] < dk1 && cv[r] >= c) pk[r] = 0u;  // entries m beats
+    bool placed = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const bool t = !placed && pk[r] == 0u;
+        if (t) {
+            pk[r] = x;
+            cv[r] = c;
+        }
+        placed = placed || t;
+    }
+    if (placed) return;
+    // full: the shallowest of the entries and m leaves, and its depth becomes the floor
+    uint32_t lo = x;
+#pragma unroll
+    for (int r = 0; r < R; ++r) lo = min(lo, pk[r]);
+    floor = (int)(lo >> kMemberBits);
+    if (lo == x) return;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        if (pk[r] == lo) {
+            pk[r] = x;
+            cv[r] = c;
+        }
+}
+
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Writes the bitmap words of every member of the wave's group for its slice
+// chunk: the lanes' entries set their bits in an LDS mask, kMaskChunk members
+// at a time.  After the first pass a word also keeps the bits it already
+// has.
+template <int kStair>
+__device__ inline void record_pass(const DevProblem &P, uint64_t *mask, const uint32_t (&pk)[kStair], bool mine,
+                                   int lane, int m0, int nm, int64_t sc, bool merge, uint64_t *bitmap) {
+    for (int base = 0; base < nm; base += kMaskChunk) {
+        const int n = min(kMaskChunk, nm - base);
+        for (int m = lane; m < n; m += kWave) mask[m] = 0;
+        wave_sync();
+        if (mine) {
+#pragma unroll
+            for (int r = 0; r < kStair; ++r) {
+                const int m = (int)(pk[r] & kMemberMask) - base;
+                if (pk[r] != 0u && m >= 0 && m < n) atomicOr((unsigned long long *)&mask[m], 1ull << lane);
+            }
+        }
+        wave_sync();
+        for (int m = lane; m < n; m += kWave) {
+            uint64_t *at = bitmap + (int64_t)P.coef[P.kb_members[m0 + base + m]].row * P.words + sc;
+            *at = merge ? (*at | mask[m]) : mask[m];
+        }
+        wave_sync();
+    }
+}
+
+template <int kStair>
 __global__ __launch_bounds__(256) void frontier_kernel(DevProblem P, const double *__restrict__ cost,
                                                        const uint8_t *__restrict__ dmax, uint64_t *bitmap,
                                                        int64_t n_tiles) {
-    extern __shared__ uint64_t smask[];
+    __shared__ uint64_t smask[kFrontWaves][kMaskChunk];
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t tile = (int64_t)blockIdx.x * kFrontWaves + wv;
-    uint64_t *mask = smask + (int64_t)wv * P.max_members;
-    const bool tv = tile < n_tiles;
-    int q = 0, m0 = 0, nm = 0;
-    int64_t sc = 0;
-    if (tv) {
-        q = (int)(tile / P.words);
-        sc = tile - (int64_t)q * P.words;
-        m0 = P.kb_off[q];
-        nm = P.kb_off[q + 1] - m0;
+    if (tile >= n_tiles) return;  // whole waves leave; nothing below synchronises the block
+    const int q = (int)(tile / P.words);
+    const int64_t sc = tile - (int64_t)q * P.words;
+    const int m0 = P.kb_off[q];
+    const int nm = P.kb_off[q + 1] - m0;
+    const int64_t s = sc * kWave + lane;
+    const int64_t NS = P.NS;
+    bool need = s < NS;
+    if (need && P.imb) {  // an unbalanced (slice, island) group has no survivors
+        const uint32_t ij = P.sij[s];
+        need = slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), P.kb_island[q]);
     }
-    for (int m = lane; m < nm; m += kWave) mask[m] = 0;
-    __syncthreads();
-    if (tv) {
-        const int64_t s = sc * kWave + lane;
-        const int64_t NS = P.NS;
-        const int K = P.K;
-        bool live = s < NS;
-        if (live && P.imb) {  // an unbalanced (slice, island) group has no survivors
-            const uint32_t ij = P.sij[s];
-            live = slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), P.kb_island[q]);
+    int hi = 1 << 30;  // members deeper than hi are settled (by an earlier pass)
+    double cap = 0.0;  // least cost among the settled members, once there are any
+    bool capped = false;
+    bool merge = false;
+    do {  // every wave records at least one pass: it writes all of its words
+        double cv[kStair];
+        uint32_t pk[kStair];
+#pragma unroll
+        for (int r = 0; r < kStair; ++r) {
+            cv[r] = 0.0;
+            pk[r] = 0u;
         }
-        int prev = 0;   // d_max of the previous rep of this lane's group
-        int top = -1;   // the group's largest d_max, known after the first pass
-        while (__ballot(live) != 0) {
-            double bc = kInf;
-            int bd = 0, bm = -1, mx = 0;
-            // members in batches of eight loads in flight; they come in ascending
-            // idx, so equal (cost, d_max) keeps the earlier one.  Depths are
-            // read first and a cost only where the member reaches past the
-            // previous rep: after the first pass most members do not, so the
-            // later passes move about one byte per member instead of nine.
-            for (int mb = 0; mb < nm; mb += 8) {
-                double c[8];
-                int d[8];
-                int64_t idx[8];
+        int floor = 0;  // members at or above this depth no longer matter in this pass
+        for (int mb = 0; mb < nm; mb += 8) {
+            int d[8];
+            double c[8];
+            const double *crow[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    d[u] = 0;
-                    idx[u] = (int64_t)P.kb_members[m0 + min(mb + u, nm - 1)] * NS + s;
-                    if (mb + u < nm && live) d[u] = dmax[idx[u]];
-                }
+            for (int u = 0; u < 8; ++u) {
+                const int64_t row = (int64_t)P.kb_members[m0 + min(mb + u, nm - 1)] * NS;
+                crow[u] = cost + row;
+                d[u] = (mb + u < nm && need) ? (int)dmax[row + s] : 0;
+            }
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    c[u] = kInf;
-                    if (d[u] > prev) c[u] = cost[idx[u]];
-                }
+            for (int u = 0; u < 8; ++u) c[u] = (d[u] > floor && d[u] <= hi) ? crow[u][s] : 0.0;
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    mx = max(mx, d[u]);
-                    if (d[u] > prev && (c[u] < bc || (c[u] == bc && d[u] > bd))) {
-                        bc = c[u];
-                        bd = d[u];
-                        bm = mb + u;
+            for (int u = 0; u < 8; ++u)
+                if (d[u] > floor && d[u] <= hi && !(capped && cap <= c[u]))
+                    stair_offer<kStair>(cv, pk, c[u], d[u], mb + u, floor);
+        }
+        record_pass<kStair>(P, smask[wv], pk, need, lane, m0, nm, sc, merge, bitmap);
+        merge = true;
+        if (need) {
+            if (floor == 0) {
+                need = false;
+            } else {  // the survivors at or above the floor are still to be found
+                uint32_t lo = 0xFFFFFFFFu;
+#pragma unroll
+                for (int r = 0; r < kStair; ++r)
+                    if (pk[r] != 0u && pk[r] < lo) {
+                        lo = pk[r];
+                        cap = cv[r];
                     }
-                }
-            }
-            if (top < 0) top = mx;
-            if (live) {
-                if (bm >= 0) {
-                    atomicOr((unsigned long long *)&mask[bm], 1ull << lane);
-                    prev = bd;
-                    // nothing reaches deeper than the group's largest d_max
-                    if (prev >= K || prev >= top) live = false;
-                } else {
-                    live = false;
-                }
+                hi = floor;
+                capped = true;
             }
         }
-    }
-    __syncthreads();
-    if (tv)
-        for (int m = lane; m < nm; m += kWave) {
-            const int32_t row = P.coef[P.kb_members[m0 + m]].row;
-            bitmap[(int64_t)row * P.words + sc] = mask[m];
-        }
+        // the next pass reads back words other lanes of this wave wrote
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    } while (__ballot(need) != 0);
 }
 
 __global__ __launch_bounds__(kCountThreads) void count_kernel(const uint64_t *__restrict__ bitmap, int64_t n_words,
@@ -220,9 +296,12 @@ static hipError_t launch_frontier(const DevProblem &P, const double *cost, const
     const int64_t n_front = (int64_t)P.n_kb * P.words;
     if (n_front > 0) {
         const int64_t blocks = (n_front + kFrontWaves - 1) / kFrontWaves;
-        const size_t lds = sizeof(uint64_t) * (size_t)kFrontWaves * (size_t)P.max_members;
-        frontier_kernel<<<dim3((unsigned)blocks), dim3(kFrontWaves * kWave), lds, s>>>(P, cost, dmax, bitmap,
-                                                                                       n_front);
+        if (P.max_members <= kSmallGroup)
+            frontier_kernel<4><<<dim3((unsigned)blocks), dim3(kFrontWaves * kWave), 0, s>>>(P, cost, dmax, bitmap,
+                                                                                            n_front);
+        else
+            frontier_kernel<8><<<dim3((unsigned)blocks), dim3(kFrontWaves * kWave), 0, s>>>(P, cost, dmax, bitmap,
+                                                                                            n_front);
     }
     return hipGetLastError();
 }

@@ -59,3 +59,40 @@ def tiny_tight():
     inst = scaled(inst, memory=1.0 / 16.0)
     inst["name"] = "tiny_tight"
     return inst
+
+
+def deep_staircase(seed):
+    """Mixture-of-experts instance on 8 islands of 8 GPUs with at most 32
+    configs per (island, micro-batch) group, where the expert-parallel degrees
+    give some (slice, island, b) groups five or six survivors (seeds 105, 111,
+    123 and 135 do)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    L, K = int(rng.integers(3, 7)), 8
+    layers = {"fwd_flops": [int(rng.integers(100, 1000)) * 10**9 for _ in range(L)],
+              "dense_params": [int(rng.integers(10, 100)) * 10**6 for _ in range(L)],
+              "expert_params": [int(rng.integers(200, 2000)) * 10**6 for _ in range(L)],
+              "act_stash_bytes": [int(rng.integers(100, 2000)) * 10**6 for _ in range(L)],
+              "tp_comm_bytes": [int(rng.integers(10, 200)) * 10**6 for _ in range(L)],
+              "a2a_bytes": [int(rng.integers(10, 400)) * 10**6 for _ in range(L)],
+              "out_act_bytes": [int(rng.integers(10, 100)) * 10**6 for _ in range(L)]}
+    hbm = [float(rng.integers(4, 60)) * 1e9 for _ in range(K)]
+    inst = instance(K=K, layers=layers, n_gpus=8, peak=[float(rng.integers(100, 900)) * 1e12 for _ in range(K)],
+                    hbm=hbm, intra=[float(rng.integers(100, 900)) * 1e9 for _ in range(K)], inter=50e9, B=64,
+                    tp=(1, 2), ep=(1, 2, 4, 8), mb=(1, 2, 4, 8), zero=(0, 3), n_experts=8)
+    inst["name"] = f"deep_staircase{seed}"
+    return inst
+
+
+def longest_staircase(oracle, survivors):
+    """Most survivors in one (slice, island, b) group, and the most
+    compatible configs in one (island, b) group."""
+    import collections
+    NS, B = oracle.NS, oracle.inst["space"]["global_batch"]
+    key = {}
+    for g in range(oracle.n_configs):
+        d = oracle.decode(g * NS)
+        key[g] = (d["island"], d["dp"] * d["mb"])
+    groups = collections.Counter((int(x) % NS, key[int(x) // NS]) for x in survivors)
+    members = collections.Counter(k for k in key.values() if B % k[1] == 0)
+    return max(groups.values(), default=0), max(members.values(), default=0)

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 
 from oracle.oracle import Oracle  # noqa: E402
 from workloads import load_instance, random_tiny  # noqa: E402
-from tests.inst_util import instance, scaled, tiny_tight  # noqa: E402
+from tests.inst_util import deep_staircase, instance, longest_staircase, scaled, tiny_tight  # noqa: E402
 from tests.golden.make_golden import load as load_golden  # noqa: E402
 
 if not torch.cuda.is_available():
@@ -108,6 +108,30 @@ def test_full_path_parity(name, make):
             plan_equal(plan, oplan)
         else:
             assert st == T.TG_ENOPLAN and plan["S"] == 0 and np.isinf(plan["T"])
+
+
+@pytest.mark.parametrize("seed", [105, 111, 123, 135])
+def test_staircases_longer_than_a_pass_keeps(seed):
+    # groups of at most 64 configs keep four staircase entries per lane and
+    # pass; these instances have groups with five or six survivors, so the
+    # frontier needs a second pass for them
+    inst = deep_staircase(seed)
+    say("case deep_staircase", seed)
+    o = Oracle(inst)
+    osurv = o.prune()
+    longest, members = longest_staircase(o, osurv)
+    assert longest > 4 and members <= 64
+    p = T.Problem(inst)
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    assert np.array_equal(surv.cpu().numpy(), osurv)
+    cost_c, dmax_c = p.tg_score_classes()
+    assert np.array_equal(p.tg_prune_classes(cost_c, dmax_c).cpu().numpy(), osurv)
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax, inst["island_order"])
+    ost, oplan, _ = o.compose(osurv, inst["island_order"])
+    assert st == ost
+    if st == 0:
+        plan_equal(plan, oplan)
 
 
 @pytest.mark.parametrize("name", MEDIUM)
