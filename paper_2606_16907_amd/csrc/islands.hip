@@ -13,8 +13,10 @@
 // least node ids) is merged if the union satisfies Eq. 3 against every node
 // outside it, else marked; the group is done when every pair of its clusters
 // is marked.  Each row keeps its best partner so a step scans rows, not
-// pairs; the Eq. 3 test gives one wave to each member and reads that
-// member's bandwidth row coalesced.  A finish pass numbers islands by their
+// pairs, a wave per row that must be scanned again.  The Eq. 3 test gives
+// one wave to each member of the union: its slowest link inside from the
+// member list, its fastest link leaving from its bandwidth row sorted once
+// per cluster (the first entry outside the union).  A finish pass numbers islands by their
 // smallest node and reduces the island attributes and island-to-island
 // bandwidths (least over node pairs).
 #include <stdint.h>
@@ -36,6 +38,7 @@ struct IslandWs {
     int32_t *gpus;      // [n]
     double *val;        // [4][n] compute, memory, intra, host per node
     double *e;          // [n][n] node bandwidth, row = source
+    int32_t *srt;       // [n][n] row u: the other nodes by bandwidth from u, fastest first
     int32_t *grp;       // [n] group after steps (1)-(2)
     int32_t *gstart;    // [n + 1] group g's nodes are gnodes[gstart[g] .. gstart[g + 1])
     int32_t *gnodes;    // [n]
@@ -65,6 +68,7 @@ static IslandWs carve_islands(int64_t n, void *base) {
     w.gpus = (int32_t *)take(4 * n);
     w.val = (double *)take(8 * 4 * n);
     w.e = (double *)take(8 * n * n);
+    w.srt = (int32_t *)take(4 * n * n);
     w.grp = (int32_t *)take(4 * n);
     w.gstart = (int32_t *)take(4 * (n + 1));
     w.gnodes = (int32_t *)take(4 * n);
@@ -162,6 +166,48 @@ __global__ __launch_bounds__(kGroupThreads) void islands_groups(int n, const int
     }
 }
 
+// Row u of the node bandwidth sorted, fastest first (ties to the lesser
+// node), u itself left out: the fastest link from u to a node outside a
+// cluster is then the first entry outside it, a few entries in for a cluster
+// whose own links are its fastest, as Eq. 3 asks.
+__global__ __launch_bounds__(1024) void islands_sort_rows(int n, const double *__restrict__ e, int32_t *srt) {
+    __shared__ double x[kMaxNodes];
+    __shared__ int32_t id[kMaxNodes];
+    const int u = blockIdx.x;
+    int np = 1;
+    while (np < n) np <<= 1;
+    for (int t = threadIdx.x; t < np; t += blockDim.x) {
+        id[t] = (t < n && t != u) ? t : n;  // n: after every real entry
+        x[t] = t < n ? e[(int64_t)u * n + t] : 0.0;
+    }
+    __syncthreads();
+    auto before = [&](int p, int q) {  // entry p sorts before entry q
+        if (id[p] >= n) return false;
+        if (id[q] >= n) return true;
+        if (x[p] != x[q]) return x[p] > x[q];
+        return id[p] < id[q];
+    };
+    for (int k = 2; k <= np; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int t = threadIdx.x; t < np; t += blockDim.x) {
+                const int o = t ^ j;
+                if (o > t) {
+                    const bool up = (t & k) == 0;
+                    if (up ? before(o, t) : before(t, o)) {
+                        const double tx = x[t];
+                        x[t] = x[o];
+                        x[o] = tx;
+                        const int32_t ti = id[t];
+                        id[t] = id[o];
+                        id[o] = ti;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    for (int t = threadIdx.x; t < n - 1; t += blockDim.x) srt[(int64_t)u * n + t] = id[t];
+}
+
 // Linkage of node pairs in one group (the slower direction), everything else
 // no pair; every node its own cluster.
 __global__ __launch_bounds__(256) void islands_link_init(int n, const double *__restrict__ e,
@@ -183,27 +229,56 @@ __global__ __launch_bounds__(256) void islands_link_init(int n, const double *__
 // ---------------------------------------------------------------------------
 // step (3): agglomerative clustering, one block per group
 // ---------------------------------------------------------------------------
-// Best partner of representative u among the group's representatives:
-// highest linkage of an unmarked pair, ties to the least partner.
+// Best partner of representative u among the group's representatives, by one
+// wave: highest linkage of an unmarked pair, ties to the least partner.
 __device__ inline void row_best(int u, int n, const int32_t *mem, int nm, const int32_t *cl, const double *link,
-                                const uint8_t *marked, double *rbest, int32_t *rarg) {
+                                const uint8_t *marked, double *rbest, int32_t *rarg, int lane) {
     double b = kNoPair;
     int a = -1;
-    for (int q = 0; q < nm; ++q) {
+    for (int q = lane; q < nm; q += kWave) {
         const int v = mem[q];
         if (v == u || cl[v] != v || marked[(int64_t)u * n + v]) continue;
         const double l = link[(int64_t)u * n + v];
-        if (l > b || (l == b && a >= 0 && v < a)) {
-            if (l == kNoPair) continue;
+        if (l == kNoPair) continue;
+        if (a < 0 || l > b || (l == b && v < a)) {
             b = l;
             a = v;
         }
     }
-    rbest[u] = b;
-    rarg[u] = a;
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double b2 = __shfl_xor(b, off);
+        const int a2 = __shfl_xor(a, off);
+        if (a2 >= 0 && (a < 0 || b2 > b || (b2 == b && a2 < a))) {
+            b = b2;
+            a = a2;
+        }
+    }
+    if (lane == 0) {
+        rbest[u] = b;
+        rarg[u] = a;
+    }
+}
+
+// The group members u with keep(u), in member order, into out (LDS); the
+// count, the same for every thread.
+template <typename Keep>
+__device__ inline int collect(const int32_t *mem, int nm, Keep keep, int32_t *out, int32_t *lds) {
+    int cnt = 0;
+    for (int base = 0; base < nm; base += blockDim.x) {
+        const int q = base + (int)threadIdx.x;
+        const int u = q < nm ? mem[q] : -1;
+        const int32_t f = (u >= 0 && keep(u)) ? 1 : 0;
+        int32_t tot;
+        const int32_t ex = block_excl_scan<int32_t>(f, lds, &tot);
+        if (f) out[cnt + ex] = u;
+        cnt += tot;
+    }
+    __syncthreads();
+    return cnt;
 }
 
 __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const double *__restrict__ e,
+                                                               const int32_t *__restrict__ srt,
                                                                const int32_t *__restrict__ gstart,
                                                                const int32_t *__restrict__ gnodes,
                                                                const int32_t *__restrict__ ngroups, double *link,
@@ -211,6 +286,9 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
                                                                int32_t *rarg) {
     __shared__ double sv[kMergeThreads];
     __shared__ int32_t su[kMergeThreads];
+    __shared__ int32_t scan_lds[kMergeThreads / kWave + 1];
+    __shared__ int32_t ulist[kMaxNodes];  // members of the candidate union
+    __shared__ int32_t rlist[kMaxNodes];  // rows whose best partner must be found again
     __shared__ int32_t s_a, s_b, s_ok;
     const int g = blockIdx.x;
     if (g >= *ngroups) return;
@@ -218,7 +296,7 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
     const int nm = gstart[g + 1] - gstart[g];
     if (nm < 2) return;
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave, nw = kMergeThreads / kWave;
-    for (int q = threadIdx.x; q < nm; q += blockDim.x) row_best(mem[q], n, mem, nm, cl, link, marked, rbest, rarg);
+    for (int q = wv; q < nm; q += nw) row_best(mem[q], n, mem, nm, cl, link, marked, rbest, rarg, lane);
     __syncthreads();
     // every pass merges two clusters or marks a pair: it ends
     for (;;) {
@@ -258,25 +336,31 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
         const int a0 = s_a, b0 = s_b;
         if (a0 < 0) break;  // every pair is marked
         const int a = a0 < b0 ? a0 : b0, b = a0 < b0 ? b0 : a0;
-        // Eq. 3 for the union: one wave per member, lanes over all nodes
-        for (int q = wv; q < nm; q += nw) {
-            const int u = mem[q];
-            if (cl[u] != a && cl[u] != b) continue;
-            double in = __builtin_huge_val(), out = kNoPair;
+        const int s = collect(mem, nm, [&](int u) { return cl[u] == a || cl[u] == b; }, ulist, scan_lds);
+        // Eq. 3 for the union, one wave per member: its slowest link inside
+        // against its fastest link to a node outside (the first entry of its
+        // sorted row that is not in the union; none if every node is in it)
+        for (int t = wv; t < s; t += nw) {
+            const int u = ulist[t];
             const double *row = e + (int64_t)u * n;
-            for (int w = lane; w < n; w += kWave) {
-                if (w == u) continue;
-                const double x = row[w];
-                if (cl[w] == a || cl[w] == b) {
-                    if (x < in) in = x;
-                } else if (x > out) {
-                    out = x;
+            double in = __builtin_huge_val(), out = kNoPair;
+            for (int k = lane; k < s; k += kWave) {
+                const int v = ulist[k];
+                if (v != u && row[v] < in) in = row[v];
+            }
+            const int32_t *order = srt + (int64_t)u * n;
+            for (int base = 0; base < n - 1; base += kWave) {
+                const int k = base + lane;
+                const int w = k < n - 1 ? order[k] : -1;
+                const bool outside = w >= 0 && cl[w] != a && cl[w] != b;
+                const uint64_t hit = __ballot(outside);
+                if (hit) {
+                    const int first = __builtin_ctzll(hit);
+                    out = row[__shfl(w, first)];
+                    break;
                 }
             }
-            for (int off = kWave / 2; off > 0; off >>= 1) {
-                in = fmin(in, __shfl_xor(in, off));
-                out = fmax(out, __shfl_xor(out, off));
-            }
+            for (int off = kWave / 2; off > 0; off >>= 1) in = fmin(in, __shfl_xor(in, off));
             if (lane == 0 && !(in >= out)) s_ok = 0;
         }
         __syncthreads();
@@ -298,27 +382,27 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
             __syncthreads();
             // rows whose best partner was a or b, and a itself, start over;
             // the others may now prefer the grown cluster
+            auto again = [&](int u) { return cl[u] == u && (u == a || rarg[u] == a || rarg[u] == b); };
+            const int r = collect(mem, nm, again, rlist, scan_lds);
             for (int q = threadIdx.x; q < nm; q += blockDim.x) {
                 const int u = mem[q];
-                if (cl[u] != u) continue;
-                if (u == a || rarg[u] == a || rarg[u] == b) {
-                    row_best(u, n, mem, nm, cl, link, marked, rbest, rarg);
-                } else {
-                    const double l = link[(int64_t)u * n + a];
-                    if (l != kNoPair && (l > rbest[u] || (l == rbest[u] && a < rarg[u]))) {
-                        rbest[u] = l;
-                        rarg[u] = a;
-                    }
+                if (cl[u] != u || again(u)) continue;
+                const double l = link[(int64_t)u * n + a];
+                if (l != kNoPair && (l > rbest[u] || (l == rbest[u] && a < rarg[u]))) {
+                    rbest[u] = l;
+                    rarg[u] = a;
                 }
             }
+            __syncthreads();  // the test above reads rarg of the listed rows too
+            for (int t = wv; t < r; t += nw) row_best(rlist[t], n, mem, nm, cl, link, marked, rbest, rarg, lane);
         } else {
             if (threadIdx.x == 0) {
                 marked[(int64_t)a * n + b] = 1;
                 marked[(int64_t)b * n + a] = 1;
             }
             __syncthreads();
-            if (threadIdx.x == 0) row_best(a, n, mem, nm, cl, link, marked, rbest, rarg);
-            if (threadIdx.x == kWave) row_best(b, n, mem, nm, cl, link, marked, rbest, rarg);
+            if (wv == 0) row_best(a, n, mem, nm, cl, link, marked, rbest, rarg, lane);
+            if (wv == 1) row_best(b, n, mem, nm, cl, link, marked, rbest, rarg, lane);
         }
         __syncthreads();
     }
@@ -418,8 +502,9 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
     const int64_t nn = (int64_t)n * n;
     islands_link_init<<<dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, s>>>(n, w.e, w.grp, w.link, w.marked,
                                                                                w.cl);
-    islands_merge<<<dim3((unsigned)n), dim3(kMergeThreads), 0, s>>>(n, w.e, w.gstart, w.gnodes, w.ngroups, w.link,
-                                                                     w.marked, w.cl, w.rbest, w.rarg);
+    islands_sort_rows<<<dim3((unsigned)n), dim3(1024), 0, s>>>(n, w.e, w.srt);
+    islands_merge<<<dim3((unsigned)n), dim3(kMergeThreads), 0, s>>>(n, w.e, w.srt, w.gstart, w.gnodes, w.ngroups,
+                                                                     w.link, w.marked, w.cl, w.rbest, w.rarg);
     islands_number<<<dim3(1), dim3(1024), 0, s>>>(n, w.cl, w.gpus, w.val, w.island_of, w.out_k, w.isl_gpus,
                                                   w.isl_val);
     e = hipGetLastError();
