@@ -259,22 +259,20 @@ __device__ inline void row_best(int u, int n, const int32_t *mem, int nm, const 
     }
 }
 
-// The group members u with keep(u), in member order, into out (LDS); the
-// count, the same for every thread.
+// The group members u with keep(u) into out (LDS, in no particular order;
+// every use is order-free); the count, the same for every thread.
 template <typename Keep>
-__device__ inline int collect(const int32_t *mem, int nm, Keep keep, int32_t *out, int32_t *lds) {
-    int cnt = 0;
-    for (int base = 0; base < nm; base += blockDim.x) {
-        const int q = base + (int)threadIdx.x;
-        const int u = q < nm ? mem[q] : -1;
-        const int32_t f = (u >= 0 && keep(u)) ? 1 : 0;
-        int32_t tot;
-        const int32_t ex = block_excl_scan<int32_t>(f, lds, &tot);
-        if (f) out[cnt + ex] = u;
-        cnt += tot;
+__device__ inline int collect(const int32_t *mem, int nm, Keep keep, int32_t *out, int32_t *cnt) {
+    if (threadIdx.x == 0) *cnt = 0;
+    __syncthreads();
+    for (int q = threadIdx.x; q < nm; q += blockDim.x) {
+        const int u = mem[q];
+        if (keep(u)) out[atomicAdd(cnt, 1)] = u;
     }
     __syncthreads();
-    return cnt;
+    const int c = *cnt;
+    __syncthreads();  // the counter is free again
+    return c;
 }
 
 __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const double *__restrict__ e,
@@ -284,9 +282,9 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
                                                                const int32_t *__restrict__ ngroups, double *link,
                                                                uint8_t *marked, int32_t *cl, double *rbest,
                                                                int32_t *rarg) {
-    __shared__ double sv[kMergeThreads];
-    __shared__ int32_t su[kMergeThreads];
-    __shared__ int32_t scan_lds[kMergeThreads / kWave + 1];
+    __shared__ double sv[kMergeThreads / kWave];
+    __shared__ int32_t su[kMergeThreads / kWave];
+    __shared__ int32_t s_cnt;
     __shared__ int32_t ulist[kMaxNodes];  // members of the candidate union
     __shared__ int32_t rlist[kMaxNodes];  // rows whose best partner must be found again
     __shared__ int32_t s_a, s_b, s_ok;
@@ -312,31 +310,34 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
                 bu = u;
             }
         }
-        sv[threadIdx.x] = bv;
-        su[threadIdx.x] = bu;
-        __syncthreads();
-        for (int h = kMergeThreads / 2; h > 0; h >>= 1) {
-            if (threadIdx.x < h) {
-                const double v2 = sv[threadIdx.x + h];
-                const int u2 = su[threadIdx.x + h];
-                const int u1 = su[threadIdx.x];
-                if (u2 >= 0 && (u1 < 0 || v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && u2 < u1))) {
-                    sv[threadIdx.x] = v2;
-                    su[threadIdx.x] = u2;
-                }
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const double v2 = __shfl_xor(bv, off);
+            const int u2 = __shfl_xor(bu, off);
+            if (u2 >= 0 && (bu < 0 || v2 > bv || (v2 == bv && u2 < bu))) {
+                bv = v2;
+                bu = u2;
             }
-            __syncthreads();
         }
+        if (lane == 0) {
+            sv[wv] = bv;
+            su[wv] = bu;
+        }
+        __syncthreads();
         if (threadIdx.x == 0) {
-            s_a = su[0];
-            s_b = su[0] >= 0 ? rarg[su[0]] : -1;
+            for (int w = 1; w < nw; ++w)
+                if (su[w] >= 0 && (bu < 0 || sv[w] > bv || (sv[w] == bv && su[w] < bu))) {
+                    bv = sv[w];
+                    bu = su[w];
+                }
+            s_a = bu;
+            s_b = bu >= 0 ? rarg[bu] : -1;
             s_ok = 1;
         }
         __syncthreads();
         const int a0 = s_a, b0 = s_b;
         if (a0 < 0) break;  // every pair is marked
         const int a = a0 < b0 ? a0 : b0, b = a0 < b0 ? b0 : a0;
-        const int s = collect(mem, nm, [&](int u) { return cl[u] == a || cl[u] == b; }, ulist, scan_lds);
+        const int s = collect(mem, nm, [&](int u) { return cl[u] == a || cl[u] == b; }, ulist, &s_cnt);
         // Eq. 3 for the union, one wave per member: its slowest link inside
         // against its fastest link to a node outside (the first entry of its
         // sorted row that is not in the union; none if every node is in it)
@@ -383,7 +384,7 @@ __global__ __launch_bounds__(kMergeThreads) void islands_merge(int n, const doub
             // rows whose best partner was a or b, and a itself, start over;
             // the others may now prefer the grown cluster
             auto again = [&](int u) { return cl[u] == u && (u == a || rarg[u] == a || rarg[u] == b); };
-            const int r = collect(mem, nm, again, rlist, scan_lds);
+            const int r = collect(mem, nm, again, rlist, &s_cnt);
             for (int q = threadIdx.x; q < nm; q += blockDim.x) {
                 const int u = mem[q];
                 if (cl[u] != u || again(u)) continue;
