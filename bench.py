@@ -115,6 +115,44 @@ def cpu_baseline(inst, n_islands):
             "compose_s": round(t3 - t2, 3), "candidates": o.N, "plan_status": st}
 
 
+def cpu_baseline_workloads(load_instance, space, imbalance_eps, gpu_rows, skip, max_candidates=1_000_000_000):
+    """The oracle on each smaller synthetic cluster, whole: score every
+    candidate, prune, compose (single thread), and whether its plan has the
+    GPU's b, stage count and T (bit for bit) from the same run."""
+    from oracle.oracle import Oracle
+    out = {}
+    for name in ("tiny", "dense8b", "dense70b", "moe"):
+        if name == skip:
+            continue
+        inst = load_instance(name)
+        if space == "extended":
+            from workloads import extended
+            inst = extended(inst)
+        inst["space"]["imbalance_eps"] = imbalance_eps
+        o = Oracle(inst)
+        if o.N > max_candidates:
+            continue
+        t0 = time.perf_counter()
+        cost, dmax = o.score()
+        t1 = time.perf_counter()
+        surv = o.prune()
+        t2 = time.perf_counter()
+        st, plan, _ = o.compose(surv)
+        t3 = time.perf_counter()
+        del cost, dmax
+        row = {"candidates": o.N, "seconds": round(t3 - t0, 4), "pairs_per_s": o.N / (t3 - t0),
+               "score_s": round(t1 - t0, 4), "prune_s": round(t2 - t1, 4), "compose_s": round(t3 - t2, 4),
+               "survivors": int(len(surv)), "plan_status": st}
+        g = (gpu_rows or {}).get(name)
+        if g is not None:
+            gp = g["plan"]
+            row["gpu_speedup"] = (t3 - t0) / (g["ms_per_step"] / 1e3)
+            row["same_plan_as_gpu"] = bool(g["survivors"] == len(surv) and gp["status"] == st and (
+                st != 0 or (gp["b"] == plan["b"] and gp["stages"] == plan["S"] and gp["T"] == plan["T"])))
+        out[name] = row
+    return out
+
+
 def time_search(torch, T, inst, steps, warmup):
     """Create the problem, size the buffers (untimed), then run `warmup` and
     `steps` whole plan searches (score, prune, compose with the plan on the
@@ -407,6 +445,8 @@ def main():
         out["island_construction"] = island_construction(T, args.island_nodes, not args.no_cpu)
     if not args.no_cpu:
         cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
+        cb["workloads"] = cpu_baseline_workloads(load_instance, args.space, args.imbalance_eps,
+                                                 out.get("workloads"), args.workload)
         out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
