@@ -14,7 +14,9 @@ before the timed region.  Prints one JSON line:
                candidate) per launch / its mean HIP-event duration, against
                the 8 TB/s HBM peak
   cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
-               workload (the same 128 layers on the first islands only)
+               workload (the same 128 layers on the first islands only); its
+               `workloads` field times the oracle on each smaller cluster,
+               whole, and compares its plan with the GPU's
   workloads    the same plan search timed on each of the five synthetic
                clusters (fewer steps), after the main measurement; for those
                with at most 16 islands also the composition over every
