@@ -27,6 +27,7 @@
 // fixed-order composition, T_d(i, j, k) never decreases with j, so a scan
 // stops at the first stage cost that cannot improve the running best.
 #include <algorithm>
+#include <type_traits>
 #include <vector>
 
 #include "compose_util.h"
@@ -37,6 +38,7 @@ namespace tg {
 
 constexpr int kMaxSetIslands = 16;
 constexpr int kMaxLayers = 512;
+constexpr size_t kStageLds = 13 * 1024;  // LDS bytes per level block with the set's rows staged
 constexpr int kOrderFinishThreads = 256;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 constexpr int64_t kTargetBlocks = 8192;  // blocks per level launch worth splitting for
@@ -239,15 +241,19 @@ __global__ __launch_bounds__(256) void orders_level1(DevProblem P, SetLevels lv,
 
 // Level d >= 2, block (part of the islands outside a (d-1)-set U', b).  kFill:
 // the fill phase at bound P*, with argmins; otherwise the bottleneck phase.
-template <int NT, bool kFill>
+template <int NT, bool kFill, bool kStage>
 __global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, int nsplit,
                                                    const int32_t *__restrict__ masks,
                                                    const uint16_t *__restrict__ rank, const double *__restrict__ T,
                                                    const double *__restrict__ X, const double *__restrict__ prev,
                                                    double *cur, double *root, const double *__restrict__ Pst,
                                                    uint16_t *argF, uint8_t *argG) {
-    __shared__ double Wl[2][kMaxLayers + 1];
+    // LDS: two continuation rows, then (kStage) the previous level's rows of
+    // the block's set U', read by every state of the block
+    extern __shared__ double lds_rows[];
     const int L = P.L, K = P.K;
+    double *Wl[2] = {lds_rows, lds_rows + (L + 1)};
+    double *Vs = lds_rows + 2 * (L + 1);
     const int rp = blockIdx.x / nsplit, part = blockIdx.x - rp * nsplit;
     const int bb = blockIdx.y;
     const uint32_t Up = (uint32_t)masks[lv.moff[d - 1] + rp];
@@ -271,6 +277,11 @@ __global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, i
     }
     const int nu = d - 1;
     constexpr int NJ = NT >= 256 ? 2 : 1;  // cuts per thread (j <= L < 2 NT)
+    constexpr int kIsl = kStage ? 8 : 4;   // islands' link loads in flight
+    if (kStage) {
+        for (int t = threadIdx.x; t < nu * (L + 1); t += NT) Vs[t] = Vp[t];
+        __syncthreads();
+    }
     int buf = 0;  // continuation rows alternate between two LDS rows, so one
                   // barrier per state separates writers from readers
     for (int q = q0; q < q1; ++q, rest &= rest - 1, buf ^= 1) {
@@ -287,16 +298,16 @@ __global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, i
             if (j > jmax) continue;
             double w = kInf;
             int arg = 255;
-            for (int t0 = 0; t0 < nu; t0 += 4) {
-                double x[4], vv[4];
+            for (int t0 = 0; t0 < nu; t0 += kIsl) {
+                double x[kIsl], vv[kIsl];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
+                for (int u = 0; u < kIsl; ++u) {
                     const int t = min(t0 + u, nu - 1);
                     x[u] = Xr[(int64_t)ks[t] * (L + 1) + j];
-                    vv[u] = Vp[(int64_t)t * (L + 1) + j];
+                    vv[u] = kStage ? Vs[t * (L + 1) + j] : Vp[(int64_t)t * (L + 1) + j];
                 }
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
+                for (int u = 0; u < kIsl; ++u) {
                     const int t = t0 + u;
                     const double v = vv[u];
                     if (t >= nu) {
@@ -564,15 +575,28 @@ static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs 
         const dim3 grid((unsigned)(binom(P.K, d - 1) * nsplit), (unsigned)P.nb);
         const double *prev = w.Vb[(d - 1) & 1];
         double *cur = w.Vb[d & 1];
+        // the set's previous-level rows go to LDS when that keeps at least 12
+        // blocks per CU
+        const size_t rows = (size_t)(L + 1) * sizeof(double);
+        const bool stage = (size_t)(d + 1) * rows <= kStageLds;
+        const size_t lds = (stage ? (size_t)(d + 1) : 2) * rows;
+        auto go = [&](auto nt, auto st) {
+            constexpr int NT = decltype(nt)::value;
+            orders_level<NT, kFill, decltype(st)::value><<<grid, dim3(NT), lds, s>>>(
+                P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev, cur, w.root, w.Pst, w.argF, w.argG);
+        };
+        auto pick = [&](auto nt) {
+            if (stage)
+                go(nt, std::true_type{});
+            else
+                go(nt, std::false_type{});
+        };
         if (L < 64)
-            orders_level<64, kFill><<<grid, dim3(64), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev, cur,
-                                                             w.root, w.Pst, w.argF, w.argG);
+            pick(std::integral_constant<int, 64>{});
         else if (L < 128)
-            orders_level<128, kFill><<<grid, dim3(128), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev,
-                                                               cur, w.root, w.Pst, w.argF, w.argG);
+            pick(std::integral_constant<int, 128>{});
         else
-            orders_level<256, kFill><<<grid, dim3(256), 0, s>>>(P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev,
-                                                               cur, w.root, w.Pst, w.argF, w.argG);
+            pick(std::integral_constant<int, 256>{});
     }
 }
 
