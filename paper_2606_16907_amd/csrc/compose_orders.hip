@@ -20,7 +20,8 @@
 // U's islands.  Every state (k, U) reads the rows V_{d-1}(., k', U \ {k}) of
 // the same smaller set for each k' in it, so a block owns one (d-1)-set U'
 // (and b) and runs the states (k, U' + {k}) for the islands k outside U' one
-// after the other: the rows come from HBM once and from the cache after that.
+// after the other: the rows come from HBM once, into LDS where they fit
+// (13 KB with the two continuation rows), else from the cache after that.
 // Where a level has few sets, the islands outside U' are split over several
 // blocks.  Per state the block writes its continuation row W_d(., k, U) to
 // LDS, then one thread per first layer i scans the cuts j.  As in the
@@ -290,7 +291,7 @@ __global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, i
         const int st = (int)rank[U] * d + __builtin_popcount(U & ((1u << k) - 1u));
         const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
         double *Wrow = Wl[buf];
-        // continuation row from X[b][k][k'][.] and V_{d-1}(., k', U'), four
+        // continuation row from X[b][k][k'][.] and V_{d-1}(., k', U'), kIsl
         // islands' loads in flight
         const double *Xr = X + ((int64_t)bb * K + k) * K * (L + 1);
         for (int c = 0; c < NJ; ++c) {
