@@ -367,7 +367,7 @@ tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_s
  * inter_bw[K * K] (capacity n_nodes^2, row-major) the least node-to-node
  * bandwidth from island a to island b, 0 on the diagonal; *n_islands = K.
  * d_ws: at least tg_build_islands_workspace_bytes(n_nodes) device bytes
- * (about 25 n_nodes^2).  Synchronises the stream.
+ * (about 29 n_nodes^2).  Synchronises the stream.
  */
 size_t tg_build_islands_workspace_bytes(int32_t n_nodes);
 tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double *node_bw, double eps_compute,
