@@ -1021,34 +1021,58 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
             plan.F = rootF[bb];
             plan.T = bestT;
             res->status = TG_OK;
-            int i = 0, o = root_o[bb];
-            bool ok = S >= 1 && S <= 255;
-            for (int t = 0; ok && t < S; ++t) {
-                const int d = S - t;
-                int j = L, o_next = -1;
-                if (d > 1) {
-                    j = argF[(((int64_t)(d - 1) * P.nb + bb) * L + i) * K + o];
-                    // an argmin on the optimal path is always set
-                    ok = j > i && j <= L - d + 1;
-                    if (ok) {
-                        o_next = argG[(((int64_t)(d - 2) * P.nb + bb) * (L + 1) + j) * K + o];
-                        ok = o_next > o && o_next < K;
+            sh_S = S;
+            sh_bb = bb;
+        }
+    }
+    __syncthreads();
+    // The walk, by wave 0: once a stage's cut j is known, the next stage's
+    // whole argmin row argF[d-2][b][j][.] is loaded with argG[d-2][b][j][o],
+    // so the next cut needs no further load (one dependent load per stage).
+    if (threadIdx.x < kWave && sh_S > 0) {
+        const int lane = threadIdx.x;
+        const int S = sh_S, bb = sh_bb;
+        int i = 0, o = root_o[bb];
+        bool ok = S >= 1 && S <= 255;
+        int j = L;
+        if (ok && S > 1) j = argF[(((int64_t)(S - 1) * P.nb + bb) * L + i) * K + o];
+        for (int t = 0; ok && t < S; ++t) {
+            const int d = S - t;
+            int o_next = -1, jn = L;
+            if (d > 1) {
+                // an argmin on the optimal path is always set
+                ok = j > i && j <= L - d + 1;
+                if (ok) {
+                    const uint16_t *row = argF + (((int64_t)(d - 2) * P.nb + bb) * L + j) * K;
+                    uint16_t rv[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int oo = lane + q * kWave;
+                        rv[q] = (d > 2 && oo < K) ? row[oo] : 0;
+                    }
+                    o_next = argG[(((int64_t)(d - 2) * P.nb + bb) * (L + 1) + j) * K + o];
+                    ok = o_next > o && o_next < K;
+                    if (ok && d > 2) {
+                        const int q = o_next / kWave;
+                        const int pick = q == 0 ? rv[0] : (q == 1 ? rv[1] : (q == 2 ? rv[2] : rv[3]));
+                        jn = __shfl(pick, o_next % kWave);
                     }
                 }
+            }
+            if (lane == 0) {
                 st_i[t] = i;
                 st_j[t] = j;
                 st_o[t] = o;
                 st_on[t] = o_next;
-                i = j;
-                o = o_next;
             }
-            if (ok) {
-                sh_S = S;
-                sh_bb = bb;
-            } else {
-                res->err = 4;
-                res->status = TG_ENOPLAN;
-            }
+            i = j;
+            o = o_next;
+            j = jn;
+        }
+        if (!ok && lane == 0) {
+            sh_S = 0;
+            res->err = 4;
+            res->status = TG_ENOPLAN;
         }
     }
     __syncthreads();
