@@ -974,9 +974,9 @@ struct LevelKernels {
 // choose b, walk the argmins, resolve each stage's candidate
 // ---------------------------------------------------------------------------
 // The walk is serial (a stage's argmins give the next stage's first layer and
-// position), so one thread follows it and records the stages in LDS; then one
-// wave per stage finds the stage's candidate in its group.
-constexpr int kFinishThreads = 256;
+// position), so one wave follows it and records the stages in LDS; then one
+// wave per stage (16 waves) finds the stage's candidate in its group.
+constexpr int kFinishThreads = 1024;
 
 
 __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, const int32_t *gcnt,

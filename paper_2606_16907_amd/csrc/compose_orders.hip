@@ -40,7 +40,7 @@ namespace tg {
 constexpr int kMaxSetIslands = 16;
 constexpr int kMaxLayers = 512;
 constexpr size_t kStageLds = 13 * 1024;  // LDS bytes per level block with the set's rows staged
-constexpr int kOrderFinishThreads = 256;
+constexpr int kOrderFinishThreads = 1024;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 constexpr int64_t kTargetBlocks = 8192;  // blocks per level launch worth splitting for
 constexpr int kReduceChunks = 64;        // partials per b in the root reductions
