@@ -6,9 +6,10 @@
 // idx = g * NS + s (g: global config, s: slice).  A wave owns 64 consecutive
 // slices and walks a run of 16 configs: the slice sums live in VGPRs for the
 // whole run, the run's coefficients are staged once in LDS, and every
-// config writes one coalesced 512-byte row of costs and 64 bytes of depths
-// with streaming (nontemporal) stores.  The kernel is bound by HBM writes
-// (9 bytes per candidate).
+// config writes one coalesced 512-byte row of costs and 64 bytes of depths,
+// the costs with streaming (nontemporal) stores, the depths too when their
+// runs are 64-byte aligned.  The kernel is bound by HBM writes (9 bytes per
+// candidate).
 #include <type_traits>
 
 #include "tg_device.h"
@@ -129,7 +130,11 @@ struct StagedCoef {
 
 // kExt: the space has context parallelism, recomputation or offloading
 // (two more slice sums, two more cost terms, the stash and depth rules).
-template <bool kDense, bool kExt>
+// kNtDepth: a wave's 64 depths of a row start on a 64-byte boundary (NS a
+// multiple of 64) and go out with streaming stores like the costs; otherwise
+// the run straddles segments that the neighbouring waves also write, and
+// ordinary stores let L2 merge them.
+template <bool kDense, bool kExt, bool kNtDepth>
 __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first, int64_t last, int64_t g_lo,
                                                     int64_t g_hi, int64_t n_stiles, int64_t n_tiles,
                                                     double *__restrict__ cost, uint8_t *__restrict__ dmax) {
@@ -224,7 +229,10 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
         if (sv && idx >= first && idx < last) {
             // streaming stores: the arrays are far larger than the caches
             __builtin_nontemporal_store(v, cost + (idx - first));
-            __builtin_nontemporal_store((uint8_t)dm, dmax + (idx - first));
+            if (kNtDepth)
+                __builtin_nontemporal_store((uint8_t)dm, dmax + (idx - first));
+            else
+                dmax[idx - first] = (uint8_t)dm;
         }
     }
 }
@@ -240,9 +248,15 @@ hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, doubl
     int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
     blocks = (blocks + kXcds - 1) / kXcds * kXcds;  // whole rounds over the XCDs
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    const bool nt_depth = (P.NS & 63) == 0;
     auto go = [&](auto dense, auto ext) {
-        score_kernel<decltype(dense)::value, decltype(ext)::value><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
-            P, first, last, g_lo, g_hi, n_stiles, n_tiles, cost, dmax);
+        constexpr bool D = decltype(dense)::value, X = decltype(ext)::value;
+        if (nt_depth)
+            score_kernel<D, X, true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi,
+                                                                                   n_stiles, n_tiles, cost, dmax);
+        else
+            score_kernel<D, X, false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, first, last, g_lo, g_hi,
+                                                                                    n_stiles, n_tiles, cost, dmax);
     };
     using T_ = std::true_type;
     using F_ = std::false_type;
