@@ -185,7 +185,8 @@ __global__ __launch_bounds__(256) void frontier_kernel(DevProblem P, const doubl
                 capped = true;
             }
         }
-        // the next pass reads back words other lanes of this wave wrote
+        // a further pass reads back the words this wave wrote (each lane the
+        // same words, so program order already holds; the fence makes it plain)
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
     } while (__ballot(need) != 0);
 }
