@@ -12,7 +12,8 @@ before the timed region.  Prints one JSON line:
   ms_per_step  end-to-end plan-search milliseconds
   roofline     the score kernel: algorithmic bytes (8 B cost + 1 B depth per
                candidate) per launch / its mean HIP-event duration, against
-               the 8 TB/s HBM peak
+               the 8 TB/s HBM peak; `write_ceiling` is what torch's fill_
+               reaches over as many bytes in the same run
   cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
                workload (the same 128 layers on the first islands only); its
                `workloads` field times the oracle on each smaller cluster,
@@ -153,6 +154,27 @@ def cpu_baseline_workloads(load_instance, space, imbalance_eps, gpu_rows, skip, 
                 st != 0 or (gp["b"] == plan["b"] and gp["stages"] == plan["S"] and gp["T"] == plan["T"])))
         out[name] = row
     return out
+
+
+def write_ceiling(torch, nbytes, reps=5):
+    """GB/s of torch's fill_ over a buffer of the score arrays' size: the
+    practical ceiling of a kernel that only writes that many bytes."""
+    buf = torch.empty(max(nbytes // 8, 1), dtype=torch.float64, device="cuda")
+    stream = torch.cuda.current_stream()
+    buf.fill_(1.0)
+    ts = []
+    for r in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        buf.fill_(float(r))
+        b.record(stream)
+        b.synchronize()
+        ts.append(a.elapsed_time(b))
+    ts.sort()
+    gbs = buf.numel() * 8 / (ts[len(ts) // 2] / 1e3) / 1e9
+    del buf
+    torch.cuda.empty_cache()
+    return gbs
 
 
 def time_search(torch, T, inst, steps, warmup):
@@ -403,6 +425,7 @@ def main():
         del rws
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
+    ceiling = write_ceiling(torch, SCORE_BYTES_PER_CANDIDATE * N)
     traffic = measured_traffic(args.workload if args.space == "named" else args.workload + "+extended", N)
     if args.imbalance_eps > 0:
         traffic = None  # the counters were taken without imbalance pruning
@@ -428,7 +451,9 @@ def main():
                    "plan": {"status": st, "b": plan["b"], "stages": plan["S"], "T": plan["T"]}},
         "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic},
+                     "traffic": traffic,
+                     "write_ceiling": {"what": "torch fill_ of as many bytes, same run", "achieved": ceiling,
+                                       "frac": achieved / ceiling}},
         "breakdown_ms": {"score": mean(score_ms), "prune": mean(prune_ms),
                          "compose": mean(compose_ms), "create": t_create * 1e3},
         "score_kernel_pairs_per_s": N / score_s,
