@@ -13,7 +13,7 @@ before the timed region.  Prints one JSON line:
   roofline     the score kernel: algorithmic bytes (8 B cost + 1 B depth per
                candidate) per launch / its mean HIP-event duration, against
                the 8 TB/s HBM peak; `write_ceiling` is what torch's fill_
-               reaches over as many bytes in the same run
+               reaches over as many bytes (at most 16 GiB) in the same run
   cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
                workload (the same 128 layers on the first islands only); its
                `workloads` field times the oracle on each smaller cluster,
@@ -425,7 +425,7 @@ def main():
         del rws
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
-    ceiling = write_ceiling(torch, SCORE_BYTES_PER_CANDIDATE * N)
+    ceiling = write_ceiling(torch, min(SCORE_BYTES_PER_CANDIDATE * N, 16 << 30))
     traffic = measured_traffic(args.workload if args.space == "named" else args.workload + "+extended", N)
     if args.imbalance_eps > 0:
         traffic = None  # the counters were taken without imbalance pruning
@@ -452,7 +452,7 @@ def main():
         "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic,
-                     "write_ceiling": {"what": "torch fill_ of as many bytes, same run", "achieved": ceiling,
+                     "write_ceiling": {"what": "torch fill_ of as many bytes (at most 16 GiB), same run", "achieved": ceiling,
                                        "frac": achieved / ceiling}},
         "breakdown_ms": {"score": mean(score_ms), "prune": mean(prune_ms),
                          "compose": mean(compose_ms), "create": t_create * 1e3},
