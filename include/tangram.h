@@ -172,15 +172,20 @@ typedef struct tg_problem tg_problem;
  *   offloading the order is lexicographic over (tp, cp, dp, ep, zero,
  *   recompute, offload, mb), tp * cp * dp <= n_gpus, and offloading needs
  *   host_bw > 0; with their defaults it is the order above.
- * Returns TG_EINVAL on any invalid value, TG_ENOMEM / TG_EDEVICE on device
- * failures; *out is NULL on failure.
+ * At most 2^23 - 1 configs in all (the pruning pass packs a config's index
+ * within its group into 23 bits); a larger space is refused with TG_EINVAL
+ * after a counting pass, before any of its tables is allocated.
+ * Returns TG_EINVAL on any invalid value, TG_ENOMEM on a failed host or
+ * device allocation, TG_EDEVICE on other device failures; *out is NULL on
+ * failure.
  */
 tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
                             const double *inter_bw, const tg_space *space, tg_problem **out);
 void tg_problem_destroy(tg_problem *p);
 tg_status tg_problem_info(const tg_problem *p, tg_info *out);
 /* Writes the n_b distinct compatible micro-batch sizes, ascending, into out
-   (capacity entries).  Returns TG_ECAPACITY if capacity < n_b. */
+   (capacity entries).  Returns TG_ECAPACITY if capacity < n_b, TG_EINVAL if
+   out is NULL and n_b > 0. */
 tg_status tg_problem_bvalues(const tg_problem *p, int64_t *out, int32_t capacity);
 
 /*

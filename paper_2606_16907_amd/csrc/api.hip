@@ -38,18 +38,15 @@ bool ascending_set(const int32_t *v, int32_t n) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Configs per problem, at most: the frontier packs a member's index within
+// its group into 23 bits.
+constexpr int64_t kMaxConfigs = (int64_t)1 << 23;
+
 }  // namespace
 
 
-extern "C" {
-
-const char *tg_last_error(void) { return g_err; }
-
-tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
-                            const double *inter_bw, const tg_space *space, tg_problem **out) {
-    g_err[0] = 0;
-    if (!out) return fail(TG_EINVAL, "out is NULL");
-    *out = nullptr;
+static tg_status problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
+                                const double *inter_bw, const tg_space *space, tg_problem **out) {
     if (!layers || !islands || !inter_bw || !space) return fail(TG_EINVAL, "NULL input table");
     if (L < 1 || L > 512) return fail(TG_EINVAL, "L=%d outside [1, 512]", L);
     if (K < 1 || K > 255) return fail(TG_EINVAL, "K=%d outside [1, 255]", K);
@@ -98,8 +95,9 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     const int dense = (pre[2 * Lp + L] == 0 && pre[5 * Lp + L] == 0) ? 1 : 0;
 
     // the config list of every island: lexicographic (tp, cp, dp, ep, z, rc,
-    // of, mb) with tp * cp * dp <= n; offloading needs a host link
-    std::vector<tg::Coef> cfg;
+    // of, mb) with tp * cp * dp <= n; offloading needs a host link.  The list
+    // is counted before it is built, so an oversized space is refused before
+    // any of it is allocated.
     std::vector<int> zs, cps, rcs, ofs;
     for (int z = 0; z < 4; ++z)
         if (sp.zero_mask & (1u << z)) zs.push_back(z);
@@ -109,44 +107,55 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         if ((sp.recompute_mask ? sp.recompute_mask : 1u) & (1u << r)) rcs.push_back(r);
         if ((sp.offload_mask ? sp.offload_mask : 1u) & (1u << r)) ofs.push_back(r);
     }
-    int ext = 0;
-    for (int k = 0; k < K; ++k) {
-        const int n = islands[k].n_gpus;
-        for (int a = 0; a < sp.n_tp; ++a) {
-            const int tp = sp.tp[a];
-            if (tp > n) continue;
-            for (int cp : cps) {
-                if ((int64_t)tp * cp > n) continue;
-                const int q = tp * cp;
-                for (int dp = 1; dp <= n / q; ++dp)
-                    for (int e = 0; e < sp.n_ep; ++e) {
-                        const int ep = sp.ep[e];
-                        if (dp % ep) continue;
-                        if (sp.n_experts == 0 ? ep != 1 : (sp.n_experts % ep) != 0) continue;
-                        for (int z : zs)
-                            for (int rc : rcs)
-                                for (int of : ofs) {
-                                    if (of && !(islands[k].host_bw > 0.0)) continue;
-                                    for (int mi = 0; mi < sp.n_mb; ++mi) {
-                                        tg::Coef c;
-                                        std::memset(&c, 0, sizeof(c));
-                                        c.k = k;
-                                        c.tp = tp;
-                                        c.cp = cp;
-                                        c.dp = dp;
-                                        c.ep = ep;
-                                        c.z = z;
-                                        c.rc = rc;
-                                        c.of = of;
-                                        c.mb = sp.mb[mi];
-                                        if (cp > 1 || rc || of) ext = 1;
-                                        cfg.push_back(c);
+    auto visit = [&](auto &&emit) -> bool {  // false once emit asks to stop
+        for (int k = 0; k < K; ++k) {
+            const int n = islands[k].n_gpus;
+            for (int a = 0; a < sp.n_tp; ++a) {
+                const int tp = sp.tp[a];
+                if (tp > n) continue;
+                for (int cp : cps) {
+                    if ((int64_t)tp * cp > n) continue;
+                    const int q = tp * cp;
+                    for (int dp = 1; dp <= n / q; ++dp)
+                        for (int e = 0; e < sp.n_ep; ++e) {
+                            const int ep = sp.ep[e];
+                            if (dp % ep) continue;
+                            if (sp.n_experts == 0 ? ep != 1 : (sp.n_experts % ep) != 0) continue;
+                            for (int z : zs)
+                                for (int rc : rcs)
+                                    for (int of : ofs) {
+                                        if (of && !(islands[k].host_bw > 0.0)) continue;
+                                        for (int mi = 0; mi < sp.n_mb; ++mi)
+                                            if (!emit(k, tp, cp, dp, ep, z, rc, of, sp.mb[mi])) return false;
                                     }
-                                }
-                    }
+                        }
+                }
             }
         }
-    }
+        return true;
+    };
+    int64_t n_listed = 0;
+    if (!visit([&](int, int, int, int, int, int, int, int, int) { return ++n_listed < kMaxConfigs; }))
+        return fail(TG_EINVAL, "candidate space too large: %lld configs or more", (long long)kMaxConfigs);
+    std::vector<tg::Coef> cfg;
+    cfg.reserve((size_t)n_listed);
+    int ext = 0;
+    visit([&](int k, int tp, int cp, int dp, int ep, int z, int rc, int of, int mb) {
+        tg::Coef c;
+        std::memset(&c, 0, sizeof(c));
+        c.k = k;
+        c.tp = tp;
+        c.cp = cp;
+        c.dp = dp;
+        c.ep = ep;
+        c.z = z;
+        c.rc = rc;
+        c.of = of;
+        c.mb = mb;
+        if (cp > 1 || rc || of) ext = 1;
+        cfg.push_back(c);
+        return true;
+    });
     const int64_t ncfg = (int64_t)cfg.size();
     const int64_t NS = (int64_t)L * (L + 1) / 2;
     if (ncfg > ((int64_t)1 << 31) - 1 || NS * ncfg >= ((int64_t)1 << 62))
@@ -314,8 +323,13 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
         p.off = total;
         total += align256(p.bytes > 0 ? p.bytes : 1);
     }
-    tg_problem *pr = new (std::nothrow) tg_problem();
-    if (!pr) return fail(TG_ENOMEM, "host allocation");
+    tg_problem *pr = new tg_problem();
+    // host copies first: nothing below the device allocation throws
+    pr->bvals = bv;
+    pr->n_compat_cfg = (int64_t)row_cfg.size();
+    pr->B = space->global_batch;
+    pr->outact = outact;
+    pr->E.assign(inter_bw, inter_bw + (size_t)K * K);
     hipError_t e = hipGetDevice(&pr->device);
     if (e != hipSuccess) {
         delete pr;
@@ -380,11 +394,6 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     P.cls = (const uint32_t *)(base + parts[19].off);
     P.cls_ij = (const uint32_t *)(base + parts[20].off);
     P.class_scores = 0;
-    pr->bvals = bv;
-    pr->n_compat_cfg = (int64_t)row_cfg.size();
-    pr->B = space->global_batch;
-    pr->outact = outact;
-    pr->E.assign(inter_bw, inter_bw + (size_t)K * K);
     // the per-config coefficients are computed on the device
     e = tg::launch_coef(P, (tg::Coef *)(base + parts[4].off), nullptr);
     if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -395,6 +404,22 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     }
     *out = pr;
     return TG_OK;
+}
+
+extern "C" {
+
+const char *tg_last_error(void) { return g_err; }
+
+tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
+                            const double *inter_bw, const tg_space *space, tg_problem **out) {
+    g_err[0] = 0;
+    if (!out) return fail(TG_EINVAL, "out is NULL");
+    *out = nullptr;
+    try {  // host tables are std::vectors; no exception crosses the C ABI
+        return problem_create(layers, L, islands, K, inter_bw, space, out);
+    } catch (const std::bad_alloc &) {
+        return fail(TG_ENOMEM, "host allocation");
+    }
 }
 
 void tg_problem_destroy(tg_problem *p) {
@@ -424,6 +449,7 @@ tg_status tg_problem_info(const tg_problem *p, tg_info *out) {
 tg_status tg_problem_bvalues(const tg_problem *p, int64_t *out, int32_t capacity) {
     if (!p) return fail(TG_EINVAL, "NULL problem");
     if (capacity < p->P.nb) return fail(TG_ECAPACITY, "capacity %d < n_b %d", capacity, p->P.nb);
+    if (p->P.nb > 0 && !out) return fail(TG_EINVAL, "NULL output");
     for (int a = 0; a < p->P.nb; ++a) out[a] = p->bvals[a];
     return TG_OK;
 }
@@ -534,11 +560,11 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
     std::memset(out, 0, sizeof(*out));
     out->P = out->F = out->T = HUGE_VAL;
     const int K = p->P.K;
-    std::vector<int> seen(K, 0);
+    bool seen[256] = {};  // K <= 255
     for (int o = 0; island_order && o < K; ++o) {
         const int k = island_order[o];
         if (k < 0 || k >= K || seen[k]) return fail(TG_EINVAL, "island_order is not a permutation");
-        seen[k] = 1;
+        seen[k] = true;
     }
     if (n_survivors < 0 || n_survivors > ((int64_t)1 << 30) || (n_survivors > 0 && !d_survivors))
         return fail(TG_EINVAL, "bad survivor list");

@@ -60,3 +60,60 @@ def test_struct_sizes_agree_with_the_c_compiler(tmp_path):
     want = [ctypes.sizeof(c) for c in (T.TgLayer, T.TgIsland, T.TgSpace, T.TgPair, T.TgStage,
                                        T.TgPlan, T.TgInfo)]
     assert got == want
+
+
+def _space(T, mb, zero_mask=0xF, recompute_mask=0, offload_mask=0):
+    sp = T.TgSpace()
+    sp.global_batch = 1024
+    sp.n_tp, sp.tp[0] = 1, 1
+    sp.n_ep, sp.ep[0] = 1, 1
+    sp.n_mb = len(mb)
+    for a, v in enumerate(mb):
+        sp.mb[a] = v
+    sp.zero_mask = zero_mask
+    sp.recompute_mask, sp.offload_mask = recompute_mask, offload_mask
+    sp.eta, sp.mem_frac = 0.5, 0.9
+    return sp
+
+
+def _create(T, lib, n_gpus, sp):
+    layers = (T.TgLayer * 2)()
+    for y in layers:
+        y.fwd_flops, y.dense_params, y.out_act_bytes = 10**9, 10**6, 10**5
+    isl = (T.TgIsland * 1)()
+    isl[0].n_gpus, isl[0].peak_flops, isl[0].hbm_bytes = n_gpus, 1e15, 1e11
+    isl[0].intra_bw, isl[0].host_bw = 1e11, 1e10
+    bw = (ctypes.c_double * 1)(0.0)
+    out = ctypes.c_void_p(123)
+    st = lib.tg_problem_create(layers, 2, isl, 1, bw, ctypes.byref(sp), ctypes.byref(out))
+    return st, out.value, lib.tg_last_error().decode()
+
+
+def test_create_refuses_a_config_space_of_2_23_configs_before_any_device_call():
+    """65536 GPUs x 4 ZeRO stages x 2 recompute x 2 offload x 8 micro-batch
+    sizes = 2^23 configs, one more than the 23-bit member index holds: the
+    counting pass refuses it before the tables (1.6 GB of config rows) or
+    any device call.  Validation only, so it runs without a GPU."""
+    import time
+    from paper_2606_16907_amd import tangram as T
+    lib = T.load_library()
+    sp = _space(T, [1, 2, 4, 8, 16, 32, 64, 128], recompute_mask=3, offload_mask=3)
+    t0 = time.perf_counter()
+    st, out, msg = _create(T, lib, 65536, sp)
+    assert st == -1 and out is None, (st, msg)
+    assert "too large" in msg
+    assert time.perf_counter() - t0 < 5.0
+
+
+def test_create_validation_errors_leave_out_null():
+    from paper_2606_16907_amd import tangram as T
+    lib = T.load_library()
+    sp = _space(T, [1, 2])
+    sp.reserved = 1
+    st, out, msg = _create(T, lib, 8, sp)
+    assert st == -1 and out is None and "reserved" in msg
+    sp = _space(T, [2, 1])  # not ascending
+    st, out, msg = _create(T, lib, 8, sp)
+    assert st == -1 and out is None and "mb set" in msg
+    st, out, msg = _create(T, lib, 0, _space(T, [1]))
+    assert st == -1 and out is None and "n_gpus" in msg
