@@ -149,12 +149,34 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _dptr(t):
-    if t is None:
-        return None
-    if not t.is_cuda:
-        raise ValueError("device buffer expected")
+def _dbuf(t, dtype, n, what, device=None):
+    """Device pointer of a caller's buffer after the checks a plain pointer
+    cannot carry: a contiguous CUDA tensor of `dtype` (on `device` when one is
+    given) with at least n elements.  A short buffer would be read or written
+    past its end by the kernels, so it is refused here."""
+    if t is None or not t.is_cuda:
+        raise ValueError(f"{what}: device buffer expected")
+    if t.dtype != dtype:
+        raise ValueError(f"{what}: dtype {t.dtype}, {dtype} expected")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: contiguous buffer expected")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{what}: on cuda:{t.device.index}, the problem is on cuda:{device}")
+    if t.numel() < n:
+        raise ValueError(f"{what}: {t.numel()} elements, at least {n} needed")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _dws(t, what, device=None):
+    """Workspace pointer and its size in bytes (a contiguous CUDA tensor of
+    any dtype; the library checks the size)."""
+    if t is None or not t.is_cuda:
+        raise ValueError(f"{what}: device buffer expected")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: contiguous buffer expected")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{what}: on cuda:{t.device.index}, the problem is on cuda:{device}")
+    return ctypes.c_void_p(t.data_ptr()), t.numel() * t.element_size()
 
 
 class Problem:
@@ -203,6 +225,7 @@ class Problem:
                                      ctypes.byref(h)), "tg_problem_create")
         self.h = h
         self.inst = inst
+        self.device = torch.cuda.current_device()
         info = TgInfo()
         _check(lib.tg_problem_info(self.h, ctypes.byref(info)), "tg_problem_info")
         self.L, self.K, self.n_b, self.dense = info.L, info.K, info.n_b, bool(info.dense)
@@ -237,7 +260,8 @@ class Problem:
             count = n.value - first
         if out is None:
             out = torch.empty((count, 12), dtype=torch.int32, device="cuda")
-        _check(lib.tg_enumerate_pairs(self.h, ctypes.byref(n), int(first), int(count), _dptr(out),
+        ptr = _dbuf(out, torch.int32, 12 * int(count), "out", self.device)
+        _check(lib.tg_enumerate_pairs(self.h, ctypes.byref(n), int(first), int(count), ptr,
                                       _stream()), "tg_enumerate_pairs")
         return out
 
@@ -248,8 +272,10 @@ class Problem:
             cost = torch.empty(count, dtype=torch.float64, device="cuda")
         if dmax is None:
             dmax = torch.empty(count, dtype=torch.uint8, device="cuda")
-        _check(load_library().tg_score_pairs(self.h, int(first), int(count), _dptr(cost), _dptr(dmax),
-                                             _stream()), "tg_score_pairs")
+        pc = _dbuf(cost, torch.float64, int(count), "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, int(count), "dmax", self.device)
+        _check(load_library().tg_score_pairs(self.h, int(first), int(count), pc, pd, _stream()),
+               "tg_score_pairs")
         return cost, dmax
 
     # -- redundancy pruning: scores by slice class --------------------------
@@ -260,8 +286,10 @@ class Problem:
             cost = torch.empty(count, dtype=torch.float64, device="cuda")
         if dmax is None:
             dmax = torch.empty(count, dtype=torch.uint8, device="cuda")
-        _check(load_library().tg_score_classes(self.h, int(first), int(count), _dptr(cost), _dptr(dmax),
-                                               _stream()), "tg_score_classes")
+        pc = _dbuf(cost, torch.float64, int(count), "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, int(count), "dmax", self.device)
+        _check(load_library().tg_score_classes(self.h, int(first), int(count), pc, pd, _stream()),
+               "tg_score_classes")
         return cost, dmax
 
     def prune_classes_workspace(self):
@@ -273,14 +301,17 @@ class Problem:
         lib = load_library()
         ws = workspace if workspace is not None else self.prune_classes_workspace()
         n = ctypes.c_int64(0)
+        n_scores = self.n_configs * self.NC
+        pc = _dbuf(cost, torch.float64, n_scores, "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, n_scores, "dmax", self.device)
+        pw, wb = _dws(ws, "workspace", self.device)
         if survivors is None:
-            st = lib.tg_prune_classes(self.h, _dptr(cost), _dptr(dmax), None, 0, ctypes.byref(n),
-                                      _dptr(ws), ws.numel(), _stream())
+            st = lib.tg_prune_classes(self.h, pc, pd, None, 0, ctypes.byref(n), pw, wb, _stream())
             if st not in (TG_OK, TG_ECAPACITY):
                 _check(st, "tg_prune_classes")
             survivors = torch.empty(max(n.value, 1), dtype=torch.int64, device="cuda")
-        st = lib.tg_prune_classes(self.h, _dptr(cost), _dptr(dmax), _dptr(survivors), survivors.numel(),
-                                  ctypes.byref(n), _dptr(ws), ws.numel(), _stream())
+        ps = _dbuf(survivors, torch.int64, 0, "survivors", self.device)
+        st = lib.tg_prune_classes(self.h, pc, pd, ps, survivors.numel(), ctypes.byref(n), pw, wb, _stream())
         _check(st, "tg_prune_classes")
         return survivors[: n.value]
 
@@ -293,8 +324,8 @@ class Problem:
         n = int(survivors.numel())
         ws = workspace if workspace is not None else self.compose_workspace(n)
         plan = TgPlan()
-        st = lib.tg_compose_pipeline_classes(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
-                                             _dptr(dmax), order, ctypes.byref(plan), _dptr(ws), ws.numel(),
+        ps, pc, pd, pw, wb = self._compose_args(survivors, cost, dmax, ws, self.n_configs * self.NC)
+        st = lib.tg_compose_pipeline_classes(self.h, ps, n, pc, pd, order, ctypes.byref(plan), pw, wb,
                                              _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline_classes")
@@ -309,20 +340,32 @@ class Problem:
         lib = load_library()
         ws = workspace if workspace is not None else self.prune_workspace()
         n = ctypes.c_int64(0)
+        pc = _dbuf(cost, torch.float64, self.N, "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, self.N, "dmax", self.device)
+        pw, wb = _dws(ws, "workspace", self.device)
         if survivors is None:
-            st = lib.tg_prune(self.h, _dptr(cost), _dptr(dmax), None, 0, ctypes.byref(n),
-                              _dptr(ws), ws.numel(), _stream())
+            st = lib.tg_prune(self.h, pc, pd, None, 0, ctypes.byref(n), pw, wb, _stream())
             if st not in (TG_OK, TG_ECAPACITY):
                 _check(st, "tg_prune")
             survivors = torch.empty(max(n.value, 1), dtype=torch.int64, device="cuda")
-        st = lib.tg_prune(self.h, _dptr(cost), _dptr(dmax), _dptr(survivors), survivors.numel(),
-                          ctypes.byref(n), _dptr(ws), ws.numel(), _stream())
+        ps = _dbuf(survivors, torch.int64, 0, "survivors", self.device)
+        st = lib.tg_prune(self.h, pc, pd, ps, survivors.numel(), ctypes.byref(n), pw, wb, _stream())
         if st == TG_ECAPACITY:
             err = TangramError(st, "tg_prune", last_error())
             err.required = n.value
             raise err
         _check(st, "tg_prune")
         return survivors[: n.value]
+
+    def _compose_args(self, survivors, cost, dmax, ws, n_scores):
+        """Checked pointers of a composition's survivor list, score arrays
+        (n_scores entries each) and workspace."""
+        n = int(survivors.numel())
+        ps = _dbuf(survivors, torch.int64, n, "survivors", self.device) if n else None
+        pc = _dbuf(cost, torch.float64, n_scores, "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, n_scores, "dmax", self.device)
+        pw, wb = _dws(ws, "workspace", self.device)
+        return ps, pc, pd, pw, wb
 
     def compose_workspace(self, n_survivors):
         n = load_library().tg_compose_workspace_bytes(self.h, int(n_survivors))
@@ -337,9 +380,8 @@ class Problem:
         n = int(survivors.numel())
         ws = workspace if workspace is not None else self.compose_workspace(n)
         plan = TgPlan()
-        st = lib.tg_compose_pipeline(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
-                                     _dptr(dmax), order, ctypes.byref(plan), _dptr(ws), ws.numel(),
-                                     _stream())
+        ps, pc, pd, pw, wb = self._compose_args(survivors, cost, dmax, ws, self.N)
+        st = lib.tg_compose_pipeline(self.h, ps, n, pc, pd, order, ctypes.byref(plan), pw, wb, _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline")
         return st, plan_to_dict(plan)
@@ -357,9 +399,9 @@ class Problem:
         n = int(survivors.numel())
         ws = workspace if workspace is not None else self.compose_relaxed_workspace(n)
         plan = TgPlan()
-        st = lib.tg_compose_pipeline_relaxed(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
-                                             _dptr(dmax), order, ctypes.byref(plan), _dptr(ws),
-                                             ws.numel(), _stream())
+        ps, pc, pd, pw, wb = self._compose_args(survivors, cost, dmax, ws, self.N)
+        st = lib.tg_compose_pipeline_relaxed(self.h, ps, n, pc, pd, order, ctypes.byref(plan), pw, wb,
+                                             _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline_relaxed")
         return st, plan_to_dict(plan)
@@ -375,9 +417,8 @@ class Problem:
         n = int(survivors.numel())
         ws = workspace if workspace is not None else self.compose_all_orders_workspace(n)
         plan = TgPlan()
-        st = lib.tg_compose_pipeline_all_orders(self.h, _dptr(survivors) if n else None, n, _dptr(cost),
-                                                _dptr(dmax), ctypes.byref(plan), _dptr(ws), ws.numel(),
-                                                _stream())
+        ps, pc, pd, pw, wb = self._compose_args(survivors, cost, dmax, ws, self.N)
+        st = lib.tg_compose_pipeline_all_orders(self.h, ps, n, pc, pd, ctypes.byref(plan), pw, wb, _stream())
         if st not in (TG_OK, TG_ENOPLAN):
             _check(st, "tg_compose_pipeline_all_orders")
         return st, plan_to_dict(plan)
@@ -427,7 +468,8 @@ def build_islands(cluster, workspace=None):
     K = ctypes.c_int32(0)
     eps = cluster["eps"]
     st = lib.tg_build_islands(nodes, n, e, float(eps["compute"]), float(eps["memory"]), float(eps["intra"]),
-                              isl_of, isl, inter, ctypes.byref(K), _dptr(ws), ws.numel(), _stream())
+                              isl_of, isl, inter, ctypes.byref(K), *_dws(ws, "workspace", torch.cuda.current_device()),
+                              _stream())
     _check(st, "tg_build_islands")
     k = K.value
     return {"island_of": list(isl_of), "K": k,

@@ -260,6 +260,38 @@ def test_errors_and_capacity():
     assert e.value.status == T.TG_ENOMEM
 
 
+def test_binding_refuses_short_or_mistyped_buffers_before_any_launch():
+    """Plain pointers carry no length: the binding refuses a buffer shorter
+    than the call reads or writes, of another dtype, or not contiguous,
+    before the library is called."""
+    p = T.Problem(load_instance("tiny"))
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    short_c = torch.empty(p.N - 1, dtype=torch.float64, device="cuda")
+    short_d = torch.empty(p.N - 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError, match="at least"):
+        p.tg_score_pairs(0, p.N, short_c, dmax)
+    with pytest.raises(ValueError, match="dtype"):
+        p.tg_score_pairs(0, p.N, cost.float(), dmax)
+    with pytest.raises(ValueError, match="at least"):
+        p.tg_enumerate_pairs(0, 4, torch.empty((3, 12), dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError, match="at least"):
+        p.tg_prune(cost, short_d)
+    with pytest.raises(ValueError, match="dtype"):
+        p.tg_prune(cost, dmax, survivors=torch.empty(p.N, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError, match="contiguous"):
+        p.tg_compose_pipeline(torch.stack([surv, surv], 1)[:, 0], cost, dmax)
+    with pytest.raises(ValueError, match="at least"):
+        p.tg_compose_pipeline_relaxed(surv, short_c, dmax)
+    with pytest.raises(ValueError, match="dtype"):
+        p.tg_compose_pipeline_all_orders(surv.int(), cost, dmax)
+    with pytest.raises(ValueError, match="device buffer"):
+        p.tg_compose_pipeline(surv, cost.cpu(), dmax)
+    # the checked calls still give the plan
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax)
+    assert st == T.TG_OK and plan["S"] >= 1
+
+
 def test_invalid_instances_rejected_like_the_oracle():
     from oracle.oracle import OracleError
     for bad in (dict(n_gpus=0), dict(tp=(2, 1)), dict(zero=()), dict(B=0), dict(inter=-1.0),

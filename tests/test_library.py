@@ -117,3 +117,48 @@ def test_create_validation_errors_leave_out_null():
     assert st == -1 and out is None and "mb set" in msg
     st, out, msg = _create(T, lib, 0, _space(T, [1]))
     assert st == -1 and out is None and "n_gpus" in msg
+
+
+class _FakeTensor:
+    """Just the attributes the binding's buffer checks read."""
+
+    def __init__(self, dtype, n, cuda=True, contiguous=True, index=0, esize=1):
+        import types
+        self.dtype, self._n, self.is_cuda, self._c, self._e = dtype, n, cuda, contiguous, esize
+        self.device = types.SimpleNamespace(index=index)
+
+    def is_contiguous(self):
+        return self._c
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return self._e
+
+    def data_ptr(self):
+        return 4096
+
+
+def test_binding_refuses_buffers_the_kernels_would_overrun():
+    """The C ABI takes plain pointers, so the binding checks each caller
+    buffer (device, dtype, contiguity, length) before any call."""
+    import torch
+    from paper_2606_16907_amd import tangram as T
+    f64 = torch.float64
+    ok = T._dbuf(_FakeTensor(f64, 10), f64, 10, "cost", 0)
+    assert ok.value == 4096
+    bad = [(None, "device buffer"),
+           (_FakeTensor(f64, 10, cuda=False), "device buffer"),
+           (_FakeTensor(torch.float32, 10), "dtype"),
+           (_FakeTensor(f64, 10, contiguous=False), "contiguous"),
+           (_FakeTensor(f64, 10, index=1), "cuda:1"),
+           (_FakeTensor(f64, 9), "at least 10")]
+    for t, msg in bad:
+        with pytest.raises(ValueError, match=msg):
+            T._dbuf(t, f64, 10, "cost", 0)
+    ptr, nbytes = T._dws(_FakeTensor(torch.int64, 5, esize=8), "workspace", 0)
+    assert ptr.value == 4096 and nbytes == 40
+    for t in (None, _FakeTensor(torch.uint8, 5, contiguous=False), _FakeTensor(torch.uint8, 5, index=2)):
+        with pytest.raises(ValueError):
+            T._dws(t, "workspace", 0)
