@@ -20,6 +20,10 @@
  *     pointers are plain host memory.  The library allocates device memory
  *     only inside tg_problem_create (small input tables) and frees it in
  *     tg_problem_destroy.
+ *   - Alignment: score cost arrays and survivor lists 8 bytes, candidate
+ *     pair buffers 4 bytes, workspaces 256 bytes (they are carved at 256-byte
+ *     offsets and hold atomic counters); a misaligned buffer is TG_EINVAL.
+ *     hipMalloc'd memory meets all of these.
  *   - `stream` is a hipStream_t (NULL: the default stream).  Calls are
  *     asynchronous on it except where a host result is returned; those calls
  *     synchronise the stream once.

@@ -38,6 +38,16 @@ bool ascending_set(const int32_t *v, int32_t n) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+bool aligned(const void *ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
+
+// Score arrays and survivor lists hold 8-byte values; workspaces are carved
+// at 256-byte offsets from their base, and their counters take atomics.
+tg_status check_alignment(const void *cost, const void *survivors, const void *ws) {
+    if ((cost && !aligned(cost, 8)) || (survivors && !aligned(survivors, 8)) || (ws && !aligned(ws, 256)))
+        return fail(TG_EINVAL, "misaligned buffer: cost and survivors need 8-byte, workspaces 256-byte alignment");
+    return TG_OK;
+}
+
 // Configs per problem, at most: the frontier packs a member's index within
 // its group into 23 bits.
 constexpr int64_t kMaxConfigs = (int64_t)1 << 23;
@@ -462,6 +472,7 @@ tg_status tg_enumerate_pairs(const tg_problem *p, int64_t *n_candidates, int64_t
     if (first < 0 || count < 0 || first > p->P.N || count > p->P.N - first)
         return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
                     (long long)p->P.N);
+    if (!aligned(d_out, 4)) return fail(TG_EINVAL, "misaligned buffer: pairs need 4-byte alignment");
     hipError_t e = tg::launch_enumerate(p->P, first, count, d_out, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "enumerate kernel");
 }
@@ -473,6 +484,7 @@ tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, doub
         return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
                     (long long)p->P.N);
     if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
+    if (check_alignment(d_cost, nullptr, nullptr) != TG_OK) return TG_EINVAL;
     hipError_t e = tg::launch_score(p->P, first, count, d_cost, d_dmax, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
 }
@@ -487,6 +499,7 @@ tg_status tg_score_classes(const tg_problem *p, int64_t first, int64_t count, do
         return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
                     (long long)C.N);
     if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
+    if (check_alignment(d_cost, nullptr, nullptr) != TG_OK) return TG_EINVAL;
     hipError_t e = tg::launch_score(C, first, count, d_cost, d_dmax, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
 }
@@ -500,6 +513,7 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
     if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
     if (!d_ws || ws_bytes < tg::prune_ws_bytes(p->P))
         return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
+    if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
@@ -521,6 +535,7 @@ tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint
     if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
     const size_t need = tg::prune_classes_ws_bytes(p->P);
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune_classes(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
@@ -571,6 +586,7 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
     if (n_survivors > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL score arrays");
     if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31)) return fail(TG_EINVAL, "stage table too large");
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    if (check_alignment(n_survivors > 0 ? d_cost : nullptr, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
     if (p->P.nb == 0) return fail(TG_ENOPLAN, "no micro-batch size divides the global batch");
     if (!island_order) return TG_OK;
     hipError_t e = hipMemcpyAsync((char *)d_ws + tg::compose_order_offset(p->P, n_survivors), island_order,
@@ -681,6 +697,7 @@ tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double
         if (!(node_bw[t] >= 0.0) || !std::isfinite(node_bw[t])) return fail(TG_EINVAL, "node_bw[%lld]", (long long)t);
     const size_t need = tg::islands_ws_bytes(n_nodes);
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
+    if (check_alignment(nullptr, nullptr, d_ws) != TG_OK) return TG_EINVAL;
     hipError_t e = tg::launch_build_islands(n_nodes, nodes, node_bw, eps_compute, eps_memory, eps_intra, d_ws,
                                             (hipStream_t)stream, island_of, islands, inter_bw, n_islands);
     if (e != hipSuccess) return hip_fail(e, "island construction kernels");

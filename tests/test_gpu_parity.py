@@ -8,6 +8,7 @@ instances and random ones; the 128-island instance is compared with the
 oracle's stored results (tests/golden, written by make_golden.py) plus
 per-candidate samples the oracle scores one by one.
 """
+import ctypes
 import hashlib
 import os
 import sys
@@ -290,6 +291,31 @@ def test_binding_refuses_short_or_mistyped_buffers_before_any_launch():
     # the checked calls still give the plan
     st, plan = p.tg_compose_pipeline(surv, cost, dmax)
     assert st == T.TG_OK and plan["S"] >= 1
+
+
+def test_library_refuses_misaligned_buffers_before_any_launch():
+    """Workspaces are carved at 256-byte offsets and hold atomic counters;
+    score and survivor arrays hold 8-byte values.  A misaligned base is
+    refused before any launch."""
+    p = T.Problem(load_instance("tiny"))
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    lib, vp = T.load_library(), ctypes.c_void_p
+    raw = torch.empty(p.prune_workspace().numel() + 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(T.TangramError) as e:
+        p.tg_prune(cost, dmax, workspace=raw[8:])
+    assert e.value.status == T.TG_EINVAL and "aligned" in str(e.value)
+    raw = torch.empty(p.compose_workspace(surv.numel()).numel() + 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(T.TangramError) as e:
+        p.tg_compose_pipeline(surv, cost, dmax, workspace=raw[64:])
+    assert e.value.status == T.TG_EINVAL
+    assert lib.tg_score_pairs(p.h, 0, 1, vp(cost.data_ptr() + 4), vp(dmax.data_ptr()), None) == T.TG_EINVAL
+    out = torch.empty(24, dtype=torch.int32, device="cuda")
+    n = ctypes.c_int64(0)
+    assert lib.tg_enumerate_pairs(p.h, ctypes.byref(n), 0, 1, vp(out.data_ptr() + 2), None) == T.TG_EINVAL
+    # aligned views of the same memory still work
+    st, plan = p.tg_compose_pipeline(surv, cost, dmax, workspace=raw[256:])
+    assert st == T.TG_OK
 
 
 def test_invalid_instances_rejected_like_the_oracle():
