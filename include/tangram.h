@@ -16,7 +16,9 @@
  *   - Units: FLOPs, parameters and bytes are per sample (one sequence), for
  *     the forward pass of one layer; FLOP/s, bytes and bytes/s are per GPU.
  *   - Device buffers ("d_" prefix) are allocated and owned by the caller and
- *     must live on the device that was current at tg_problem_create; host
+ *     must live on the device that was current at tg_problem_create, and
+ *     that device must be current at every call that takes the problem
+ *     (TG_EINVAL otherwise); host
  *     pointers are plain host memory.  The library allocates device memory
  *     only inside tg_problem_create (small input tables) and frees it in
  *     tg_problem_destroy.

@@ -38,6 +38,17 @@ bool ascending_set(const int32_t *v, int32_t n) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Kernels launch on the current device; the problem's tables live on the
+// device that was current at create.
+tg_status check_device(const tg_problem *p) {
+    int cur = -1;
+    const hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur != p->device)
+        return fail(TG_EINVAL, "device %d is current; the problem lives on device %d", cur, p->device);
+    return TG_OK;
+}
+
 bool aligned(const void *ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
 
 // Score arrays and survivor lists hold 8-byte values; workspaces are carved
@@ -473,6 +484,7 @@ tg_status tg_enumerate_pairs(const tg_problem *p, int64_t *n_candidates, int64_t
         return fail(TG_EINVAL, "range [%lld, +%lld) outside [0, %lld)", (long long)first, (long long)count,
                     (long long)p->P.N);
     if (!aligned(d_out, 4)) return fail(TG_EINVAL, "misaligned buffer: pairs need 4-byte alignment");
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     hipError_t e = tg::launch_enumerate(p->P, first, count, d_out, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "enumerate kernel");
 }
@@ -485,6 +497,7 @@ tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, doub
                     (long long)p->P.N);
     if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
     if (check_alignment(d_cost, nullptr, nullptr) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     hipError_t e = tg::launch_score(p->P, first, count, d_cost, d_dmax, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
 }
@@ -500,6 +513,7 @@ tg_status tg_score_classes(const tg_problem *p, int64_t first, int64_t count, do
                     (long long)C.N);
     if (count > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL output");
     if (check_alignment(d_cost, nullptr, nullptr) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     hipError_t e = tg::launch_score(C, first, count, d_cost, d_dmax, (hipStream_t)stream);
     return e == hipSuccess ? TG_OK : hip_fail(e, "score kernel");
 }
@@ -514,6 +528,7 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
     if (!d_ws || ws_bytes < tg::prune_ws_bytes(p->P))
         return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
     if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
@@ -536,6 +551,7 @@ tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint
     const size_t need = tg::prune_classes_ws_bytes(p->P);
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune_classes(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
@@ -587,6 +603,7 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
     if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31)) return fail(TG_EINVAL, "stage table too large");
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (check_alignment(n_survivors > 0 ? d_cost : nullptr, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
     if (p->P.nb == 0) return fail(TG_ENOPLAN, "no micro-batch size divides the global batch");
     if (!island_order) return TG_OK;
     hipError_t e = hipMemcpyAsync((char *)d_ws + tg::compose_order_offset(p->P, n_survivors), island_order,
