@@ -29,6 +29,11 @@
  *   - `stream` is a hipStream_t (NULL: the default stream).  Calls are
  *     asynchronous on it except where a host result is returned; those calls
  *     synchronise the stream once.
+ *   - Concurrency: a problem is read-only after create, so calls on
+ *     different streams or host threads may share it.  A workspace belongs
+ *     to one call at a time: calls whose workspaces overlap must be ordered
+ *     on one stream (or by events), or they race on its counters and tables.
+ *     tg_problem_destroy must not overlap a call that uses the problem.
  *   - Errors are returned as tg_status; no call throws.  tg_last_error()
  *     returns a message for the calling thread's most recent failure.
  *   - Results are a pure function of the inputs, independent of launch
