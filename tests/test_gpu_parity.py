@@ -318,6 +318,34 @@ def test_library_refuses_misaligned_buffers_before_any_launch():
     assert st == T.TG_OK
 
 
+def test_two_streams_share_one_problem():
+    """A problem is read-only after create: two streams with their own
+    buffers and workspaces, issued so that one's scoring overlaps the
+    other's pruning, give the one-stream results bit for bit."""
+    p = T.Problem(load_instance("dense8b"))
+    c0, d0 = p.tg_score_pairs()
+    s0 = p.tg_prune(c0, d0)
+    st0, plan0 = p.tg_compose_pipeline(s0, c0, d0)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    scores, survs = [], []
+    for st in streams:
+        with torch.cuda.stream(st):
+            scores.append(p.tg_score_pairs())
+    for st, (c, d) in zip(streams, scores):
+        with torch.cuda.stream(st):
+            survs.append(p.tg_prune(c, d))
+    plans = []
+    for st, (c, d), sv in zip(streams, scores, survs):
+        with torch.cuda.stream(st):
+            plans.append(p.tg_compose_pipeline(sv, c, d))
+    torch.cuda.synchronize()
+    for (c, d), sv, (st, plan) in zip(scores, survs, plans):
+        assert torch.equal(c.view(torch.int64), c0.view(torch.int64)) and torch.equal(d, d0)
+        assert torch.equal(sv, s0)
+        assert st == st0 and plan == plan0
+
+
 def test_invalid_instances_rejected_like_the_oracle():
     from oracle.oracle import OracleError
     for bad in (dict(n_gpus=0), dict(tp=(2, 1)), dict(zero=()), dict(B=0), dict(inter=-1.0),
