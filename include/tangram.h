@@ -168,7 +168,10 @@ typedef struct {
 typedef struct tg_problem tg_problem;
 
 /*
- * Validates and copies one planning instance to the current device.
+ * Validates and copies one planning instance to the current device: the
+ * model's layers (the atoms slices are cut from, Sec. 4.2), the GPU islands
+ * and their links (Sec. 4.1) and the intra-island configuration space
+ * (Sec. 2.1).
  *   layers[L], L in [1, 512]; islands[K], K in [1, 255];
  *   inter_bw: K*K row-major bytes/s from island a to island b (>= 0 or +inf;
  *             0 means no link; the diagonal is ignored);
@@ -192,11 +195,15 @@ typedef struct tg_problem tg_problem;
  */
 tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *islands, int32_t K,
                             const double *inter_bw, const tg_space *space, tg_problem **out);
+/* Frees the problem's device tables (NULL is ignored).  Must not overlap a
+   call that uses the problem. */
 void tg_problem_destroy(tg_problem *p);
+/* Fills *out with the problem's sizes; TG_EINVAL if p or out is NULL. */
 tg_status tg_problem_info(const tg_problem *p, tg_info *out);
-/* Writes the n_b distinct compatible micro-batch sizes, ascending, into out
-   (capacity entries).  Returns TG_ECAPACITY if capacity < n_b, TG_EINVAL if
-   out is NULL and n_b > 0. */
+/* Writes the n_b distinct compatible micro-batch sizes b (the composition
+   of Sec. 5.2 runs once per b), ascending, into out (capacity entries).
+   Returns TG_ECAPACITY if capacity < n_b, TG_EINVAL if out is NULL and
+   n_b > 0. */
 tg_status tg_problem_bvalues(const tg_problem *p, int64_t *out, int32_t capacity);
 
 /*
