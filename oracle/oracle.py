@@ -17,7 +17,12 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "tangram_oracle.c")
-LIB = os.path.join(HERE, "libtg_oracle.so")
+# TG_ORACLE_LIB names a separately built copy (the sanitizer run builds one
+# with AddressSanitizer and UndefinedBehaviorSanitizer); build() leaves it as is
+LIB_OVERRIDE = os.environ.get("TG_ORACLE_LIB")
+LIB = LIB_OVERRIDE or os.path.join(HERE, "libtg_oracle.so")
+CFLAGS = ["-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-Wall",
+          "-Wno-unused-function"]
 
 LAYER_FIELDS = ("fwd_flops", "dense_params", "expert_params", "act_stash_bytes",
                 "tp_comm_bytes", "a2a_bytes", "out_act_bytes", "cp_comm_bytes")
@@ -30,16 +35,19 @@ SPACE_DEFAULTS = {"cp": [1], "recompute": [0], "offload": [0], "imbalance_eps": 
 OK, EINVAL, ENOMEM, ECAPACITY, ENOPLAN = 0, -1, -2, -4, -5
 
 
-def build(force=True):
-    """Compile the oracle with gcc: -O2, no FMA contraction, no fast-math."""
-    if not force and os.path.exists(LIB) and os.path.getmtime(LIB) >= os.path.getmtime(SRC):
-        return LIB
-    tmp = LIB + ".tmp"
-    subprocess.check_call(["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
-                           "-fPIC", "-shared", "-Wall", "-Wno-unused-function",
-                           "-o", tmp, SRC, "-lm"])
-    os.replace(tmp, LIB)
-    return LIB
+def build(force=True, out=None, extra=()):
+    """Compile the oracle with gcc: -O2, no FMA contraction, no fast-math.
+    `out` and `extra` build another copy (e.g. with sanitizers) elsewhere."""
+    if out is None:
+        if LIB_OVERRIDE:
+            return LIB
+        out = LIB
+        if not force and os.path.exists(out) and os.path.getmtime(out) >= os.path.getmtime(SRC):
+            return out
+    tmp = out + ".tmp"
+    subprocess.check_call(["gcc"] + CFLAGS + list(extra) + ["-o", tmp, SRC, "-lm"])
+    os.replace(tmp, out)
+    return out
 
 
 class Stage(ctypes.Structure):

@@ -582,11 +582,11 @@ int tgo_prune(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
     free(mem);
     free(coef);
     free(members);
-    qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64);
+    if (surv.n > 0) qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64); /* no set: no array */
     *n_out = surv.n;
     int rc = TGO_OK;
     if (surv.n > cap) rc = TGO_ECAPACITY;
-    else if (out) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
+    else if (out && surv.n > 0) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
     free(surv.v);
     return rc;
 }
@@ -692,11 +692,11 @@ int tgo_prune_classes(void *h, int64_t *out, int64_t cap, int64_t *n_out) {
         }
     }
     free(mem); free(coef); free(members); free(kept); free(cls); free(rep);
-    qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64);
+    if (surv.n > 0) qsort(surv.v, (size_t)surv.n, sizeof(int64_t), cmp_i64); /* no set: no array */
     *n_out = surv.n;
     int rc = TGO_OK;
     if (surv.n > cap) rc = TGO_ECAPACITY;
-    else if (out) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
+    else if (out && surv.n > 0) memcpy(out, surv.v, sizeof(int64_t) * surv.n);
     free(surv.v);
     return rc;
 }
