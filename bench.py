@@ -8,16 +8,23 @@ model-slice/island/config candidate (tg_score_pairs), prune to the surviving
 set (tg_prune), compose the pipeline (tg_compose_pipeline, plan returned to
 the host).  The instance's tables and the score buffers are on the device
 before the timed region.  Prints one JSON line:
-  value        candidates per second of whole plan search (N * K / elapsed)
-  ms_per_step  end-to-end plan-search milliseconds
+  value        candidates per second of whole plan search: N * steps / the
+               host-clock time of the K timed steps (score + prune + compose,
+               plan on the host); `score_kernel_pairs_per_s` is N over the
+               score call alone
+  ms_per_step  end-to-end plan-search milliseconds (host clock, mean of the K
+               steps); `ms_per_step_median` the median of the per-step HIP
+               event spans
   roofline     the score kernel: algorithmic bytes (8 B cost + 1 B depth per
                candidate) per launch / its mean HIP-event duration, against
                the 8 TB/s HBM peak; `write_ceiling` is what torch's fill_
                reaches over as many bytes (at most 16 GiB) in the same run
-  cpu_baseline the CPU oracle, single thread, on a bounded sample of the same
-               workload (the same 128 layers on the first islands only); its
-               `workloads` field times the oracle on each smaller cluster,
-               whole, and compares its plan with the GPU's
+  cpu_baseline the CPU oracle, single thread, on the same workload, whole:
+               score every candidate, prune, compose, in the same run on the
+               GPU machine's host (CPU model, logical CPUs, the all-cores
+               projection); its surviving set and plan are compared with the
+               GPU's bit for bit.  `workloads` times the oracle (median of 3)
+               on each smaller cluster and compares its plan with the GPU's
   workloads    the same plan search timed on each of the five synthetic
                clusters (fewer steps), after the main measurement; for those
                with at most 16 islands also the composition over every
@@ -67,8 +74,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-islands", type=int, default=24,
-                    help="islands of the CPU-baseline sample (first islands of the workload)")
+    ap.add_argument("--cpu-islands", type=int, default=0,
+                    help="time the CPU baseline on the workload's first islands only (0: the whole "
+                         "workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
     ap.add_argument("--relaxed-steps", type=int, default=5,
                     help="also time the composition with the step-(4) relaxation this many times "
@@ -92,36 +100,96 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(inst, n_islands):
-    """The oracle, as it stands, on the workload restricted to its first
-    n_islands islands: score every candidate, prune, compose."""
-    from oracle.oracle import Oracle
-    sub = dict(inst)
-    keep = list(range(n_islands))
-    sub["islands"] = {f: [v[k] for k in keep] for f, v in inst["islands"].items()}
-    sub["inter_bw"] = [[inst["inter_bw"][a][b] for b in keep] for a in keep]
-    sub["island_order"] = [k for k in inst["island_order"] if k < n_islands]
-    o = Oracle(sub)
+def host_info():
+    """The CPU the oracle runs on: model name, logical CPUs of the machine and
+    of this process's affinity set."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": os.cpu_count() or 1, "affinity_cpus": usable, "cores_used": 1}
+
+
+def oracle_search(o):
+    """One whole plan search by the oracle: score every candidate, prune,
+    compose.  Returns (seconds per phase, survivors, status, plan)."""
     t0 = time.perf_counter()
     cost, dmax = o.score()
     t1 = time.perf_counter()
+    del cost, dmax
+    t1b = time.perf_counter()
     surv = o.prune()
     t2 = time.perf_counter()
     st, plan, _ = o.compose(surv)
     t3 = time.perf_counter()
-    del cost, dmax
-    el = t3 - t0
-    return {"value": o.N / el, "unit": "pairs/s", "cores": 1, "kind": "oracle",
-            "sample": f"same workload on its first {n_islands} of {len(inst['island_order'])} islands "
-                      f"(N={o.N} candidates): score all, prune, compose; single thread",
-            "seconds": round(el, 3), "score_s": round(t1 - t0, 3), "prune_s": round(t2 - t1, 3),
-            "compose_s": round(t3 - t2, 3), "candidates": o.N, "plan_status": st}
+    return {"score_s": t1 - t0, "prune_s": t2 - t1b, "compose_s": t3 - t2}, surv, st, plan
 
 
-def cpu_baseline_workloads(load_instance, space, imbalance_eps, gpu_rows, skip, max_candidates=1_000_000_000):
+def same_plan(gpu_status, gpu_plan, st, plan):
+    """The oracle's plan equals the GPU's: status, b, m, S, P, F, T bit for
+    bit and every stage field."""
+    if gpu_status != st:
+        return False
+    if st != 0:
+        return True
+    if any(gpu_plan[f] != plan[f] for f in ("b", "m", "S", "P", "F", "T")):
+        return False
+    return all(all(a[f] == b[f] for f in a) for a, b in zip(gpu_plan["stages"], plan["stages"]))
+
+
+def cpu_baseline(inst, n_islands, gpu):
+    """The oracle, as it stands, on the workload (or, with n_islands, on its
+    first islands only): score every candidate, prune, compose, one thread,
+    timed once (the whole 128-island search takes tens of seconds).  `gpu`
+    holds the GPU's survivors digest, plan and ms per step from this run."""
+    import hashlib
+    import numpy as np
+    from oracle.oracle import Oracle
+    K = len(inst["island_order"])
+    whole = n_islands <= 0 or n_islands >= K
+    sub = inst
+    if not whole:
+        sub = dict(inst)
+        keep = list(range(n_islands))
+        sub["islands"] = {f: [v[k] for k in keep] for f, v in inst["islands"].items()}
+        sub["inter_bw"] = [[inst["inter_bw"][a][b] for b in keep] for a in keep]
+        sub["island_order"] = [k for k in inst["island_order"] if k < n_islands]
+    print(f"bench: CPU baseline, the oracle on {'the whole workload' if whole else f'{n_islands} islands'}",
+          file=sys.stderr, flush=True)
+    o = Oracle(sub)
+    ph, surv, st, plan = oracle_search(o)
+    el = sum(ph.values())
+    host = host_info()
+    out = {"value": o.N / el, "unit": "pairs/s", "cores": 1, "kind": "oracle",
+           "sample": (f"the whole workload ({K} islands, N={o.N} candidates)" if whole else
+                      f"same workload on its first {n_islands} of {K} islands (N={o.N} candidates)")
+                     + ": score every candidate, prune, compose; single thread, timed once",
+           "seconds": round(el, 3), "score_s": round(ph["score_s"], 3), "prune_s": round(ph["prune_s"], 3),
+           "compose_s": round(ph["compose_s"], 3), "candidates": o.N, "survivors": int(len(surv)),
+           "plan_status": st, "host": host,
+           "all_cores_projection_s": el / host["affinity_cpus"]}
+    if whole and gpu is not None:
+        digest = hashlib.sha256(np.ascontiguousarray(surv, dtype=np.int64).tobytes()).hexdigest()
+        out["same_survivors_as_gpu"] = bool(digest == gpu["survivors_sha256"] and len(surv) == gpu["survivors"])
+        out["same_plan_as_gpu"] = same_plan(gpu["status"], gpu["plan"], st, plan)
+        out["gpu_speedup"] = el / (gpu["ms_per_step"] / 1e3)
+        out["gpu_speedup_vs_all_cores_projection"] = out["all_cores_projection_s"] / (gpu["ms_per_step"] / 1e3)
+    return out
+
+
+def cpu_baseline_workloads(load_instance, space, imbalance_eps, gpu_rows, skip, reps=3):
     """The oracle on each smaller synthetic cluster, whole: score every
-    candidate, prune, compose (single thread), and whether its plan has the
-    GPU's b, stage count and T (bit for bit) from the same run."""
+    candidate, prune, compose (single thread, median of `reps` runs), and
+    whether its surviving set and plan equal the GPU's from the same run."""
     from oracle.oracle import Oracle
     out = {}
     for name in ("tiny", "dense8b", "dense70b", "moe"):
@@ -133,25 +201,20 @@ def cpu_baseline_workloads(load_instance, space, imbalance_eps, gpu_rows, skip, 
             inst = extended(inst)
         inst["space"]["imbalance_eps"] = imbalance_eps
         o = Oracle(inst)
-        if o.N > max_candidates:
-            continue
-        t0 = time.perf_counter()
-        cost, dmax = o.score()
-        t1 = time.perf_counter()
-        surv = o.prune()
-        t2 = time.perf_counter()
-        st, plan, _ = o.compose(surv)
-        t3 = time.perf_counter()
-        del cost, dmax
-        row = {"candidates": o.N, "seconds": round(t3 - t0, 4), "pairs_per_s": o.N / (t3 - t0),
-               "score_s": round(t1 - t0, 4), "prune_s": round(t2 - t1, 4), "compose_s": round(t3 - t2, 4),
-               "survivors": int(len(surv)), "plan_status": st}
+        runs = []
+        for _ in range(reps):
+            ph, surv, st, plan = oracle_search(o)
+            runs.append((sum(ph.values()), ph))
+        runs.sort(key=lambda r: r[0])
+        el, ph = runs[len(runs) // 2]
+        row = {"candidates": o.N, "seconds": round(el, 4), "runs": reps, "pairs_per_s": o.N / el,
+               "score_s": round(ph["score_s"], 4), "prune_s": round(ph["prune_s"], 4),
+               "compose_s": round(ph["compose_s"], 4), "survivors": int(len(surv)), "plan_status": st}
         g = (gpu_rows or {}).get(name)
         if g is not None:
-            gp = g["plan"]
-            row["gpu_speedup"] = (t3 - t0) / (g["ms_per_step"] / 1e3)
-            row["same_plan_as_gpu"] = bool(g["survivors"] == len(surv) and gp["status"] == st and (
-                st != 0 or (gp["b"] == plan["b"] and gp["stages"] == plan["S"] and gp["T"] == plan["T"])))
+            row["gpu_speedup"] = el / (g["ms_per_step"] / 1e3)
+            row["same_plan_as_gpu"] = bool(g["survivors"] == len(surv) and same_plan(
+                g["plan"]["status"], g["plan_full"], st, plan))
         out[name] = row
     return out
 
@@ -278,6 +341,7 @@ def workload_row(run, steps):
             "score_hbm_frac": SCORE_BYTES_PER_CANDIDATE * run["N"] / (sc / 1e3) / 1e9 / HBM_PEAK_GBS,
             "plan": {"status": run["status"], "b": run["plan"]["b"], "stages": run["plan"]["S"],
                      "T": run["plan"]["T"]},
+            "plan_full": run["plan"],
             "all_orders_compose": run["all_orders"]}
 
 
@@ -425,6 +489,12 @@ def main():
         del rws
     score_s = mean(score_ms) / 1e3
     achieved = SCORE_BYTES_PER_CANDIDATE * N / score_s / 1e9
+    step_ms = sorted(a + b + c for a, b, c in zip(score_ms, prune_ms, compose_ms))
+    # what the CPU baseline compares with: the GPU's surviving set (digest) and plan
+    import hashlib
+    gpu_result = {"survivors": int(s.numel()), "status": st, "plan": plan,
+                  "survivors_sha256": hashlib.sha256(s.cpu().numpy().astype("int64").tobytes()).hexdigest(),
+                  "ms_per_step": elapsed / args.steps * 1e3}
     ceiling = write_ceiling(torch, min(SCORE_BYTES_PER_CANDIDATE * N, 16 << 30))
     traffic = measured_traffic(args.workload if args.space == "named" else args.workload + "+extended", N)
     if args.imbalance_eps > 0:
@@ -454,8 +524,11 @@ def main():
                      "traffic": traffic,
                      "write_ceiling": {"what": "torch fill_ of as many bytes (at most 16 GiB), same run", "achieved": ceiling,
                                        "frac": achieved / ceiling}},
+        "ms_per_step_median": step_ms[len(step_ms) // 2],
         "breakdown_ms": {"score": mean(score_ms), "prune": mean(prune_ms),
                          "compose": mean(compose_ms), "create": t_create * 1e3},
+        "breakdown_ms_median": {k: sorted(v)[len(v) // 2] for k, v in
+                                (("score", score_ms), ("prune", prune_ms), ("compose", compose_ms))},
         "score_kernel_pairs_per_s": N / score_s,
         "relaxed_compose": relaxed,
         "end_to_end_s": elapsed / args.steps,
@@ -471,10 +544,12 @@ def main():
     if args.island_nodes:
         out["island_construction"] = island_construction(T, args.island_nodes, not args.no_cpu)
     if not args.no_cpu:
-        cb = cpu_baseline(inst, min(args.cpu_islands, p.K))
+        cb = cpu_baseline(inst, args.cpu_islands, gpu_result)
         cb["workloads"] = cpu_baseline_workloads(load_instance, args.space, args.imbalance_eps,
                                                  out.get("workloads"), args.workload)
         out["cpu_baseline"] = cb
+    for row in (out.get("workloads") or {}).values():
+        row.pop("plan_full", None)
     print(json.dumps(out), flush=True)
 
 

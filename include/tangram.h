@@ -76,7 +76,8 @@ typedef struct {
                                 sequence), circulated by ring attention under context parallelism */
 } tg_layer;
 
-/* One GPU island (Sec. 4.1): nodes of identical GPUs.  n_gpus in [1, 65536];
+/* One GPU island (Sec. 4.1): nodes of identical GPUs.  n_gpus in [1, 2^28]
+   (every island tg_build_islands returns is accepted);
    peak_flops, hbm_bytes and intra_bw are finite and > 0; host_bw is finite
    and >= 0 (0: no host link, activation offloading is not admitted). */
 typedef struct {
@@ -107,7 +108,7 @@ typedef struct {
    survive, and the compositions reject them.  A model with no FLOPs is never
    pruned. */
 typedef struct {
-    int64_t global_batch; /* samples per iteration, >= 1 */
+    int64_t global_batch; /* samples per iteration, >= 1; every compatible b and B / b below 2^31 */
     int32_t n_experts;
     int32_t n_tp;
     int32_t tp[8];

@@ -188,7 +188,7 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
         return TGO_EINVAL;
     if (!(imb_eps >= 0.0) || !isfinite(imb_eps)) return TGO_EINVAL;
     for (int k = 0; k < K; k++) {
-        if (n_gpus[k] < 1 || n_gpus[k] > 65536) return TGO_EINVAL;
+        if (n_gpus[k] < 1 || n_gpus[k] > (1 << 28)) return TGO_EINVAL; /* any island built from nodes */
         if (!(peak[k] > 0.0) || !isfinite(peak[k])) return TGO_EINVAL;
         if (!(hbm[k] > 0.0) || !isfinite(hbm[k])) return TGO_EINVAL;
         if (!(intra[k] > 0.0) || !isfinite(intra[k])) return TGO_EINVAL;
@@ -284,8 +284,13 @@ int tgo_create(const int64_t *layers, int L, const int32_t *n_gpus, const double
         for (int64_t a = 0; a < nb; a++) if (p->bvals[a] == b) { seen = 1; break; }
         if (!seen) p->bvals[nb++] = b;
     }
-    qsort(p->bvals, (size_t)nb, sizeof(int64_t), cmp_i64);
+    if (nb > 0) qsort(p->bvals, (size_t)nb, sizeof(int64_t), cmp_i64);
     p->nb = (int)nb;
+    /* a plan reports b and m = B / b as 32-bit integers */
+    if (nb > 0 && (p->bvals[nb - 1] > INT32_MAX || p->B / p->bvals[0] > INT32_MAX)) {
+        tgo_destroy(p);
+        return TGO_EINVAL;
+    }
     *out = p;
     return TGO_OK;
 }

@@ -1,6 +1,7 @@
 // api.hip -- the C ABI declared in include/tangram.h: validation, the
 // problem's device tables, and the entry points that launch the kernels.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -62,6 +63,20 @@ tg_status check_alignment(const void *cost, const void *survivors, const void *w
 // Configs per problem, at most: the frontier packs a member's index within
 // its group into 23 bits.
 constexpr int64_t kMaxConfigs = (int64_t)1 << 23;
+// GPUs per island, at most: 4096 nodes of 65536 GPUs, the largest island
+// tg_build_islands can return.
+constexpr int32_t kMaxIslandGpus = 1 << 28;
+constexpr int32_t kMaxNodeGpus = 1 << 16;
+
+// Host containers may throw std::bad_alloc; no exception crosses the C ABI.
+template <typename F>
+tg_status no_throw(F f) {
+    try {
+        return f();
+    } catch (const std::bad_alloc &) {
+        return fail(TG_ENOMEM, "host allocation");
+    }
+}
 
 }  // namespace
 
@@ -89,7 +104,7 @@ static tg_status problem_create(const tg_layer *layers, int32_t L, const tg_isla
         return fail(TG_EINVAL, "imbalance_eps invalid");
     for (int k = 0; k < K; ++k) {
         const tg_island &is = islands[k];
-        if (is.n_gpus < 1 || is.n_gpus > 65536) return fail(TG_EINVAL, "island %d: n_gpus", k);
+        if (is.n_gpus < 1 || is.n_gpus > kMaxIslandGpus) return fail(TG_EINVAL, "island %d: n_gpus", k);
         if (is.reserved != 0) return fail(TG_EINVAL, "island %d: reserved field not 0", k);
         if (!(is.peak_flops > 0.0) || !std::isfinite(is.peak_flops)) return fail(TG_EINVAL, "island %d: peak", k);
         if (!(is.hbm_bytes > 0.0) || !std::isfinite(is.hbm_bytes)) return fail(TG_EINVAL, "island %d: hbm", k);
@@ -191,6 +206,9 @@ static tg_status problem_create(const tg_layer *layers, int32_t L, const tg_isla
     std::sort(bv.begin(), bv.end());
     bv.erase(std::unique(bv.begin(), bv.end()), bv.end());
     const int nb = (int)bv.size();
+    // a plan reports b and m = B / b as int32
+    if (nb > 0 && (bv.back() > INT32_MAX || sp.global_batch / bv.front() > INT32_MAX))
+        return fail(TG_EINVAL, "global_batch %lld: b or B / b exceeds 2^31 - 1", (long long)sp.global_batch);
     std::vector<int32_t> row_cfg;
     for (int64_t g = 0; g < ncfg; ++g) {
         const int64_t b = (int64_t)cfg[g].dp * cfg[g].mb;
@@ -436,11 +454,7 @@ tg_status tg_problem_create(const tg_layer *layers, int32_t L, const tg_island *
     g_err[0] = 0;
     if (!out) return fail(TG_EINVAL, "out is NULL");
     *out = nullptr;
-    try {  // host tables are std::vectors; no exception crosses the C ABI
-        return problem_create(layers, L, islands, K, inter_bw, space, out);
-    } catch (const std::bad_alloc &) {
-        return fail(TG_ENOMEM, "host allocation");
-    }
+    return no_throw([&] { return problem_create(layers, L, islands, K, inter_bw, space, out); });
 }
 
 void tg_problem_destroy(tg_problem *p) {
@@ -680,13 +694,15 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
     tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, island_order, out, d_ws, ws_bytes,
                                  need, s);
     if (st != TG_OK) return st;
-    const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B};
-    tg::ComposeResult *res_dev = nullptr;
-    int rounds = 0;
-    hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax, d_ws,
-                                              s, &res_dev, &rounds);
-    if (e != hipSuccess) return hip_fail(e, "relaxed compose kernels");
-    return compose_end(res_dev, out, s);
+    return no_throw([&] {
+        const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B};
+        tg::ComposeResult *res_dev = nullptr;
+        int rounds = 0;
+        hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax,
+                                                  d_ws, s, &res_dev, &rounds);
+        if (e != hipSuccess) return hip_fail(e, "relaxed compose kernels");
+        return compose_end(res_dev, out, s);
+    });
 }
 
 size_t tg_build_islands_workspace_bytes(int32_t n_nodes) {
@@ -704,7 +720,7 @@ tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double
         if (!(x >= 0.0) || !std::isfinite(x)) return fail(TG_EINVAL, "tolerance invalid");
     for (int u = 0; u < n_nodes; ++u) {
         const tg_island &v = nodes[u];
-        if (v.n_gpus < 1 || v.n_gpus > 65536 || v.reserved != 0) return fail(TG_EINVAL, "node %d GPU count", u);
+        if (v.n_gpus < 1 || v.n_gpus > kMaxNodeGpus || v.reserved != 0) return fail(TG_EINVAL, "node %d GPU count", u);
         if (!(v.peak_flops > 0.0) || !std::isfinite(v.peak_flops) || !(v.hbm_bytes > 0.0) ||
             !std::isfinite(v.hbm_bytes) || !(v.intra_bw > 0.0) || !std::isfinite(v.intra_bw) ||
             !(v.host_bw >= 0.0) || !std::isfinite(v.host_bw))
@@ -715,10 +731,12 @@ tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double
     const size_t need = tg::islands_ws_bytes(n_nodes);
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (check_alignment(nullptr, nullptr, d_ws) != TG_OK) return TG_EINVAL;
-    hipError_t e = tg::launch_build_islands(n_nodes, nodes, node_bw, eps_compute, eps_memory, eps_intra, d_ws,
-                                            (hipStream_t)stream, island_of, islands, inter_bw, n_islands);
-    if (e != hipSuccess) return hip_fail(e, "island construction kernels");
-    return TG_OK;
+    return no_throw([&] {
+        hipError_t e = tg::launch_build_islands(n_nodes, nodes, node_bw, eps_compute, eps_memory, eps_intra, d_ws,
+                                                (hipStream_t)stream, island_of, islands, inter_bw, n_islands);
+        if (e != hipSuccess) return hip_fail(e, "island construction kernels");
+        return TG_OK;
+    });
 }
 
 tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,

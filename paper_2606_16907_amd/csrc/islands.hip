@@ -21,6 +21,8 @@
 // bandwidths (least over node pairs).
 #include <stdint.h>
 
+#include <vector>
+
 #include "tg_device.h"
 
 #pragma clang fp contract(off)
@@ -482,8 +484,8 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
                                 tg_island *islands, double *inter_bw, int32_t *n_islands) {
     const IslandWs w = carve_islands(n, ws);
     // node columns, uploaded from the caller's arrays
-    int32_t *hg = new int32_t[n];
-    double *hv = new double[(size_t)4 * n];
+    std::vector<int32_t> hg(n);
+    std::vector<double> hv((size_t)4 * n);
     for (int u = 0; u < n; ++u) {
         hg[u] = nodes_host[u].n_gpus;
         hv[u] = nodes_host[u].peak_flops;
@@ -491,12 +493,10 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
         hv[2 * n + u] = nodes_host[u].intra_bw;
         hv[3 * n + u] = nodes_host[u].host_bw;
     }
-    hipError_t e = hipMemcpyAsync(w.gpus, hg, 4 * (size_t)n, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(w.val, hv, 8 * 4 * (size_t)n, hipMemcpyHostToDevice, s);
+    hipError_t e = hipMemcpyAsync(w.gpus, hg.data(), 4 * (size_t)n, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(w.val, hv.data(), 8 * 4 * (size_t)n, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemcpyAsync(w.e, e_host, 8 * (size_t)n * n, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host staging arrays go away
-    delete[] hg;
-    delete[] hv;
     if (e != hipSuccess) return e;
     islands_groups<<<dim3(1), dim3(kGroupThreads), 0, s>>>(n, w.gpus, w.val, eps_c, eps_m, eps_i, w.grp, w.gstart,
                                                            w.gnodes, w.ngroups);
@@ -519,11 +519,11 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
     islands_inter<<<dim3((unsigned)n), dim3(256), 0, s>>>(n, w.out_k, w.e, w.island_of, w.isl_e);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    int32_t *og = new int32_t[K];
-    double *ov = new double[(size_t)4 * n];
+    std::vector<int32_t> og(K > 0 ? K : 1);
+    std::vector<double> ov((size_t)4 * n);
     e = hipMemcpyAsync(island_of, w.island_of, 4 * (size_t)n, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(og, w.isl_gpus, 4 * (size_t)K, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(ov, w.isl_val, 8 * 4 * (size_t)n, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(og.data(), w.isl_gpus, 4 * (size_t)K, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(ov.data(), w.isl_val, 8 * 4 * (size_t)n, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(inter_bw, w.isl_e, 8 * (size_t)kk, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e == hipSuccess) {
@@ -537,8 +537,6 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
         }
         *n_islands = K;
     }
-    delete[] og;
-    delete[] ov;
     return e;
 }
 

@@ -119,6 +119,31 @@ def test_create_validation_errors_leave_out_null():
     assert st == -1 and out is None and "n_gpus" in msg
 
 
+def test_create_refuses_plans_whose_b_or_m_overflow_int32():
+    """A plan reports b and m = B / b as int32: a global batch whose smallest
+    compatible b leaves B / b >= 2^31 is refused at create (validation only,
+    before any device call)."""
+    from paper_2606_16907_amd import tangram as T
+    lib = T.load_library()
+    sp = _space(T, [1])
+    sp.global_batch = 1 << 31  # b = 1 divides it, m = 2^31
+    st, out, msg = _create(T, lib, 8, sp)
+    assert st == -1 and out is None and "2^31" in msg, (st, msg)
+
+
+def test_create_takes_islands_of_up_to_2_28_gpus():
+    """Islands from tg_build_islands sum their nodes' GPUs (4096 nodes of at
+    most 65536): create accepts n_gpus up to 2^28 and refuses more.  At 2^28
+    the space itself is refused as too large, which is validation, not the
+    GPU count."""
+    from paper_2606_16907_amd import tangram as T
+    lib = T.load_library()
+    st, out, msg = _create(T, lib, (1 << 28) + 1, _space(T, [1]))
+    assert st == -1 and out is None and "n_gpus" in msg
+    st, out, msg = _create(T, lib, 1 << 28, _space(T, [1]))
+    assert st == -1 and out is None and "too large" in msg, msg
+
+
 class _FakeTensor:
     """Just the attributes the binding's buffer checks read."""
 

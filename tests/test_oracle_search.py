@@ -285,3 +285,14 @@ def test_named_instance_plan_invariants(name):
     assert st == 0
     check_plan_invariants(o, plan, s)
     assert plan["T"] == min(per_b[:, 2])
+
+
+def test_oracle_refuses_plans_whose_m_overflows_int32():
+    """The plan reports m = B / b as a 32-bit integer: B = 2^31 with b = 1
+    compatible is refused at create."""
+    from oracle.oracle import OracleError
+    from tests.inst_util import instance
+    with pytest.raises(OracleError) as e:
+        Oracle(instance(L=2, K=1, layer={"fwd_flops": 2**30}, B=2**31))
+    assert e.value.status == EINVAL
+    Oracle(instance(L=2, K=1, layer={"fwd_flops": 2**30}, B=2**31 - 1))
