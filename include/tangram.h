@@ -271,6 +271,23 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
                    int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream);
 
 /*
+ * tg_prune without a workspace, for callers that cannot allocate device
+ * memory: code being captured into a HIP graph, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, result and errors as
+ * tg_prune; the workspace is instead a static device array of 64 MiB that
+ * the library holds on each GPU it runs on until the process ends (enough for
+ * every problem whose tg_prune_workspace_bytes is at most 64 MiB, e.g. 128
+ * layers x 33,536 compatible configs).  A larger problem is refused with
+ * TG_ENOMEM before any work is queued.  The call allocates nothing (no
+ * hipMalloc, no host or device allocation by the library).  Every call on one
+ * GPU uses that GPU's array: calls that overlap on one GPU (other streams or
+ * threads) race and must be serialised by the caller.  Each call rewrites all
+ * the scratch it reads, so earlier calls leave nothing behind that matters.
+ */
+tg_status tg_prune_no_alloc(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax,
+                            int64_t *d_survivors, int64_t capacity, int64_t *n_survivors, tg_stream stream);
+
+/*
  * Redundancy pruning (Sec. 5.1 (i): slices of the same composition are one
  * query).  Two slices are equivalent when all eight of their per-slice sums
  * (the tg_layer fields summed over the slice) are equal; every config scores

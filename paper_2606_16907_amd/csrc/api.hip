@@ -534,15 +534,11 @@ tg_status tg_score_classes(const tg_problem *p, int64_t first, int64_t count, do
 
 size_t tg_prune_classes_workspace_bytes(const tg_problem *p) { return p ? tg::prune_classes_ws_bytes(p->P) : 0; }
 
-tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
-                   int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream) {
-    if (!p || !n_survivors) return fail(TG_EINVAL, "NULL argument");
-    if (!d_cost || !d_dmax) return fail(TG_EINVAL, "NULL score arrays");
-    if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
-    if (!d_ws || ws_bytes < tg::prune_ws_bytes(p->P))
-        return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
-    if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
-    if (tg_status st = check_device(p); st != TG_OK) return st;
+}  // extern "C"
+
+// The prune kernels on a checked workspace, then the survivor count.
+static tg_status prune_run(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                           int64_t capacity, int64_t *n_survivors, void *d_ws, tg_stream stream) {
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
@@ -555,6 +551,41 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
     if (total > capacity)
         return fail(TG_ECAPACITY, "%lld survivors exceed capacity %lld", (long long)total, (long long)capacity);
     return TG_OK;
+}
+
+static tg_status prune_args(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax,
+                            const int64_t *d_survivors, int64_t capacity, const int64_t *n_survivors) {
+    if (!p || !n_survivors) return fail(TG_EINVAL, "NULL argument");
+    if (!d_cost || !d_dmax) return fail(TG_EINVAL, "NULL score arrays");
+    if (capacity < 0 || (capacity > 0 && !d_survivors)) return fail(TG_EINVAL, "bad survivor buffer");
+    return TG_OK;
+}
+
+extern "C" {
+
+tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                   int64_t capacity, int64_t *n_survivors, void *d_ws, size_t ws_bytes, tg_stream stream) {
+    if (tg_status st = prune_args(p, d_cost, d_dmax, d_survivors, capacity, n_survivors); st != TG_OK) return st;
+    if (!d_ws || ws_bytes < tg::prune_ws_bytes(p->P))
+        return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
+    if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
+    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, d_ws, stream);
+}
+
+tg_status tg_prune_no_alloc(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
+                            int64_t capacity, int64_t *n_survivors, tg_stream stream) {
+    if (tg_status st = prune_args(p, d_cost, d_dmax, d_survivors, capacity, n_survivors); st != TG_OK) return st;
+    const size_t need = tg::prune_ws_bytes(p->P);
+    if (need > tg::kStaticScratchBytes)
+        return fail(TG_ENOMEM, "the surviving set of this problem needs %zu bytes of scratch; the static scratch "
+                               "holds %zu (use tg_prune with a workspace)", need, tg::kStaticScratchBytes);
+    if (check_alignment(d_cost, d_survivors, nullptr) != TG_OK) return TG_EINVAL;
+    if (tg_status st = check_device(p); st != TG_OK) return st;
+    void *ws = nullptr;
+    const hipError_t e = tg::static_scratch(p->device, &ws);
+    if (e != hipSuccess) return hip_fail(e, "static scratch address");
+    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, ws, stream);
 }
 
 tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,

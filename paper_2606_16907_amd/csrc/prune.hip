@@ -28,6 +28,7 @@
 // Compaction: popcount per tile, scan of tile counts, then each thread writes
 // the candidate indices of its words' set bits in ascending order.
 #include <algorithm>
+#include <mutex>
 
 #include "tg_device.h"
 
@@ -331,6 +332,30 @@ hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *
     hipError_t e = launch_frontier(P, cost, dmax, (uint64_t *)ws, s);
     if (e != hipSuccess) return e;
     return launch_compact(P, surv, capacity, ws, s, d_total_out);
+}
+
+// Scratch of the prune variant that allocates nothing: a device array the
+// code object carries, one copy per GPU, held until the process ends.  Host
+// code never names it in a kernel argument or a copy (the name is a host-side
+// stand-in there); it reaches the array through the device address that
+// hipGetSymbolAddress returns for the current GPU, resolved once per GPU.
+// Every call rewrites all the workspace it reads (each bitmap word, tile
+// count and the total), so nothing needs clearing between calls.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+hipError_t static_scratch(int device, void **out) {
+    static std::mutex mu;
+    static void *addr[kMaxScratchDevices] = {};
+    if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress((void **)&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[device] = ptr;
+    }
+    *out = addr[device];
+    return hipSuccess;
 }
 
 // Class bitmap after the slice-level workspace of launch_prune.

@@ -151,6 +151,12 @@ hipError_t launch_prune_classes(const DevProblem &P, const double *cost, const u
                                 int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
 hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
                         int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
+// The static scratch of the prune variant that allocates nothing: its size,
+// and its device address on `device` (which must be current), resolved once
+// per GPU.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+constexpr int kMaxScratchDevices = 64;
+hipError_t static_scratch(int device, void **out);
 
 size_t compose_ws_bytes(const DevProblem &P, int64_t n_surv);
 // Runs composition; on return (after the stream is synchronised by the

@@ -84,7 +84,7 @@ EXPORTS = ("tg_problem_create", "tg_problem_destroy", "tg_problem_info", "tg_pro
            "tg_compose_pipeline_relaxed", "tg_compose_all_orders_workspace_bytes",
            "tg_compose_pipeline_all_orders", "tg_build_islands_workspace_bytes", "tg_build_islands",
            "tg_score_classes", "tg_prune_classes_workspace_bytes", "tg_prune_classes",
-           "tg_compose_pipeline_classes",
+           "tg_compose_pipeline_classes", "tg_prune_no_alloc",
            "tg_last_error")
 
 _lib = None
@@ -112,6 +112,7 @@ def load_library(path=LIB_PATH):
     L.tg_prune_workspace_bytes.argtypes = [vp]
     L.tg_prune_workspace_bytes.restype = sz
     L.tg_prune.argtypes = [vp, vp, vp, vp, i64, P(i64), vp, sz, vp]
+    L.tg_prune_no_alloc.argtypes = [vp, vp, vp, vp, i64, P(i64), vp]
     L.tg_compose_workspace_bytes.argtypes = [vp, i64]
     L.tg_compose_workspace_bytes.restype = sz
     L.tg_compose_pipeline.argtypes = [vp, vp, i64, vp, vp, P(i32), P(TgPlan), vp, sz, vp]
@@ -355,6 +356,23 @@ class Problem:
             err.required = n.value
             raise err
         _check(st, "tg_prune")
+        return survivors[: n.value]
+
+    def tg_prune_no_alloc(self, cost, dmax, survivors):
+        """tg_prune on the library's static scratch: no workspace and no
+        allocation (the caller's `survivors` buffer receives the list).
+        Returns the filled prefix of `survivors`."""
+        lib = load_library()
+        n = ctypes.c_int64(0)
+        pc = _dbuf(cost, torch.float64, self.N, "cost", self.device)
+        pd = _dbuf(dmax, torch.uint8, self.N, "dmax", self.device)
+        ps = _dbuf(survivors, torch.int64, 0, "survivors", self.device)
+        st = lib.tg_prune_no_alloc(self.h, pc, pd, ps, survivors.numel(), ctypes.byref(n), _stream())
+        if st == TG_ECAPACITY:
+            err = TangramError(st, "tg_prune_no_alloc", last_error())
+            err.required = n.value
+            raise err
+        _check(st, "tg_prune_no_alloc")
         return survivors[: n.value]
 
     def _compose_args(self, survivors, cost, dmax, ws, n_scores):
