@@ -646,6 +646,7 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
         return fail(TG_EINVAL, "bad survivor list");
     if (n_survivors > 0 && (!d_cost || !d_dmax)) return fail(TG_EINVAL, "NULL score arrays");
     if ((int64_t)p->P.nb * p->P.NS * K >= ((int64_t)1 << 31)) return fail(TG_EINVAL, "stage table too large");
+    if (p->P.nb > 65535) return fail(TG_EINVAL, "more than 65535 micro-batch sizes");
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (check_alignment(n_survivors > 0 ? d_cost : nullptr, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
     if (tg_status st = check_device(p); st != TG_OK) return st;

@@ -37,7 +37,7 @@
 namespace tg {
 
 constexpr int kScanThreads = 256;
-constexpr int kScanPerThread = 8;
+constexpr int kScanPerThread = 16;  // four 16-byte loads of consecutive counts per thread
 constexpr int kScanTile = kScanThreads * kScanPerThread;
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -52,12 +52,6 @@ __global__ __launch_bounds__(256) void fill_kernel(T *a, int64_t n, T v) {
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void copy_kernel(const T *a, T *b, int64_t n) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) b[i] = a[i];
-}
-
-template <typename T>
 static void fill(T *a, int64_t n, T v, hipStream_t s) {
     if (n <= 0) return;
     int64_t blocks = (n + 255) / 256;
@@ -65,12 +59,33 @@ static void fill(T *a, int64_t n, T v, hipStream_t s) {
     fill_kernel<T><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(a, n, v);
 }
 
+// A thread's kScanPerThread consecutive int32 counts (zeros past n); the
+// array base is 16-byte aligned (workspace offsets are multiples of 256).
+__device__ inline void load_counts(const int32_t *a, int64_t n, int64_t first, int32_t (&v)[kScanPerThread]) {
+    if (first + kScanPerThread <= n) {
+        const int4 *q = (const int4 *)(a + first);
+#pragma unroll
+        for (int u = 0; u < kScanPerThread / 4; ++u) {
+            const int4 x = q[u];
+            v[4 * u] = x.x;
+            v[4 * u + 1] = x.y;
+            v[4 * u + 2] = x.z;
+            v[4 * u + 3] = x.w;
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < kScanPerThread; ++u) v[u] = first + u < n ? a[first + u] : 0;
+    }
+}
+
 __global__ __launch_bounds__(kScanThreads) void scan_reduce_i32(const int32_t *a, int64_t n, int64_t *tile_sum) {
     __shared__ int64_t lds[kScanThreads / kWave + 1];
-    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPerThread;
+    const int64_t first = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPerThread;
+    int32_t v[kScanPerThread];
+    load_counts(a, n, first, v);
     int64_t c = 0;
-    for (int t = 0; t < kScanPerThread; ++t)
-        if (base + t < n) c += a[base + t];
+#pragma unroll
+    for (int u = 0; u < kScanPerThread; ++u) c += v[u];
     int64_t total;
     block_excl_scan<int64_t>(c, lds, &total);
     if (threadIdx.x == 0) tile_sum[blockIdx.x] = total;
@@ -91,18 +106,28 @@ __global__ __launch_bounds__(1024) void scan_tiles_i64(int64_t *a, int64_t n) {
 
 __global__ __launch_bounds__(kScanThreads) void scan_apply_i32(int32_t *a, int64_t n, const int64_t *tile_off) {
     __shared__ int64_t lds[kScanThreads / kWave + 1];
-    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPerThread;
+    const int64_t first = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPerThread;
     int32_t v[kScanPerThread];
+    load_counts(a, n, first, v);
     int64_t c = 0;
-    for (int t = 0; t < kScanPerThread; ++t) {
-        v[t] = (base + t < n) ? a[base + t] : 0;
-        c += v[t];
-    }
+#pragma unroll
+    for (int u = 0; u < kScanPerThread; ++u) c += v[u];
     int64_t total;
     int64_t run = tile_off[blockIdx.x] + block_excl_scan<int64_t>(c, lds, &total);
-    for (int t = 0; t < kScanPerThread; ++t) {
-        if (base + t < n) a[base + t] = (int32_t)run;
-        run += v[t];
+    int32_t out[kScanPerThread];
+#pragma unroll
+    for (int u = 0; u < kScanPerThread; ++u) {
+        out[u] = (int32_t)run;
+        run += v[u];
+    }
+    if (first + kScanPerThread <= n) {
+        int4 *q = (int4 *)(a + first);
+#pragma unroll
+        for (int u = 0; u < kScanPerThread / 4; ++u) q[u] = make_int4(out[4 * u], out[4 * u + 1], out[4 * u + 2], out[4 * u + 3]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < kScanPerThread; ++u)
+            if (first + u < n) a[first + u] = out[u];
     }
 }
 
@@ -127,16 +152,17 @@ struct Ws {
     int32_t *rec_g;    // [n] group of list entry r, -1 if unused
     double *rec_c;     // [n] its cost
     uint8_t *rec_d;    // [n] its d_max
-    int32_t *gcnt;     // [n_groups] counts -> offsets -> ends
+    int32_t *gcnt;     // [n_groups] counts -> offsets -> ends (group order)
     double *ent_c;     // [n] grouped entries: cost
     uint8_t *ent_d;    // [n] d_max
     int64_t *ent_i;    // [n] candidate index
-    int32_t *bcnt;     // [n_buckets + 1] event counts -> bucket starts (last = total)
+    int32_t *rowev;    // [nb][L][D+1] per row (b, i): where the events of each level start (last = end)
+    int32_t *ev_total; // [1] events reserved so far
     int32_t *ev_cell;  // [2n]
     double *ev_val;    // [2n]
-    double *T;         // [n_groups] current stage table, layout [b][s][o]
+    double *T;         // [n_groups] current stage table of phase 1, layout [b][s][o] (= group order)
+    double *T0;        // [n_groups] the same starting table for phase 2
     double *T1;        // [nb][L][K] depth-1 table of the slices (i, L)
-    int32_t *bcur;     // [n_buckets + 1] per-bucket write cursors
     int32_t *jlo_pos;  // [K][L] first balanced cut by island position (imbalance pruning)
     double *Wb[2];     // [nb][L+1][K] continuation rows, double-buffered by level
     uint16_t *argF;    // [D][nb][L][K]
@@ -145,13 +171,17 @@ struct Ws {
     double *rootF;     // [nb]
     int32_t *root_o;   // [nb]
     int32_t *root_d;   // [nb]
+    double *Rv;        // [D][nb] least bottleneck of a whole plan with d stages (phase 1, per level)
+    double *RF;        // [D][nb] least root fill with d stages (phase 2, per level)
+    int32_t *RO;       // [D][nb] its first position (least on ties), -1 if none
+    int32_t *dlim;     // [nb] deepest level whose root bottleneck reaches P* (0: no plan)
     int64_t *tmp;      // scan tiles
     size_t bytes;
 };
 
-static int64_t n_groups(const DevProblem &P) { return (int64_t)P.nb * P.NS * P.K; }
+__host__ __device__ inline int64_t n_groups(const DevProblem &P) { return (int64_t)P.nb * P.NS * P.K; }
 static int levels(const DevProblem &P) { return P.K < P.L ? P.K : P.L; }
-static int64_t n_buckets(const DevProblem &P) { return (int64_t)levels(P) * P.nb * P.L; }
+static int64_t n_rowev(const DevProblem &P) { return (int64_t)P.nb * P.L * (levels(P) + 1); }
 
 static Ws carve(const DevProblem &P, int64_t n, void *base) {
     Ws w{};
@@ -162,9 +192,9 @@ static Ws carve(const DevProblem &P, int64_t n, void *base) {
         off += align256(bytes > 0 ? bytes : 1);
         return r;
     };
-    const int64_t G = n_groups(P), D = levels(P), nbk = n_buckets(P);
+    const int64_t G = n_groups(P), D = levels(P);
     const int64_t rows = (int64_t)P.nb * (P.L + 1) * P.K;
-    const int64_t tiles = (std::max(G, nbk) + kScanTile - 1) / kScanTile + 1;
+    const int64_t tiles = (G + kScanTile - 1) / kScanTile + 1;
     const int64_t K2 = (int64_t)P.K * P.K;
     w.res = (ComposeResult *)take(sizeof(ComposeResult));
     w.order = (int32_t *)take(sizeof(int32_t) * P.K);
@@ -178,12 +208,13 @@ static Ws carve(const DevProblem &P, int64_t n, void *base) {
     w.ent_c = (double *)take(sizeof(double) * n);
     w.ent_d = (uint8_t *)take(n);
     w.ent_i = (int64_t *)take(sizeof(int64_t) * n);
-    w.bcnt = (int32_t *)take(sizeof(int32_t) * (nbk + 1));
+    w.rowev = (int32_t *)take(sizeof(int32_t) * n_rowev(P));
+    w.ev_total = (int32_t *)take(sizeof(int32_t));
     w.ev_cell = (int32_t *)take(sizeof(int32_t) * 2 * n);
     w.ev_val = (double *)take(sizeof(double) * 2 * n);
     w.T = (double *)take(sizeof(double) * G);
+    w.T0 = (double *)take(sizeof(double) * G);
     w.T1 = (double *)take(sizeof(double) * P.nb * P.L * P.K);
-    w.bcur = (int32_t *)take(sizeof(int32_t) * (nbk + 1));
     w.jlo_pos = (int32_t *)take(P.imb ? sizeof(int32_t) * P.K * P.L : 1);
     w.Wb[0] = (double *)take(sizeof(double) * rows);
     w.Wb[1] = (double *)take(sizeof(double) * rows);
@@ -193,6 +224,10 @@ static Ws carve(const DevProblem &P, int64_t n, void *base) {
     w.rootF = (double *)take(sizeof(double) * P.nb);
     w.root_o = (int32_t *)take(sizeof(int32_t) * P.nb);
     w.root_d = (int32_t *)take(sizeof(int32_t) * P.nb);
+    w.Rv = (double *)take(sizeof(double) * D * P.nb);
+    w.RF = (double *)take(sizeof(double) * D * P.nb);
+    w.RO = (int32_t *)take(sizeof(int32_t) * D * P.nb);
+    w.dlim = (int32_t *)take(sizeof(int32_t) * P.nb);
     w.tmp = (int64_t *)take(sizeof(int64_t) * tiles);
     w.bytes = off;
     return w;
@@ -242,37 +277,68 @@ __global__ __launch_bounds__(256) void jlo_kernel(DevProblem P, const int32_t *o
 // grouping: candidate list -> per-group entry records -> per-level events
 // ---------------------------------------------------------------------------
 // Reads each listed candidate's score once (the list is ascending, so the
-// reads walk the score arrays forward) and counts the group sizes.
+// reads walk the score arrays forward) and counts the group sizes.  A thread
+// takes kGatherPer entries, a block's threads apart, with all their loads in
+// flight together.
+constexpr int kGatherPer = 4;
+constexpr int kGatherBlock = 256 * kGatherPer;
+
 __global__ __launch_bounds__(256) void gather_kernel(DevProblem P, const int64_t *surv, int64_t n,
                                                      const double *cost, const uint8_t *dmax, const int32_t *pos,
                                                      int32_t *rec_g, double *rec_c, uint8_t *rec_d, int32_t *gcnt,
                                                      ComposeResult *res) {
-    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
-        int32_t G = -1;
-        const int64_t idx = surv[r];
-        if (idx < 0 || idx >= P.N || (r > 0 && surv[r - 1] >= idx)) {
-            atomicOr(&res->err, 1);
-        } else {
-            const int64_t g = idx / P.NS, s = idx - g * P.NS;
-            const Coef &c = P.coef[g];
-            const uint32_t ij = P.sij[s];
-            if (c.b_idx < 0 || !slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), c.k)) {
-                atomicOr(&res->err, 2);
-            } else {
-                // scores by candidate, or by class candidate (equal on every
-                // slice of the class)
-                const int64_t si = P.class_scores ? g * P.NC + P.cls[s] : idx;
-                const uint8_t d = dmax[si];
-                if (d > 0) {
-                    G = (int32_t)group_id(P, pos[c.k], c.b_idx, s);
-                    rec_c[r] = cost[si];
-                    rec_d[r] = d;
-                    atomicAdd(&gcnt[G], 1);
-                }
-            }
-        }
-        rec_g[r] = G;
+    const int64_t r0 = (int64_t)blockIdx.x * kGatherBlock + threadIdx.x;
+    int64_t idx[kGatherPer], prev[kGatherPer];
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) {
+        const int64_t r = r0 + u * 256;
+        idx[u] = r < n ? surv[r] : 0;
+        prev[u] = (r < n && r > 0) ? surv[r - 1] : -1;
     }
+    int32_t G[kGatherPer];
+    int64_t si[kGatherPer];
+    int err = 0;
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) {
+        const int64_t r = r0 + u * 256;
+        G[u] = -1;
+        si[u] = -1;
+        if (r >= n) continue;
+        if (idx[u] < 0 || idx[u] >= P.N || prev[u] >= idx[u]) {
+            err |= 1;
+            continue;
+        }
+        const int64_t g = idx[u] / P.NS, s = idx[u] - g * P.NS;
+        const Coef &c = P.coef[g];
+        const uint32_t ij = P.sij[s];
+        if (c.b_idx < 0 || !slice_balanced(P, P.pre, (int)(ij & 0xFFFFu), (int)(ij >> 16), c.k)) {
+            err |= 2;
+            continue;
+        }
+        G[u] = (int32_t)group_id(P, pos[c.k], c.b_idx, s);
+        // scores by candidate, or by class candidate (equal on every slice of the class)
+        si[u] = P.class_scores ? g * P.NC + P.cls[s] : idx[u];
+    }
+    uint8_t d[kGatherPer];
+    double cv[kGatherPer];
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) {
+        d[u] = si[u] >= 0 ? dmax[si[u]] : 0;
+        cv[u] = si[u] >= 0 ? cost[si[u]] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) {
+        const int64_t r = r0 + u * 256;
+        if (r >= n) continue;
+        if (d[u] == 0) G[u] = -1;  // fits nowhere: not a group entry
+        if (G[u] >= 0) {
+            rec_c[r] = cv[u];
+            rec_d[r] = d[u];
+            atomicAdd(&gcnt[G[u]], 1);
+        }
+        rec_g[r] = G[u];
+    }
+    if (err) atomicOr(&res->err, err);
 }
 
 __global__ __launch_bounds__(256) void scatter_kernel(const int64_t *surv, int64_t n, const int32_t *rec_g,
@@ -296,56 +362,15 @@ void launch_grouping(const DevProblem &P, const int64_t *surv, int64_t n, const 
     const int64_t G = n_groups(P);
     fill<int32_t>(g.gcnt, G, 0, s);
     if (n > 0) {
-        int64_t blocks = (n + 255) / 256;
-        if (blocks > 65536) blocks = 65536;
+        const int64_t blocks = (n + kGatherBlock - 1) / kGatherBlock;
         gather_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, surv, n, cost, dmax, pos, g.rec_g, g.rec_c,
                                                                     g.rec_d, g.gcnt, res);
         scan_i32(g.gcnt, G, g.tmp, s);
-        scatter_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(surv, n, g.rec_g, g.rec_c, g.rec_d, g.gcnt,
-                                                                     g.ent_c, g.ent_d, g.ent_i);
+        const int64_t sblocks = std::min<int64_t>((n + 255) / 256, 65536);
+        scatter_kernel<<<dim3((unsigned)sblocks), dim3(256), 0, s>>>(surv, n, g.rec_g, g.rec_c, g.rec_d, g.gcnt,
+                                                                      g.ent_c, g.ent_d, g.ent_i);
     } else {
         scan_i32(g.gcnt, G, g.tmp, s);  // all zeros: offsets stay zero
-    }
-}
-
-// Starting tables.  Depth 1 is read only for the slices (i, L) (a single
-// stage covers the rest of the model), so those values go to a small table
-// T1[b][i][o]; the full table starts at depth 2.  A block transposes a tile
-// of 64 slices x 32 positions of one b through LDS, so it reads the group
-// offsets along slices and writes the table along positions.
-constexpr int kTileS = 64, kTileO = 32;
-
-__global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *__restrict__ gcnt,
-                                                  const double *__restrict__ ent_c, const uint8_t *__restrict__ ent_d,
-                                                  double *__restrict__ T, double *__restrict__ T1) {
-    __shared__ double tile[kTileO][kTileS + 1];
-    const int64_t s0 = (int64_t)blockIdx.x * kTileS;
-    const int o0 = blockIdx.y * kTileO, bi = blockIdx.z;
-    for (int t = threadIdx.x; t < kTileS * kTileO; t += blockDim.x) {
-        const int sl = t % kTileS, ol = t / kTileS;
-        const int64_t s = s0 + sl;
-        const int o = o0 + ol;
-        double v2 = kInf;
-        if (s < P.NS && o < P.K) {
-            const int64_t G = group_id(P, o, bi, s);
-            const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
-            double v1 = kInf;
-            for (int32_t e = st; e < en; ++e) {
-                const double c = ent_c[e];
-                v1 = fmin(v1, c);
-                if (ent_d[e] >= 2) v2 = fmin(v2, c);
-            }
-            const uint32_t ij = P.sij[s];
-            if ((int)(ij >> 16) == P.L) T1[((int64_t)bi * P.L + (ij & 0xFFFFu)) * P.K + o] = v1;
-        }
-        tile[ol][sl] = v2;
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < kTileS * kTileO; t += blockDim.x) {
-        const int ol = t % kTileO, sl = t / kTileO;
-        const int64_t s = s0 + sl;
-        const int o = o0 + ol;
-        if (s < P.NS && o < P.K) T[cell_id(P, bi, s, o)] = tile[ol][sl];
     }
 }
 
@@ -353,13 +378,17 @@ __global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *_
 // D_e = the largest d_max among entries with a smaller key; it sets T at
 // level D_e + 1.  After the group's largest d_max M nothing fits: T = +inf
 // from level M + 1.  At most one change per (group, level).  Levels 1 and 2
-// come from table_init, so only changes at levels >= 3 become events.
-constexpr int kGroupRegs = 8;
+// come from the starting tables, so only changes at levels >= 3 become
+// events.  Also returns the starting values: v1 the least cost of the group
+// (depth 1), v2 the least cost fitting at depth 2.
+constexpr int kGroupRegs = 4;
 
 template <typename Emit>
 __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const double *__restrict__ ent_c,
                                    const uint8_t *__restrict__ ent_d, const int64_t *__restrict__ ent_i, int64_t G,
-                                   int D, Emit emit) {
+                                   int D, double &v1, double &v2, Emit emit) {
+    v1 = kInf;
+    v2 = kInf;
     const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
     if (st == en) return;
     int M = 0;
@@ -379,6 +408,8 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
         for (int e = 0; e < kGroupRegs; ++e) {
             if (e >= n) break;
             M = max(M, d[e]);
+            v1 = fmin(v1, c[e]);
+            if (d[e] >= 2) v2 = fmin(v2, c[e]);
             int De = 0;
 #pragma unroll
             for (int q = 0; q < kGroupRegs; ++q) {
@@ -394,6 +425,8 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
             const int de = ent_d[e];
             const int64_t ie = ent_i[e];
             M = max(M, de);
+            v1 = fmin(v1, ce);
+            if (de >= 2) v2 = fmin(v2, ce);
             int De = 0;
             for (int32_t q = st; q < en; ++q) {
                 const double cq = ent_c[q];
@@ -407,59 +440,115 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
     if (M >= 2 && M + 1 <= D) emit(M + 1, kInf);
 }
 
-// Events are bucketed by (level, b, first layer i).  A row's cells (slices
-// starting at i, times positions) are split over `nch` blocks of at most
-// kEventCells cells; a block counts its events per level in LDS.  The count
-// pass adds the block's counts to the buckets; the emit pass recounts,
-// reserves its ranges from per-bucket cursors and writes.  The order of
-// events inside a bucket does not matter: they touch distinct cells.
-constexpr int kEventCells = 1024;
+// Starting tables and events, one block per row (b, first layer i): its
+// cells are the slices starting at i times the positions, taken in tiles of
+// 64 slices x 16 positions.  A wave reads the offsets and entries of 64
+// consecutive groups (the group order runs along slices) and the block writes
+// the tile through LDS along positions (the table order), 128-byte runs.  A
+// first sweep writes the starting stage table (depth 2; two copies, one per
+// phase) and, for the slice (i, L), the depth-1 table T1[b][i][o], and counts
+// the row's events per level in LDS; the block then reserves one range for
+// all of them (one atomic) and records where each level's events start in
+// rowev[b][i][.]; a second sweep (whose reads hit the caches) writes the
+// events grouped by level.  The level kernel that owns row i at level d then
+// applies the events of level d + 1 from one contiguous range.
+constexpr int kRowThreads = 1024;
+constexpr int kRowTileS = 64, kRowTileO = kRowThreads / kRowTileS;
 
-template <bool kEmit>
-__global__ __launch_bounds__(256) void group_events(DevProblem P, int nch, const int32_t *__restrict__ gcnt,
-                                                    const double *__restrict__ ent_c,
-                                                    const uint8_t *__restrict__ ent_d,
-                                                    const int64_t *__restrict__ ent_i, int32_t *bcnt,
-                                                    int32_t *__restrict__ ev_cell, double *__restrict__ ev_val) {
+// 16-wave blocks at 8 waves per SIMD: two blocks per CU (64 VGPRs), so one
+// block's tile barriers overlap the other's loads
+__global__ __launch_bounds__(kRowThreads, 8) void row_tables(DevProblem P, const int32_t *__restrict__ gcnt,
+                                                             const double *__restrict__ ent_c,
+                                                             const uint8_t *__restrict__ ent_d,
+                                                             const int64_t *__restrict__ ent_i,
+                                                             double *__restrict__ T, double *__restrict__ T0,
+                                                             double *__restrict__ T1, int32_t *rowev,
+                                                             int32_t *ev_total, int32_t *__restrict__ ev_cell,
+                                                             double *__restrict__ ev_val) {
     __shared__ int32_t hist[256];
-    __shared__ int32_t base[256];
-    const int i = blockIdx.x / nch, ch = blockIdx.x % nch, bi = blockIdx.y;
+    __shared__ int64_t scan_lds[kRowThreads / kWave + 1];
+    __shared__ double tile[kRowTileO][kRowTileS + 1];
+    __shared__ int32_t base;
+    const int i = blockIdx.x, bi = blockIdx.y;
     const int L = P.L, K = P.K;
     const int D = K < L ? K : L;
     const int64_t s0 = slice_of(L, i, i + 1);
-    const int64_t n_sl = L - i;
-    const int64_t ncell = n_sl * K;
-    const int64_t per = (ncell + nch - 1) / nch;
-    const int64_t c0 = (int64_t)ch * per, c1 = min(ncell, c0 + per);
-    if (c0 >= c1) return;
-    for (int lev = threadIdx.x; lev < D; lev += blockDim.x) hist[lev] = 0;
+    const int n_sl = L - i;
+    const int64_t t1row = ((int64_t)bi * L + i) * K;
+    const int ol = threadIdx.x / kRowTileS, jl = threadIdx.x % kRowTileS;  // reading: 64 slices per wave
+    const int ow = threadIdx.x % kRowTileO, jw = threadIdx.x / kRowTileO;  // writing: 16 positions per run
+    for (int lev = threadIdx.x; lev < 256; lev += kRowThreads) hist[lev] = 0;
     __syncthreads();
-    auto bucket = [&](int lev) { return ((int64_t)lev * P.nb + bi) * L + i; };  // lev = level - 1
-    for (int64_t t = c0 + threadIdx.x; t < c1; t += blockDim.x) {
-        const int64_t o = t / n_sl, s = s0 + (t - o * n_sl);
-        cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s), D,
-                    [&](int level, double) { atomicAdd(&hist[level - 1], 1); });
-    }
+    for (int j0 = 0; j0 < n_sl; j0 += kRowTileS)
+        for (int o0 = 0; o0 < K; o0 += kRowTileO) {
+            const int js = j0 + jl, o = o0 + ol;
+            double v2 = kInf;
+            if (js < n_sl && o < K) {
+                double v1;
+                cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s0 + js), D, v1, v2,
+                            [&](int level, double) { atomicAdd(&hist[level - 1], 1); });
+                if (js == n_sl - 1) T1[t1row + o] = v1;  // the slice (i, L)
+            }
+            tile[ol][jl] = v2;
+            __syncthreads();
+            const int jo = j0 + jw, oo = o0 + ow;
+            if (jo < n_sl && oo < K) {
+                const int64_t c = cell_id(P, bi, s0 + jo, oo);
+                const double v = tile[ow][jw];
+                T[c] = v;
+                T0[c] = v;
+            }
+            __syncthreads();
+        }
+    // the row's event range and the start of each level in it
+    const int lev = threadIdx.x;
+    const int64_t cnt = lev < D ? hist[lev] : 0;
+    int64_t total;
+    const int64_t off = block_excl_scan<int64_t>(cnt, scan_lds, &total);
+    if (threadIdx.x == 0) base = total ? atomicAdd(ev_total, (int32_t)total) : 0;
     __syncthreads();
-    if (!kEmit) {
-        for (int lev = threadIdx.x; lev < D; lev += blockDim.x)
-            if (hist[lev]) atomicAdd(&bcnt[bucket(lev)], hist[lev]);
-        return;
+    int32_t *re = rowev + ((int64_t)bi * L + i) * (D + 1);
+    if (lev < D) {
+        hist[lev] = base + (int32_t)off;
+        re[lev] = base + (int32_t)off;
     }
-    for (int lev = threadIdx.x; lev < D; lev += blockDim.x) {
-        base[lev] = hist[lev] ? atomicAdd(&bcnt[bucket(lev)], hist[lev]) : 0;
-        hist[lev] = 0;
-    }
+    if (lev == D) re[D] = base + (int32_t)total;
     __syncthreads();
-    for (int64_t t = c0 + threadIdx.x; t < c1; t += blockDim.x) {
-        const int64_t o = t / n_sl, s = s0 + (t - o * n_sl);
-        const int64_t cell = cell_id(P, bi, s, o);
-        cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s), D, [&](int level, double v) {
-            const int32_t slot = base[level - 1] + atomicAdd(&hist[level - 1], 1);
-            ev_cell[slot] = (int32_t)cell;
-            ev_val[slot] = v;
-        });
+    if (total == 0) return;
+    for (int j0 = 0; j0 < n_sl; j0 += kRowTileS)
+        for (int o0 = 0; o0 < K; o0 += kRowTileO) {
+            const int js = j0 + jl, o = o0 + ol;
+            if (js >= n_sl || o >= K) continue;
+            const int64_t c = cell_id(P, bi, s0 + js, o);
+            double v1, v2;
+            cell_events(gcnt, ent_c, ent_d, ent_i, group_id(P, o, bi, s0 + js), D, v1, v2, [&](int level, double v) {
+                const int32_t slot = atomicAdd(&hist[level - 1], 1);
+                ev_cell[slot] = (int32_t)c;
+                ev_val[slot] = v;
+            });
+        }
+}
+
+// The starting tables again (the relaxed search reruns the fill from them):
+// depth 2 for every cell, depth 1 for the slices (i, L).  Thread per group,
+// in group order.
+__global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *__restrict__ gcnt,
+                                                  const double *__restrict__ ent_c, const uint8_t *__restrict__ ent_d,
+                                                  double *__restrict__ T, double *__restrict__ T1) {
+    const int64_t G = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (G >= n_groups(P)) return;
+    const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
+    double v1 = kInf, v2 = kInf;
+    for (int32_t e = st; e < en; ++e) {
+        const double x = ent_c[e];
+        v1 = fmin(v1, x);
+        if (ent_d[e] >= 2) v2 = fmin(v2, x);
     }
+    const int64_t s = G % P.NS, ob = G / P.NS;
+    const int64_t bi = ob % P.nb, o = ob / P.nb;
+    T[cell_id(P, bi, s, o)] = v2;
+    const uint32_t ij = P.sij[s];
+    if ((int)(ij >> 16) == P.L) T1[((int64_t)bi * P.L + (ij & 0xFFFFu)) * P.K + o] = v1;
 }
 
 // ---------------------------------------------------------------------------
@@ -489,34 +578,37 @@ struct RowEvents {
     double v[kEvRegs];
 };
 
-__device__ inline void event_bounds(RowEvents &R, const DevProblem &P, int d, int bi, int i, const int32_t *bcnt) {
+// The events of level d + 1 in row (b, i): rowev[b][i][d] .. rowev[b][i][d + 1].
+__device__ inline void event_bounds(RowEvents &R, const DevProblem &P, int d, int bi, int i, const int32_t *rowev) {
     const int D = P.K < P.L ? P.K : P.L;
     R.st = 0;
     R.en = 0;
     if (d < D) {
-        const int64_t bucket = ((int64_t)d * P.nb + bi) * P.L + i;
-        R.st = bcnt[bucket];
-        R.en = bcnt[bucket + 1];
+        const int32_t *re = rowev + ((int64_t)bi * P.L + i) * (D + 1);
+        R.st = re[d];
+        R.en = re[d + 1];
     }
 }
 
+template <int THREADS>
 __device__ inline void load_events(RowEvents &R, const int32_t *__restrict__ ev_cell,
                                    const double *__restrict__ ev_val) {
 #pragma unroll
     for (int k = 0; k < kEvRegs; ++k) {
-        const int32_t e = R.st + (int32_t)threadIdx.x + k * (int32_t)blockDim.x;
+        const int32_t e = R.st + (int32_t)threadIdx.x + k * THREADS;
         R.c[k] = e < R.en ? ev_cell[e] : -1;
         R.v[k] = e < R.en ? ev_val[e] : 0.0;
     }
 }
 
+template <int THREADS>
 __device__ inline void store_events(const RowEvents &R, const int32_t *__restrict__ ev_cell,
                                     const double *__restrict__ ev_val, double *__restrict__ T) {
 #pragma unroll
     for (int k = 0; k < kEvRegs; ++k)
         if (R.c[k] >= 0) T[R.c[k]] = R.v[k];
     // large buckets (the first levels): the rest in batches of loads in flight
-    const int32_t step = (int32_t)blockDim.x;
+    const int32_t step = THREADS;
     for (int32_t base = R.st + (int32_t)threadIdx.x + kEvRegs * step; base < R.en; base += kEvBatch * step) {
         int32_t c[kEvBatch];
         double v[kEvBatch];
@@ -680,6 +772,27 @@ __device__ inline void scan_next(int o, int sub, int top, const LiveList &lv, co
     }
 }
 
+// Least value over a wave.
+__device__ inline double wave_min(double v) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v = fmin(v, __shfl_xor(v, off));
+    return v;
+}
+
+// Least (value, index) pair over a wave: the smaller value, ties to the
+// smaller index.
+__device__ inline void wave_min_arg(double &v, int &a) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double v2 = __shfl_xor(v, off);
+        const int a2 = __shfl_xor(a, off);
+        if (v2 < v || (v2 == v && a2 < a)) {
+            v = v2;
+            a = a2;
+        }
+    }
+}
+
 // Sub-thread k of a cell scans j = i+1+k, i+1+k+SPLIT, ...  It may stop at
 // its own first T not below its own running best: everything it skips is no
 // smaller than that best, which it reached at a smaller j, so neither the
@@ -688,12 +801,14 @@ __device__ inline void scan_next(int o, int sub, int top, const LiveList &lv, co
 // Phase 1: bottleneck values.  KP = K padded to whole waves.
 template <int KP, int SPLIT>
 __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bottleneck(
-    DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
-    const double *T1, const double *Wprev, double *Wnext, const double *EoT, const uint8_t *EiT, double *Pst) {
+    DevProblem P, int d, const int32_t *rowev, const int32_t *ev_cell, const double *ev_val, double *T,
+    const double *T1, const double *Wprev, double *Wnext, const double *EoT, const uint8_t *EiT, double *Rv) {
+    constexpr int THREADS = SPLIT * KP;
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
     __shared__ double part[SPLIT][KP];
     __shared__ double Vs[KP];
+    __shared__ double wred[KP / kWave];
     __shared__ double xs[kMaxDistinctE];
     __shared__ uint64_t lmask[KP / kWave];
     __shared__ int32_t list[KP];
@@ -702,7 +817,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bot
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     const int top = K - d;
     RowEvents ev;
-    event_bounds(ev, P, d, bi, i, bcnt);
+    event_bounds(ev, P, d, bi, i, rowev);
     LinkRegs<SPLIT * KP, KP> lr;
     const Links X = load_links(lr, P, i, bi, top, EiT, EoT, xs, tri_s);
     const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);  // slice (i, j) is srow + j-i-1
@@ -741,22 +856,27 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bot
     store_links(lr, X, P, i, top, xs, tri_s);
     __syncthreads();
     // every read of this row's table is done
-    load_events(ev, ev_cell, ev_val);
+    load_events<THREADS>(ev, ev_cell, ev_val);
     if (sub == 0) {
         double m = part[0][o];
 #pragma unroll
         for (int k = 1; k < SPLIT; ++k) m = fmin(m, part[k][o]);
         Vs[o] = m;
         publish_live(o <= top && m < kInf, lmask);
+        if (i == 0) {  // the whole-plan bottleneck at this depth: least over first positions
+            const double r = wave_min(m);
+            if ((threadIdx.x & (kWave - 1)) == 0) wred[threadIdx.x / kWave] = r;
+        }
     }
     __syncthreads();
     if (i == 0) {
         if (threadIdx.x == 0) {
-            double m = kInf;
-            for (int t = 0; t < K; ++t) m = fmin(m, Vs[t]);
-            Pst[bi] = fmin(Pst[bi], m);
+            double m = wred[0];
+#pragma unroll
+            for (int u = 1; u < KP / kWave; ++u) m = fmin(m, wred[u]);
+            Rv[(int64_t)(d - 1) * P.nb + bi] = m;
         }
-        store_events(ev, ev_cell, ev_val, T);
+        store_events<THREADS>(ev, ev_cell, ev_val, T);
         return;
     }
     const LiveList lv = build_live<KP>(o, sub, top, lmask, list);
@@ -776,7 +896,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_bot
         for (int k = 1; k < SPLIT; ++k) m = fmin(m, part[k][o]);
         Wnext[((int64_t)bi * (L + 1) + i) * K + o] = m;
     }
-    store_events(ev, ev_cell, ev_val, T);
+    store_events<THREADS>(ev, ev_cell, ev_val, T);
 }
 
 // (value, index) pairs: the smaller value, ties to the smaller index.
@@ -786,7 +906,11 @@ __device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
 
 // Phase 2: fill values and argmins at a bound on every stage and link (the
 // bottleneck P* of phase 1, or a relaxed bound).  Block (i, b) with b's bound
-// bound[b]; a b whose bound is +inf is skipped.  With kJobs, block (i, job)
+// bound[b]; a b whose bound is +inf is skipped, and so is a level deeper than
+// dlim[b] when dlim is given (no whole plan of that depth stays within the
+// bound).  The first row's blocks record the level's least root fill and its
+// first position in RF/RO[d][b].
+// With kJobs, block (i, job)
 // computes fill values only for job = (job_b, job_tau): its own continuation
 // rows (Gprev/Gnext indexed by job), its least root fill in rootF[job], no
 // argmins.  Several jobs may share one b's table, so the row's table changes
@@ -795,15 +919,18 @@ __device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
 // and the last one writes the changes and resets the counter.
 template <int KP, int SPLIT, bool kJobs>
 __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fill(
-    DevProblem P, int d, const int32_t *bcnt, const int32_t *ev_cell, const double *ev_val, double *T,
+    DevProblem P, int d, const int32_t *rowev, const int32_t *ev_cell, const double *ev_val, double *T,
     const double *T1, const double *Gprev, double *Gnext, const double *EoT, const uint8_t *EiT, const double *bound,
     const int32_t *job_b, const double *job_tau, const int32_t *jobs_of_b, int32_t *row_cnt, uint16_t *argF,
-    uint8_t *argG, double *rootF, int32_t *root_o, int32_t *root_d) {
+    uint8_t *argG, double *rootF, const int32_t *dlim, double *RF, int32_t *RO) {
+    constexpr int THREADS = SPLIT * KP;
     extern __shared__ uint32_t tri_w[];
     uint8_t *tri_s = (uint8_t *)tri_w;
     __shared__ double part[SPLIT][KP];
     __shared__ int32_t parg[SPLIT][KP];
     __shared__ double Fs[KP];
+    __shared__ double wred[KP / kWave];
+    __shared__ int32_t wreo[KP / kWave];
     __shared__ double xs[kMaxDistinctE];
     __shared__ uint64_t lmask[KP / kWave];
     __shared__ int32_t list[KP];
@@ -814,9 +941,10 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     const int top = K - d;
     const double Ps = kJobs ? job_tau[row] : bound[bi];
-    if (!(Ps < kInf)) return;
+    const int dl = (kJobs || !dlim) ? INT_MAX : dlim[bi];
+    if (!(Ps < kInf) || d > dl) return;
     RowEvents ev;
-    event_bounds(ev, P, d, bi, i, bcnt);
+    event_bounds(ev, P, d, bi, i, rowev);
     LinkRegs<SPLIT * KP, KP> lr;
     const Links X = load_links(lr, P, i, bi, top, EiT, EoT, xs, tri_s);
     const int64_t srow = (int64_t)bi * P.NS + slice_of(L, i, i + 1);
@@ -876,7 +1004,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
         __syncthreads();
         apply = last_reader != 0;
     }
-    if (apply) load_events(ev, ev_cell, ev_val);
+    if (apply) load_events<THREADS>(ev, ev_cell, ev_val);
     if (sub == 0) {
         double m = part[0][o];
         int a = parg[0][o];
@@ -890,27 +1018,35 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
         if (!kJobs && o < K)
             argF[(((int64_t)(d - 1) * P.nb + bi) * L + i) * K + o] = (uint16_t)(m < kInf ? a : 0xFFFF);
         publish_live(o <= top && m < kInf, lmask);
+        if (i == 0) {  // the level's least root fill, ties to the least first position
+            double r = m;
+            int ro = m < kInf ? o : INT_MAX;
+            wave_min_arg(r, ro);
+            if ((threadIdx.x & (kWave - 1)) == 0) {
+                wred[threadIdx.x / kWave] = r;
+                wreo[threadIdx.x / kWave] = ro;
+            }
+        }
     }
     __syncthreads();
     if (i == 0) {
         if (threadIdx.x == 0) {
-            double m = kInf;
-            int mo = -1;
-            for (int t = 0; t < K; ++t)
-                if (Fs[t] < m) {
-                    m = Fs[t];
-                    mo = t;
+            double m = wred[0];
+            int mo = wreo[0];
+#pragma unroll
+            for (int u = 1; u < KP / kWave; ++u)
+                if (wred[u] < m || (wred[u] == m && wreo[u] < mo)) {
+                    m = wred[u];
+                    mo = wreo[u];
                 }
             if (kJobs) {
                 if (m < rootF[row]) rootF[row] = m;
-            } else if (mo >= 0 && (m < rootF[bi] || (m == rootF[bi] && mo < root_o[bi]))) {
-                // lexicographic (fill, position, depth); depths arrive in ascending order
-                rootF[bi] = m;
-                root_o[bi] = mo;
-                root_d[bi] = d;
+            } else {
+                RF[(int64_t)(d - 1) * P.nb + bi] = m;
+                RO[(int64_t)(d - 1) * P.nb + bi] = m < kInf ? mo : -1;
             }
         }
-        if (apply) store_events(ev, ev_cell, ev_val, T);
+        if (apply) store_events<THREADS>(ev, ev_cell, ev_val, T);
         if (kJobs && apply && threadIdx.x == 0) atomicExch(&row_cnt[(int64_t)bi * L + i], 0);
         return;
     }
@@ -946,8 +1082,56 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
         Gnext[((int64_t)row * (L + 1) + i) * K + o] = m;
         if (!kJobs) argG[(((int64_t)(d - 1) * P.nb + bi) * (L + 1) + i) * K + o] = (uint8_t)(m < kInf ? aa : 0xFF);
     }
-    if (apply) store_events(ev, ev_cell, ev_val, T);
+    if (apply) store_events<THREADS>(ev, ev_cell, ev_val, T);
     if (kJobs && apply && threadIdx.x == 0) atomicExch(&row_cnt[(int64_t)bi * L + i], 0);
+}
+
+// P*_b = least whole-plan bottleneck over the levels; dlim[b] = the deepest
+// level whose whole-plan bottleneck reaches P*_b (the fill of step (3) has
+// no plan deeper than that), 0 when b has no plan.  One wave per b.
+__global__ __launch_bounds__(256) void pst_kernel(DevProblem P, int D, const double *Rv, double *Pst,
+                                                  int32_t *dlim) {
+    const int bi = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (bi >= P.nb) return;
+    double m = kInf;
+    for (int d = lane; d < D; d += kWave) m = fmin(m, Rv[(int64_t)d * P.nb + bi]);
+    m = wave_min(m);
+    int top = 0;
+    for (int d = lane; d < D; d += kWave)
+        if (m < kInf && Rv[(int64_t)d * P.nb + bi] <= m) top = d + 1;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) top = max(top, __shfl_xor(top, off));
+    if (lane == 0) {
+        Pst[bi] = m;
+        dlim[bi] = top;
+    }
+}
+
+// The root of each b: the least fill over the levels, ties to the least first
+// position, then the least depth.  One wave per b.
+__global__ __launch_bounds__(256) void roots_kernel(DevProblem P, int D, const double *RF, const int32_t *RO,
+                                                    double *rootF, int32_t *root_o, int32_t *root_d) {
+    const int bi = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (bi >= P.nb) return;
+    double v = kInf;
+    int key = INT_MAX;  // position * 2^16 + level: (position, depth) in that order
+    for (int d = lane; d < D; d += kWave) {
+        const double f = RF[(int64_t)d * P.nb + bi];
+        const int o = RO[(int64_t)d * P.nb + bi];
+        const int k = o >= 0 ? (o << 16) | d : INT_MAX;
+        if (f < kInf && (f < v || (f == v && k < key))) {
+            v = f;
+            key = k;
+        }
+    }
+    wave_min_arg(v, key);
+    if (lane == 0) {
+        rootF[bi] = v;
+        root_o[bi] = v < kInf ? key >> 16 : -1;
+        root_d[bi] = v < kInf ? (key & 0xFFFF) + 1 : -1;
+    }
 }
 
 // Threads per cell for a level of `blocks` blocks: the most (up to 4) whose
@@ -1088,7 +1272,8 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
             const double E = EoT[(int64_t)o_next * K + o];
             link = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;
         }
-        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, i, j, o, order[o], d, bb, link, plan.stage[t], res);
+        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, group_id(P, o, bb, slice_of(L, i, j)), i, j, order[o], d, link,
+                      plan.stage[t], res);
     }
 }
 
@@ -1210,6 +1395,10 @@ __global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_
         }
 }
 
+// Pipelines of at least this many levels read the fill's depth limits back
+// before phase 2 and launch only the levels some b needs.
+constexpr int kSyncLevels = 64;
+
 // Sequencing of the composition kernels on one workspace.
 struct Driver {
     DevProblem P;  // this call's copy: carries the table of first balanced cuts by position
@@ -1218,43 +1407,30 @@ struct Driver {
     int D;
     int64_t rows;
     size_t tri_lds;
-    dim3 tgrid;
     int n_cu = 0;
 
     Driver(const DevProblem &P_, int64_t n_surv, void *ws, hipStream_t s_)
         : P(P_), w(carve(P_, n_surv, ws)), s(s_), D(levels(P_)), rows((int64_t)P_.nb * (P_.L + 1) * P_.K) {
         tri_lds = P.n_ev ? (size_t)(P.K * (P.K - 1) / 2 + 4) : 0;
         P.jlo_pos = P.imb ? w.jlo_pos : nullptr;
-        tgrid = dim3((unsigned)((P.NS + kTileS - 1) / kTileS), (unsigned)((P.K + kTileO - 1) / kTileO),
-                     (unsigned)P.nb);
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             n_cu = 0;
     }
 
-    // candidate list -> grouped entries -> per-level table changes
+    // candidate list -> grouped entries -> starting tables (one copy per
+    // phase) and per-row, per-level table changes
     void setup(const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax) {
-        const int64_t nbk = n_buckets(P);
         prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT,
                                                                                      w.EiT, w.res);
         if (P.imb)
             jlo_kernel<<<dim3((unsigned)((P.K * P.L + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.jlo_pos);
-        fill<int32_t>(w.bcnt, nbk + 1, 0, s);
-        fill<double>(w.Pst, P.nb, kInf, s);
+        fill<int32_t>(w.ev_total, 1, 0, s);
         const Groups g{w.rec_g, w.rec_c, w.rec_d, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.tmp};
         launch_grouping(P, surv, n_surv, cost, dmax, w.pos, g, w.res, s);
-        if (n_surv > 0) {
-            const int nch = (int)(((int64_t)P.L * P.K + kEventCells - 1) / kEventCells);
-            const dim3 egrid((unsigned)(P.L * nch), (unsigned)P.nb);
-            group_events<false><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcnt,
-                                                           w.ev_cell, w.ev_val);
-            scan_i32(w.bcnt, nbk + 1, w.tmp, s);
-            copy_kernel<int32_t><<<dim3((unsigned)((nbk + 1 + 255) / 256)), dim3(256), 0, s>>>(w.bcnt, w.bcur,
-                                                                                              nbk + 1);
-            group_events<true><<<egrid, dim3(256), 0, s>>>(P, nch, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.bcur,
-                                                          w.ev_cell, w.ev_val);
-        }
+        row_tables<<<dim3((unsigned)P.L, (unsigned)P.nb), dim3(kRowThreads), 0, s>>>(
+            P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.T, w.T0, w.T1, w.rowev, w.ev_total, w.ev_cell, w.ev_val);
     }
 
     template <typename F>
@@ -1278,13 +1454,18 @@ struct Driver {
         return blocks <= cap3 ? 3 : 2;
     }
 
-    void start_tables(double *G0, double *G1, int64_t n) {
-        table_init<<<tgrid, dim3(256), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.T, w.T1);
+    // the continuation rows start at +inf; with `table`, the starting stage
+    // table is rebuilt there first (the relaxed search reruns the fill)
+    void start_tables(double *G0, double *G1, int64_t n, double *table = nullptr) {
+        if (table)
+            table_init<<<dim3((unsigned)((n_groups(P) + 255) / 256)), dim3(256), 0, s>>>(P, w.gcnt, w.ent_c,
+                                                                                         w.ent_d, table, w.T1);
         fill<double>(G0, n, kInf, s);
         fill<double>(G1, n, kInf, s);
     }
 
-    // phase 1: least bottleneck per b into w.Pst
+    // phase 1: least bottleneck per b into w.Pst, the fill's depth limit per b
+    // into w.dlim
     void phase1() {
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
@@ -1297,7 +1478,7 @@ struct Driver {
                 auto go = [&](auto spc) {
                     constexpr int SP = decltype(spc)::value;
                     level_bottleneck<KP, SP><<<grid, dim3(SP * KP), tri_lds, s>>>(
-                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Wp, Wn, w.EoT, w.EiT, w.Pst);
+                        P, d, w.rowev, w.ev_cell, w.ev_val, w.T, w.T1, Wp, Wn, w.EoT, w.EiT, w.Rv);
                 };
                 if (sp == 4)
                     go(std::integral_constant<int, 4>{});
@@ -1307,17 +1488,39 @@ struct Driver {
                     go(std::integral_constant<int, 2>{});
             }
         });
+        pst_kernel<<<dim3((unsigned)((P.nb + 3) / 4)), dim3(256), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
     }
 
-    // phase 2 at bound[b] (+inf skips b): fills, argmins and roots per b
-    void phase2(const double *bound) {
-        fill<double>(w.rootF, P.nb, kInf, s);
-        fill<int32_t>(w.root_o, P.nb, -1, s);
-        fill<int32_t>(w.root_d, P.nb, -1, s);
+    // The deepest fill level any b needs.  Reading w.dlim back costs one host
+    // synchronisation (tens of microseconds of idle GPU), which pays only when
+    // many levels may be skipped: with fewer than kSyncLevels levels every
+    // level is launched and the blocks of a b past its limit leave at once.
+    hipError_t fill_levels(int *nlev) {
+        if (D < kSyncLevels) {
+            *nlev = D;
+            return hipSuccess;
+        }
+        std::vector<int32_t> dl(P.nb);
+        hipError_t e = hipMemcpyAsync(dl.data(), w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return e;
+        int n = 0;
+        for (int v : dl) n = std::max(n, std::min(v, D));
+        *nlev = n;
+        return hipSuccess;
+    }
+
+    // phase 2 at bound[b] (+inf skips b), levels 1..nlev, each b up to
+    // dlim[b] when given: fills, argmins and roots per b.  The stage table is
+    // phase 2's starting copy, or (fresh) rebuilt in phase 1's.
+    void phase2(const double *bound, const int32_t *dlim, int nlev, bool fresh = false) {
+        double *table = fresh ? w.T : w.T0;
+        fill<double>(w.RF, (int64_t)D * P.nb, kInf, s);
+        fill<int32_t>(w.RO, (int64_t)D * P.nb, -1, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(w.Wb[0], w.Wb[1], rows);
-            for (int d = 1; d <= D; ++d) {
+            start_tables(w.Wb[0], w.Wb[1], rows, fresh ? table : nullptr);
+            for (int d = 1; d <= nlev; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
                 const double *Gp = w.Wb[(d - 1) & 1];
@@ -1325,8 +1528,8 @@ struct Driver {
                 auto go = [&](auto spc) {
                     constexpr int SP = decltype(spc)::value;
                     level_fill<KP, SP, false><<<grid, dim3(SP * KP), tri_lds, s>>>(
-                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, bound, nullptr,
-                        nullptr, nullptr, nullptr, w.argF, w.argG, w.rootF, w.root_o, w.root_d);
+                        P, d, w.rowev, w.ev_cell, w.ev_val, table, w.T1, Gp, Gn, w.EoT, w.EiT, bound, nullptr,
+                        nullptr, nullptr, nullptr, w.argF, w.argG, nullptr, dlim, w.RF, w.RO);
                 };
                 if (sp == 4)
                     go(std::integral_constant<int, 4>{});
@@ -1336,6 +1539,8 @@ struct Driver {
                     go(std::integral_constant<int, 2>{});
             }
         });
+        roots_kernel<<<dim3((unsigned)((P.nb + 3) / 4)), dim3(256), 0, s>>>(P, D, w.RF, w.RO, w.rootF, w.root_o,
+                                                                            w.root_d);
     }
 
     // fill values only, for J <= kMaxJobs (b, bound) jobs staged in r
@@ -1345,7 +1550,7 @@ struct Driver {
         fill<int32_t>(r.row_cnt, (int64_t)P.nb * P.L, 0, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K);
+            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K, w.T);
             for (int d = 1; d <= D; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)J);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
@@ -1354,8 +1559,8 @@ struct Driver {
                 auto go = [&](auto spc) {
                     constexpr int SP = decltype(spc)::value;
                     level_fill<KP, SP, true><<<grid, dim3(SP * KP), tri_lds, s>>>(
-                        P, d, w.bcnt, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, nullptr, r.job_b,
-                        r.job_tau, r.jobs_of_b, r.row_cnt, nullptr, nullptr, r.job_F, nullptr, nullptr);
+                        P, d, w.rowev, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, nullptr, r.job_b,
+                        r.job_tau, r.jobs_of_b, r.row_cnt, nullptr, nullptr, r.job_F, nullptr, nullptr, nullptr);
                 };
                 if (sp == 4)
                     go(std::integral_constant<int, 4>{});
@@ -1384,7 +1589,10 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dr.phase1();
-    dr.phase2(dr.w.Pst);
+    int nlev = 0;
+    e = dr.fill_levels(&nlev);
+    if (e != hipSuccess) return e;
+    dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
     dr.finish(dr.w.Pst);
     return hipGetLastError();
 }
@@ -1422,7 +1630,10 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dr.phase1();
-    dr.phase2(dr.w.Pst);
+    int nlev = 0;
+    e = dr.fill_levels(&nlev);
+    if (e != hipSuccess) return e;
+    dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
     const int nb = P.nb;
     std::vector<double> Pst(nb), F0(nb);
     int32_t err = 0;
@@ -1597,7 +1808,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     bound[bstar] = bs[bstar].tau;
     e = hipMemcpyAsync(r.bound, bound.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return e;
-    dr.phase2(r.bound);
+    dr.phase2(r.bound, nullptr, dr.D, true);  // a relaxed bound: every level, from a rebuilt table
     dr.finish(r.bound);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host vectors above must outlive the copies

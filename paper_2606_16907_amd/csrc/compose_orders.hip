@@ -555,7 +555,8 @@ __global__ __launch_bounds__(kOrderFinishThreads) void orders_finish(
     for (int t = wv; t < S; t += kOrderFinishThreads / kWave) {
         const int d = S - t, i = st_i[t], j = st_j[t], k = st_k[t], kn = st_kn[t];
         const double link = d > 1 ? X[(((int64_t)bb * K + k) * K + kn) * (L + 1) + j] : 0.0;
-        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, i, j, k, k, d, bb, link, plan.stage[t], res);
+        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, group_id(P, k, bb, slice_of(P.L, i, j)), i, j, k, d, link,
+                      plan.stage[t], res);
     }
 }
 

@@ -10,7 +10,8 @@ namespace tg {
 
 // Groups (slice, island position, b) are numbered position-major, then b,
 // then slice: the candidate list runs through each config's slices in
-// ascending order, so building the groups touches consecutive counters.
+// ascending order, so building the groups touches consecutive counters
+// (their atomics stay within few cache lines).
 __host__ __device__ inline int64_t group_id(const DevProblem &P, int64_t o, int64_t bi, int64_t s) {
     return (o * P.nb + bi) * P.NS + s;
 }
@@ -48,14 +49,13 @@ void launch_grouping(const DevProblem &P, const int64_t *surv, int64_t n, const 
 // candidate fitting at d, its config and memory, written to sg by lane 0.
 // `link` is the transfer time to the next stage (0 for the last).  A group
 // with no fitting candidate sets res->err = 4 (the stage table said one fits).
+// G is the group's index in the grouped entries (callers number groups their
+// own way).
 __device__ inline void resolve_stage(const DevProblem &P, const int32_t *gcnt, const double *ent_c,
-                                     const uint8_t *ent_d, const int64_t *ent_i, int i, int j, int o,
-                                     int island, int d, int bb, double link, tg_stage &sg,
-                                     ComposeResult *res) {
+                                     const uint8_t *ent_d, const int64_t *ent_i, int64_t G, int i, int j,
+                                     int island, int d, double link, tg_stage &sg, ComposeResult *res) {
     const int L = P.L;
     const int lane = threadIdx.x % kWave;
-    const int64_t s = slice_of(L, i, j);
-    const int64_t G = group_id(P, o, bb, s);
     const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
     int64_t best = -1;
     double bc = kInf;
