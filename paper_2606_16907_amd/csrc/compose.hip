@@ -529,28 +529,6 @@ __global__ __launch_bounds__(kRowThreads, 8) void row_tables(DevProblem P, const
         }
 }
 
-// The starting tables again (the relaxed search reruns the fill from them):
-// depth 2 for every cell, depth 1 for the slices (i, L).  Thread per group,
-// in group order.
-__global__ __launch_bounds__(256) void table_init(DevProblem P, const int32_t *__restrict__ gcnt,
-                                                  const double *__restrict__ ent_c, const uint8_t *__restrict__ ent_d,
-                                                  double *__restrict__ T, double *__restrict__ T1) {
-    const int64_t G = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (G >= n_groups(P)) return;
-    const int32_t st = G ? gcnt[G - 1] : 0, en = gcnt[G];
-    double v1 = kInf, v2 = kInf;
-    for (int32_t e = st; e < en; ++e) {
-        const double x = ent_c[e];
-        v1 = fmin(v1, x);
-        if (ent_d[e] >= 2) v2 = fmin(v2, x);
-    }
-    const int64_t s = G % P.NS, ob = G / P.NS;
-    const int64_t bi = ob % P.nb, o = ob / P.nb;
-    T[cell_id(P, bi, s, o)] = v2;
-    const uint32_t ij = P.sij[s];
-    if ((int)(ij >> 16) == P.L) T1[((int64_t)bi * P.L + (ij & 0xFFFFu)) * P.K + o] = v1;
-}
-
 // ---------------------------------------------------------------------------
 // dynamic program, one launch per level
 // ---------------------------------------------------------------------------
@@ -911,12 +889,13 @@ __device__ inline bool lex_less(double v1, int a1, double v2, int a2) {
 // bound).  The first row's blocks record the level's least root fill and its
 // first position in RF/RO[d][b].
 // With kJobs, block (i, job)
-// computes fill values only for job = (job_b, job_tau): its own continuation
-// rows (Gprev/Gnext indexed by job), its least root fill in rootF[job], no
-// argmins.  Several jobs may share one b's table, so the row's table changes
-// are applied by the last of its jobs' blocks to finish reading: each block
-// counts itself on row_cnt[b][i] after its reads (jobs_of_b[b] blocks in all),
-// and the last one writes the changes and resets the counter.
+// computes fill values only for job = (job_b, job_tau) up to its depth limit
+// dlim[job]: its own continuation rows (Gprev/Gnext indexed by job), its least
+// root fill in rootF[job], no argmins.  Several jobs may share one b's table,
+// so the row's table changes are applied by the last of its jobs' blocks to
+// finish reading: each block counts itself on row_cnt[b][i] after its reads
+// (jobs_of_b[d-1][b] blocks in all: the jobs of b at least d deep), and the
+// last one writes the changes and resets the counter.
 template <int KP, int SPLIT, bool kJobs>
 __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fill(
     DevProblem P, int d, const int32_t *rowev, const int32_t *ev_cell, const double *ev_val, double *T,
@@ -941,7 +920,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
     const int o = threadIdx.x % KP, sub = threadIdx.x / KP;
     const int top = K - d;
     const double Ps = kJobs ? job_tau[row] : bound[bi];
-    const int dl = (kJobs || !dlim) ? INT_MAX : dlim[bi];
+    const int dl = !dlim ? INT_MAX : dlim[kJobs ? row : bi];
     if (!(Ps < kInf) || d > dl) return;
     RowEvents ev;
     event_bounds(ev, P, d, bi, i, rowev);
@@ -1000,7 +979,9 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
     // kernel boundary)
     bool apply = true;
     if (kJobs) {
-        if (threadIdx.x == 0) last_reader = atomicAdd(&row_cnt[(int64_t)bi * L + i], 1) == jobs_of_b[bi] - 1;
+        if (threadIdx.x == 0)
+            last_reader =
+                atomicAdd(&row_cnt[(int64_t)bi * L + i], 1) == jobs_of_b[(int64_t)(d - 1) * P.nb + bi] - 1;
         __syncthreads();
         apply = last_reader != 0;
     }
@@ -1288,15 +1269,17 @@ struct RelaxWs {
     int32_t *th_b;    // [n_surv] their b
     int32_t *th_cnt;  // [1]
     double *lo;       // [nb] P* per b (bounds must exceed it)
-    double *hi;       // [nb] T at P* per b
+    double *hi;       // [nb] the best T found so far
     double *mm1;      // [nb] m - 1 per b
     int32_t *job_b;   // [kMaxJobs]
-    int32_t *jobs_of_b;  // [nb] jobs of each b in the current run
+    int32_t *job_dlim;   // [kMaxJobs] deepest level with a whole plan within the job's bound
+    int32_t *jobs_of_b;  // [D][nb] jobs of each b at least d deep in the current run
     int32_t *row_cnt;    // [nb][L] readers done per row (job runs)
     double *job_tau;  // [kMaxJobs]
     double *job_F;    // [kMaxJobs]
     double *job_G;    // [2][kMaxJobs][L+1][K]
     double *bound;    // [nb]
+    double *Tp;       // [n_groups] pristine starting stage table (each fill run starts from it)
     size_t bytes;
 };
 
@@ -1317,12 +1300,14 @@ static RelaxWs carve_relax(const DevProblem &P, int64_t n, void *base) {
     r.hi = (double *)take(sizeof(double) * P.nb);
     r.mm1 = (double *)take(sizeof(double) * P.nb);
     r.job_b = (int32_t *)take(sizeof(int32_t) * kMaxJobs);
-    r.jobs_of_b = (int32_t *)take(sizeof(int32_t) * P.nb);
+    r.job_dlim = (int32_t *)take(sizeof(int32_t) * kMaxJobs);
+    r.jobs_of_b = (int32_t *)take(sizeof(int32_t) * levels(P) * P.nb);
     r.row_cnt = (int32_t *)take(sizeof(int32_t) * P.nb * P.L);
     r.job_tau = (double *)take(sizeof(double) * kMaxJobs);
     r.job_F = (double *)take(sizeof(double) * kMaxJobs);
     r.job_G = (double *)take(sizeof(double) * 2 * jrows);
     r.bound = (double *)take(sizeof(double) * P.nb);
+    r.Tp = (double *)take(sizeof(double) * n_groups(P));
     r.bytes = off;
     return r;
 }
@@ -1332,8 +1317,9 @@ size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv) {
 }
 
 // Stage costs that can serve as relaxed bounds for their b: above P*_b and
-// with (m-1) * cost below the iteration time at P*_b (a plan bounded by a
-// larger value cannot beat it, its fill being non-negative).  Every listed
+// with (m-1) * cost not above hi[b], the best iteration time found so far (a
+// plan bounded by a larger value cannot reach it, its fill being
+// non-negative).  Every listed
 // candidate that fits somewhere (a grouped record) is a candidate bound; one
 // thread per record, duplicates removed on the host.
 constexpr int kBoundRecs = 8;  // records per thread, loads in flight together
@@ -1370,7 +1356,7 @@ __global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_
             const double l = b < kMaxB ? slo[b] : lo[b];
             const double h = b < kMaxB ? shi[b] : hi[b];
             const double f = b < kMaxB ? smm[b] : mm1[b];
-            if (c[k] > l && c[k] < kInf && (f * c[k]) < h) {
+            if (c[k] > l && c[k] < kInf && (f * c[k]) <= h) {
                 bi[k] = b;
                 ++cnt;
             }
@@ -1454,12 +1440,8 @@ struct Driver {
         return blocks <= cap3 ? 3 : 2;
     }
 
-    // the continuation rows start at +inf; with `table`, the starting stage
-    // table is rebuilt there first (the relaxed search reruns the fill)
-    void start_tables(double *G0, double *G1, int64_t n, double *table = nullptr) {
-        if (table)
-            table_init<<<dim3((unsigned)((n_groups(P) + 255) / 256)), dim3(256), 0, s>>>(P, w.gcnt, w.ent_c,
-                                                                                         w.ent_d, table, w.T1);
+    // the continuation rows start at +inf
+    void start_tables(double *G0, double *G1, int64_t n) {
         fill<double>(G0, n, kInf, s);
         fill<double>(G1, n, kInf, s);
     }
@@ -1511,15 +1493,15 @@ struct Driver {
     }
 
     // phase 2 at bound[b] (+inf skips b), levels 1..nlev, each b up to
-    // dlim[b] when given: fills, argmins and roots per b.  The stage table is
-    // phase 2's starting copy, or (fresh) rebuilt in phase 1's.
-    void phase2(const double *bound, const int32_t *dlim, int nlev, bool fresh = false) {
-        double *table = fresh ? w.T : w.T0;
+    // dlim[b] when given: fills, argmins and roots per b, from the starting
+    // stage table in `table` (phase 2's own copy unless given).
+    void phase2(const double *bound, const int32_t *dlim, int nlev, double *table = nullptr) {
+        if (!table) table = w.T0;
         fill<double>(w.RF, (int64_t)D * P.nb, kInf, s);
         fill<int32_t>(w.RO, (int64_t)D * P.nb, -1, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(w.Wb[0], w.Wb[1], rows, fresh ? table : nullptr);
+            start_tables(w.Wb[0], w.Wb[1], rows);
             for (int d = 1; d <= nlev; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
@@ -1543,15 +1525,36 @@ struct Driver {
                                                                             w.root_d);
     }
 
-    // fill values only, for J <= kMaxJobs (b, bound) jobs staged in r
-    void phase2_jobs(RelaxWs &r, int J) {
+    // the starting stage table of the b with used[b] back into w.T from the
+    // pristine copy (layout [b][s][o]: one contiguous run per b)
+    hipError_t restore_tables(const double *Tp, const std::vector<char> &used) {
+        const size_t per_b = (size_t)P.NS * P.K;
+        for (int b0 = 0; b0 < P.nb;) {
+            if (!used[b0]) {
+                ++b0;
+                continue;
+            }
+            int b1 = b0;
+            while (b1 < P.nb && used[b1]) ++b1;
+            const hipError_t e = hipMemcpyAsync(w.T + per_b * b0, Tp + per_b * b0, sizeof(double) * per_b * (b1 - b0),
+                                                hipMemcpyDeviceToDevice, s);
+            if (e != hipSuccess) return e;
+            b0 = b1;
+        }
+        return hipSuccess;
+    }
+
+    // fill values only, for J <= kMaxJobs (b, bound) jobs staged in r, levels
+    // 1..nlev, each job up to its own depth limit, from the starting stage
+    // table in w.T
+    void phase2_jobs(RelaxWs &r, int J, int nlev) {
         const int64_t jrows = (int64_t)kMaxJobs * (P.L + 1) * P.K;
         fill<double>(r.job_F, J, kInf, s);
         fill<int32_t>(r.row_cnt, (int64_t)P.nb * P.L, 0, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K, w.T);
-            for (int d = 1; d <= D; ++d) {
+            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K);
+            for (int d = 1; d <= nlev; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)J);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
                 const double *Gp = r.job_G + ((d - 1) & 1) * jrows;
@@ -1560,7 +1563,7 @@ struct Driver {
                     constexpr int SP = decltype(spc)::value;
                     level_fill<KP, SP, true><<<grid, dim3(SP * KP), tri_lds, s>>>(
                         P, d, w.rowev, w.ev_cell, w.ev_val, w.T, w.T1, Gp, Gn, w.EoT, w.EiT, nullptr, r.job_b,
-                        r.job_tau, r.jobs_of_b, r.row_cnt, nullptr, nullptr, r.job_F, nullptr, nullptr, nullptr);
+                        r.job_tau, r.jobs_of_b, r.row_cnt, nullptr, nullptr, r.job_F, r.job_dlim, nullptr, nullptr);
                 };
                 if (sp == 4)
                     go(std::integral_constant<int, 4>{});
@@ -1604,19 +1607,39 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
 // (u, v] the iteration time is at least (m-1) * (its first bound) + F(v): the
 // search evaluates F at up to kSplitWays points per open interval per round
 // (all jobs of a round in one batched run), drops an interval when that lower
-// bound cannot beat the best found (ties go to the smaller bound) or when F is
-// equal at both ends, and splits the rest.  The result is the least T, ties
-// to the smallest bound, as a plain ascending sweep would find.
+// bound cannot beat the best (T, b, bound) found over every b (ties go to the
+// smaller b, then the smaller bound) or when F is equal at both ends, and
+// splits the rest.  Only b* needs its exact optimum: any other b is dropped
+// once it cannot beat the incumbent.  The result is the least (T, b, bound),
+// as a plain ascending sweep of every b would find.
 constexpr int kSplitWays = 8;
 
 struct BSearch {
     bool active = false;
-    double Pst = 0, F0 = 0, mm1 = 0, best = 0, tau = 0;
+    double Pst = 0, F0 = 0, mm1 = 0;
     std::vector<double> th;  // distinct bounds above P*, ascending
     std::vector<double> F;   // F at th[k], NaN if unknown
     std::vector<std::pair<int, int>> iv;  // open intervals (a, c]: F(a) known (a = -1 is P*)
     double Fat(int k) const { return k < 0 ? F0 : F[k]; }
     double tat(int k) const { return k < 0 ? Pst : th[k]; }
+};
+
+// The incumbent over every b: least T, ties to the least b, then the least
+// bound.
+struct Incumbent {
+    double T = kInf;
+    int b = INT_MAX;
+    double tau = kInf;
+    bool beaten_by(double T2, int b2, double tau2) const {
+        return T2 < T || (T2 == T && (b2 < b || (b2 == b && tau2 < tau)));
+    }
+    void offer(double T2, int b2, double tau2) {
+        if (beaten_by(T2, b2, tau2)) {
+            T = T2;
+            b = b2;
+            tau = tau2;
+        }
+    }
 };
 
 hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
@@ -1628,17 +1651,20 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     if (rounds_out) *rounds_out = 0;
     dr.setup(surv, n_surv, cost, dmax);
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(r.Tp, dr.w.T0, sizeof(double) * n_groups(P), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
     dr.phase1();
     int nlev = 0;
     e = dr.fill_levels(&nlev);
     if (e != hipSuccess) return e;
     dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
-    const int nb = P.nb;
-    std::vector<double> Pst(nb), F0(nb);
+    const int nb = P.nb, D = dr.D;
+    std::vector<double> Pst(nb), F0(nb), Rv((size_t)D * nb);
     int32_t err = 0;
     e = hipMemcpyAsync(Pst.data(), dr.w.Pst, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(F0.data(), dr.w.rootF, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(Rv.data(), dr.w.Rv, sizeof(double) * D * nb, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(&err, &dr.w.res->err, sizeof(err), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return e;
@@ -1646,20 +1672,35 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         dr.finish(dr.w.Pst);
         return hipGetLastError();
     }
+    // the fill at bound tau has no whole plan deeper than the deepest level
+    // whose least whole-plan bottleneck (phase 1) is within tau: its levels
+    // stop there
+    auto dlim_of = [&](int bi, double tau) {
+        int top = 0;
+        for (int d = 1; d <= D; ++d)
+            if (Rv[(size_t)(d - 1) * nb + bi] <= tau) top = d;
+        return top;
+    };
     std::vector<BSearch> bs(nb);
-    std::vector<double> hi(nb, -kInf), mm1(nb, 0.0);
-    bool any = false;
+    std::vector<double> mm1(nb, 0.0);
+    Incumbent inc;
     for (int bi = 0; bi < nb; ++bi) {
         BSearch &q = bs[bi];
         const int64_t m = H.B / H.bvals[bi];
         q.mm1 = mm1[bi] = (double)(m - 1);
         if (!(Pst[bi] < kInf) || !(F0[bi] < kInf)) continue;
-        q.active = any = true;
+        q.active = true;
         q.Pst = Pst[bi];
         q.F0 = F0[bi];
-        q.best = (q.mm1 * q.Pst) + q.F0;
-        q.tau = q.Pst;
-        hi[bi] = q.best;
+        inc.offer((q.mm1 * q.Pst) + q.F0, bi, q.Pst);
+    }
+    // a bound tau of b gives T >= (m-1) tau (the fill is non-negative): b
+    // takes part only while (m-1) P*_b can still reach the incumbent
+    bool any = false;
+    for (int bi = 0; bi < nb; ++bi) {
+        BSearch &q = bs[bi];
+        if (q.active && !((q.mm1 * q.Pst) <= inc.T)) q.active = false;
+        any = any || q.active;
     }
     if (any) {
         // candidate bounds: stage costs (device) and link times (host)
@@ -1667,6 +1708,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         for (int bi = 0; bi < nb; ++bi)
             if (!bs[bi].active) lo[bi] = kInf;
         e = hipMemcpyAsync(r.lo, lo.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+        std::vector<double> hi(nb, inc.T);
         if (e == hipSuccess) e = hipMemcpyAsync(r.hi, hi.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
         if (e == hipSuccess) e = hipMemcpyAsync(r.mm1, mm1.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
         if (e != hipSuccess) return e;
@@ -1714,7 +1756,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
                 auto it = std::partition_point(oa.begin(), oa.end(), [&](int64_t a) { return !(x_of(a) > q.Pst); });
                 for (; it != oa.end(); ++it) {
                     const double x = x_of(*it);
-                    if (!(x < kInf) || !((q.mm1 * x) < q.best)) break;
+                    if (!(x < kInf) || !((q.mm1 * x) <= inc.T)) break;
                     q.th.push_back(x);
                 }
             }
@@ -1746,18 +1788,28 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
             if (rounds_out) *rounds_out = round + 1;
             for (size_t c0 = 0; c0 < req.size(); c0 += kMaxJobs) {
                 const int J = (int)std::min<size_t>(kMaxJobs, req.size() - c0);
-                std::vector<int32_t> jb(J), nj(nb, 0);
+                std::vector<int32_t> jb(J), jd(J);
                 std::vector<double> jt(J), jf(J);
+                int nlev_j = 0;
                 for (int t = 0; t < J; ++t) {
                     jb[t] = req[c0 + t].first;
                     jt[t] = bs[jb[t]].th[req[c0 + t].second];
-                    ++nj[jb[t]];
+                    jd[t] = dlim_of(jb[t], jt[t]);
+                    nlev_j = std::max(nlev_j, jd[t]);
                 }
+                std::vector<int32_t> nj((size_t)std::max(nlev_j, 1) * nb, 0);
+                for (int t = 0; t < J; ++t)
+                    for (int d = 1; d <= jd[t]; ++d) ++nj[(size_t)(d - 1) * nb + jb[t]];
                 e = hipMemcpyAsync(r.job_b, jb.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, s);
-                if (e == hipSuccess) e = hipMemcpyAsync(r.jobs_of_b, nj.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess) e = hipMemcpyAsync(r.job_dlim, jd.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess)
+                    e = hipMemcpyAsync(r.jobs_of_b, nj.data(), sizeof(int32_t) * nj.size(), hipMemcpyHostToDevice, s);
                 if (e == hipSuccess) e = hipMemcpyAsync(r.job_tau, jt.data(), sizeof(double) * J, hipMemcpyHostToDevice, s);
+                std::vector<char> used(nb, 0);
+                for (int t = 0; t < J; ++t) used[jb[t]] = 1;
+                if (e == hipSuccess) e = dr.restore_tables(r.Tp, used);
                 if (e != hipSuccess) return e;
-                dr.phase2_jobs(r, J);
+                dr.phase2_jobs(r, J, nlev_j);
                 e = hipMemcpyAsync(jf.data(), r.job_F, sizeof(double) * J, hipMemcpyDeviceToHost, s);
                 if (e == hipSuccess) e = hipStreamSynchronize(s);
                 if (e != hipSuccess) return e;
@@ -1765,11 +1817,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
                     BSearch &q = bs[jb[t]];
                     const int k = req[c0 + t].second;
                     q.F[k] = jf[t];
-                    const double Tt = (q.mm1 * q.th[k]) + jf[t];
-                    if (Tt < q.best || (Tt == q.best && q.th[k] < q.tau)) {
-                        q.best = Tt;
-                        q.tau = q.th[k];
-                    }
+                    inc.offer((q.mm1 * q.th[k]) + jf[t], jb[t], q.th[k]);
                 }
             }
             for (int bi = 0; bi < nb; ++bi) {
@@ -1783,7 +1831,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
                         const int v = k;
                         if (v > u + 1 && q.Fat(u) != q.F[v]) {
                             const double lb = (q.mm1 * q.th[u + 1]) + q.F[v];
-                            if (lb < q.best || (lb == q.best && q.th[u + 1] < q.tau)) next.push_back({u, v});
+                            if (inc.beaten_by(lb, bi, q.th[u + 1])) next.push_back({u, v});
                         }
                         u = v;
                     }
@@ -1793,22 +1841,22 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         }
     }
     // the best b and its bound: reuse the phase-2 argmins when the bound is P*
-    int bstar = -1;
-    double bestT = kInf;
-    for (int bi = 0; bi < nb; ++bi)
-        if (bs[bi].active && bs[bi].best < bestT) {
-            bestT = bs[bi].best;
-            bstar = bi;
-        }
-    if (bstar < 0 || bs[bstar].tau == bs[bstar].Pst) {
+    const int bstar = inc.T < kInf ? inc.b : -1;
+    if (bstar < 0 || inc.tau == Pst[bstar]) {
         dr.finish(dr.w.Pst);
         return hipGetLastError();
     }
     std::vector<double> bound(nb, kInf);
-    bound[bstar] = bs[bstar].tau;
+    std::vector<int32_t> fdl(nb, 0);
+    bound[bstar] = inc.tau;
+    fdl[bstar] = dlim_of(bstar, inc.tau);
     e = hipMemcpyAsync(r.bound, bound.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(dr.w.dlim, fdl.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+    std::vector<char> used(nb, 0);
+    used[bstar] = 1;
+    if (e == hipSuccess) e = dr.restore_tables(r.Tp, used);
     if (e != hipSuccess) return e;
-    dr.phase2(r.bound, nullptr, dr.D, true);  // a relaxed bound: every level, from a rebuilt table
+    dr.phase2(r.bound, dr.w.dlim, fdl[bstar], dr.w.T);  // the relaxed bound
     dr.finish(r.bound);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host vectors above must outlive the copies
