@@ -463,6 +463,7 @@ void tg_problem_destroy(tg_problem *p) {
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(p->device);
     (void)hipFree(p->dev_block);
+    p->relax_stage.release();
     (void)hipSetDevice(cur);
     delete p;
 }
@@ -727,7 +728,10 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
                                  need, s);
     if (st != TG_OK) return st;
     return no_throw([&] {
-        const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B};
+        std::lock_guard<std::mutex> lock(p->relax_mu);  // one relaxed call at a time uses the handle's staging
+        const hipError_t es = p->relax_stage.reserve(tg::compose_relaxed_stage_bytes(p->P));
+        if (es != hipSuccess) return hip_fail(es, "pinned host staging");
+        const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B, &p->relax_stage};
         tg::ComposeResult *res_dev = nullptr;
         int rounds = 0;
         hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax,

@@ -1264,6 +1264,55 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
 // Workspace of the relaxed search, after the composition workspace.
 constexpr int kMaxJobs = 128;  // fill evaluations per launch
 
+constexpr int64_t kSpecBounds = 4096;  // collected bounds read back with the phase results
+
+// Byte offsets of the relaxed search's packed transfers.  The device read-back
+// and upload regions and the pinned host buffer share the layout, so each
+// transfer is one copy: `down` (after phase 2: phase results, the collected
+// bound count and the first kSpecBounds bounds), `up` (before each fill run:
+// its jobs; before the last fill: its bound and depth limit).  The host
+// buffer holds down, then up, then the fill results of a run and m - 1 per b.
+struct RelaxXfer {
+    size_t pst, f0, rv, thv, err, cnt, thb, down;
+    size_t mm1, tau, bound, jb, jd, fdl, njob, up;
+    size_t h_up, h_jf, h_mm1, host;
+};
+
+static RelaxXfer xfer_layout(const DevProblem &P) {
+    const size_t nb = P.nb, D = levels(P), J = kMaxJobs, S = kSpecBounds;
+    RelaxXfer x{};
+    size_t o = 0;
+    auto put = [&](size_t bytes) {
+        const size_t at = o;
+        o += (bytes + 15) & ~(size_t)15;
+        return at;
+    };
+    x.pst = put(8 * nb);
+    x.f0 = put(8 * nb);
+    x.rv = put(8 * D * nb);
+    x.thv = put(8 * S);
+    x.err = put(4);
+    x.cnt = put(4);
+    x.thb = put(4 * S);
+    x.down = o;
+    o = 0;
+    x.tau = put(8 * J);
+    x.bound = put(8 * nb);
+    x.jb = put(4 * J);
+    x.jd = put(4 * J);
+    x.fdl = put(4 * nb);
+    x.njob = put(4 * D * nb);
+    x.up = o;
+    o = x.down;
+    x.h_up = put(x.up);
+    x.h_jf = put(8 * J);
+    x.h_mm1 = put(8 * nb);
+    x.host = o;
+    return x;
+}
+
+size_t compose_relaxed_stage_bytes(const DevProblem &P) { return xfer_layout(P).host; }
+
 struct RelaxWs {
     double *th_val;   // [n_surv] collected stage-cost bounds
     int32_t *th_b;    // [n_surv] their b
@@ -1271,14 +1320,17 @@ struct RelaxWs {
     double *lo;       // [nb] P* per b (bounds must exceed it)
     double *hi;       // [nb] the best T found so far
     double *mm1;      // [nb] m - 1 per b
-    int32_t *job_b;   // [kMaxJobs]
+    char *down;       // packed read-back (RelaxXfer)
+    char *up;         // packed uploads (RelaxXfer): the arrays below point into it
+    double *job_tau;     // [kMaxJobs]
+    double *bound;       // [nb] the last fill's bound per b
+    int32_t *job_b;      // [kMaxJobs]
     int32_t *job_dlim;   // [kMaxJobs] deepest level with a whole plan within the job's bound
+    int32_t *fdl;        // [nb] the last fill's depth limit per b
     int32_t *jobs_of_b;  // [D][nb] jobs of each b at least d deep in the current run
     int32_t *row_cnt;    // [nb][L] readers done per row (job runs)
-    double *job_tau;  // [kMaxJobs]
     double *job_F;    // [kMaxJobs]
     double *job_G;    // [2][kMaxJobs][L+1][K]
-    double *bound;    // [nb]
     double *Tp;       // [n_groups] pristine starting stage table (each fill run starts from it)
     size_t bytes;
 };
@@ -1292,6 +1344,7 @@ static RelaxWs carve_relax(const DevProblem &P, int64_t n, void *base) {
         off += align256(bytes > 0 ? bytes : 1);
         return x;
     };
+    const RelaxXfer X = xfer_layout(P);
     const int64_t jrows = (int64_t)kMaxJobs * (P.L + 1) * P.K;
     r.th_val = (double *)take(sizeof(double) * n);
     r.th_b = (int32_t *)take(sizeof(int32_t) * n);
@@ -1299,17 +1352,46 @@ static RelaxWs carve_relax(const DevProblem &P, int64_t n, void *base) {
     r.lo = (double *)take(sizeof(double) * P.nb);
     r.hi = (double *)take(sizeof(double) * P.nb);
     r.mm1 = (double *)take(sizeof(double) * P.nb);
-    r.job_b = (int32_t *)take(sizeof(int32_t) * kMaxJobs);
-    r.job_dlim = (int32_t *)take(sizeof(int32_t) * kMaxJobs);
-    r.jobs_of_b = (int32_t *)take(sizeof(int32_t) * levels(P) * P.nb);
+    r.down = (char *)take(X.down);
+    r.up = (char *)take(X.up);
+    if (base) {
+        r.job_tau = (double *)(r.up + X.tau);
+        r.bound = (double *)(r.up + X.bound);
+        r.job_b = (int32_t *)(r.up + X.jb);
+        r.job_dlim = (int32_t *)(r.up + X.jd);
+        r.fdl = (int32_t *)(r.up + X.fdl);
+        r.jobs_of_b = (int32_t *)(r.up + X.njob);
+    }
     r.row_cnt = (int32_t *)take(sizeof(int32_t) * P.nb * P.L);
-    r.job_tau = (double *)take(sizeof(double) * kMaxJobs);
     r.job_F = (double *)take(sizeof(double) * kMaxJobs);
     r.job_G = (double *)take(sizeof(double) * 2 * jrows);
-    r.bound = (double *)take(sizeof(double) * P.nb);
     r.Tp = (double *)take(sizeof(double) * n_groups(P));
     r.bytes = off;
     return r;
+}
+
+// The phase results, the collected bound count and the first `spec` collected
+// bounds into the packed read-back region.
+__global__ __launch_bounds__(256) void pack_readback(int nb, int D, const double *__restrict__ Pst,
+                                                     const double *__restrict__ F0, const double *__restrict__ Rv,
+                                                     const ComposeResult *__restrict__ res,
+                                                     const int32_t *__restrict__ cnt,
+                                                     const double *__restrict__ thv, const int32_t *__restrict__ thb,
+                                                     int64_t spec, char *__restrict__ down, RelaxXfer X) {
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = t0; t < nb; t += step) {
+        ((double *)(down + X.pst))[t] = Pst[t];
+        ((double *)(down + X.f0))[t] = F0[t];
+    }
+    for (int64_t t = t0; t < (int64_t)D * nb; t += step) ((double *)(down + X.rv))[t] = Rv[t];
+    for (int64_t t = t0; t < spec; t += step) {
+        ((double *)(down + X.thv))[t] = thv[t];
+        ((int32_t *)(down + X.thb))[t] = thb[t];
+    }
+    if (t0 == 0) {
+        *(int32_t *)(down + X.err) = res->err;
+        *(int32_t *)(down + X.cnt) = *cnt;
+    }
 }
 
 size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv) {
@@ -1379,6 +1461,51 @@ __global__ __launch_bounds__(256) void collect_bounds(DevProblem P, const int32_
             }
             ++slot;
         }
+}
+
+// The relaxed search's starting incumbent, the least (T, b) with T = (m-1)
+// P*_b + F(P*_b) (its bound is P*_b), and the window of stage costs worth
+// collecting: lo[b] = P*_b for a b still in the race ((m-1) P*_b not above the
+// incumbent, a fill being non-negative), +inf for the rest; hi[b] = the
+// incumbent T.  One block; the host repeats the same arithmetic on the values
+// it reads back.
+constexpr int kInitThreads = 256;
+
+__global__ __launch_bounds__(kInitThreads) void relax_init(DevProblem P, const double *__restrict__ Pst,
+                                                           const double *__restrict__ F0,
+                                                           const double *__restrict__ mm1, double *lo, double *hi) {
+    __shared__ double sT[kInitThreads];
+    __shared__ int32_t sb[kInitThreads];
+    double bt = kInf;
+    int bb = INT_MAX;
+    for (int b = threadIdx.x; b < P.nb; b += kInitThreads)
+        if (Pst[b] < kInf && F0[b] < kInf) {
+            const double t = (mm1[b] * Pst[b]) + F0[b];
+            if (t < bt || (t == bt && b < bb)) {
+                bt = t;
+                bb = b;
+            }
+        }
+    sT[threadIdx.x] = bt;
+    sb[threadIdx.x] = bb;
+    __syncthreads();
+    for (int h = kInitThreads / 2; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) {
+            const double t = sT[threadIdx.x + h];
+            const int b = sb[threadIdx.x + h];
+            if (t < sT[threadIdx.x] || (t == sT[threadIdx.x] && b < sb[threadIdx.x])) {
+                sT[threadIdx.x] = t;
+                sb[threadIdx.x] = b;
+            }
+        }
+        __syncthreads();
+    }
+    const double inc = sT[0];
+    for (int b = threadIdx.x; b < P.nb; b += kInitThreads) {
+        const bool live = Pst[b] < kInf && F0[b] < kInf && (mm1[b] * Pst[b]) <= inc;
+        lo[b] = live ? Pst[b] : kInf;
+        hi[b] = inc;
+    }
 }
 
 // Pipelines of at least this many levels read the fill's depth limits back
@@ -1647,10 +1774,19 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
                                   void *ws, hipStream_t s, ComposeResult **result_dev, int *rounds_out) {
     Driver dr(P, n_surv, ws, s);
     RelaxWs r = carve_relax(P, n_surv, (char *)ws + compose_ws_bytes(P, n_surv));
+    const RelaxXfer X = xfer_layout(P);
     *result_dev = dr.w.res;
     if (rounds_out) *rounds_out = 0;
+    if (!H.stage || !H.stage->ptr || H.stage->bytes < X.host) return hipErrorInvalidValue;
+    char *hs = (char *)H.stage->ptr;  // pinned: the copies below do not stall the host
+    char *hd = hs, *hu = hs + X.h_up;
+    double *h_jf = (double *)(hs + X.h_jf), *h_mm1 = (double *)(hs + X.h_mm1);
+    const int nb = P.nb, D = dr.D;
+    for (int bi = 0; bi < nb; ++bi) h_mm1[bi] = (double)(H.B / H.bvals[bi] - 1);
+    hipError_t e = hipMemcpyAsync(r.mm1, h_mm1, sizeof(double) * nb, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
     dr.setup(surv, n_surv, cost, dmax);
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e == hipSuccess)
         e = hipMemcpyAsync(r.Tp, dr.w.T0, sizeof(double) * n_groups(P), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
@@ -1659,16 +1795,31 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     e = dr.fill_levels(&nlev);
     if (e != hipSuccess) return e;
     dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
-    const int nb = P.nb, D = dr.D;
-    std::vector<double> Pst(nb), F0(nb), Rv((size_t)D * nb);
-    int32_t err = 0;
-    e = hipMemcpyAsync(Pst.data(), dr.w.Pst, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(F0.data(), dr.w.rootF, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(Rv.data(), dr.w.Rv, sizeof(double) * D * nb, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(&err, &dr.w.res->err, sizeof(err), hipMemcpyDeviceToHost, s);
+    // the starting incumbent and the stage costs worth collecting, on the
+    // device; one packed read-back brings the phase results, the collected
+    // count and the first kSpecBounds collected bounds
+    relax_init<<<dim3(1), dim3(kInitThreads), 0, s>>>(P, dr.w.Pst, dr.w.rootF, r.mm1, r.lo, r.hi);
+    fill<int32_t>(r.th_cnt, 1, 0, s);
+    {
+        int64_t blocks = (n_surv + 256 * kBoundRecs - 1) / (256 * kBoundRecs);
+        if (blocks < 1) blocks = 1;
+        collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.rec_g, dr.w.rec_c, n_surv, r.lo, r.hi,
+                                                                   r.mm1, r.th_val, r.th_b, r.th_cnt,
+                                                                   (int32_t)std::min<int64_t>(n_surv, INT32_MAX));
+    }
+    const int64_t spec = std::min<int64_t>(n_surv, kSpecBounds);
+    {
+        const int64_t most = std::max<int64_t>((int64_t)D * nb, spec);
+        const unsigned blocks = (unsigned)std::min<int64_t>(std::max<int64_t>((most + 255) / 256, 1), 64);
+        pack_readback<<<dim3(blocks), dim3(256), 0, s>>>(nb, D, dr.w.Pst, dr.w.rootF, dr.w.Rv, dr.w.res, r.th_cnt,
+                                                         r.th_val, r.th_b, spec, r.down, X);
+    }
+    e = hipMemcpyAsync(hd, r.down, X.down, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return e;
-    if (err) {  // invalid list: the finish kernel reports it
+    const double *Pst = (const double *)(hd + X.pst), *F0 = (const double *)(hd + X.f0);
+    const double *Rv = (const double *)(hd + X.rv);
+    if (*(const int32_t *)(hd + X.err)) {  // invalid list: the finish kernel reports it
         dr.finish(dr.w.Pst);
         return hipGetLastError();
     }
@@ -1682,12 +1833,10 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         return top;
     };
     std::vector<BSearch> bs(nb);
-    std::vector<double> mm1(nb, 0.0);
     Incumbent inc;
     for (int bi = 0; bi < nb; ++bi) {
         BSearch &q = bs[bi];
-        const int64_t m = H.B / H.bvals[bi];
-        q.mm1 = mm1[bi] = (double)(m - 1);
+        q.mm1 = h_mm1[bi];
         if (!(Pst[bi] < kInf) || !(F0[bi] < kInf)) continue;
         q.active = true;
         q.Pst = Pst[bi];
@@ -1695,7 +1844,8 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         inc.offer((q.mm1 * q.Pst) + q.F0, bi, q.Pst);
     }
     // a bound tau of b gives T >= (m-1) tau (the fill is non-negative): b
-    // takes part only while (m-1) P*_b can still reach the incumbent
+    // takes part only while (m-1) P*_b can still reach the incumbent (the
+    // rule relax_init applied on the device)
     bool any = false;
     for (int bi = 0; bi < nb; ++bi) {
         BSearch &q = bs[bi];
@@ -1703,35 +1853,24 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         any = any || q.active;
     }
     if (any) {
-        // candidate bounds: stage costs (device) and link times (host)
-        std::vector<double> lo(Pst);
-        for (int bi = 0; bi < nb; ++bi)
-            if (!bs[bi].active) lo[bi] = kInf;
-        e = hipMemcpyAsync(r.lo, lo.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
-        std::vector<double> hi(nb, inc.T);
-        if (e == hipSuccess) e = hipMemcpyAsync(r.hi, hi.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
-        if (e == hipSuccess) e = hipMemcpyAsync(r.mm1, mm1.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
-        if (e != hipSuccess) return e;
-        fill<int32_t>(r.th_cnt, 1, 0, s);
-        int64_t blocks = (n_surv + 256 * kBoundRecs - 1) / (256 * kBoundRecs);
-        if (blocks < 1) blocks = 1;
-        collect_bounds<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(P, dr.w.rec_g, dr.w.rec_c, n_surv, r.lo, r.hi,
-                                                                   r.mm1, r.th_val, r.th_b, r.th_cnt,
-                                                                   (int32_t)std::min<int64_t>(n_surv, INT32_MAX));
-        int32_t cnt = 0;
-        e = hipMemcpyAsync(&cnt, r.th_cnt, sizeof(cnt), hipMemcpyDeviceToHost, s);
-        if (e == hipSuccess) e = hipStreamSynchronize(s);
-        if (e != hipSuccess) return e;
-        cnt = (int32_t)std::min<int64_t>(cnt, n_surv);  // each entry is collected at most once
-        std::vector<double> tv(cnt);
-        std::vector<int32_t> tb(cnt);
-        if (cnt > 0) {
-            e = hipMemcpyAsync(tv.data(), r.th_val, sizeof(double) * cnt, hipMemcpyDeviceToHost, s);
-            if (e == hipSuccess) e = hipMemcpyAsync(tb.data(), r.th_b, sizeof(int32_t) * cnt, hipMemcpyDeviceToHost, s);
+        // candidate bounds: stage costs (collected on the device) and link
+        // times (host); the rest of the collected list when it outgrew the
+        // packed read-back
+        const int32_t cnt = (int32_t)std::min<int64_t>(*(const int32_t *)(hd + X.cnt), n_surv);
+        const double *tv = (const double *)(hd + X.thv);
+        const int32_t *tb = (const int32_t *)(hd + X.thb);
+        for (int32_t t = 0; t < cnt && t < spec; ++t) bs[tb[t]].th.push_back(tv[t]);
+        if (cnt > spec) {
+            std::vector<double> tv2(cnt - spec);
+            std::vector<int32_t> tb2(cnt - spec);
+            e = hipMemcpyAsync(tv2.data(), r.th_val + spec, sizeof(double) * (cnt - spec), hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(tb2.data(), r.th_b + spec, sizeof(int32_t) * (cnt - spec), hipMemcpyDeviceToHost,
+                                   s);
             if (e == hipSuccess) e = hipStreamSynchronize(s);
             if (e != hipSuccess) return e;
+            for (int64_t t = 0; t < cnt - spec; ++t) bs[tb2[t]].th.push_back(tv2[t]);
         }
-        for (int32_t t = 0; t < cnt; ++t) bs[tb[t]].th.push_back(tv[t]);
         // link times x = (2 b * OA[j-1]) / E over links between positions
         // o < o2 of the order; x grows with OA, so each distinct E gives one
         // run of distinct OA values inside the window
@@ -1766,9 +1905,11 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
             if (!q.th.empty()) q.iv.push_back({-1, (int)q.th.size() - 1});
         }
         // branch and bound over the bounds, one batched fill run per round
+        double *h_tau = (double *)(hu + X.tau);
+        int32_t *h_jb = (int32_t *)(hu + X.jb), *h_jd = (int32_t *)(hu + X.jd);
+        int32_t *h_nj = (int32_t *)(hu + X.njob);
         for (int round = 0;; ++round) {
             std::vector<std::pair<int, int>> req;  // (b, index)
-            std::vector<std::vector<int>> pts(nb);
             for (int bi = 0; bi < nb; ++bi) {
                 BSearch &q = bs[bi];
                 for (auto &ab : q.iv) {
@@ -1788,36 +1929,30 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
             if (rounds_out) *rounds_out = round + 1;
             for (size_t c0 = 0; c0 < req.size(); c0 += kMaxJobs) {
                 const int J = (int)std::min<size_t>(kMaxJobs, req.size() - c0);
-                std::vector<int32_t> jb(J), jd(J);
-                std::vector<double> jt(J), jf(J);
                 int nlev_j = 0;
-                for (int t = 0; t < J; ++t) {
-                    jb[t] = req[c0 + t].first;
-                    jt[t] = bs[jb[t]].th[req[c0 + t].second];
-                    jd[t] = dlim_of(jb[t], jt[t]);
-                    nlev_j = std::max(nlev_j, jd[t]);
-                }
-                std::vector<int32_t> nj((size_t)std::max(nlev_j, 1) * nb, 0);
-                for (int t = 0; t < J; ++t)
-                    for (int d = 1; d <= jd[t]; ++d) ++nj[(size_t)(d - 1) * nb + jb[t]];
-                e = hipMemcpyAsync(r.job_b, jb.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, s);
-                if (e == hipSuccess) e = hipMemcpyAsync(r.job_dlim, jd.data(), sizeof(int32_t) * J, hipMemcpyHostToDevice, s);
-                if (e == hipSuccess)
-                    e = hipMemcpyAsync(r.jobs_of_b, nj.data(), sizeof(int32_t) * nj.size(), hipMemcpyHostToDevice, s);
-                if (e == hipSuccess) e = hipMemcpyAsync(r.job_tau, jt.data(), sizeof(double) * J, hipMemcpyHostToDevice, s);
                 std::vector<char> used(nb, 0);
-                for (int t = 0; t < J; ++t) used[jb[t]] = 1;
+                for (int t = 0; t < J; ++t) {
+                    h_jb[t] = req[c0 + t].first;
+                    h_tau[t] = bs[h_jb[t]].th[req[c0 + t].second];
+                    h_jd[t] = dlim_of(h_jb[t], h_tau[t]);
+                    nlev_j = std::max(nlev_j, (int)h_jd[t]);
+                    used[h_jb[t]] = 1;
+                }
+                std::fill(h_nj, h_nj + (size_t)D * nb, 0);
+                for (int t = 0; t < J; ++t)
+                    for (int d = 1; d <= h_jd[t]; ++d) ++h_nj[(size_t)(d - 1) * nb + h_jb[t]];
+                e = hipMemcpyAsync(r.up, hu, X.up, hipMemcpyHostToDevice, s);
                 if (e == hipSuccess) e = dr.restore_tables(r.Tp, used);
                 if (e != hipSuccess) return e;
                 dr.phase2_jobs(r, J, nlev_j);
-                e = hipMemcpyAsync(jf.data(), r.job_F, sizeof(double) * J, hipMemcpyDeviceToHost, s);
-                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                e = hipMemcpyAsync(h_jf, r.job_F, sizeof(double) * J, hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);  // also frees the upload buffer for reuse
                 if (e != hipSuccess) return e;
                 for (int t = 0; t < J; ++t) {
-                    BSearch &q = bs[jb[t]];
+                    BSearch &q = bs[h_jb[t]];
                     const int k = req[c0 + t].second;
-                    q.F[k] = jf[t];
-                    inc.offer((q.mm1 * q.th[k]) + jf[t], jb[t], q.th[k]);
+                    q.F[k] = h_jf[t];
+                    inc.offer((q.mm1 * q.th[k]) + h_jf[t], h_jb[t], q.th[k]);
                 }
             }
             for (int bi = 0; bi < nb; ++bi) {
@@ -1846,21 +1981,23 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         dr.finish(dr.w.Pst);
         return hipGetLastError();
     }
-    std::vector<double> bound(nb, kInf);
-    std::vector<int32_t> fdl(nb, 0);
-    bound[bstar] = inc.tau;
-    fdl[bstar] = dlim_of(bstar, inc.tau);
-    e = hipMemcpyAsync(r.bound, bound.data(), sizeof(double) * nb, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(dr.w.dlim, fdl.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+    double *h_bound = (double *)(hu + X.bound);
+    int32_t *h_fdl = (int32_t *)(hu + X.fdl);
+    for (int bi = 0; bi < nb; ++bi) {
+        h_bound[bi] = kInf;
+        h_fdl[bi] = 0;
+    }
+    h_bound[bstar] = inc.tau;
+    h_fdl[bstar] = dlim_of(bstar, inc.tau);
+    const int last_lev = h_fdl[bstar];
+    e = hipMemcpyAsync(r.up, hu, X.up, hipMemcpyHostToDevice, s);
     std::vector<char> used(nb, 0);
     used[bstar] = 1;
     if (e == hipSuccess) e = dr.restore_tables(r.Tp, used);
     if (e != hipSuccess) return e;
-    dr.phase2(r.bound, dr.w.dlim, fdl[bstar], dr.w.T);  // the relaxed bound
+    dr.phase2(r.bound, r.fdl, last_lev, dr.w.T);  // the relaxed bound
     dr.finish(r.bound);
-    e = hipGetLastError();
-    if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host vectors above must outlive the copies
-    return e;
+    return hipGetLastError();
 }
 
 }  // namespace tg

@@ -173,11 +173,33 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
 size_t compose_order_offset(const DevProblem &P, int64_t n_surv);  // where the order table lives in ws
 
 // Host tables the relaxed search reads (link times are enumerated on the host).
+// Pinned host memory owned by a caller and reused across calls (small
+// transfers that the host waits for).
+struct HostStage {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+    hipError_t reserve(size_t n) {  // contents are not kept
+        if (n <= bytes) return hipSuccess;
+        if (ptr) (void)hipHostFree(ptr);
+        ptr = nullptr;
+        bytes = 0;
+        const hipError_t e = hipHostMalloc(&ptr, n, hipHostMallocPortable);
+        if (e == hipSuccess) bytes = n;
+        return e;
+    }
+    void release() {
+        if (ptr) (void)hipHostFree(ptr);
+        ptr = nullptr;
+        bytes = 0;
+    }
+};
+size_t compose_relaxed_stage_bytes(const DevProblem &P);
 struct RelaxHost {
     const int64_t *outact;  // [L] output activation bytes per layer
     const double *E;        // [K*K] inter-island bandwidth, island ids, row-major
     const int64_t *bvals;   // [nb] compatible micro-batch sizes, ascending
     int64_t B;              // global batch
+    HostStage *stage;       // at least compose_relaxed_stage_bytes(P) bytes of pinned memory
 };
 size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv);
 // Island construction from nodes (n <= 4096); synchronises the stream.

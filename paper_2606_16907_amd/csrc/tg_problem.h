@@ -1,6 +1,7 @@
 // tg_problem.h -- host-side definition of the opaque tg_problem handle.
 #pragma once
 
+#include <mutex>
 #include <vector>
 
 #include "tg_device.h"
@@ -14,4 +15,9 @@ struct tg_problem {
     int64_t B;                    // global batch
     std::vector<int64_t> outact;  // [L] output activation bytes (host copy)
     std::vector<double> E;        // [K*K] inter-island bandwidth (host copy)
+    // pinned host memory for the relaxed composition's packed read-backs and
+    // uploads: allocated at its first call, grown when a call needs more,
+    // freed at destroy; relaxed calls on one handle take turns on it
+    mutable std::mutex relax_mu;
+    mutable tg::HostStage relax_stage;
 };
