@@ -762,15 +762,15 @@ tg_status tg_build_islands(const tg_island *nodes, int32_t n_nodes, const double
             !(v.host_bw >= 0.0) || !std::isfinite(v.host_bw))
             return fail(TG_EINVAL, "node %d specs", u);
     }
-    for (int64_t t = 0; t < (int64_t)n_nodes * n_nodes; ++t)
-        if (!(node_bw[t] >= 0.0) || !std::isfinite(node_bw[t])) return fail(TG_EINVAL, "node_bw[%lld]", (long long)t);
     const size_t need = tg::islands_ws_bytes(n_nodes);
     if (!d_ws || ws_bytes < need) return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, need);
     if (check_alignment(nullptr, nullptr, d_ws) != TG_OK) return TG_EINVAL;
     return no_throw([&] {
+        int64_t bad = -1;  // node_bw is checked on the device, right after its upload
         hipError_t e = tg::launch_build_islands(n_nodes, nodes, node_bw, eps_compute, eps_memory, eps_intra, d_ws,
-                                                (hipStream_t)stream, island_of, islands, inter_bw, n_islands);
+                                                (hipStream_t)stream, island_of, islands, inter_bw, n_islands, &bad);
         if (e != hipSuccess) return hip_fail(e, "island construction kernels");
+        if (bad >= 0) return fail(TG_EINVAL, "node_bw[%lld]", (long long)bad);
         return TG_OK;
     });
 }

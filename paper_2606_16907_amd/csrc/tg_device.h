@@ -204,9 +204,11 @@ struct RelaxHost {
 size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv);
 // Island construction from nodes (n <= 4096); synchronises the stream.
 size_t islands_ws_bytes(int n);
+// *bad_bw: the first node_bw entry that is negative or not finite (checked on
+// the device after the upload; nothing else runs then), else -1.
 hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double *e_host, double eps_c,
                                 double eps_m, double eps_i, void *ws, hipStream_t s, int32_t *island_of,
-                                tg_island *islands, double *inter_bw, int32_t *n_islands);
+                                tg_island *islands, double *inter_bw, int32_t *n_islands, int64_t *bad_bw);
 // Composition over every island subset and order (K <= 16).
 size_t compose_orders_ws_bytes(const DevProblem &P, int64_t n_surv);
 hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,

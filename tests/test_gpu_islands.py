@@ -44,6 +44,24 @@ GEN = ([(f"n{n}_s{s}", lambda n=n, s=s: node_cluster(s, n, n_types=4, leaf=4, po
         for n in (8, 24, 63, 130) for s in range(3)]
        + [(f"fabric{n}_s{s}", lambda n=n, s=s: node_cluster(s, n)) for n in (256, 1024) for s in (1, 2)])
 
+def tied_links(seed):
+    """One group of 5-12 nodes whose links take four speeds only (symmetric
+    for even seeds): many ties between links inside a cluster and links
+    leaving it, the case where a node's fastest link leaving a union can sit
+    behind a member of its own cluster in its sorted row."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(5, 13))
+    e = np.array([100e9, 200e9, 300e9, 400e9])[rng.integers(0, 4, size=(n, n))]
+    if seed % 2 == 0:
+        e = np.minimum(e, e.T)
+    np.fill_diagonal(e, 0.0)
+    return cluster([8] * n, [100e12] * n, e.tolist())
+
+
+# seeds 7, 46, 68 and 116 give a different partition if that scan stops at a
+# member of the node's own cluster (checked on a CPU model of the merge loop)
+TIES = [(f"ties_s{s}", lambda s=s: tied_links(s)) for s in range(120)]
+
 PEAKS_INTERLEAVED = [100e12 if u % 4 < 2 else 200e12 for u in range(8)]
 HAND = [("homogeneous", lambda: cluster([8] * 16, [300e12] * 16, fabric(16, 4, 2))),
         ("tolerance", lambda: cluster([8] * 4, [100e12, 112e12, 105e12, 120e12], fabric(4, 4, 1))),
@@ -55,7 +73,7 @@ HAND = [("homogeneous", lambda: cluster([8] * 16, [300e12] * 16, fabric(16, 4, 2
         ("one_node", lambda: cluster([8], [100e12], [[0.0]]))]
 
 
-@pytest.mark.parametrize("name,make", GEN + HAND, ids=[n for n, _ in GEN + HAND])
+@pytest.mark.parametrize("name,make", GEN + TIES + HAND, ids=[n for n, _ in GEN + TIES + HAND])
 def test_islands_parity(name, make):
     cl = make()
     say("case", name, len(cl["nodes"]["gpus"]), "nodes")
