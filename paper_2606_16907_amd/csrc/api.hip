@@ -785,7 +785,8 @@ tg_status tg_compose_pipeline_all_orders(const tg_problem *p, const int64_t *d_s
     tg_status st = compose_begin(p, d_survivors, n_survivors, d_cost, d_dmax, nullptr, out, d_ws, ws_bytes, need, s);
     if (st != TG_OK) return st;
     tg::ComposeResult *res_dev = nullptr;
-    hipError_t e = tg::launch_compose_orders(p->P, d_survivors, n_survivors, d_cost, d_dmax, d_ws, s, &res_dev);
+    hipError_t e = tg::launch_compose_orders(p->P, p->bvals.data(), d_survivors, n_survivors, d_cost, d_dmax, d_ws, s,
+                                             &res_dev);
     if (e != hipSuccess) return hip_fail(e, "all-orders compose kernels");
     return compose_end(res_dev, out, s);
 }

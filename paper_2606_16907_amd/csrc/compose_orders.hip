@@ -39,7 +39,9 @@ namespace tg {
 
 constexpr int kMaxSetIslands = 16;
 constexpr int kMaxLayers = 512;
-constexpr size_t kStageLds = 13 * 1024;  // LDS bytes per level block with the set's rows staged
+constexpr size_t kLevelLds = 12 * 1024;  // LDS bytes per level block: staged rows and continuation rows
+constexpr int kLevelThreads = 128;
+constexpr int64_t kPruneCells = (int64_t)1 << 22;  // fill cells below which every b runs at once
 constexpr int kOrderFinishThreads = 1024;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 constexpr int64_t kTargetBlocks = 8192;  // blocks per level launch worth splitting for
@@ -100,6 +102,7 @@ struct OrdersWs {
     uint32_t *rootKey;  // [nb] (k << 24 | d << 16 | U) of the chosen root
     double *part_v;     // [nb][kReduceChunks] partial reductions
     uint32_t *part_k;   // [nb][kReduceChunks]
+    int32_t *blist;     // [nb] the b of each grid row in a fill run
     size_t bytes;
 };
 
@@ -136,6 +139,7 @@ static OrdersWs carve_orders(const DevProblem &P, int64_t n, void *base) {
     w.Pst = (double *)take(sizeof(double) * nb);
     w.rootF = (double *)take(sizeof(double) * nb);
     w.rootKey = (uint32_t *)take(sizeof(uint32_t) * nb);
+    w.blist = (int32_t *)take(sizeof(int32_t) * nb);
     w.part_v = (double *)take(sizeof(double) * nb * kReduceChunks);
     w.part_k = (uint32_t *)take(sizeof(uint32_t) * nb * kReduceChunks);
     w.bytes = off;
@@ -226,8 +230,9 @@ __global__ __launch_bounds__(256) void orders_links(DevProblem P, double *X) {
 // Level 1: one stage on island k covering [i, L).
 template <bool kFill>
 __global__ __launch_bounds__(256) void orders_level1(DevProblem P, SetLevels lv, const double *__restrict__ T,
-                                                     const double *__restrict__ Pst, double *cur, double *root) {
-    const int L = P.L, K = P.K, bb = blockIdx.y;
+                                                     const double *__restrict__ Pst, double *cur, double *root,
+                                                     const int32_t *__restrict__ blist) {
+    const int L = P.L, K = P.K, bb = blist ? blist[blockIdx.y] : blockIdx.y;
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= (int64_t)K * (L + 1)) return;
     const int k = (int)(e / (L + 1)), i = (int)(e - (int64_t)k * (L + 1));
@@ -242,140 +247,201 @@ __global__ __launch_bounds__(256) void orders_level1(DevProblem P, SetLevels lv,
 
 // Level d >= 2, block (part of the islands outside a (d-1)-set U', b).  kFill:
 // the fill phase at bound P*, with argmins; otherwise the bottleneck phase.
+// The block's states (k, U' + {k}) go in chunks of C: first every
+// continuation row of the chunk into LDS (thread per (state, cut)), then every
+// stage scan (thread per (state, first layer)), two barriers per chunk and
+// every lane busy whatever L is.  kStage: the previous level's rows of U',
+// read by every state, are staged in LDS first.
 template <int NT, bool kFill, bool kStage>
-__global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, int nsplit,
+__global__ __launch_bounds__(NT) void orders_level(DevProblem P, SetLevels lv, int d, int nsplit, int C,
                                                    const int32_t *__restrict__ masks,
                                                    const uint16_t *__restrict__ rank, const double *__restrict__ T,
                                                    const double *__restrict__ X, const double *__restrict__ prev,
                                                    double *cur, double *root, const double *__restrict__ Pst,
-                                                   uint16_t *argF, uint8_t *argG) {
-    // LDS: two continuation rows, then (kStage) the previous level's rows of
-    // the block's set U', read by every state of the block
+                                                   uint16_t *argF, uint8_t *argG, const int32_t *__restrict__ blist) {
+    // LDS: (kStage) the set's previous-level rows, then C continuation rows
     extern __shared__ double lds_rows[];
-    const int L = P.L, K = P.K;
-    double *Wl[2] = {lds_rows, lds_rows + (L + 1)};
-    double *Vs = lds_rows + 2 * (L + 1);
+    __shared__ int16_t s_k[kMaxSetIslands];
+    __shared__ int32_t s_st[kMaxSetIslands];
+    // per state: the first and last cut with a finite continuation (a scan
+    // skips the cuts outside, where every candidate is +inf)
+    __shared__ int32_t s_jlo[kMaxSetIslands], s_jhi[kMaxSetIslands];
+    const int L = P.L, K = P.K, R = L + 1;
     const int rp = blockIdx.x / nsplit, part = blockIdx.x - rp * nsplit;
-    const int bb = blockIdx.y;
+    const int bb = blist ? blist[blockIdx.y] : blockIdx.y;  // a fill run covers a list of b
     const uint32_t Up = (uint32_t)masks[lv.moff[d - 1] + rp];
     const int nk = K - (d - 1);
     const int per = (nk + nsplit - 1) / nsplit;
     const int q0 = part * per, q1 = min(nk, q0 + per);
-    uint32_t rest = ((1u << K) - 1u) & ~Up;  // islands outside U', ascending
-    for (int q = 0; q < q0; ++q) rest &= rest - 1;
+    const int nu = d - 1;
     const int jmax = L - d + 1;
     const double bound = kFill ? Pst[bb] : 0.0;
-    const double *Vp = prev + ((int64_t)bb * lv.n[d - 1] + (int64_t)rp * (d - 1)) * (L + 1);
-    // the islands of U' in ascending order (the same for every thread)
-    int ks[kMaxSetIslands];
+    const double *Vp = prev + ((int64_t)bb * lv.n[d - 1] + (int64_t)rp * nu) * R;
+    // (offsets from the LDS array itself keep these accesses LDS instructions)
+    const double *Vs = lds_rows;
+    double *Wl = lds_rows + (kStage ? nu * R : 0);
+    // the islands of U' in ascending order (the same for every thread), and
+    // each one's row offset in an X block
+    int ks[kMaxSetIslands], koff[kMaxSetIslands];
     {
         uint32_t r2 = Up;
 #pragma unroll
         for (int q = 0; q < kMaxSetIslands; ++q) {
             ks[q] = r2 ? __builtin_ctz(r2) : 0;
+            koff[q] = ks[q] * R;
             r2 &= r2 - 1;
         }
     }
-    const int nu = d - 1;
-    constexpr int NJ = NT >= 256 ? 2 : 1;  // cuts per thread (j <= L < 2 NT)
-    constexpr int kIsl = kStage ? 8 : 4;   // islands' link loads in flight
-    if (kStage) {
-        for (int t = threadIdx.x; t < nu * (L + 1); t += NT) Vs[t] = Vp[t];
-        __syncthreads();
-    }
-    int buf = 0;  // continuation rows alternate between two LDS rows, so one
-                  // barrier per state separates writers from readers
-    for (int q = q0; q < q1; ++q, rest &= rest - 1, buf ^= 1) {
-        const int k = __builtin_ctz(rest);
+    constexpr int kIsl = kStage ? 8 : 4;  // islands' link loads in flight
+    // the block's states: island k (the q-th outside U', from q0 on) and the
+    // state number of (k, U' + {k})
+    if ((int)threadIdx.x < q1 - q0) {
+        uint32_t r2 = ((1u << K) - 1u) & ~Up;
+        for (int t = 0; t < q0 + (int)threadIdx.x; ++t) r2 &= r2 - 1;
+        const int k = __builtin_ctz(r2);
         const uint32_t U = Up | (1u << k);
-        const int st = (int)rank[U] * d + __builtin_popcount(U & ((1u << k) - 1u));
-        const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
-        double *Wrow = Wl[buf];
-        // continuation row from X[b][k][k'][.] and V_{d-1}(., k', U'), kIsl
-        // islands' loads in flight
-        const double *Xr = X + ((int64_t)bb * K + k) * K * (L + 1);
-        for (int c = 0; c < NJ; ++c) {
-            const int j = threadIdx.x + 1 + c * NT;
-            if (j > jmax) continue;
-            double w = kInf;
-            int arg = 255;
-            for (int t0 = 0; t0 < nu; t0 += kIsl) {
-                double x[kIsl], vv[kIsl];
+        s_k[threadIdx.x] = (int16_t)k;
+        s_st[threadIdx.x] = (int)rank[U] * d + __builtin_popcount(U & ((1u << k) - 1u));
+        s_jlo[threadIdx.x] = INT_MAX;
+        s_jhi[threadIdx.x] = -1;
+    }
+    if (kStage)
+        for (int t = threadIdx.x; t < nu * R; t += NT) lds_rows[t] = Vp[t];
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int c0 = 0; c0 < q1 - q0; c0 += C) {
+        const int nst = min(C, q1 - q0 - c0);
+        // continuation rows W(j, k, U') of the chunk's states
+        const int nwork = nst * jmax;
+        for (int p0 = 0; p0 < nwork; p0 += NT) {
+            const int p = p0 + (int)threadIdx.x;
+            const bool act = p < nwork;
+            const int s = act ? p / jmax : nst;  // lanes past the end: a state of their own
+            const int j = act ? p - s * jmax + 1 : 0;
+            int jf = INT_MAX;  // j if W is finite
+            if (act) {
+                const int qs = c0 + s;
+                const int k = s_k[qs];
+                const double *Xr = X + ((int64_t)bb * K + k) * K * R;
+                double w = kInf;
+                int arg = 255;
+                for (int t0 = 0; t0 < nu; t0 += kIsl) {
+                    // a link only matters next to a finite continuation: its
+                    // load is skipped where V is +inf
+                    double x[kIsl], vv[kIsl];
 #pragma unroll
-                for (int u = 0; u < kIsl; ++u) {
-                    const int t = min(t0 + u, nu - 1);
-                    x[u] = Xr[(int64_t)ks[t] * (L + 1) + j];
-                    vv[u] = kStage ? Vs[t * (L + 1) + j] : Vp[(int64_t)t * (L + 1) + j];
-                }
-#pragma unroll
-                for (int u = 0; u < kIsl; ++u) {
-                    const int t = t0 + u;
-                    const double v = vv[u];
-                    if (t >= nu) {
-                    } else if (kFill) {
-                        if (x[u] <= bound) {
-                            const double y = x[u] + v;
-                            if (y < w) {
-                                w = y;
-                                arg = ks[t];
-                            }
-                        }
-                    } else {
-                        const double y = x[u] > v ? x[u] : v;
-                        if (y < w) w = y;
+                    for (int u = 0; u < kIsl; ++u) {
+                        const int t = min(t0 + u, nu - 1);
+                        vv[u] = kStage ? Vs[t * R + j] : Vp[(int64_t)t * R + j];
                     }
-                }
-            }
-            Wrow[j] = w;
-            if (kFill) argG[gst * (L + 1) + j] = (uint8_t)arg;
-        }
-        __syncthreads();
-        const double *Tr = T + (((int64_t)(d - 1) * P.nb + bb) * K + k) * L * L;
-        double *out = cur + ((int64_t)bb * lv.n[d] + st) * (L + 1);
-        for (int i = threadIdx.x; i <= L; i += NT) {
-            double best = kInf;
-            int bj = 0;
-            if (i <= L - d) {
-                // T_d(i, j, k) = Tr[(j - i - 1) * L + i]: the threads of a wave
-                // read consecutive first layers
-                const double *Ti = Tr + i;
-                bool go = true;
-                // with imbalance pruning the scan starts at the first balanced cut
-                const int js = P.jlo ? max(i + 1, P.jlo[k * L + i]) : i + 1;
-                // four cuts' stage costs in flight at a time (clamped to the row)
-                for (int j0 = js; go && j0 <= jmax; j0 += 4) {
-                    double tv[4];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) tv[u] = Ti[(int64_t)(min(j0 + u, jmax) - i - 1) * L];
+                    for (int u = 0; u < kIsl; ++u) {
+                        const int t = min(t0 + u, nu - 1);
+                        x[u] = vv[u] < kInf ? Xr[koff[t] + j] : kInf;
+                    }
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int j = j0 + u;
-                        if (!go || j > jmax) {
+                    for (int u = 0; u < kIsl; ++u) {
+                        const int t = t0 + u;
+                        const double v = vv[u];
+                        if (t >= nu) {
                         } else if (kFill) {
-                            if (tv[u] > bound || tv[u] >= best) {
-                                go = false;
-                            } else {
-                                const double y = tv[u] + Wrow[j];
-                                if (y < best) {
-                                    best = y;
-                                    bj = j;
+                            if (x[u] <= bound) {
+                                const double y = x[u] + v;
+                                if (y < w) {
+                                    w = y;
+                                    arg = ks[t];
                                 }
                             }
                         } else {
-                            if (tv[u] >= best) {
-                                go = false;
-                            } else {
-                                const double y = tv[u] > Wrow[j] ? tv[u] : Wrow[j];
-                                if (y < best) best = y;
-                            }
+                            const double y = x[u] > v ? x[u] : v;
+                            if (y < w) w = y;
+                        }
+                    }
+                }
+                Wl[s * R + j] = w;
+                if (kFill) {
+                    const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + s_st[qs];
+                    argG[gst * R + j] = (uint8_t)arg;
+                }
+                if (w < kInf) jf = j;
+            }
+            // per state the least and greatest finite cut: a wave's lanes hold
+            // runs of consecutive (state, cut) pairs, so a segmented reduction
+            // over same-state lanes leaves each run's totals at its first lane
+            int lo = jf, hi = jf == INT_MAX ? -1 : jf;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int lo2 = __shfl_down(lo, off), hi2 = __shfl_down(hi, off), s2 = __shfl_down(s, off);
+                if (lane + off < kWave && s2 == s) {
+                    lo = min(lo, lo2);
+                    hi = max(hi, hi2);
+                }
+            }
+            const int sprev = __shfl_up(s, 1);
+            if (act && (lane == 0 || sprev != s) && hi >= 0) {
+                atomicMin(&s_jlo[c0 + s], lo);
+                atomicMax(&s_jhi[c0 + s], hi);
+            }
+        }
+        __syncthreads();
+        // the stage scans: one thread per (state, first layer i) walks the cuts j
+        const int nrow = nst * R;
+        for (int p = threadIdx.x; p < nrow; p += NT) {
+            const int s = p / R, i = p - s * R;
+            const int qs = c0 + s;
+            const int k = s_k[qs];
+            const int st = s_st[qs];
+            const int64_t gst = (int64_t)bb * lv.total + lv.soff[d] + st;
+            const double *Wrow = Wl + s * R;
+            double best = kInf;
+            int bj = 0;
+            if (i <= L - d) {
+                const int jend = min(jmax, s_jhi[qs]);
+                // T_d(i, j, k) = Tr[(j - i - 1) * L + i]: the threads of a wave
+                // read consecutive first layers
+                const double *Ti = T + (((int64_t)(d - 1) * P.nb + bb) * K + k) * L * L + i;
+                bool go = true;
+                // with imbalance pruning the scan starts at the first balanced
+                // cut; it starts no earlier than the first finite continuation
+                const int js = max(P.jlo ? max(i + 1, P.jlo[k * L + i]) : i + 1, s_jlo[qs]);
+                // four cuts' stage costs and continuation values read at a
+                // time (clamped to the row), then taken in order without
+                // branches: the scan stops at the first cost that cannot
+                // improve the running best
+                for (int j0 = js; go && j0 <= jend; j0 += 4) {
+                    double tv[4], wv[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int jc = min(j0 + u, jend);
+                        tv[u] = Ti[__umul24(jc - i - 1, L)];  // < L^2 <= 2^18
+                        wv[u] = Wrow[jc];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int j = j0 + u;
+                        const bool live = go && j <= jend;
+                        if (kFill) {
+                            const bool stop = live && (tv[u] > bound || tv[u] >= best);
+                            const double y = tv[u] + wv[u];
+                            const bool take = live && !stop && y < best;
+                            best = take ? y : best;
+                            bj = take ? j : bj;
+                            go = go && !stop;
+                        } else {
+                            const bool stop = live && tv[u] >= best;
+                            const double y = tv[u] > wv[u] ? tv[u] : wv[u];
+                            const bool take = live && !stop && y < best;
+                            best = take ? y : best;
+                            go = go && !stop;
                         }
                     }
                 }
             }
-            out[i] = best;
+            cur[((int64_t)bb * lv.n[d] + st) * R + i] = best;
             if (kFill && i < L) argF[gst * L + i] = (uint16_t)bj;
             if (i == 0) root[gst] = best;
         }
+        __syncthreads();  // the chunk's rows are read; the next chunk rewrites them
     }
 }
 
@@ -419,10 +485,10 @@ __device__ inline void block_argmin(double *sv, uint32_t *sk) {
 template <bool kRoot>
 __global__ __launch_bounds__(256) void orders_reduce_part(SetLevels lv, const int32_t *__restrict__ masks,
                                                           const double *__restrict__ root, double *part_v,
-                                                          uint32_t *part_k) {
+                                                          uint32_t *part_k, const int32_t *__restrict__ blist) {
     __shared__ double sv[256];
     __shared__ uint32_t sk[256];
-    const int c = blockIdx.x, bb = blockIdx.y;
+    const int c = blockIdx.x, bb = blist ? blist[blockIdx.y] : blockIdx.y;
     const int64_t per = (lv.total + kReduceChunks - 1) / kReduceChunks;
     const int64_t q0 = (int64_t)c * per, q1 = min(lv.total, q0 + per);
     const double *rv = root + (int64_t)bb * lv.total;
@@ -453,12 +519,21 @@ __global__ __launch_bounds__(256) void orders_reduce_part(SetLevels lv, const in
     }
 }
 
+// No fill root yet for any b (a b whose fill does not run keeps none).
+__global__ __launch_bounds__(256) void orders_clear_roots(int nb, double *rootF, uint32_t *rootKey) {
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < nb) {
+        rootF[t] = kInf;
+        rootKey[t] = kNoKey;
+    }
+}
+
 __global__ __launch_bounds__(256) void orders_reduce_final(const double *__restrict__ part_v,
                                                            const uint32_t *__restrict__ part_k, double *out_v,
-                                                           uint32_t *out_key) {
+                                                           uint32_t *out_key, const int32_t *__restrict__ blist) {
     __shared__ double sv[256];
     __shared__ uint32_t sk[256];
-    const int bb = blockIdx.x;
+    const int bb = blist ? blist[blockIdx.x] : blockIdx.x;
     const bool in = threadIdx.x < kReduceChunks;
     sv[threadIdx.x] = in ? part_v[(int64_t)bb * kReduceChunks + threadIdx.x] : kInf;
     sk[threadIdx.x] = in ? part_k[(int64_t)bb * kReduceChunks + threadIdx.x] : kNoKey;
@@ -563,29 +638,34 @@ __global__ __launch_bounds__(kOrderFinishThreads) void orders_finish(
 // ---------------------------------------------------------------------------
 // host-side sequencing
 // ---------------------------------------------------------------------------
+// One phase's levels for nrow b: the b of grid row y is blist[y] (all b in
+// order without a list).
 template <bool kFill>
-static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs &w, hipStream_t s) {
+static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs &w, hipStream_t s, int nrow,
+                       const int32_t *blist) {
     const int L = P.L;
-    const dim3 g1((unsigned)(((int64_t)P.K * (L + 1) + 255) / 256), (unsigned)P.nb);
-    orders_level1<kFill><<<g1, dim3(256), 0, s>>>(P, lv, w.T, w.Pst, w.Vb[1], w.root);
+    const dim3 g1((unsigned)(((int64_t)P.K * (L + 1) + 255) / 256), (unsigned)nrow);
+    orders_level1<kFill><<<g1, dim3(256), 0, s>>>(P, lv, w.T, w.Pst, w.Vb[1], w.root, blist);
     for (int d = 2; d <= lv.D; ++d) {
         // blocks: the (d-1)-sets times b, each split over the islands outside
         // the set until there are enough blocks to fill the device
-        const int64_t sets = binom(P.K, d - 1) * P.nb;
+        const int64_t sets = binom(P.K, d - 1) * nrow;
         const int nk = P.K - (d - 1);
         const int nsplit = (int)std::max<int64_t>(1, std::min<int64_t>(nk, (kTargetBlocks + sets - 1) / sets));
-        const dim3 grid((unsigned)(binom(P.K, d - 1) * nsplit), (unsigned)P.nb);
+        const dim3 grid((unsigned)(binom(P.K, d - 1) * nsplit), (unsigned)nrow);
         const double *prev = w.Vb[(d - 1) & 1];
         double *cur = w.Vb[d & 1];
-        // the set's previous-level rows go to LDS when that keeps at least 12
-        // blocks per CU
-        const size_t rows = (size_t)(L + 1) * sizeof(double);
-        const bool stage = (size_t)(d + 1) * rows <= kStageLds;
-        const size_t lds = (stage ? (size_t)(d + 1) : 2) * rows;
+        // LDS per block: the set's previous-level rows (when they fit) and a
+        // chunk of continuation rows, within kLevelLds
+        const size_t rowb = (size_t)(L + 1) * sizeof(double);
+        const int fit = (int)std::max<size_t>(1, kLevelLds / rowb);  // rows within the budget
+        const bool stage = d < fit;                                   // nu = d - 1 rows and one more
+        const int C = std::max(1, std::min(std::min(nk, kMaxSetIslands), fit - (stage ? d - 1 : 0)));
+        const size_t lds = ((stage ? (size_t)(d - 1) : 0) + (size_t)C) * rowb;
         auto go = [&](auto nt, auto st) {
             constexpr int NT = decltype(nt)::value;
             orders_level<NT, kFill, decltype(st)::value><<<grid, dim3(NT), lds, s>>>(
-                P, lv, d, nsplit, w.masks, w.rank, w.T, w.X, prev, cur, w.root, w.Pst, w.argF, w.argG);
+                P, lv, d, nsplit, C, w.masks, w.rank, w.T, w.X, prev, cur, w.root, w.Pst, w.argF, w.argG, blist);
         };
         auto pick = [&](auto nt) {
             if (stage)
@@ -593,17 +673,13 @@ static void run_levels(const DevProblem &P, const SetLevels &lv, const OrdersWs 
             else
                 go(nt, std::false_type{});
         };
-        if (L < 64)
-            pick(std::integral_constant<int, 64>{});
-        else if (L < 128)
-            pick(std::integral_constant<int, 128>{});
-        else
-            pick(std::integral_constant<int, 256>{});
+        pick(std::integral_constant<int, kLevelThreads>{});
     }
 }
 
-hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
-                                 const uint8_t *dmax, void *ws, hipStream_t s, ComposeResult **result_dev) {
+hipError_t launch_compose_orders(const DevProblem &P, const int64_t *bvals_host, const int64_t *surv, int64_t n_surv,
+                                 const double *cost, const uint8_t *dmax, void *ws, hipStream_t s,
+                                 ComposeResult **result_dev) {
     if (P.K > kMaxSetIslands || P.L > kMaxLayers || P.nb > 65535) return hipErrorInvalidValue;
     const SetLevels lv = set_levels(P);
     const OrdersWs w = carve_orders(P, n_surv, ws);
@@ -616,17 +692,81 @@ hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64
                                                                                    w.g.ent_d, w.T);
     const int64_t nx = (int64_t)P.nb * P.K * P.K * (P.L + 1);
     orders_links<<<dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s>>>(P, w.X);
-    const dim3 rgrid(kReduceChunks, (unsigned)P.nb);
-    run_levels<false>(P, lv, w, s);
-    orders_reduce_part<false><<<rgrid, dim3(256), 0, s>>>(lv, w.masks, w.root, w.part_v, w.part_k);
-    orders_reduce_final<<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.Pst, nullptr);
-    run_levels<true>(P, lv, w, s);
-    orders_reduce_part<true><<<rgrid, dim3(256), 0, s>>>(lv, w.masks, w.root, w.part_v, w.part_k);
-    orders_reduce_final<<<dim3((unsigned)P.nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.rootF, w.rootKey);
+    // phase 1 for every b: the least bottleneck P*_b
+    const int nb = P.nb;
+    run_levels<false>(P, lv, w, s, nb, nullptr);
+    orders_reduce_part<false><<<dim3(kReduceChunks, (unsigned)nb), dim3(256), 0, s>>>(lv, w.masks, w.root, w.part_v,
+                                                                                     w.part_k, nullptr);
+    orders_reduce_final<<<dim3((unsigned)nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.Pst, nullptr, nullptr);
+    // phase 2 only where a b can still win: its fill is at least P*_b (every
+    // stage and link adds a non-negative time and one of them is at least
+    // P*_b), so T_b >= (m - 1) P*_b + P*_b.  The most promising b runs first;
+    // then every b whose bound beats its T (ties to the smaller b).
+    orders_clear_roots<<<dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, s>>>(nb, w.rootF, w.rootKey);
+    std::vector<int32_t> rows;
+    if ((int64_t)nb * lv.total * (P.L + 1) < kPruneCells) {
+        // a small search: every b in one run beats two host round trips
+        for (int bi = 0; bi < nb; ++bi) rows.push_back(bi);
+        hipError_t e = hipMemcpyAsync(w.blist, rows.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return e;
+        run_levels<true>(P, lv, w, s, nb, w.blist);
+        orders_reduce_part<true><<<dim3(kReduceChunks, (unsigned)nb), dim3(256), 0, s>>>(lv, w.masks, w.root,
+                                                                                        w.part_v, w.part_k, w.blist);
+        orders_reduce_final<<<dim3((unsigned)nb), dim3(256), 0, s>>>(w.part_v, w.part_k, w.rootF, w.rootKey,
+                                                                    w.blist);
+        orders_finish<<<dim3(1), dim3(kOrderFinishThreads), 0, s>>>(P, lv, w.masks, w.rank, w.g.gcnt, w.g.ent_c,
+                                                                    w.g.ent_d, w.g.ent_i, w.X, w.Pst, w.rootF,
+                                                                    w.rootKey, w.argF, w.argG, w.res);
+        e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(s);  // the b list above must outlive its copy
+        return e;
+    }
+    std::vector<double> pst(nb);
+    hipError_t e = hipMemcpyAsync(pst.data(), w.Pst, sizeof(double) * nb, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    std::vector<double> lb(nb, kInf), mm1(nb);
+    int b0 = -1;
+    for (int bi = 0; bi < nb; ++bi) {
+        mm1[bi] = (double)(P.B / bvals_host[bi] - 1);
+        if (!(pst[bi] < kInf)) continue;
+        lb[bi] = (mm1[bi] * pst[bi]) + pst[bi];
+        if (b0 < 0 || lb[bi] < lb[b0]) b0 = bi;
+    }
+    auto fill_run = [&](const std::vector<int32_t> &bl) -> hipError_t {
+        hipError_t e2 = hipMemcpyAsync(w.blist, bl.data(), sizeof(int32_t) * bl.size(), hipMemcpyHostToDevice, s);
+        if (e2 != hipSuccess) return e2;
+        const int n = (int)bl.size();
+        run_levels<true>(P, lv, w, s, n, w.blist);
+        orders_reduce_part<true><<<dim3(kReduceChunks, (unsigned)n), dim3(256), 0, s>>>(lv, w.masks, w.root,
+                                                                                       w.part_v, w.part_k, w.blist);
+        orders_reduce_final<<<dim3((unsigned)n), dim3(256), 0, s>>>(w.part_v, w.part_k, w.rootF, w.rootKey,
+                                                                   w.blist);
+        return hipGetLastError();
+    };
+    if (b0 >= 0) {
+        rows.assign(1, b0);
+        e = fill_run(rows);
+        double f0 = kInf;
+        if (e == hipSuccess) e = hipMemcpyAsync(&f0, w.rootF + b0, sizeof(double), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return e;
+        const double t0 = (mm1[b0] * pst[b0]) + f0;
+        std::vector<int32_t> rest;
+        for (int bi = 0; bi < nb; ++bi)
+            if (bi != b0 && lb[bi] < kInf && (lb[bi] < t0 || (lb[bi] == t0 && bi < b0))) rest.push_back(bi);
+        if (!rest.empty()) {
+            rows = rest;
+            e = fill_run(rows);
+            if (e != hipSuccess) return e;
+        }
+    }
     orders_finish<<<dim3(1), dim3(kOrderFinishThreads), 0, s>>>(P, lv, w.masks, w.rank, w.g.gcnt, w.g.ent_c,
                                                                 w.g.ent_d, w.g.ent_i, w.X, w.Pst, w.rootF,
                                                                 w.rootKey, w.argF, w.argG, w.res);
-    return hipGetLastError();
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);  // the b list above must outlive its copy
+    return e;
 }
 
 }  // namespace tg

@@ -211,8 +211,9 @@ hipError_t launch_build_islands(int n, const tg_island *nodes_host, const double
                                 tg_island *islands, double *inter_bw, int32_t *n_islands, int64_t *bad_bw);
 // Composition over every island subset and order (K <= 16).
 size_t compose_orders_ws_bytes(const DevProblem &P, int64_t n_surv);
-hipError_t launch_compose_orders(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
-                                 const uint8_t *dmax, void *ws, hipStream_t s, ComposeResult **result_dev);
+hipError_t launch_compose_orders(const DevProblem &P, const int64_t *bvals_host, const int64_t *surv, int64_t n_surv,
+                                 const double *cost, const uint8_t *dmax, void *ws, hipStream_t s,
+                                 ComposeResult **result_dev);
 // Synchronises the stream several times (once per search round).
 hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
                                   const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,
