@@ -121,3 +121,33 @@ def test_extended_named_against_stored(name):
     plan_equal(plan, g["plan"])
     del cost, dmax, surv
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,ext", [("large", False), ("large", True), ("moe", False), ("dense70b", True)])
+def test_full_size_scores_against_the_oracle(name, ext):
+    """Per-candidate scores at full size in the launch configuration bench.py
+    times, against the oracle one candidate at a time: 48 whole config rows
+    (every slice of configs spread over the islands, the first and the last
+    included), 250,000 seeded random candidates and the last 4,096 (on the
+    extended 128-island instance N > 2^32, so the 64-bit index path is
+    covered end to end)."""
+    import zlib
+    inst = load_instance(name)
+    if ext:
+        inst = extended(inst)
+    print("case", name, "extended" if ext else "", flush=True)
+    p = T.Problem(inst)
+    N, NS, C = p.N, p.NS, p.n_configs
+    rng = np.random.default_rng(zlib.crc32(f"{name}/{ext}".encode()))
+    rows = np.unique(np.r_[0, C - 1, np.linspace(0, C - 1, 46).astype(np.int64)])
+    idx = np.unique(np.r_[(rows[:, None] * NS + np.arange(NS)[None, :]).ravel(),
+                          rng.integers(0, N, size=250_000), np.arange(max(0, N - 4096), N)])
+    cost, dmax = p.tg_score_pairs()
+    t = torch.from_numpy(idx).cuda()
+    gc, gd = cost[t].cpu().numpy(), dmax[t].cpu().numpy()
+    del cost, dmax, t
+    torch.cuda.empty_cache()
+    oc, od = Oracle(inst).score_list(idx)
+    bad = np.nonzero((bits(gc) != bits(oc)) | (gd != od))[0]
+    assert bad.size == 0, [(int(idx[b]), float(gc[b]), float(oc[b]), int(gd[b]), int(od[b])) for b in bad[:5]]
+    assert len(idx) >= 250_000 and (idx >= 2 ** 32).any() == (N > 2 ** 32)
