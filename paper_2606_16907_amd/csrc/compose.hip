@@ -1089,6 +1089,41 @@ __global__ __launch_bounds__(256) void pst_kernel(DevProblem P, int D, const dou
     }
 }
 
+// The b that cannot win skip the fill.  T_b = (m - 1) P*_b + F_b with F_b at
+// least P*_b (the fill adds non-negative stage and link times, one of them at
+// least P*_b), so T_b >= LB_b = (m - 1) P*_b + P*_b, rounded as T_b is.  The
+// least-bottleneck plan of the shallowest level d reaching P*_b has d stages
+// and d - 1 links, each within P*_b, so F_b <= (2 d - 1) P*_b and T_b <= UB_b
+// (with a margin far above the rounding of a sum of at most 2D terms).  A b
+// with LB_b above the least UB can neither win nor tie: its depth limit
+// becomes 0, and the fill of step (3) skips it.  One block.
+__global__ __launch_bounds__(256) void bound_b_kernel(DevProblem P, int D, const double *__restrict__ Rv,
+                                                      const double *__restrict__ Pst, int32_t *dlim) {
+    __shared__ double red[256];
+    double ub = kInf;
+    for (int bi = threadIdx.x; bi < P.nb; bi += blockDim.x) {
+        const double ps = Pst[bi];
+        if (!(ps < kInf)) continue;
+        int d = 1;
+        while (d < D && !(Rv[(int64_t)(d - 1) * P.nb + bi] <= ps)) ++d;
+        const double mm1 = (double)(P.B / P.bvals[bi] - 1);
+        ub = fmin(ub, ((mm1 * ps) + ((double)(2 * d - 1) * ps)) * (1.0 + 1e-12));
+    }
+    red[threadIdx.x] = ub;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] = fmin(red[threadIdx.x], red[threadIdx.x + h]);
+        __syncthreads();
+    }
+    ub = red[0];
+    for (int bi = threadIdx.x; bi < P.nb; bi += blockDim.x) {
+        const double ps = Pst[bi];
+        if (!(ps < kInf)) continue;
+        const double mm1 = (double)(P.B / P.bvals[bi] - 1);
+        if ((mm1 * ps) + ps > ub) dlim[bi] = 0;
+    }
+}
+
 // The root of each b: the least fill over the levels, ties to the least first
 // position, then the least depth.  One wave per b.
 __global__ __launch_bounds__(256) void roots_kernel(DevProblem P, int D, const double *RF, const int32_t *RO,
@@ -1598,6 +1633,7 @@ struct Driver {
             }
         });
         pst_kernel<<<dim3((unsigned)((P.nb + 3) / 4)), dim3(256), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
+        bound_b_kernel<<<dim3(1), dim3(256), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
     }
 
     // The deepest fill level any b needs.  Reading w.dlim back costs one host
