@@ -240,7 +240,7 @@ def write_ceiling(torch, nbytes, reps=5):
     return gbs
 
 
-def time_search(torch, T, inst, steps, warmup):
+def time_search(torch, T, inst, steps, warmup, relaxed_steps=0):
     """Create the problem, size the buffers (untimed), then run `warmup` and
     `steps` whole plan searches (score, prune, compose with the plan on the
     host), with HIP events between the three calls of every timed step."""
@@ -303,7 +303,23 @@ def time_search(torch, T, inst, steps, warmup):
                   "stages": oplan["S"], "T": oplan["T"],
                   "islands": [x["island"] for x in oplan["stages"]]}
         del ows
-    return {"problem": p, "all_orders": orders, "N": N, "cost": cost, "dmax": dmax, "survivors": s, "status": st,
+    relaxed = None
+    if relaxed_steps > 0 and steps > 0:
+        # the composition with the step-(4) relaxation on the same survivors
+        # (host clock around each call: it synchronises per search round)
+        rws = p.compose_relaxed_workspace(int(s.numel()))
+        p.tg_compose_pipeline_relaxed(s, cost, dmax, workspace=rws)  # warm-up
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(relaxed_steps):
+            t1 = time.perf_counter()
+            rst, rplan = p.tg_compose_pipeline_relaxed(s, cost, dmax, workspace=rws)
+            times.append((time.perf_counter() - t1) * 1e3)
+        times.sort()
+        relaxed = {"compose_ms_median": times[len(times) // 2], "status": rst, "b": rplan["b"],
+                   "stages": rplan["S"], "T": rplan["T"]}
+        del rws
+    return {"problem": p, "all_orders": orders, "relaxed": relaxed, "N": N, "cost": cost, "dmax": dmax, "survivors": s, "status": st,
             "plan": plan, "elapsed": elapsed, "create_s": t_create,
             "score_ms": [ev[k][0].elapsed_time(ev[k][1]) for k in range(steps)],
             "prune_ms": [ev[k][1].elapsed_time(ev[k][2]) for k in range(steps)],
@@ -324,7 +340,7 @@ def five_workloads(torch, T, load_instance, space, steps, main_name, main_row, i
             from workloads import extended
             inst = extended(inst)
         inst["space"]["imbalance_eps"] = imbalance_eps
-        run = time_search(torch, T, inst, steps, 2)
+        run = time_search(torch, T, inst, steps, 2, relaxed_steps=min(steps, 5))
         out[name] = workload_row(run, steps)
         del run
         torch.cuda.empty_cache()
@@ -342,7 +358,8 @@ def workload_row(run, steps):
             "plan": {"status": run["status"], "b": run["plan"]["b"], "stages": run["plan"]["S"],
                      "T": run["plan"]["T"]},
             "plan_full": run["plan"],
-            "all_orders_compose": run["all_orders"]}
+            "all_orders_compose": run["all_orders"],
+            "relaxed_compose": run.get("relaxed")}
 
 
 def redundancy_search(torch, T, p, steps, order=None):
@@ -535,6 +552,7 @@ def main():
     }
     if args.other_steps > 0:
         main_row = workload_row(run, args.steps)
+        main_row["relaxed_compose"] = relaxed
         del run, cost, dmax, s
         torch.cuda.empty_cache()
         out["workloads"] = five_workloads(torch, T, load_instance, args.space, args.other_steps,
