@@ -1069,54 +1069,52 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
 
 // P*_b = least whole-plan bottleneck over the levels; dlim[b] = the deepest
 // level whose whole-plan bottleneck reaches P*_b (the fill of step (3) has
-// no plan deeper than that), 0 when b has no plan.  One wave per b.
-__global__ __launch_bounds__(256) void pst_kernel(DevProblem P, int D, const double *Rv, double *Pst,
-                                                  int32_t *dlim) {
-    const int bi = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    const int lane = threadIdx.x & (kWave - 1);
-    if (bi >= P.nb) return;
-    double m = kInf;
-    for (int d = lane; d < D; d += kWave) m = fmin(m, Rv[(int64_t)d * P.nb + bi]);
-    m = wave_min(m);
-    int top = 0;
-    for (int d = lane; d < D; d += kWave)
-        if (m < kInf && Rv[(int64_t)d * P.nb + bi] <= m) top = d + 1;
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) top = max(top, __shfl_xor(top, off));
-    if (lane == 0) {
-        Pst[bi] = m;
-        dlim[bi] = top;
-    }
-}
-
-// The b that cannot win skip the fill.  T_b = (m - 1) P*_b + F_b with F_b at
-// least P*_b (the fill adds non-negative stage and link times, one of them at
-// least P*_b), so T_b >= LB_b = (m - 1) P*_b + P*_b, rounded as T_b is.  The
+// no plan deeper than that), 0 when b has no plan.  Then the b that cannot
+// win skip the fill: T_b = (m - 1) P*_b + F_b with F_b at least P*_b (the
+// fill adds non-negative stage and link times, one of them at least P*_b),
+// so T_b >= LB_b = (m - 1) P*_b + P*_b, rounded as T_b is.  The
 // least-bottleneck plan of the shallowest level d reaching P*_b has d stages
 // and d - 1 links, each within P*_b, so F_b <= (2 d - 1) P*_b and T_b <= UB_b
 // (with a margin far above the rounding of a sum of at most 2D terms).  A b
 // with LB_b above the least UB can neither win nor tie: its depth limit
-// becomes 0, and the fill of step (3) skips it.  One block.
-__global__ __launch_bounds__(256) void bound_b_kernel(DevProblem P, int D, const double *__restrict__ Rv,
-                                                      const double *__restrict__ Pst, int32_t *dlim) {
-    __shared__ double red[256];
+// becomes 0.  One block; a wave per b searches the levels.
+constexpr int kPstThreads = 1024;
+
+__global__ __launch_bounds__(kPstThreads) void pst_kernel(DevProblem P, int D, const double *__restrict__ Rv,
+                                                          double *Pst, int32_t *dlim) {
+    __shared__ double red[kPstThreads / kWave];
+    const int wv = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
     double ub = kInf;
-    for (int bi = threadIdx.x; bi < P.nb; bi += blockDim.x) {
-        const double ps = Pst[bi];
-        if (!(ps < kInf)) continue;
-        int d = 1;
-        while (d < D && !(Rv[(int64_t)(d - 1) * P.nb + bi] <= ps)) ++d;
-        const double mm1 = (double)(P.B / P.bvals[bi] - 1);
-        ub = fmin(ub, ((mm1 * ps) + ((double)(2 * d - 1) * ps)) * (1.0 + 1e-12));
+    for (int bi = wv; bi < P.nb; bi += kPstThreads / kWave) {
+        double m = kInf;
+        for (int d = lane; d < D; d += kWave) m = fmin(m, Rv[(int64_t)d * P.nb + bi]);
+        m = wave_min(m);
+        int top = 0, first = INT_MAX;
+        for (int d = lane; d < D; d += kWave)
+            if (m < kInf && Rv[(int64_t)d * P.nb + bi] <= m) {
+                top = d + 1;
+                first = min(first, d + 1);
+            }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            top = max(top, __shfl_xor(top, off));
+            first = min(first, __shfl_xor(first, off));
+        }
+        if (lane == 0) {
+            Pst[bi] = m;
+            dlim[bi] = top;
+        }
+        if (m < kInf) {
+            const double mm1 = (double)(P.B / P.bvals[bi] - 1);
+            ub = fmin(ub, ((mm1 * m) + ((double)(2 * first - 1) * m)) * (1.0 + 1e-12));
+        }
     }
-    red[threadIdx.x] = ub;
+    if (lane == 0) red[wv] = ub;
     __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-        if ((int)threadIdx.x < h) red[threadIdx.x] = fmin(red[threadIdx.x], red[threadIdx.x + h]);
-        __syncthreads();
-    }
     ub = red[0];
-    for (int bi = threadIdx.x; bi < P.nb; bi += blockDim.x) {
+#pragma unroll
+    for (int u = 1; u < kPstThreads / kWave; ++u) ub = fmin(ub, red[u]);
+    for (int bi = threadIdx.x; bi < P.nb; bi += kPstThreads) {
         const double ps = Pst[bi];
         if (!(ps < kInf)) continue;
         const double mm1 = (double)(P.B / P.bvals[bi] - 1);
@@ -1632,8 +1630,7 @@ struct Driver {
                     go(std::integral_constant<int, 2>{});
             }
         });
-        pst_kernel<<<dim3((unsigned)((P.nb + 3) / 4)), dim3(256), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
-        bound_b_kernel<<<dim3(1), dim3(256), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
+        pst_kernel<<<dim3(1), dim3(kPstThreads), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
     }
 
     // The deepest fill level any b needs.  Reading w.dlim back costs one host
