@@ -249,7 +249,7 @@ __host__ __device__ inline int64_t cell_id(const DevProblem &P, int64_t bi, int6
 __host__ __device__ inline int tri(int o, int o2) { return o2 * (o2 - 1) / 2 + o; }
 
 __global__ __launch_bounds__(256) void prep_kernel(DevProblem P, const int32_t *order, int32_t *pos, double *EoT,
-                                                   uint8_t *EiT, ComposeResult *res) {
+                                                   uint8_t *EiT, ComposeResult *res, int32_t *ev_total) {
     const int K = P.K;
     const int t = blockIdx.x * blockDim.x + threadIdx.x;
     if (t < K) pos[order[t]] = t;
@@ -262,6 +262,7 @@ __global__ __launch_bounds__(256) void prep_kernel(DevProblem P, const int32_t *
     if (t == 0) {
         res->err = 0;
         res->status = TG_ENOPLAN;
+        *ev_total = 0;
     }
 }
 
@@ -1569,10 +1570,9 @@ struct Driver {
     // phase) and per-row, per-level table changes
     void setup(const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax) {
         prep_kernel<<<dim3((unsigned)((P.K * P.K + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.pos, w.EoT,
-                                                                                     w.EiT, w.res);
+                                                                                     w.EiT, w.res, w.ev_total);
         if (P.imb)
             jlo_kernel<<<dim3((unsigned)((P.K * P.L + 255) / 256)), dim3(256), 0, s>>>(P, w.order, w.jlo_pos);
-        fill<int32_t>(w.ev_total, 1, 0, s);
         const Groups g{w.rec_g, w.rec_c, w.rec_d, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.tmp};
         launch_grouping(P, surv, n_surv, cost, dmax, w.pos, g, w.res, s);
         row_tables<<<dim3((unsigned)P.L, (unsigned)P.nb), dim3(kRowThreads), 0, s>>>(
@@ -1600,18 +1600,16 @@ struct Driver {
         return blocks <= cap3 ? 3 : 2;
     }
 
-    // the continuation rows start at +inf
-    void start_tables(double *G0, double *G1, int64_t n) {
-        fill<double>(G0, n, kInf, s);
-        fill<double>(G1, n, kInf, s);
-    }
+    // The continuation rows need no clearing: level d reads rows j of level
+    // d - 1 only for i < j <= L - d + 1 (the cut scan stops there), and level
+    // d - 1 wrote every row 1..L - d + 1 at every position (a b or job that
+    // skips a level skips every deeper one too).
 
     // phase 1: least bottleneck per b into w.Pst, the fill's depth limit per b
     // into w.dlim
     void phase1() {
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(w.Wb[0], w.Wb[1], rows);
             for (int d = 1; d <= D; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
@@ -1661,7 +1659,6 @@ struct Driver {
         fill<int32_t>(w.RO, (int64_t)D * P.nb, -1, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(w.Wb[0], w.Wb[1], rows);
             for (int d = 1; d <= nlev; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
@@ -1713,7 +1710,6 @@ struct Driver {
         fill<int32_t>(r.row_cnt, (int64_t)P.nb * P.L, 0, s);
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            start_tables(r.job_G, r.job_G + jrows, (int64_t)J * (P.L + 1) * P.K);
             for (int d = 1; d <= nlev; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)J);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));

@@ -1,0 +1,72 @@
+"""The compositions read nothing of their workspace that the same call did not
+write first.  A workspace is dirtied by a call on a thinned candidate list
+(every third survivor dropped: different groups, tables and continuation
+rows), then reused for the full surviving set; the plan must equal, bit for
+bit, the plan computed on a fresh workspace."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from tests.test_gpu_parity import bits  # noqa: E402
+from workloads import load_instance, random_tiny  # noqa: E402
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2606_16907_amd import tangram as T  # noqa: E402
+
+
+def same_plan(a, b):
+    assert (a["b"], a["m"], a["S"]) == (b["b"], b["m"], b["S"])
+    for f in ("P", "F", "T"):
+        assert bits(a[f]) == bits(b[f]), f
+    assert a["stages"] == b["stages"]
+
+
+def cases():
+    out = [(n, lambda n=n: load_instance(n)) for n in ("tiny", "dense8b", "dense70b", "moe")]
+    out += [(f"random{s}", lambda s=s: random_tiny(s)) for s in (3, 11)]
+    return out
+
+
+CASES = cases()
+
+
+@pytest.mark.parametrize("which", ["fixed", "relaxed", "all_orders"])
+@pytest.mark.parametrize("name,make", CASES, ids=[c[0] for c in CASES])
+def test_dirty_workspace_gives_the_same_plan(name, make, which):
+    print("case", name, which, flush=True)
+    inst = make()
+    p = T.Problem(inst)
+    if which == "all_orders" and p.K > 16:
+        pytest.skip("all-orders composition takes at most 16 islands")
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    n = int(surv.numel())
+    keep = torch.ones(n, dtype=torch.bool, device=surv.device)
+    keep[::3] = False
+    thin = surv[keep].contiguous()
+    call = {"fixed": (p.tg_compose_pipeline, p.compose_workspace),
+            "relaxed": (p.tg_compose_pipeline_relaxed, p.compose_relaxed_workspace),
+            "all_orders": (p.tg_compose_pipeline_all_orders, p.compose_all_orders_workspace)}[which]
+    compose, workspace = call
+    fresh_st, fresh = compose(surv, cost, dmax, workspace=workspace(n))
+    ws = workspace(n)
+    try:  # only dirties the workspace: a thinned list need not give a plan
+        compose(thin, cost, dmax, workspace=ws)
+    except T.TangramError:
+        pass
+    st, plan = compose(surv, cost, dmax, workspace=ws)
+    torch.cuda.synchronize()
+    assert st == fresh_st
+    if st == T.TG_OK:
+        same_plan(plan, fresh)
+    # and once more after a full-list call on the same workspace
+    st2, plan2 = compose(surv, cost, dmax, workspace=ws)
+    assert st2 == fresh_st
+    if st2 == T.TG_OK:
+        same_plan(plan2, fresh)
+    assert np.isfinite(fresh["T"]) or fresh_st != T.TG_OK
