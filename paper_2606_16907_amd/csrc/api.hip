@@ -464,6 +464,8 @@ void tg_problem_destroy(tg_problem *p) {
     (void)hipSetDevice(p->device);
     (void)hipFree(p->dev_block);
     p->relax_stage.release();
+    p->compose_stage.release();
+    if (p->compose_ev) (void)hipEventDestroy(p->compose_ev);
     (void)hipSetDevice(cur);
     delete p;
 }
@@ -696,7 +698,21 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
                                  need, s);
     if (st != TG_OK) return st;
     tg::ComposeResult *res_dev = nullptr;
-    hipError_t e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev);
+    // the handle's pinned read-back words, when no other call holds them
+    std::unique_lock<std::mutex> lock(p->compose_mu, std::try_to_lock);
+    tg::ComposeHost host{nullptr, nullptr};
+    if (lock.owns_lock()) {
+        // a failed allocation only means the synchronous read-back
+        if (p->compose_stage.reserve(sizeof(int32_t) * (size_t)p->P.nb) != hipSuccess) {
+            (void)hipGetLastError();
+        } else if (!p->compose_ev && hipEventCreateWithFlags(&p->compose_ev, hipEventDisableTiming) != hipSuccess) {
+            p->compose_ev = nullptr;
+            (void)hipGetLastError();
+        }
+        if (p->compose_stage.ptr && p->compose_ev) host = tg::ComposeHost{p->compose_stage.ptr, p->compose_ev};
+    }
+    hipError_t e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev,
+                                      host.pinned ? &host : nullptr);
     if (e != hipSuccess) return hip_fail(e, "compose kernels");
     return compose_end(res_dev, out, s);
 }

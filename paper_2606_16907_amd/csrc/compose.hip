@@ -1654,12 +1654,20 @@ struct Driver {
     // dlim[b] when given: fills, argmins and roots per b, from the starting
     // stage table in `table` (phase 2's own copy unless given).
     void phase2(const double *bound, const int32_t *dlim, int nlev, double *table = nullptr) {
-        if (!table) table = w.T0;
+        phase2_begin();
+        phase2_levels(bound, dlim, 1, nlev, table);
+        phase2_end();
+    }
+    void phase2_begin() {
         fill<double>(w.RF, (int64_t)D * P.nb, kInf, s);
         fill<int32_t>(w.RO, (int64_t)D * P.nb, -1, s);
+    }
+    // levels d0..d1 (a level past a b's limit costs only its early return)
+    void phase2_levels(const double *bound, const int32_t *dlim, int d0, int d1, double *table = nullptr) {
+        if (!table) table = w.T0;
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
-            for (int d = 1; d <= nlev; ++d) {
+            for (int d = d0; d <= d1; ++d) {
                 const dim3 grid((unsigned)(P.L - d + 1), (unsigned)P.nb);
                 const int sp = split_for<KP>((int)(grid.x * grid.y));
                 const double *Gp = w.Wb[(d - 1) & 1];
@@ -1678,6 +1686,8 @@ struct Driver {
                     go(std::integral_constant<int, 2>{});
             }
         });
+    }
+    void phase2_end() {
         roots_kernel<<<dim3((unsigned)((P.nb + 3) / 4)), dim3(256), 0, s>>>(P, D, w.RF, w.RO, w.rootF, w.root_o,
                                                                             w.root_d);
     }
@@ -1738,9 +1748,13 @@ struct Driver {
     }
 };
 
+// Fill levels queued ahead of the read-back of the depth limits, so the GPU
+// is not idle while the host waits for them.
+constexpr int kLeadLevels = 8;
+
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
-                          ComposeResult **result_dev) {
+                          ComposeResult **result_dev, const ComposeHost *host) {
     (void)order_dev;
     Driver dr(P, n_surv, ws, s);
     *result_dev = dr.w.res;
@@ -1748,10 +1762,29 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dr.phase1();
-    int nlev = 0;
-    e = dr.fill_levels(&nlev);
-    if (e != hipSuccess) return e;
-    dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
+    if (dr.D >= kSyncLevels && host && host->pinned && host->ev) {
+        // the depth limits go to pinned memory right after phase 1; the first
+        // fill levels are queued behind the copy, and the host waits for the
+        // copy alone before queueing the levels some b still needs
+        e = hipMemcpyAsync(host->pinned, dr.w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipEventRecord(host->ev, s);
+        if (e != hipSuccess) return e;
+        const int lead = std::min(dr.D, kLeadLevels);
+        dr.phase2_begin();
+        dr.phase2_levels(dr.w.Pst, dr.w.dlim, 1, lead);
+        e = hipEventSynchronize(host->ev);
+        if (e != hipSuccess) return e;
+        int nlev = 0;
+        const int32_t *dl = (const int32_t *)host->pinned;
+        for (int b = 0; b < P.nb; ++b) nlev = std::max(nlev, std::min((int)dl[b], dr.D));
+        dr.phase2_levels(dr.w.Pst, dr.w.dlim, lead + 1, nlev);
+        dr.phase2_end();
+    } else {
+        int nlev = 0;
+        e = dr.fill_levels(&nlev);
+        if (e != hipSuccess) return e;
+        dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
+    }
     dr.finish(dr.w.Pst);
     return hipGetLastError();
 }

@@ -167,9 +167,17 @@ struct ComposeResult {
     int32_t pad[2];
     tg_plan plan;
 };
+// Pinned host words (at least nb int32) and an event on the current device,
+// with which the composition reads its fill depth limits back while the
+// first fill levels run; without them (null) the read-back synchronises the
+// stream.
+struct ComposeHost {
+    void *pinned;
+    hipEvent_t ev;
+};
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
-                          ComposeResult **result_dev);
+                          ComposeResult **result_dev, const ComposeHost *host = nullptr);
 size_t compose_order_offset(const DevProblem &P, int64_t n_surv);  // where the order table lives in ws
 
 // Host tables the relaxed search reads (link times are enumerated on the host).

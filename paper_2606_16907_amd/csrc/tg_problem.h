@@ -20,4 +20,10 @@ struct tg_problem {
     // freed at destroy; relaxed calls on one handle take turns on it
     mutable std::mutex relax_mu;
     mutable tg::HostStage relax_stage;
+    // pinned words and an event for the composition's read-back of the fill
+    // depth limits: taken by one call at a time (a call that finds them busy
+    // reads back synchronously), freed at destroy
+    mutable std::mutex compose_mu;
+    mutable tg::HostStage compose_stage;
+    mutable hipEvent_t compose_ev = nullptr;
 };
