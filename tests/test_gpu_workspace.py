@@ -2,7 +2,12 @@
 write first.  A workspace is dirtied by a call on a thinned candidate list
 (every third survivor dropped: different groups, tables and continuation
 rows), then reused for the full surviving set; the plan must equal, bit for
-bit, the plan computed on a fresh workspace."""
+bit, the plan computed on a fresh workspace.  And calls on one handle from
+several threads and streams (which share the handle's pinned read-back
+words: one call at a time uses them, the others read back synchronously)
+give the single-threaded plan."""
+import threading
+
 import numpy as np
 import pytest
 
@@ -10,6 +15,7 @@ torch = pytest.importorskip("torch")
 
 pytestmark = pytest.mark.gpu
 
+from tests.edge_instances import wide_instance  # noqa: E402
 from tests.test_gpu_parity import bits  # noqa: E402
 from workloads import load_instance, random_tiny  # noqa: E402
 
@@ -70,3 +76,42 @@ def test_dirty_workspace_gives_the_same_plan(name, make, which):
     if st2 == T.TG_OK:
         same_plan(plan2, fresh)
     assert np.isfinite(fresh["T"]) or fresh_st != T.TG_OK
+
+
+def test_threads_on_one_handle_give_the_same_plan():
+    # 70 islands x 70 layers: 70 levels, so the composition reads its fill
+    # depth limits back part-way through
+    inst = wide_instance(21, 70, 70, "few")
+    print("case", inst["name"], flush=True)
+    p = T.Problem(inst)
+    cost, dmax = p.tg_score_pairs()
+    surv = p.tg_prune(cost, dmax)
+    n = int(surv.numel())
+    ref_st, ref = p.tg_compose_pipeline(surv, cost, dmax)
+    torch.cuda.synchronize()
+    out, errors = [[], [], []], []
+
+    def worker(k):
+        try:
+            ws = p.compose_workspace(n)
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s):
+                for _ in range(5):
+                    out[k].append(p.tg_compose_pipeline(surv, cost, dmax, workspace=ws))
+            s.synchronize()
+        except Exception as e:  # reported below, in the test's own thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(3)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for runs in out:
+        assert len(runs) == 5
+        for st, plan in runs:
+            assert st == ref_st
+            if st == T.TG_OK:
+                same_plan(plan, ref)
