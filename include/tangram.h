@@ -329,12 +329,13 @@ tg_status tg_compose_pipeline_classes(const tg_problem *p, const int64_t *d_surv
  * fewer stages, then the earliest cut, then the earliest next island.
  * Writes *out; TG_ENOPLAN (out->S = 0, out->T = +inf) if nothing fits.
  * d_ws: at least tg_compose_workspace_bytes(p, n_survivors) bytes.
- * Synchronises the stream at its end.  With 64 or more levels (min(K, L))
+ * Synchronises the stream at its end.  With more than 8 levels (min(K, L))
  * the host also waits once part-way, for a copy of the fill depth limits
  * into a few pinned bytes the handle owns (allocated at the first call,
  * freed by tg_problem_destroy), while the first fill levels run; a call that
  * finds them in use by another call on the same handle synchronises the
- * stream there instead.
+ * stream there instead when there are 64 levels or more, and otherwise
+ * launches every fill level.
  */
 size_t tg_compose_workspace_bytes(const tg_problem *p, int64_t n_survivors);
 tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,

@@ -1762,10 +1762,11 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dr.phase1();
-    if (dr.D >= kSyncLevels && host && host->pinned && host->ev) {
+    if (dr.D > kLeadLevels && host && host->pinned && host->ev) {
         // the depth limits go to pinned memory right after phase 1; the first
         // fill levels are queued behind the copy, and the host waits for the
-        // copy alone before queueing the levels some b still needs
+        // copy alone before queueing the levels some b still needs (the GPU
+        // keeps busy meanwhile, so this pays at any depth past the lead)
         e = hipMemcpyAsync(host->pinned, dr.w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
         if (e == hipSuccess) e = hipEventRecord(host->ev, s);
         if (e != hipSuccess) return e;
