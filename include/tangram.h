@@ -357,11 +357,12 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
  * requirements and errors as for tg_compose_pipeline; d_ws: at least
  * tg_compose_relaxed_workspace_bytes(p, n_survivors) bytes.  Synchronises the
  * stream after the bottleneck and fill phases and once per search round (a
- * few rounds; each evaluates F at a batch of bounds on the device).  The
- * host side of the search reads back and uploads through a small pinned host
- * buffer that the handle owns (allocated at the first call, freed by
- * tg_problem_destroy); relaxed calls on one handle from several threads take
- * turns.
+ * few rounds; each evaluates F at a batch of bounds on the device), and with
+ * more than 8 levels waits once more part-way, for a copy of the fill depth
+ * limits, while the first fill levels run.  The host side of the search reads
+ * back and uploads through a small pinned host buffer that the handle owns
+ * (allocated at the first call, freed by tg_problem_destroy); relaxed calls on
+ * one handle from several threads take turns.
  */
 size_t tg_compose_relaxed_workspace_bytes(const tg_problem *p, int64_t n_survivors);
 tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,

@@ -466,6 +466,7 @@ void tg_problem_destroy(tg_problem *p) {
     p->relax_stage.release();
     p->compose_stage.release();
     if (p->compose_ev) (void)hipEventDestroy(p->compose_ev);
+    if (p->relax_ev) (void)hipEventDestroy(p->relax_ev);
     (void)hipSetDevice(cur);
     delete p;
 }
@@ -747,7 +748,11 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
         std::lock_guard<std::mutex> lock(p->relax_mu);  // one relaxed call at a time uses the handle's staging
         const hipError_t es = p->relax_stage.reserve(tg::compose_relaxed_stage_bytes(p->P));
         if (es != hipSuccess) return hip_fail(es, "pinned host staging");
-        const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B, &p->relax_stage};
+        if (!p->relax_ev && hipEventCreateWithFlags(&p->relax_ev, hipEventDisableTiming) != hipSuccess) {
+            p->relax_ev = nullptr;  // the depth limits are then read back by a stream synchronisation
+            (void)hipGetLastError();
+        }
+        const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B, &p->relax_stage, p->relax_ev};
         tg::ComposeResult *res_dev = nullptr;
         int rounds = 0;
         hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax,

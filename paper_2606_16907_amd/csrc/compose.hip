@@ -1545,6 +1545,9 @@ __global__ __launch_bounds__(kInitThreads) void relax_init(DevProblem P, const d
 // Pipelines of at least this many levels read the fill's depth limits back
 // before phase 2 and launch only the levels some b needs.
 constexpr int kSyncLevels = 64;
+// Fill levels queued ahead of the read-back of the depth limits when they go
+// through pinned memory, so the GPU is not idle while the host waits.
+constexpr int kLeadLevels = 8;
 
 // Sequencing of the composition kernels on one workspace.
 struct Driver {
@@ -1658,6 +1661,27 @@ struct Driver {
         phase2_levels(bound, dlim, 1, nlev, table);
         phase2_end();
     }
+    // Phase 2 at P* with the depth limits read back through `pinned` (at least
+    // nb int32 of pinned host memory) and the event `ev`: the limits are copied
+    // right after phase 1, the first kLeadLevels fill levels are queued
+    // behind the copy, and the host waits for the copy alone before queueing
+    // the levels some b still needs, so the GPU keeps busy meanwhile.
+    hipError_t phase2_read_back(void *pinned, hipEvent_t ev) {
+        hipError_t e = hipMemcpyAsync(pinned, w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipEventRecord(ev, s);
+        if (e != hipSuccess) return e;
+        const int lead = std::min(D, kLeadLevels);
+        phase2_begin();
+        phase2_levels(w.Pst, w.dlim, 1, lead);
+        e = hipEventSynchronize(ev);
+        if (e != hipSuccess) return e;
+        int nlev = 0;
+        const int32_t *dl = (const int32_t *)pinned;
+        for (int b = 0; b < P.nb; ++b) nlev = std::max(nlev, std::min((int)dl[b], D));
+        phase2_levels(w.Pst, w.dlim, lead + 1, nlev);
+        phase2_end();
+        return hipSuccess;
+    }
     void phase2_begin() {
         fill<double>(w.RF, (int64_t)D * P.nb, kInf, s);
         fill<int32_t>(w.RO, (int64_t)D * P.nb, -1, s);
@@ -1748,10 +1772,6 @@ struct Driver {
     }
 };
 
-// Fill levels queued ahead of the read-back of the depth limits, so the GPU
-// is not idle while the host waits for them.
-constexpr int kLeadLevels = 8;
-
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
                           const uint8_t *dmax, const int32_t *order_dev, void *ws, hipStream_t s,
                           ComposeResult **result_dev, const ComposeHost *host) {
@@ -1763,23 +1783,9 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     if (e != hipSuccess) return e;
     dr.phase1();
     if (dr.D > kLeadLevels && host && host->pinned && host->ev) {
-        // the depth limits go to pinned memory right after phase 1; the first
-        // fill levels are queued behind the copy, and the host waits for the
-        // copy alone before queueing the levels some b still needs (the GPU
-        // keeps busy meanwhile, so this pays at any depth past the lead)
-        e = hipMemcpyAsync(host->pinned, dr.w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
-        if (e == hipSuccess) e = hipEventRecord(host->ev, s);
+        // pays at any depth past the lead: the GPU keeps busy while the host waits
+        e = dr.phase2_read_back(host->pinned, host->ev);
         if (e != hipSuccess) return e;
-        const int lead = std::min(dr.D, kLeadLevels);
-        dr.phase2_begin();
-        dr.phase2_levels(dr.w.Pst, dr.w.dlim, 1, lead);
-        e = hipEventSynchronize(host->ev);
-        if (e != hipSuccess) return e;
-        int nlev = 0;
-        const int32_t *dl = (const int32_t *)host->pinned;
-        for (int b = 0; b < P.nb; ++b) nlev = std::max(nlev, std::min((int)dl[b], dr.D));
-        dr.phase2_levels(dr.w.Pst, dr.w.dlim, lead + 1, nlev);
-        dr.phase2_end();
     } else {
         int nlev = 0;
         e = dr.fill_levels(&nlev);
@@ -1854,10 +1860,15 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
         e = hipMemcpyAsync(r.Tp, dr.w.T0, sizeof(double) * n_groups(P), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
     dr.phase1();
-    int nlev = 0;
-    e = dr.fill_levels(&nlev);
-    if (e != hipSuccess) return e;
-    dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
+    if (D > kLeadLevels && H.ev) {
+        e = dr.phase2_read_back(hd, H.ev);  // hd is read again only after pack_readback
+        if (e != hipSuccess) return e;
+    } else {
+        int nlev = 0;
+        e = dr.fill_levels(&nlev);
+        if (e != hipSuccess) return e;
+        dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
+    }
     // the starting incumbent and the stage costs worth collecting, on the
     // device; one packed read-back brings the phase results, the collected
     // count and the first kSpecBounds collected bounds

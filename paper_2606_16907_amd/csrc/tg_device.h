@@ -208,6 +208,8 @@ struct RelaxHost {
     const int64_t *bvals;   // [nb] compatible micro-batch sizes, ascending
     int64_t B;              // global batch
     HostStage *stage;       // at least compose_relaxed_stage_bytes(P) bytes of pinned memory
+    hipEvent_t ev;          // an event on the current device, or null (then the fill depth
+                            // limits are read back by a stream synchronisation)
 };
 size_t compose_relaxed_ws_bytes(const DevProblem &P, int64_t n_surv);
 // Island construction from nodes (n <= 4096); synchronises the stream.

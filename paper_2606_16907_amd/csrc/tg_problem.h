@@ -20,6 +20,7 @@ struct tg_problem {
     // freed at destroy; relaxed calls on one handle take turns on it
     mutable std::mutex relax_mu;
     mutable tg::HostStage relax_stage;
+    mutable hipEvent_t relax_ev = nullptr;  // for the read-back of the fill depth limits
     // pinned words and an event for the composition's read-back of the fill
     // depth limits: taken by one call at a time (a call that finds them busy
     // reads back synchronously), freed at destroy
