@@ -264,7 +264,11 @@ tg_status tg_score_pairs(const tg_problem *p, int64_t first, int64_t count, doub
  * *n_survivors (host) receives the count; if it exceeds `capacity`, nothing
  * past capacity is written and TG_ECAPACITY is returned.  d_ws: caller
  * workspace of at least tg_prune_workspace_bytes(p) bytes (TG_ENOMEM if
- * smaller).  Synchronises the stream once to read the count.
+ * smaller).  Synchronises the stream once to read the count, which the
+ * kernels also store into about 20 KB of pinned host memory that the handle
+ * owns (its read-back words: allocated at the first prune or composition
+ * call, freed by tg_problem_destroy); a call that finds them in use by
+ * another call on the same handle copies the count back instead.
  */
 size_t tg_prune_workspace_bytes(const tg_problem *p);
 tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
@@ -327,15 +331,16 @@ tg_status tg_compose_pipeline_classes(const tg_problem *p, const int64_t *d_surv
  * plans with that bottleneck; across b it minimises T = (m - 1) P + F, ties
  * to the smaller b.  Ties inside a b go to the earliest first island, then
  * fewer stages, then the earliest cut, then the earliest next island.
- * Writes *out; TG_ENOPLAN (out->S = 0, out->T = +inf) if nothing fits.
- * d_ws: at least tg_compose_workspace_bytes(p, n_survivors) bytes.
- * Synchronises the stream at its end.  With more than 8 levels (min(K, L))
- * the host also waits once part-way, for a copy of the fill depth limits
- * into a few pinned bytes the handle owns (allocated at the first call,
- * freed by tg_problem_destroy), while the first fill levels run; a call that
- * finds them in use by another call on the same handle synchronises the
- * stream there instead when there are 64 levels or more, and otherwise
- * launches every fill level.
+ * Writes *out (stages past out->S zero); TG_ENOPLAN (out->S = 0, out->T =
+ * +inf) if nothing fits.  d_ws: at least tg_compose_workspace_bytes(p,
+ * n_survivors) bytes.  Synchronises the stream at its end.  The kernels
+ * store the fill depth limits and the result into the handle's read-back
+ * words (those of tg_prune); with more than 8 levels (min(K, L)) the host
+ * also waits once part-way, for the depth limits, while the first fill
+ * levels run.  A call that finds the words in use by another call on the
+ * same handle copies the result back instead, and reads the depth limits by
+ * a stream synchronisation when there are 64 levels or more, otherwise
+ * launching every fill level.
  */
 size_t tg_compose_workspace_bytes(const tg_problem *p, int64_t n_survivors);
 tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
@@ -358,11 +363,12 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
  * tg_compose_relaxed_workspace_bytes(p, n_survivors) bytes.  Synchronises the
  * stream after the bottleneck and fill phases and once per search round (a
  * few rounds; each evaluates F at a batch of bounds on the device), and with
- * more than 8 levels waits once more part-way, for a copy of the fill depth
- * limits, while the first fill levels run.  The host side of the search reads
- * back and uploads through a small pinned host buffer that the handle owns
- * (allocated at the first call, freed by tg_problem_destroy); relaxed calls on
- * one handle from several threads take turns.
+ * more than 8 levels waits once more part-way, for the fill depth limits,
+ * while the first fill levels run.  The host side of the search reads back
+ * and uploads through a small pinned host buffer that the handle owns
+ * (allocated at the first call, freed by tg_problem_destroy), into which the
+ * kernels also store the depth limits and the result; relaxed calls on one
+ * handle from several threads take turns.  Stages past out->S are zero.
  */
 size_t tg_compose_relaxed_workspace_bytes(const tg_problem *p, int64_t n_survivors);
 tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,

@@ -4,6 +4,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdarg>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -464,7 +465,7 @@ void tg_problem_destroy(tg_problem *p) {
     (void)hipSetDevice(p->device);
     (void)hipFree(p->dev_block);
     p->relax_stage.release();
-    p->compose_stage.release();
+    p->readback_stage.release();
     if (p->compose_ev) (void)hipEventDestroy(p->compose_ev);
     if (p->relax_ev) (void)hipEventDestroy(p->relax_ev);
     (void)hipSetDevice(cur);
@@ -540,17 +541,45 @@ size_t tg_prune_classes_workspace_bytes(const tg_problem *p) { return p ? tg::pr
 
 }  // extern "C"
 
-// The prune kernels on a checked workspace, then the survivor count.
+// The handle's pinned read-back words, which kernels store into: the
+// composition's result block at 0 (the prune's count there too, in calls of
+// its own), then the fill depth limits (nb int32).
+static size_t readback_dlim_at() { return (sizeof(tg::ComposeResult) + 255) & ~(size_t)255; }
+static size_t readback_bytes(const tg_problem *p) { return readback_dlim_at() + sizeof(int32_t) * (size_t)p->P.nb; }
+
+// The read-back words (the first call allocates them) when no other call
+// holds them: locks `lock` and returns them, else null (the caller reads back
+// into pageable memory).
+static const tg::HostStage *pinned_words(const tg_problem *p, std::unique_lock<std::mutex> &lock) {
+    lock = std::unique_lock<std::mutex>(p->readback_mu, std::try_to_lock);
+    if (!lock.owns_lock()) return nullptr;
+    // coherent: the kernels' stores go straight to host memory
+    if (p->readback_stage.reserve(readback_bytes(p), hipHostMallocPortable | hipHostMallocCoherent) != hipSuccess) {
+        (void)hipGetLastError();  // a failed allocation only means the pageable read-back
+        return nullptr;
+    }
+    return &p->readback_stage;
+}
+
+// The prune kernels on a checked workspace, then the survivor count (through
+// the pinned words only when the call may allocate them).
 static tg_status prune_run(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
-                           int64_t capacity, int64_t *n_survivors, void *d_ws, tg_stream stream) {
+                           int64_t capacity, int64_t *n_survivors, void *d_ws, tg_stream stream, bool may_alloc) {
     int64_t *d_total = nullptr;
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total);
-    if (e != hipSuccess) return hip_fail(e, "prune kernels");
+    std::unique_lock<std::mutex> lock;
+    const tg::HostStage *pw = may_alloc ? pinned_words(p, lock) : nullptr;  // the count is stored there too
+    hipError_t e = tg::launch_prune(p->P, d_cost, d_dmax, d_survivors, capacity, d_ws, s, &d_total,
+                                    pw ? (int64_t *)pw->dev : nullptr);
+    if (e != hipSuccess) {
+        (void)hipStreamSynchronize(s);  // nothing queued may store into the words once they are let go
+        return hip_fail(e, "prune kernels");
+    }
     int64_t total = 0;
-    e = hipMemcpyAsync(&total, d_total, sizeof(total), hipMemcpyDeviceToHost, s);
+    e = pw ? hipSuccess : hipMemcpyAsync(&total, d_total, sizeof(total), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "prune count");
+    if (pw) total = *(const int64_t *)pw->ptr;
     *n_survivors = total;
     if (total > capacity)
         return fail(TG_ECAPACITY, "%lld survivors exceed capacity %lld", (long long)total, (long long)capacity);
@@ -574,7 +603,7 @@ tg_status tg_prune(const tg_problem *p, const double *d_cost, const uint8_t *d_d
         return fail(TG_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, tg::prune_ws_bytes(p->P));
     if (check_alignment(d_cost, d_survivors, d_ws) != TG_OK) return TG_EINVAL;
     if (tg_status st = check_device(p); st != TG_OK) return st;
-    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, d_ws, stream);
+    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, d_ws, stream, true);
 }
 
 tg_status tg_prune_no_alloc(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
@@ -589,7 +618,7 @@ tg_status tg_prune_no_alloc(const tg_problem *p, const double *d_cost, const uin
     void *ws = nullptr;
     const hipError_t e = tg::static_scratch(p->device, &ws);
     if (e != hipSuccess) return hip_fail(e, "static scratch address");
-    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, ws, stream);
+    return prune_run(p, d_cost, d_dmax, d_survivors, capacity, n_survivors, ws, stream, false);
 }
 
 tg_status tg_prune_classes(const tg_problem *p, const double *d_cost, const uint8_t *d_dmax, int64_t *d_survivors,
@@ -663,13 +692,17 @@ static tg_status compose_begin(const tg_problem *p, const int64_t *d_survivors, 
 }
 
 // Reads the device result after the composition kernels.
-static tg_status compose_end(tg::ComposeResult *res_dev, tg_plan *out, hipStream_t s) {
-    tg::ComposeResult *res = new (std::nothrow) tg::ComposeResult;
+// stored: the pinned host copy the kernels stored the result into (header
+// and the plan's stages), or null (then it is copied from res_dev)
+static tg_status compose_end(tg::ComposeResult *res_dev, tg_plan *out, hipStream_t s,
+                             const tg::ComposeResult *stored = nullptr) {
+    tg::ComposeResult *owned = stored ? nullptr : new (std::nothrow) tg::ComposeResult;
+    const tg::ComposeResult *res = stored ? stored : owned;
     if (!res) return fail(TG_ENOMEM, "host allocation");
-    hipError_t e = hipMemcpyAsync(res, res_dev, sizeof(*res), hipMemcpyDeviceToHost, s);
+    hipError_t e = stored ? hipSuccess : hipMemcpyAsync(owned, res_dev, sizeof(*owned), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
-        delete res;
+        delete owned;
         return hip_fail(e, "compose result");
     }
     tg_status st = TG_OK;
@@ -680,10 +713,12 @@ static tg_status compose_end(tg::ComposeResult *res_dev, tg_plan *out, hipStream
         st = fail(TG_EDEVICE, "internal consistency check failed during backtracking (code %d)", res->err);
     } else if (res->status != TG_OK) {
         st = fail(TG_ENOPLAN, "no pipeline fits");
-    } else {
-        *out = res->plan;
+    } else {  // the header and the S stages; the stages past S are zero
+        const int S = std::min(std::max(res->plan.S, 0), 255);
+        std::memcpy(out, &res->plan, offsetof(tg_plan, stage) + sizeof(tg_stage) * S);
+        std::memset(out->stage + S, 0, sizeof(tg_stage) * (255 - S));
     }
-    delete res;
+    delete owned;
     return st;
 }
 
@@ -699,23 +734,28 @@ tg_status tg_compose_pipeline(const tg_problem *p, const int64_t *d_survivors, i
                                  need, s);
     if (st != TG_OK) return st;
     tg::ComposeResult *res_dev = nullptr;
-    // the handle's pinned read-back words, when no other call holds them
-    std::unique_lock<std::mutex> lock(p->compose_mu, std::try_to_lock);
-    tg::ComposeHost host{nullptr, nullptr};
-    if (lock.owns_lock()) {
-        // a failed allocation only means the synchronous read-back
-        if (p->compose_stage.reserve(sizeof(int32_t) * (size_t)p->P.nb) != hipSuccess) {
-            (void)hipGetLastError();
-        } else if (!p->compose_ev && hipEventCreateWithFlags(&p->compose_ev, hipEventDisableTiming) != hipSuccess) {
-            p->compose_ev = nullptr;
-            (void)hipGetLastError();
-        }
-        if (p->compose_stage.ptr && p->compose_ev) host = tg::ComposeHost{p->compose_stage.ptr, p->compose_ev};
+    // the handle's pinned read-back words, when no other call holds them: the
+    // kernels store the depth limits and the result there
+    std::unique_lock<std::mutex> lock;
+    const tg::HostStage *pw = pinned_words(p, lock);
+    if (pw && !p->compose_ev && hipEventCreateWithFlags(&p->compose_ev, hipEventDisableTiming) != hipSuccess) {
+        p->compose_ev = nullptr;  // then the depth limits are read back by a stream synchronisation
+        (void)hipGetLastError();
+    }
+    tg::ComposeHost host{};
+    if (pw) {
+        const size_t at = readback_dlim_at();
+        host = tg::ComposeHost{(int32_t *)((char *)pw->ptr + at), (int32_t *)((char *)pw->dev + at),
+                               (tg::ComposeResult *)pw->ptr, (tg::ComposeResult *)pw->dev, p->compose_ev};
+        if (!host.ev) host.dlim = host.dlim_dev = nullptr;
     }
     hipError_t e = tg::launch_compose(p->P, d_survivors, n_survivors, d_cost, d_dmax, nullptr, d_ws, s, &res_dev,
-                                      host.pinned ? &host : nullptr);
-    if (e != hipSuccess) return hip_fail(e, "compose kernels");
-    return compose_end(res_dev, out, s);
+                                      pw ? &host : nullptr);
+    if (e != hipSuccess) {
+        (void)hipStreamSynchronize(s);  // nothing queued may store into the words once they are let go
+        return hip_fail(e, "compose kernels");
+    }
+    return compose_end(res_dev, out, s, host.res);
 }
 
 tg_status tg_compose_pipeline_classes(const tg_problem *p, const int64_t *d_survivors, int64_t n_survivors,
@@ -746,7 +786,9 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
     if (st != TG_OK) return st;
     return no_throw([&] {
         std::lock_guard<std::mutex> lock(p->relax_mu);  // one relaxed call at a time uses the handle's staging
-        const hipError_t es = p->relax_stage.reserve(tg::compose_relaxed_stage_bytes(p->P));
+        // coherent: kernels store the depth limits and the result straight to host memory
+        const hipError_t es = p->relax_stage.reserve(tg::compose_relaxed_stage_bytes(p->P),
+                                                     hipHostMallocPortable | hipHostMallocCoherent);
         if (es != hipSuccess) return hip_fail(es, "pinned host staging");
         if (!p->relax_ev && hipEventCreateWithFlags(&p->relax_ev, hipEventDisableTiming) != hipSuccess) {
             p->relax_ev = nullptr;  // the depth limits are then read back by a stream synchronisation
@@ -754,11 +796,15 @@ tg_status tg_compose_pipeline_relaxed(const tg_problem *p, const int64_t *d_surv
         }
         const tg::RelaxHost H{p->outact.data(), p->E.data(), p->bvals.data(), p->B, &p->relax_stage, p->relax_ev};
         tg::ComposeResult *res_dev = nullptr;
+        const tg::ComposeResult *res_host = nullptr;
         int rounds = 0;
         hipError_t e = tg::launch_compose_relaxed(p->P, H, island_order, d_survivors, n_survivors, d_cost, d_dmax,
-                                                  d_ws, s, &res_dev, &rounds);
-        if (e != hipSuccess) return hip_fail(e, "relaxed compose kernels");
-        return compose_end(res_dev, out, s);
+                                                  d_ws, s, &res_dev, &res_host, &rounds);
+        if (e != hipSuccess) {
+            (void)hipStreamSynchronize(s);  // nothing queued may use the staging once it is let go
+            return hip_fail(e, "relaxed compose kernels");
+        }
+        return compose_end(res_dev, out, s, res_host);
     });
 }
 

@@ -28,6 +28,7 @@
 #include <cmath>
 #include <vector>
 #include <climits>
+#include <cstddef>
 #include <type_traits>
 
 #include "compose_util.h"
@@ -1082,7 +1083,7 @@ __global__ __launch_bounds__(SPLIT * KP, level_waves(SPLIT * KP)) void level_fil
 constexpr int kPstThreads = 1024;
 
 __global__ __launch_bounds__(kPstThreads) void pst_kernel(DevProblem P, int D, const double *__restrict__ Rv,
-                                                          double *Pst, int32_t *dlim) {
+                                                          double *Pst, int32_t *dlim, int32_t *dlim_host) {
     __shared__ double red[kPstThreads / kWave];
     const int wv = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
     double ub = kInf;
@@ -1117,9 +1118,12 @@ __global__ __launch_bounds__(kPstThreads) void pst_kernel(DevProblem P, int D, c
     for (int u = 1; u < kPstThreads / kWave; ++u) ub = fmin(ub, red[u]);
     for (int bi = threadIdx.x; bi < P.nb; bi += kPstThreads) {
         const double ps = Pst[bi];
-        if (!(ps < kInf)) continue;
-        const double mm1 = (double)(P.B / P.bvals[bi] - 1);
-        if ((mm1 * ps) + ps > ub) dlim[bi] = 0;
+        int32_t lim = dlim[bi];
+        if (ps < kInf && ((double)(P.B / P.bvals[bi] - 1) * ps) + ps > ub) {
+            lim = 0;
+            dlim[bi] = 0;
+        }
+        if (dlim_host) dlim_host[bi] = lim;
     }
 }
 
@@ -1184,7 +1188,8 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
                                                                 const double *EoT, const double *Pst,
                                                                 const double *rootF, const int32_t *root_o,
                                                                 const int32_t *root_d, const uint16_t *argF,
-                                                                const uint8_t *argG, ComposeResult *res) {
+                                                                const uint8_t *argG, ComposeResult *res,
+                                                                ComposeResult *res_host) {
     __shared__ int32_t st_i[256], st_j[256], st_o[256], st_on[256];
     __shared__ int32_t sh_S, sh_bb;
     const int L = P.L, K = P.K;
@@ -1276,20 +1281,30 @@ __global__ __launch_bounds__(kFinishThreads) void finish_kernel(DevProblem P, co
     }
     __syncthreads();
     const int S = sh_S;
-    if (S == 0) return;
-    const int bb = sh_bb;
-    const int64_t b = P.bvals[bb];
     const int wv = threadIdx.x / kWave;
-    for (int t = wv; t < S; t += kFinishThreads / kWave) {
-        const int d = S - t, i = st_i[t], j = st_j[t], o = st_o[t], o_next = st_on[t];
-        double link = 0.0;
-        if (d > 1) {
-            const double E = EoT[(int64_t)o_next * K + o];
-            link = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;
+    if (S > 0) {
+        const int bb = sh_bb;
+        const int64_t b = P.bvals[bb];
+        for (int t = wv; t < S; t += kFinishThreads / kWave) {
+            const int d = S - t, i = st_i[t], j = st_j[t], o = st_o[t], o_next = st_on[t];
+            double link = 0.0;
+            if (d > 1) {
+                const double E = EoT[(int64_t)o_next * K + o];
+                link = E == 0.0 ? kInf : ((2.0 * (double)b) * (double)P.outact[j - 1]) / E;
+            }
+            resolve_stage(P, gcnt, ent_c, ent_d, ent_i, group_id(P, o, bb, slice_of(L, i, j)), i, j, order[o], d,
+                          link, plan.stage[t], res);
         }
-        resolve_stage(P, gcnt, ent_c, ent_d, ent_i, group_id(P, o, bb, slice_of(L, i, j)), i, j, order[o], d, link,
-                      plan.stage[t], res);
     }
+    if (!res_host) return;
+    // the header and the S stages into host memory (8-byte words)
+    __syncthreads();
+    static_assert(offsetof(ComposeResult, plan) % 8 == 0 && offsetof(tg_plan, stage) % 8 == 0 &&
+                      sizeof(tg_stage) % 8 == 0, "result words");
+    const int n = (int)((offsetof(ComposeResult, plan) + offsetof(tg_plan, stage) + sizeof(tg_stage) * S) / 8);
+    const uint64_t *src = (const uint64_t *)res;
+    uint64_t *dst = (uint64_t *)res_host;
+    for (int k = threadIdx.x; k < n; k += kFinishThreads) dst[k] = src[k];
 }
 
 // ---------------------------------------------------------------------------
@@ -1309,7 +1324,7 @@ constexpr int64_t kSpecBounds = 4096;  // collected bounds read back with the ph
 struct RelaxXfer {
     size_t pst, f0, rv, thv, err, cnt, thb, down;
     size_t mm1, tau, bound, jb, jd, fdl, njob, up;
-    size_t h_up, h_jf, h_mm1, host;
+    size_t h_up, h_jf, h_mm1, h_res, host;
 };
 
 static RelaxXfer xfer_layout(const DevProblem &P) {
@@ -1341,6 +1356,7 @@ static RelaxXfer xfer_layout(const DevProblem &P) {
     x.h_up = put(x.up);
     x.h_jf = put(8 * J);
     x.h_mm1 = put(8 * nb);
+    x.h_res = put(sizeof(ComposeResult));
     x.host = o;
     return x;
 }
@@ -1610,7 +1626,7 @@ struct Driver {
 
     // phase 1: least bottleneck per b into w.Pst, the fill's depth limit per b
     // into w.dlim
-    void phase1() {
+    void phase1(int32_t *dlim_host = nullptr) {
         with_kp([&](auto kp) {
             constexpr int KP = decltype(kp)::value;
             for (int d = 1; d <= D; ++d) {
@@ -1631,7 +1647,7 @@ struct Driver {
                     go(std::integral_constant<int, 2>{});
             }
         });
-        pst_kernel<<<dim3(1), dim3(kPstThreads), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim);
+        pst_kernel<<<dim3(1), dim3(kPstThreads), 0, s>>>(P, D, w.Rv, w.Pst, w.dlim, dlim_host);
     }
 
     // The deepest fill level any b needs.  Reading w.dlim back costs one host
@@ -1661,14 +1677,14 @@ struct Driver {
         phase2_levels(bound, dlim, 1, nlev, table);
         phase2_end();
     }
-    // Phase 2 at P* with the depth limits read back through `pinned` (at least
-    // nb int32 of pinned host memory) and the event `ev`: the limits are copied
-    // right after phase 1, the first kLeadLevels fill levels are queued
-    // behind the copy, and the host waits for the copy alone before queueing
-    // the levels some b still needs, so the GPU keeps busy meanwhile.
-    hipError_t phase2_read_back(void *pinned, hipEvent_t ev) {
-        hipError_t e = hipMemcpyAsync(pinned, w.dlim, sizeof(int32_t) * P.nb, hipMemcpyDeviceToHost, s);
-        if (e == hipSuccess) e = hipEventRecord(ev, s);
+    // Phase 2 at P* with the depth limits that phase1(dlim_dev) stored into
+    // the pinned host words `dlim` (at least nb int32), read once the event
+    // `ev` has passed: the event is recorded right after phase 1, the first
+    // kLeadLevels fill levels are queued behind it, and the host waits for
+    // the event alone before queueing the levels some b still needs, so the
+    // GPU keeps busy meanwhile.
+    hipError_t phase2_read_back(const int32_t *dlim, hipEvent_t ev) {
+        hipError_t e = hipEventRecord(ev, s);
         if (e != hipSuccess) return e;
         const int lead = std::min(D, kLeadLevels);
         phase2_begin();
@@ -1676,8 +1692,7 @@ struct Driver {
         e = hipEventSynchronize(ev);
         if (e != hipSuccess) return e;
         int nlev = 0;
-        const int32_t *dl = (const int32_t *)pinned;
-        for (int b = 0; b < P.nb; ++b) nlev = std::max(nlev, std::min((int)dl[b], D));
+        for (int b = 0; b < P.nb; ++b) nlev = std::max(nlev, std::min((int)dlim[b], D));
         phase2_levels(w.Pst, w.dlim, lead + 1, nlev);
         phase2_end();
         return hipSuccess;
@@ -1765,10 +1780,12 @@ struct Driver {
         });
     }
 
-    void finish(const double *bound) {
+    // the plan into w.res and, when given, into res_host (device view of
+    // pinned host memory)
+    void finish(const double *bound, ComposeResult *res_host = nullptr) {
         finish_kernel<<<dim3(1), dim3(kFinishThreads), 0, s>>>(P, w.gcnt, w.ent_c, w.ent_d, w.ent_i, w.order, w.EoT,
                                                                  bound, w.rootF, w.root_o, w.root_d, w.argF, w.argG,
-                                                                 w.res);
+                                                                 w.res, res_host);
     }
 };
 
@@ -1781,10 +1798,12 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
     dr.setup(surv, n_surv, cost, dmax);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dr.phase1();
-    if (dr.D > kLeadLevels && host && host->pinned && host->ev) {
-        // pays at any depth past the lead: the GPU keeps busy while the host waits
-        e = dr.phase2_read_back(host->pinned, host->ev);
+    // the overlapped read-back pays at any depth past the lead: the GPU keeps
+    // busy while the host waits
+    const bool overlap = dr.D > kLeadLevels && host && host->dlim && host->ev;
+    dr.phase1(overlap ? host->dlim_dev : nullptr);
+    if (overlap) {
+        e = dr.phase2_read_back(host->dlim, host->ev);
         if (e != hipSuccess) return e;
     } else {
         int nlev = 0;
@@ -1792,7 +1811,7 @@ hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_su
         if (e != hipSuccess) return e;
         dr.phase2(dr.w.Pst, dr.w.dlim, nlev);
     }
-    dr.finish(dr.w.Pst);
+    dr.finish(dr.w.Pst, host ? host->res_dev : nullptr);
     return hipGetLastError();
 }
 
@@ -1840,7 +1859,8 @@ struct Incumbent {
 
 hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
                                   const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,
-                                  void *ws, hipStream_t s, ComposeResult **result_dev, int *rounds_out) {
+                                  void *ws, hipStream_t s, ComposeResult **result_dev,
+                                  const ComposeResult **result_host, int *rounds_out) {
     Driver dr(P, n_surv, ws, s);
     RelaxWs r = carve_relax(P, n_surv, (char *)ws + compose_ws_bytes(P, n_surv));
     const RelaxXfer X = xfer_layout(P);
@@ -1849,6 +1869,9 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     if (!H.stage || !H.stage->ptr || H.stage->bytes < X.host) return hipErrorInvalidValue;
     char *hs = (char *)H.stage->ptr;  // pinned: the copies below do not stall the host
     char *hd = hs, *hu = hs + X.h_up;
+    // the finish kernel stores the result into the stage too (every success below finishes)
+    ComposeResult *res_hd = (ComposeResult *)((char *)H.stage->dev + X.h_res);
+    *result_host = (const ComposeResult *)(hs + X.h_res);
     double *h_jf = (double *)(hs + X.h_jf), *h_mm1 = (double *)(hs + X.h_mm1);
     const int nb = P.nb, D = dr.D;
     for (int bi = 0; bi < nb; ++bi) h_mm1[bi] = (double)(H.B / H.bvals[bi] - 1);
@@ -1859,9 +1882,10 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     if (e == hipSuccess)
         e = hipMemcpyAsync(r.Tp, dr.w.T0, sizeof(double) * n_groups(P), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
-    dr.phase1();
-    if (D > kLeadLevels && H.ev) {
-        e = dr.phase2_read_back(hd, H.ev);  // hd is read again only after pack_readback
+    const bool overlap = D > kLeadLevels && H.ev;
+    dr.phase1(overlap ? (int32_t *)H.stage->dev : nullptr);  // into hd, the host view of the same words
+    if (overlap) {
+        e = dr.phase2_read_back((const int32_t *)hd, H.ev);  // hd is written again only by the copy below
         if (e != hipSuccess) return e;
     } else {
         int nlev = 0;
@@ -1894,7 +1918,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     const double *Pst = (const double *)(hd + X.pst), *F0 = (const double *)(hd + X.f0);
     const double *Rv = (const double *)(hd + X.rv);
     if (*(const int32_t *)(hd + X.err)) {  // invalid list: the finish kernel reports it
-        dr.finish(dr.w.Pst);
+        dr.finish(dr.w.Pst, res_hd);
         return hipGetLastError();
     }
     // the fill at bound tau has no whole plan deeper than the deepest level
@@ -2052,7 +2076,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     // the best b and its bound: reuse the phase-2 argmins when the bound is P*
     const int bstar = inc.T < kInf ? inc.b : -1;
     if (bstar < 0 || inc.tau == Pst[bstar]) {
-        dr.finish(dr.w.Pst);
+        dr.finish(dr.w.Pst, res_hd);
         return hipGetLastError();
     }
     double *h_bound = (double *)(hu + X.bound);
@@ -2070,7 +2094,7 @@ hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const
     if (e == hipSuccess) e = dr.restore_tables(r.Tp, used);
     if (e != hipSuccess) return e;
     dr.phase2(r.bound, r.fdl, last_lev, dr.w.T);  // the relaxed bound
-    dr.finish(r.bound);
+    dr.finish(r.bound, res_hd);
     return hipGetLastError();
 }
 

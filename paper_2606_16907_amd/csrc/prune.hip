@@ -205,8 +205,9 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(const uint64_t *__
     if (threadIdx.x == 0) tile_cnt[blockIdx.x] = total;
 }
 
-// Exclusive scan of n int64 values in place by one block; writes the sum to *total.
-__global__ __launch_bounds__(1024) void scan_small_i64(int64_t *a, int64_t n, int64_t *total) {
+// Exclusive scan of n int64 values in place by one block; writes the sum to
+// *total and, when given, to *total_host.
+__global__ __launch_bounds__(1024) void scan_small_i64(int64_t *a, int64_t n, int64_t *total, int64_t *total_host) {
     __shared__ int64_t lds[1024 / kWave + 1];
     int64_t carry = 0;
     for (int64_t base = 0; base < n; base += blockDim.x) {
@@ -217,7 +218,10 @@ __global__ __launch_bounds__(1024) void scan_small_i64(int64_t *a, int64_t n, in
         if (i < n) a[i] = carry + ex;
         carry += sum;
     }
-    if (threadIdx.x == 0) *total = carry;
+    if (threadIdx.x == 0) {
+        *total = carry;
+        if (total_host) *total_host = carry;
+    }
 }
 
 __global__ __launch_bounds__(kCountThreads) void emit_kernel(DevProblem P, const uint64_t *__restrict__ bitmap,
@@ -310,7 +314,7 @@ static hipError_t launch_frontier(const DevProblem &P, const double *cost, const
 
 // Survivor bitmap (at the start of ws) -> ascending candidate indices.
 static hipError_t launch_compact(const DevProblem &P, int64_t *surv, int64_t capacity, void *ws, hipStream_t s,
-                                 int64_t **d_total_out) {
+                                 int64_t **d_total_out, int64_t *total_host = nullptr) {
     const int64_t nw = bitmap_words(P);
     const int64_t nt = (nw + kTileWords - 1) / kTileWords;
     char *p = (char *)ws;
@@ -321,17 +325,17 @@ static hipError_t launch_compact(const DevProblem &P, int64_t *surv, int64_t cap
     int64_t *total = (int64_t *)p;
     *d_total_out = total;
     if (nt > 0) count_kernel<<<dim3((unsigned)nt), dim3(kCountThreads), 0, s>>>(bitmap, nw, tiles);
-    scan_small_i64<<<dim3(1), dim3(1024), 0, s>>>(tiles, nt, total);
+    scan_small_i64<<<dim3(1), dim3(1024), 0, s>>>(tiles, nt, total, total_host);
     if (nt > 0)
         emit_kernel<<<dim3((unsigned)nt), dim3(kCountThreads), 0, s>>>(P, bitmap, nw, tiles, surv, capacity);
     return hipGetLastError();
 }
 
 hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
-                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out) {
+                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out, int64_t *total_host) {
     hipError_t e = launch_frontier(P, cost, dmax, (uint64_t *)ws, s);
     if (e != hipSuccess) return e;
-    return launch_compact(P, surv, capacity, ws, s, d_total_out);
+    return launch_compact(P, surv, capacity, ws, s, d_total_out, total_host);
 }
 
 // Scratch of the prune variant that allocates nothing: a device array the

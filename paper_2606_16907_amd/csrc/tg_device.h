@@ -149,8 +149,11 @@ size_t prune_ws_bytes(const DevProblem &P);
 size_t prune_classes_ws_bytes(const DevProblem &P);
 hipError_t launch_prune_classes(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
                                 int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
+// total_host: the device view of a pinned host word the count is also stored
+// to, or null
 hipError_t launch_prune(const DevProblem &P, const double *cost, const uint8_t *dmax, int64_t *surv,
-                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out);
+                        int64_t capacity, void *ws, hipStream_t s, int64_t **d_total_out,
+                        int64_t *total_host = nullptr);
 // The static scratch of the prune variant that allocates nothing: its size,
 // and its device address on `device` (which must be current), resolved once
 // per GPU.
@@ -167,12 +170,15 @@ struct ComposeResult {
     int32_t pad[2];
     tg_plan plan;
 };
-// Pinned host words (at least nb int32) and an event on the current device,
-// with which the composition reads its fill depth limits back while the
-// first fill levels run; without them (null) the read-back synchronises the
-// stream.
+// Pinned host memory, each block seen from the host and from the device (the
+// address kernels store to).  The kernels store the fill depth limits (at
+// least nb int32) and the result straight into it, and the host waits on the
+// event `ev` (on the current device) for the limits while the first fill
+// levels run.  Without it (null) the limits are copied back by a stream
+// synchronisation and the result stays on the device alone.
 struct ComposeHost {
-    void *pinned;
+    int32_t *dlim, *dlim_dev;
+    ComposeResult *res, *res_dev;
     hipEvent_t ev;
 };
 hipError_t launch_compose(const DevProblem &P, const int64_t *surv, int64_t n_surv, const double *cost,
@@ -183,21 +189,26 @@ size_t compose_order_offset(const DevProblem &P, int64_t n_surv);  // where the 
 // Host tables the relaxed search reads (link times are enumerated on the host).
 // Pinned host memory owned by a caller and reused across calls (small
 // transfers that the host waits for).
+// `dev` is the same memory's device address (kernels store to it; the host
+// reads what they stored once it has waited for them).
 struct HostStage {
-    void *ptr = nullptr;
+    void *ptr = nullptr, *dev = nullptr;
     size_t bytes = 0;
-    hipError_t reserve(size_t n) {  // contents are not kept
+    hipError_t reserve(size_t n, unsigned flags = hipHostMallocPortable) {  // contents are not kept
         if (n <= bytes) return hipSuccess;
-        if (ptr) (void)hipHostFree(ptr);
-        ptr = nullptr;
-        bytes = 0;
-        const hipError_t e = hipHostMalloc(&ptr, n, hipHostMallocPortable);
-        if (e == hipSuccess) bytes = n;
+        release();
+        hipError_t e = hipHostMalloc(&ptr, n, flags);
+        if (e == hipSuccess) e = hipHostGetDevicePointer(&dev, ptr, 0);
+        if (e != hipSuccess) {
+            release();
+            return e;
+        }
+        bytes = n;
         return e;
     }
     void release() {
         if (ptr) (void)hipHostFree(ptr);
-        ptr = nullptr;
+        ptr = dev = nullptr;
         bytes = 0;
     }
 };
@@ -224,8 +235,11 @@ size_t compose_orders_ws_bytes(const DevProblem &P, int64_t n_surv);
 hipError_t launch_compose_orders(const DevProblem &P, const int64_t *bvals_host, const int64_t *surv, int64_t n_surv,
                                  const double *cost, const uint8_t *dmax, void *ws, hipStream_t s,
                                  ComposeResult **result_dev);
-// Synchronises the stream several times (once per search round).
+// Synchronises the stream several times (once per search round).  On
+// success the result is also stored into the stage at *result_host (host
+// view), read once the stream is synchronised.
 hipError_t launch_compose_relaxed(const DevProblem &P, const RelaxHost &H, const int32_t *order_host,
                                   const int64_t *surv, int64_t n_surv, const double *cost, const uint8_t *dmax,
-                                  void *ws, hipStream_t s, ComposeResult **result_dev, int *rounds_out);
+                                  void *ws, hipStream_t s, ComposeResult **result_dev,
+                                  const ComposeResult **result_host, int *rounds_out);
 }  // namespace tg

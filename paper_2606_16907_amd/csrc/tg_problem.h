@@ -21,10 +21,11 @@ struct tg_problem {
     mutable std::mutex relax_mu;
     mutable tg::HostStage relax_stage;
     mutable hipEvent_t relax_ev = nullptr;  // for the read-back of the fill depth limits
-    // pinned words and an event for the composition's read-back of the fill
-    // depth limits: taken by one call at a time (a call that finds them busy
-    // reads back synchronously), freed at destroy
-    mutable std::mutex compose_mu;
-    mutable tg::HostStage compose_stage;
+    // pinned words for the small read-backs of the prune (survivor count) and
+    // the composition (fill depth limits, then the result), and an event for
+    // the composition's overlapped one: taken by one call at a time (a call
+    // that finds them busy reads back into pageable memory), freed at destroy
+    mutable std::mutex readback_mu;
+    mutable tg::HostStage readback_stage;
     mutable hipEvent_t compose_ev = nullptr;
 };
