@@ -395,7 +395,10 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
     if (st == en) return;
     int M = 0;
     if (en - st <= kGroupRegs) {
-        // small group (the usual staircase): entries in registers, compared there
+        // small group (the usual staircase): entries in registers, compared
+        // there; the indices only break cost ties, so they load only when
+        // two entries cost the same (never among a surviving set's entries of
+        // one group, where the deeper or earlier of two equal costs dominates)
         double c[kGroupRegs];
         int d[kGroupRegs];
         int64_t id[kGroupRegs];
@@ -404,8 +407,14 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
         for (int e = 0; e < kGroupRegs; ++e) {
             c[e] = e < n ? ent_c[st + e] : kInf;
             d[e] = e < n ? (int)ent_d[st + e] : 0;
-            id[e] = e < n ? ent_i[st + e] : 0;
         }
+        bool tie = false;
+#pragma unroll
+        for (int e = 0; e < kGroupRegs; ++e)
+#pragma unroll
+            for (int q = e + 1; q < kGroupRegs; ++q) tie = tie || (q < n && c[q] == c[e]);
+#pragma unroll
+        for (int e = 0; e < kGroupRegs; ++e) id[e] = (tie && e < n) ? ent_i[st + e] : 0;
 #pragma unroll
         for (int e = 0; e < kGroupRegs; ++e) {
             if (e >= n) break;
@@ -425,7 +434,6 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
         for (int32_t e = st; e < en; ++e) {
             const double ce = ent_c[e];
             const int de = ent_d[e];
-            const int64_t ie = ent_i[e];
             M = max(M, de);
             v1 = fmin(v1, ce);
             if (de >= 2) v2 = fmin(v2, ce);
@@ -433,7 +441,8 @@ __device__ inline void cell_events(const int32_t *__restrict__ gcnt, const doubl
             for (int32_t q = st; q < en; ++q) {
                 const double cq = ent_c[q];
                 const int dq = ent_d[q];
-                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ie)));
+                // indices only for an exact tie in cost and depth
+                const bool less = cq < ce || (cq == ce && (dq > de || (dq == de && ent_i[q] < ent_i[e])));
                 if (less) De = max(De, dq);
             }
             if (De >= 2 && De < de && De + 1 <= D) emit(De + 1, ce);
