@@ -94,22 +94,31 @@ constexpr int kScoreConfigs = 16;  // configs per wave tile
 // monotone in d, so a first guess d0 from (H - state) / A1 (K once the
 // stash saturates at m micro-batches) is the answer exactly when d0 fits and
 // d0 + 1 does not; otherwise a short walk from d0 finds it.  Every decision
-// is an exact evaluation of fits(); the guess only picks where to look.
-__device__ inline int max_depth(double state, double A1, double H, double m_real, double guess_scale, int K) {
+// is an exact evaluation of fits(); the guess only picks where to look.  The
+// guess and both checks run on every lane without branches (in doubles: the
+// guess is a small integer, so min(d0, m) and min(d0 + 1, m) are the values
+// fits() takes); the wave walks only when a lane that scores a candidate
+// (`live`) has a wrong guess, and the walk returns d0 to a lane whose guess
+// is right.
+__device__ inline int max_depth(double state, double A1, double H, double m_real, double guess_scale, int K,
+                                bool live) {
     auto fits = [&](int d) -> bool {
         const double inflight = fmin((double)d, m_real);
         return state + inflight * A1 <= H;
     };
+    const double Kd = (double)K;
     const double q = (H - state) * guess_scale;
-    const int d0 = (q >= m_real) ? K : (q >= 1.0 ? (int)fmin(q, (double)K) : 0);
-    const bool lo_ok = d0 == 0 || fits(d0);
-    const bool hi_ok = d0 == K || !fits(d0 + 1);
-    if (lo_ok && hi_ok) return d0;
+    // floor(q) within [0, K] (NaN: 0)
+    const double g = q >= m_real ? Kd : floor(fmin(fmax(q, 0.0), Kd));
+    const bool lo_ok = g == 0.0 || state + fmin(g, m_real) * A1 <= H;
+    const bool hi_ok = g == Kd || !(state + fmin(g + 1.0, m_real) * A1 <= H);
+    const int d0 = (int)g;
+    if (__builtin_expect(__ballot(live && !(lo_ok && hi_ok)) == 0, 1)) return d0;
     int d = d0 > K - 1 ? K - 1 : d0;
 #pragma nounroll
-    while (d > 0 && !fits(d)) --d;
+    while (live && d > 0 && !fits(d)) --d;
 #pragma nounroll
-    while (d < K && fits(d + 1)) ++d;
+    while (live && d < K && fits(d + 1)) ++d;
     return d;
 }
 
@@ -202,6 +211,10 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
     }
     const int K = P.K;
     const int64_t NS = P.NS;
+    // a tile wholly inside [first, last) with a slice for every lane stores
+    // without per-candidate checks, from a per-row base
+    const int64_t t0 = g_beg * NS + st * kWave;
+    const bool whole = (st + 1) * kWave <= NS && t0 >= first && t0 + (int64_t)(ng - 1) * NS + (kWave - 1) < last;
     for (int t = 0; t < ng; ++t) {
         const StagedCoef &c = cs[wv][t];
         // with recomputation only the layer boundaries (outputs) are stashed
@@ -223,7 +236,16 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
             // offloaded: one micro-batch on the device at every depth
             dm = (state + (fmin(1.0, c.m_real) * A1)) <= c.H ? K : 0;
         } else {
-            dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * ((kExt && c.rc) ? inv_oa : inv_act), K);
+            dm = max_depth(state, A1, c.H, c.m_real, c.inv_rho * ((kExt && c.rc) ? inv_oa : inv_act), K, sv);
+        }
+        if (whole) {
+            const int64_t row = t0 + (int64_t)t * NS - first;
+            __builtin_nontemporal_store(v, cost + row + lane);
+            if (kNtDepth)
+                __builtin_nontemporal_store((uint8_t)dm, dmax + row + lane);
+            else
+                dmax[row + lane] = (uint8_t)dm;
+            continue;
         }
         const int64_t idx = (g_beg + t) * NS + s;
         if (sv && idx >= first && idx < last) {
