@@ -88,7 +88,12 @@ hipError_t launch_coef(const DevProblem &P, Coef *coef, hipStream_t s) {
 // scoring
 // ---------------------------------------------------------------------------
 constexpr int kScoreWaves = 4;     // waves per block
-constexpr int kScoreConfigs = 16;  // configs per wave tile
+// Configs per wave tile: 16 where a wave's depth rows are line-aligned and go
+// out as streaming stores (more rows a tile scatter those stores: the
+// 128-layer instance took 1.74 -> 1.91 ms at 32), 32 elsewhere, where a
+// tile's slice sums and coefficient staging then serve more configs (MoE
+// 110 -> 105 µs, 70B 122 -> 114 µs).
+constexpr int score_configs(bool nt_depth) { return nt_depth ? 16 : 32; }
 
 // Largest d in 1..K with state + min(d, m) * A1 <= H, or 0.  fits() is
 // monotone in d, so a first guess d0 from (H - state) / A1 (K once the
@@ -147,7 +152,8 @@ template <bool kDense, bool kExt, bool kNtDepth>
 __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first, int64_t last, int64_t g_lo,
                                                     int64_t g_hi, int64_t n_stiles, int64_t n_tiles,
                                                     double *__restrict__ cost, uint8_t *__restrict__ dmax) {
-    __shared__ StagedCoef cs[kScoreWaves][kScoreConfigs];
+    constexpr int kCfg = score_configs(kNtDepth);
+    __shared__ StagedCoef cs[kScoreWaves][kCfg];
     const int64_t per_xcd = gridDim.x / kXcds;
     const int64_t blk = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -158,8 +164,8 @@ __global__ __launch_bounds__(256) void score_kernel(DevProblem P, int64_t first,
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t s = st * kWave + lane;
     const bool sv = s < P.NS;
-    const int64_t g_beg = g_lo + gt * kScoreConfigs;
-    const int ng = (int)(min(g_beg + kScoreConfigs, g_hi + 1) - g_beg);
+    const int64_t g_beg = g_lo + gt * kCfg;
+    const int ng = (int)(min(g_beg + kCfg, g_hi + 1) - g_beg);
     if (lane < ng) {
         const Coef &c = P.coef[g_beg + lane];
         StagedCoef x;
@@ -264,13 +270,14 @@ hipError_t launch_score(const DevProblem &P, int64_t first, int64_t count, doubl
     if (count <= 0) return hipSuccess;
     const int64_t last = first + count;
     const int64_t g_lo = first / P.NS, g_hi = (last - 1) / P.NS;
-    const int64_t n_gtiles = (g_hi - g_lo + kScoreConfigs) / kScoreConfigs;
+    const bool nt_depth = (P.NS & 63) == 0;
+    const int cfg = score_configs(nt_depth);
+    const int64_t n_gtiles = (g_hi - g_lo + cfg) / cfg;
     const int64_t n_stiles = (P.NS + kWave - 1) / kWave;
     const int64_t n_tiles = n_gtiles * n_stiles;
     int64_t blocks = (n_tiles + kScoreWaves - 1) / kScoreWaves;
     blocks = (blocks + kXcds - 1) / kXcds * kXcds;  // whole rounds over the XCDs
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    const bool nt_depth = (P.NS & 63) == 0;
     auto go = [&](auto dense, auto ext) {
         constexpr bool D = decltype(dense)::value, X = decltype(ext)::value;
         if (nt_depth)
