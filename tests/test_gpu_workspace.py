@@ -4,8 +4,8 @@ write first.  A workspace is dirtied by a call on a thinned candidate list
 rows), then reused for the full surviving set; the plan must equal, bit for
 bit, the plan computed on a fresh workspace.  And calls on one handle from
 several threads and streams (which share the handle's pinned read-back
-words: one call at a time uses them, the others read back synchronously)
-give the single-threaded plan."""
+words: one call at a time uses them, the others read back another way)
+give the single-threaded plan, also with prunes running beside them."""
 import threading
 
 import numpy as np
@@ -115,3 +115,58 @@ def test_threads_on_one_handle_give_the_same_plan():
             assert st == ref_st
             if st == T.TG_OK:
                 same_plan(plan, ref)
+
+
+def test_prunes_and_compositions_from_threads_share_the_read_back_words():
+    """Prunes (survivor count) and compositions (depth limits and plan) on one
+    handle from several threads and streams at once: whichever call finds the
+    handle's pinned words held reads back another way, and every call returns
+    the single-threaded result."""
+    inst = wide_instance(21, 70, 70, "few")
+    print("case", inst["name"], flush=True)
+    p = T.Problem(inst)
+    cost, dmax = p.tg_score_pairs()
+    ref_surv = p.tg_prune(cost, dmax)
+    n = int(ref_surv.numel())
+    ref_st, ref = p.tg_compose_pipeline(ref_surv, cost, dmax)
+    ref_host = ref_surv.cpu().numpy()
+    torch.cuda.synchronize()
+    errors, counts = [], []
+
+    def pruner():
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s):
+                ws = p.prune_workspace()
+                buf = torch.empty(n + 64, dtype=torch.int64, device="cuda")
+                for _ in range(8):
+                    sv = p.tg_prune(cost, dmax, survivors=buf, workspace=ws)
+                    counts.append(int(sv.numel()))
+                    assert np.array_equal(sv.cpu().numpy(), ref_host)
+            s.synchronize()
+        except Exception as e:  # reported below, in the test's own thread
+            errors.append(e)
+
+    def composer():
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s):
+                ws = p.compose_workspace(n)
+                for _ in range(5):
+                    st, plan = p.tg_compose_pipeline(ref_surv, cost, dmax, workspace=ws)
+                    assert st == ref_st
+                    if st == T.TG_OK:
+                        same_plan(plan, ref)
+            s.synchronize()
+        except Exception as e:
+            errors.append(e)
+
+    threads = [threading.Thread(target=f) for f in (pruner, composer, pruner, composer)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    assert counts == [n] * 16
